@@ -1,0 +1,216 @@
+/*
+ * neuroute.h -- C ABI of the MI355X (gfx950) batched query-time search of
+ * NeuRoute (arXiv 2608.15438).
+ *
+ * The search returns, for each query q, the k database rows S_k(q) that the
+ * method deems nearest under the Euclidean distance (problem statement,
+ * Sec. 3.1, Eq. 1-2).  It runs the five query-time steps of the paper:
+ *   1. encoder forward pass to logits l_q            (Sec. 3.2.1; Sec. 4.5 "Architecture")
+ *   2. binarisation a_j = [l_j >= tau_j] (Eq. 10), deviation scores
+ *      delta_j = |l_j - tau_j| and the ordered probe sequence of bucket
+ *      enumeration                                    (Sec. 3.4.1, Algorithm 1)
+ *   3. bucket lookup in a CSR directory               (Sec. 3.3 "Bucket allocation"; Sec. 3.4 "Implementation")
+ *   4. centroid stage with calibrated gate theta = d_min + M(d_min) and
+ *      heap-quality early stop                        (Sec. 3.4.2, Algorithm 2)
+ *   5. exact refinement of C(q) = C_dir u C_cent in the original space to a
+ *      per-query top-k                                (Sec. 3.4 intro; Sec. 3.5)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - DEVICE pointers are HIP device memory of the current device, owned by the
+ *   caller.  HOST pointers are ordinary host memory, read during the call.
+ * - Work is enqueued on `stream` and the call returns after launch.  Argument
+ *   and index errors are reported synchronously as an nr_status and nothing is
+ *   enqueued; a HIP launch failure is reported as NR_EDEVICE.  Faults inside a
+ *   kernel surface at the caller's next synchronisation of the stream.
+ * - No C++ exception crosses this interface.  nr_last_error() returns a
+ *   thread-local message describing the last failure of the calling thread.
+ * - Distances are SQUARED Euclidean distances (squaring does not change the
+ *   ranking, Sec. 3.5); uint8 distances are exact integers, fp32 distances
+ *   are accumulated in fp32.  Every result row is sorted by (distance, original
+ *   id); rows with fewer than k candidates are padded with id -1, distance +inf.
+ * - Calls on one index from different streams may overlap; each stream gets
+ *   its own workspace.  The index itself is read-only after upload.
+ * - Limits: 1 <= k <= 64, 1 <= probe_budget <= 1024, 1 <= b <= 30,
+ *   L_sel <= min(b, 32), 1 <= B_batch <= 64, K_c limited by LDS (16384),
+ *   encoder widths <= 4096; anything beyond returns NR_EUNSUPPORTED.
+ */
+#ifndef NEUROUTE_H
+#define NEUROUTE_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  NR_OK = 0,
+  NR_EINVAL = 1,         /* bad argument */
+  NR_ENOMEM = 2,         /* device or host allocation failed */
+  NR_EDEVICE = 3,        /* a HIP call failed */
+  NR_EUNSUPPORTED = 4,   /* valid but beyond the limits above */
+  NR_ECORRUPT = 5        /* index arrays fail validation at upload */
+} nr_status;
+
+typedef enum { NR_U8 = 0, NR_F32 = 1 } nr_dtype;
+
+#define NR_MAX_LAYERS 8
+#define NR_MAX_KNOTS 32
+#define NR_MAX_K 64
+#define NR_MAX_PROBES 1024
+
+typedef struct nr_index nr_index;   /* opaque, library-owned */
+
+/*
+ * Index description (index construction, Sec. 3.3).  Rows are stored permuted
+ * so that every bucket-local cluster is one contiguous row span:
+ *   bucket (code) c   -> clusters [bc_off[c], bc_off[c+1])
+ *   cluster g         -> rows     [cl_off[g], cl_off[g+1])
+ *   permuted row r    -> original id row_ids[r]
+ * Code bit j is latent dimension j.  The encoder has n_layers linear layers:
+ * hidden layers are Linear -> eval-mode BatchNorm folded to a per-channel
+ * affine (bn_scale, bn_shift; NULL = identity) -> ReLU; the last layer is
+ * Linear and yields the b logits.  The input is multiplied by input_scale
+ * (1/255 for uint8 rows).
+ */
+typedef struct {
+  int64_t n;                      /* database rows, >= 1 */
+  int32_t d;                      /* E_dim; d * sizeof(element) must be a multiple of 16 */
+  int32_t dtype;                  /* nr_dtype of rows and queries */
+  int32_t b;                      /* L_dim = number of code bits */
+  int32_t n_layers;               /* 1..NR_MAX_LAYERS */
+  const int32_t *widths;          /* HOST [n_layers+1]; widths[0] = d, widths[n_layers] = b */
+  const float *const *weights;    /* HOST [n_layers] -> HOST [widths[l+1] x widths[l]], row-major */
+  const float *const *biases;     /* HOST [n_layers] -> HOST [widths[l+1]]; NULL array or entry = 0 */
+  const float *const *bn_scale;   /* HOST [n_layers] -> HOST [widths[l+1]] (hidden layers); NULL = 1 */
+  const float *const *bn_shift;   /* HOST, as bn_scale; NULL = 0 */
+  float input_scale;
+  const float *tau;               /* HOST [b] binarisation thresholds (median per dim, Sec. 3.2.3) */
+  /* DEVICE arrays, BORROWED: they must stay valid and unchanged until
+   * nr_index_free.  They are never copied (the payload may be ~128 GB). */
+  const void *rows;               /* [n x d] permuted payload, 16-byte aligned */
+  const int64_t *row_ids;         /* [n] original id of each permuted row (a permutation of 0..n-1) */
+  const uint32_t *bc_off;         /* [2^b + 1] non-decreasing, bc_off[0] = 0, bc_off[2^b] = n_clusters */
+  const uint64_t *cl_off;         /* [n_clusters + 1] non-decreasing, cl_off[0] = 0, cl_off[n_clusters] = n */
+  const float *centroids;         /* [n_clusters x b] cluster centroids in latent space */
+  int64_t n_clusters;             /* >= 1, < 2^32 */
+} nr_index_desc;
+
+/*
+ * Query-time knobs of Algorithms 1 and 2 (the "gate params").  Alg. 1 keeps
+ * flip sets of the l_sel least stable dimensions with at most r_max flips and
+ * score <= s_max; with finite s_max the scores are put in n_bins equal-width
+ * bins, with s_max = +inf every probe is its own bin.  The probe sequence is
+ * ordered by (score, rank mask) and cut to probe_budget entries.  Alg. 2
+ * scores centroids of multi-cluster buckets in batches of <= b_batch, keeps
+ * the k_c best under the gate d <= d_min + M(d_min) (gate_on), and stops
+ * (early_stop_on) once the heap is full, at least b_min bins were visited and
+ * t_low consecutive batches were low quality: fewer than u_heap entries kept
+ * AND (OR when lowq_or) fewer than u_front of them within
+ * d_min + alpha_front * M(d_min).  M is piecewise linear through m_knots
+ * knots (m_x strictly increasing, m_y non-decreasing), constant outside them,
+ * and 0 when m_knots == 0; distances are squared L2 in latent space.
+ */
+typedef struct {
+  int32_t l_sel;
+  int32_t r_max;
+  float s_max;
+  int32_t n_bins;
+  int32_t k_c;
+  int32_t b_batch;
+  int32_t b_min;
+  int32_t t_low;
+  int32_t u_heap;
+  int32_t u_front;
+  float alpha_front;
+  int32_t gate_on;
+  int32_t early_stop_on;
+  int32_t lowq_or;
+  int32_t m_knots;
+  float m_x[NR_MAX_KNOTS];
+  float m_y[NR_MAX_KNOTS];
+} nr_params;
+
+/* Per-query counters written by nr_search_ex when `qstats` is not NULL. */
+#define NR_QSTATS 8
+enum {
+  NR_QS_PROBES = 0,      /* probes in the sequence */
+  NR_QS_CLUSTERS = 1,    /* |C(q)| */
+  NR_QS_DIRECT = 2,      /* |C_dir(q)| */
+  NR_QS_SCORED = 3,      /* centroids scored */
+  NR_QS_STOPPED = 4,     /* 1 if the early stop fired */
+  NR_QS_ROWS = 5,        /* rows refined (candidates), low 32 bits */
+  NR_QS_TILES = 6,       /* refinement tiles */
+  NR_QS_BATCHES = 7      /* centroid batches */
+};
+
+/* Upload an index: validates the description and the device CSR arrays
+ * (monotone offsets, bounds, row_ids a permutation), copies the encoder and
+ * tau to the device and borrows the DEVICE arrays.  Synchronises `stream`.
+ * On success *out owns the library's copies until nr_index_free. */
+nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t stream);
+
+/* Release an index and its workspaces (synchronises the device). */
+nr_status nr_index_free(nr_index *index);
+
+/* Batched search (all five steps).  queries: DEVICE [nq x d] of the index
+ * dtype; out_ids: DEVICE int64 [nq x k]; out_dists: DEVICE fp32 [nq x k]. */
+nr_status nr_search(const nr_index *index, const void *queries, int64_t nq, int32_t k,
+                    int32_t probe_budget, const nr_params *params, int64_t *out_ids,
+                    float *out_dists, hipStream_t stream);
+
+/* As nr_search; logits (DEVICE fp32 [nq x b]) replace step 1 when not NULL;
+ * qstats (DEVICE int32 [nq x NR_QSTATS]) receives per-query counters when not
+ * NULL. */
+nr_status nr_search_ex(const nr_index *index, const void *queries, const float *logits,
+                       int64_t nq, int32_t k, int32_t probe_budget, const nr_params *params,
+                       int64_t *out_ids, float *out_dists, int32_t *qstats, hipStream_t stream);
+
+/* Step 1 only: logits DEVICE fp32 [nq x b]. */
+nr_status nr_encode(const nr_index *index, const void *queries, int64_t nq, float *logits,
+                    hipStream_t stream);
+
+/* Step 2 only (Algorithm 1): for each query the first counts[q] <= probe_budget
+ * entries of codes/costs/bins (DEVICE [nq x probe_budget]) hold the ordered
+ * probe sequence; the rest is unspecified. */
+nr_status nr_probe(const nr_index *index, const float *logits, int64_t nq, int32_t probe_budget,
+                   const nr_params *params, uint32_t *codes, float *costs, int32_t *bins,
+                   int32_t *counts, hipStream_t stream);
+
+/* Steps 2-4: candidate clusters C(q) = C_dir (visiting order) followed by
+ * C_cent in (distance, cluster) order.  clusters: DEVICE uint32 [nq x cap],
+ * n_clusters: DEVICE int32 [nq].  cap must be >= nr_route_capacity(). */
+nr_status nr_route(const nr_index *index, const float *logits, int64_t nq, int32_t probe_budget,
+                   const nr_params *params, uint32_t *clusters, int32_t *n_clusters, int64_t cap,
+                   hipStream_t stream);
+
+/* Capacity a C(q) list can need: probe_budget + min(k_c, n_clusters). */
+int64_t nr_route_capacity(const nr_index *index, int32_t probe_budget, const nr_params *params);
+
+/* Step 5 only: exact top-k over the rows of the given clusters (same layout
+ * as nr_route's output). */
+nr_status nr_refine(const nr_index *index, const void *queries, int64_t nq, int32_t k,
+                    const uint32_t *clusters, const int32_t *n_clusters, int64_t cap,
+                    int64_t *out_ids, float *out_dists, hipStream_t stream);
+
+/* Stage timing with HIP events on the launch stream (off by default).
+ * nr_profile_read synchronises the recorded events and returns the summed
+ * milliseconds per stage {encode, probe, route, plan, refine, merge} and the
+ * number of timed searches since the last reset. */
+#define NR_STAGES 6
+nr_status nr_profile_enable(nr_index *index, int32_t on);
+nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches, int32_t reset);
+
+/* Number of refinement tiles and rows of the last search on `stream`
+ * (synchronises the stream). */
+nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *tiles, int64_t *rows);
+
+const char *nr_status_string(nr_status status);
+const char *nr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NEUROUTE_H */

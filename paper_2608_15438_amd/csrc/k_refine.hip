@@ -1,0 +1,376 @@
+// Step 5: exact refinement of C(q) in the original space (Sec. 3.4 intro,
+// Sec. 3.5) -- the HBM-bound part of the search.
+//
+//  plan   (one wave per query)  row prefix over the query's clusters, total
+//         rows R_q, tile size T_q = max(TILE_MIN_ROWS, ceil(R_q / 64)), then
+//         a scan over queries numbers the (query, row range) tiles;
+//  refine (persistent waves)    each wave takes tiles from an atomic counter
+//         and walks the tile's virtual rows; 8 lanes cover one 128-byte row
+//         segment with one 16-byte load each, so a wave instruction reads 8
+//         full cache lines; U rows per lane group are in flight;
+//         uint8:  |x - q|^2 = x.x - 2 x.q + q.q with packed u8 dot products,
+//                 exact in int32;   fp32: fmaf((x-q), (x-q), acc);
+//         the 8 partial sums are combined with xor shuffles; a sorted top-k
+//         of (distance, original id) lives in lanes 0..k-1 and a candidate
+//         reads its original id only when it can enter it;
+//  merge  (one wave per query)  the tiles' partial top-k lists are merged.
+#include "nr_internal.h"
+
+namespace nr {
+
+// ------------------------------------------------------------------ plan
+// cluster counts come from the caller in nr_refine: keep them in [0, cap]
+__device__ __forceinline__ int clamp_count(int32_t n, int64_t cap) {
+  return n < 0 ? 0 : (n > cap ? (int)cap : n);
+}
+
+__global__ void __launch_bounds__(256) k_plan_rows(PlanArgs a) {
+  const int lane = lane_id();
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (q >= a.nq) return;
+  const int n = clamp_count(a.nclus[q], a.cap);
+  const uint32_t *cl = a.clus + q * a.cap;
+  uint32_t *pre = a.rowpre + q * (a.cap + 1);
+  uint64_t run = 0;
+  if (lane == 0) pre[0] = 0;
+  for (int i0 = 0; i0 < n; i0 += WAVE) {
+    const int i = i0 + lane;
+    uint64_t sz = 0;
+    if (i < n) {
+      const uint32_t c = cl[i];
+      if (c < a.n_clusters) sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
+    }
+    const uint64_t incl = wave_incl_scan_u64(sz);
+    if (i < n) pre[i + 1] = (uint32_t)(run + incl);
+    run += bcast_u64(incl, WAVE - 1);
+  }
+  if (lane == 0) {
+    // a list of more than 2^32 - 1 rows (only possible with repeated clusters
+    // given to nr_refine) is refused: it returns no candidates
+    const uint32_t tot = run > 0xffffffffull ? 0u : (uint32_t)run;
+    uint32_t t = (tot + MAX_TILES_PER_QUERY - 1) / MAX_TILES_PER_QUERY;
+    if (t < TILE_MIN_ROWS) t = TILE_MIN_ROWS;
+    a.rtot[q] = tot;
+    a.tsize[q] = t;
+    a.ntile[q] = (int32_t)(((uint64_t)tot + t - 1) / t);
+  }
+}
+
+// exclusive scan of ntile over all queries in one block; resets the counter
+__global__ void __launch_bounds__(1024) k_plan_scan(PlanArgs a) {
+  __shared__ int32_t part[1024];
+  const int tid = threadIdx.x;
+  const int64_t per = (a.nq + 1023) / 1024;
+  const int64_t s0 = tid * per;
+  int32_t sum = 0;
+  for (int64_t i = s0; i < s0 + per && i < a.nq; ++i) sum += a.ntile[i];
+  part[tid] = sum;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    int32_t v = tid >= o ? part[tid - o] : 0;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  int32_t run = part[tid] - sum;
+  for (int64_t i = s0; i < s0 + per && i < a.nq; ++i) {
+    a.tile_off[i] = run;
+    run += a.ntile[i];
+  }
+  if (tid == 1023) {
+    a.tile_off[a.nq] = part[1023];
+    *a.counter = 0;
+  }
+}
+
+// one thread per (query, tile slot): tile -> query and first cluster
+__global__ void __launch_bounds__(256) k_plan_tiles(PlanArgs a) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t q = g / MAX_TILES_PER_QUERY;
+  const int t = (int)(g % MAX_TILES_PER_QUERY);
+  if (q >= a.nq || t >= a.ntile[q]) return;
+  const int32_t tix = a.tile_off[q] + t;
+  const uint32_t v0 = (uint32_t)t * a.tsize[q];
+  const uint32_t *pre = a.rowpre + q * (a.cap + 1);
+  // last cluster i with pre[i] <= v0 (clusters of zero rows are skipped)
+  int lo = 0, hi = clamp_count(a.nclus[q], a.cap) - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (pre[mid] <= v0) lo = mid; else hi = mid - 1;
+  }
+  a.tile_q[tix] = (int32_t)q;
+  a.tile_c0[tix] = lo;
+}
+
+hipError_t launch_plan(const PlanArgs &a, hipStream_t s) {
+  if (a.nq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_plan_rows, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(1024), 0, s, a);
+  int64_t th = a.nq * MAX_TILES_PER_QUERY;
+  hipLaunchKernelGGL(k_plan_tiles, dim3((unsigned)((th + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ top-k in lanes
+// Lanes 0..k-1 hold a list sorted by (key, id); `kth` is the last entry when full.
+struct TopK {
+  uint32_t key;
+  int64_t id;
+  int cnt;
+  uint32_t kth_key;
+  int64_t kth_id;
+};
+
+__device__ __forceinline__ void topk_init(TopK &t) {
+  t.key = 0xffffffffu;
+  t.id = -1;
+  t.cnt = 0;
+  t.kth_key = 0xffffffffu;
+  t.kth_id = INT64_MAX;
+}
+
+// insert (ck, cid) if it ranks among the k best (wave-uniform arguments)
+__device__ __forceinline__ void topk_insert(TopK &t, int k, uint32_t ck, int64_t cid) {
+  const int lane = lane_id();
+  if (t.cnt == k && (ck > t.kth_key || (ck == t.kth_key && cid >= t.kth_id))) return;
+  const bool less = lane < t.cnt && (t.key < ck || (t.key == ck && t.id < cid));
+  const int pos = popc64(ballot(less));
+  const uint32_t up_key = (uint32_t)__shfl_up((int)t.key, 1);
+  const int64_t up_id = (int64_t)shfl_up_u64((uint64_t)t.id, 1);
+  if (lane == pos) { t.key = ck; t.id = cid; }
+  else if (lane > pos && lane < k) { t.key = up_key; t.id = up_id; }
+  t.cnt = t.cnt + 1 < k ? t.cnt + 1 : k;
+  if (t.cnt == k) {
+    t.kth_key = bcast_u32(t.key, k - 1);
+    t.kth_id = (int64_t)bcast_u64((uint64_t)t.id, k - 1);
+  }
+}
+
+// ------------------------------------------------------------------ refine
+template <int IS_U8, int NSEG, int U>
+__global__ void __launch_bounds__(256) k_refine(RefineArgs a) {
+  __shared__ uint32_t s_vs[4][STAGE_CLUSTERS + 1];
+  __shared__ uint64_t s_ps[4][STAGE_CLUSTERS];
+  const int lane = lane_id();
+  const int w = threadIdx.x >> 6;
+  const int g = lane >> 3;      // lane group: one row at a time
+  const int gl = lane & 7;      // 16-byte slot inside a 128-byte row segment
+  uint32_t *vs = s_vs[w];
+  uint64_t *ps = s_ps[w];
+  const int total = a.tile_off[a.nq];
+  const int rb = a.row_bytes;
+  const int k = a.k;
+  const unsigned char *rows = (const unsigned char *)a.rows;
+
+  for (;;) {
+    int t = 0;
+    if (lane == 0) t = atomicAdd(a.counter, 1);
+    t = __builtin_amdgcn_readfirstlane(t);
+    if (t >= total) break;
+    const int64_t q = a.tile_q[t];
+    const uint32_t T = a.tsize[q];
+    const uint32_t R = a.rtot[q];
+    const uint32_t v0 = (uint32_t)(t - a.tile_off[q]) * T;
+    const uint32_t v1 = v0 + T < R ? v0 + T : R;
+    const uint32_t *pre = a.rowpre + q * (a.cap + 1);
+    const uint32_t *cl = a.clus + q * a.cap;
+    const int n_cl = clamp_count(a.nclus[q], a.cap);
+    int c = a.tile_c0[t];
+
+    // this lane's slices of the query
+    uint4 qv[NSEG];
+    const unsigned char *qb = (const unsigned char *)a.queries + q * (int64_t)rb;
+#pragma unroll
+    for (int s = 0; s < NSEG; ++s) {
+      const int off = 128 * s + 16 * gl;
+      qv[s] = off < rb ? *(const uint4 *)(qb + off) : make_uint4(0, 0, 0, 0);
+    }
+    int32_t qq = 0;
+    if (IS_U8) {
+#pragma unroll
+      for (int s = 0; s < NSEG; ++s) {
+        uint32_t acc = (uint32_t)qq;
+        acc = __builtin_amdgcn_udot4(qv[s].x, qv[s].x, acc, false);
+        acc = __builtin_amdgcn_udot4(qv[s].y, qv[s].y, acc, false);
+        acc = __builtin_amdgcn_udot4(qv[s].z, qv[s].z, acc, false);
+        acc = __builtin_amdgcn_udot4(qv[s].w, qv[s].w, acc, false);
+        qq = (int32_t)acc;
+      }
+      qq += __shfl_xor(qq, 1);
+      qq += __shfl_xor(qq, 2);
+      qq += __shfl_xor(qq, 4);
+    }
+    TopK tk;
+    topk_init(tk);
+
+    uint32_t v = v0;
+    while (v < v1) {
+      // stage clusters c .. c+ns-1: virtual and physical first rows
+      const int ns = n_cl - c < STAGE_CLUSTERS ? n_cl - c : STAGE_CLUSTERS;
+      for (int j = lane; j < ns; j += WAVE) {
+        vs[j] = pre[c + j];
+        const uint32_t cj = cl[c + j];
+        ps[j] = cj < a.n_clusters ? a.cl_off[cj] : 0;
+      }
+      if (lane == 0) vs[ns] = pre[c + ns];
+      __builtin_amdgcn_wave_barrier();
+      const uint32_t vend = v1 < vs[ns] ? v1 : vs[ns];
+      int cur = 0;  // per lane group; rows of a group only increase
+      for (uint32_t vb = v; vb < vend; vb += 8 * U) {
+        uint64_t phys[U];
+        bool ok[U];
+        uint4 xv[U][NSEG];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const uint32_t rv = vb + 8 * u + g;
+          ok[u] = rv < vend;
+          phys[u] = 0;
+          if (ok[u]) {
+            while (vs[cur + 1] <= rv) ++cur;
+            phys[u] = ps[cur] + (rv - vs[cur]);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const unsigned char *rp = rows + phys[u] * (uint64_t)rb;
+#pragma unroll
+          for (int s = 0; s < NSEG; ++s) {
+            const int off = 128 * s + 16 * gl;
+            xv[u][s] = (ok[u] && off < rb) ? *(const uint4 *)(rp + off) : make_uint4(0, 0, 0, 0);
+          }
+        }
+        uint32_t key[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (IS_U8) {
+            uint32_t xx = 0, xq = 0;
+#pragma unroll
+            for (int s = 0; s < NSEG; ++s) {
+              xx = __builtin_amdgcn_udot4(xv[u][s].x, xv[u][s].x, xx, false);
+              xx = __builtin_amdgcn_udot4(xv[u][s].y, xv[u][s].y, xx, false);
+              xx = __builtin_amdgcn_udot4(xv[u][s].z, xv[u][s].z, xx, false);
+              xx = __builtin_amdgcn_udot4(xv[u][s].w, xv[u][s].w, xx, false);
+              xq = __builtin_amdgcn_udot4(xv[u][s].x, qv[s].x, xq, false);
+              xq = __builtin_amdgcn_udot4(xv[u][s].y, qv[s].y, xq, false);
+              xq = __builtin_amdgcn_udot4(xv[u][s].z, qv[s].z, xq, false);
+              xq = __builtin_amdgcn_udot4(xv[u][s].w, qv[s].w, xq, false);
+            }
+            int32_t part = (int32_t)xx - 2 * (int32_t)xq;
+            part += __shfl_xor(part, 1);
+            part += __shfl_xor(part, 2);
+            part += __shfl_xor(part, 4);
+            key[u] = (uint32_t)(part + qq);
+          } else {
+            float acc = 0.0f;
+#pragma unroll
+            for (int s = 0; s < NSEG; ++s) {
+              float t0 = __uint_as_float(xv[u][s].x) - __uint_as_float(qv[s].x);
+              float t1 = __uint_as_float(xv[u][s].y) - __uint_as_float(qv[s].y);
+              float t2 = __uint_as_float(xv[u][s].z) - __uint_as_float(qv[s].z);
+              float t3 = __uint_as_float(xv[u][s].w) - __uint_as_float(qv[s].w);
+              acc = fmaf(t0, t0, acc);
+              acc = fmaf(t1, t1, acc);
+              acc = fmaf(t2, t2, acc);
+              acc = fmaf(t3, t3, acc);
+            }
+            acc += __shfl_xor(acc, 1);
+            acc += __shfl_xor(acc, 2);
+            acc += __shfl_xor(acc, 4);
+            key[u] = __float_as_uint(acc);
+          }
+        }
+        // candidates that may enter the top-k read their original id
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          uint64_t m = ballot(ok[u] && gl == 0 && key[u] <= tk.kth_key);
+          while (m) {
+            const int src = __ffsll((unsigned long long)m) - 1;
+            m &= m - 1;
+            const uint32_t ck = bcast_u32(key[u], src);
+            if (tk.cnt == k && ck > tk.kth_key) continue;
+            const uint64_t cp = bcast_u64(phys[u], src);
+            const int64_t id = a.row_ids[cp];
+            topk_insert(tk, k, ck, id);
+          }
+        }
+      }
+      v = vend;
+      c += ns;
+      __builtin_amdgcn_wave_barrier();
+    }
+    // partial result of this tile
+    if (lane < k) {
+      a.pkey[(int64_t)t * k + lane] = lane < tk.cnt ? tk.key : 0xffffffffu;
+      a.pid[(int64_t)t * k + lane] = lane < tk.cnt ? tk.id : -1;
+    }
+  }
+}
+
+template <int IS_U8>
+static hipError_t launch_refine_t(const RefineArgs &a, int nseg, int grid, hipStream_t s) {
+#define NR_REFINE_CASE(NS, UU)                                                     \
+  if (nseg <= NS) {                                                                \
+    hipLaunchKernelGGL((k_refine<IS_U8, NS, UU>), dim3(grid), dim3(256), 0, s, a); \
+    return hipGetLastError();                                                      \
+  }
+  NR_REFINE_CASE(1, 8)
+  NR_REFINE_CASE(2, 4)
+  NR_REFINE_CASE(3, 4)
+  NR_REFINE_CASE(4, 2)
+  NR_REFINE_CASE(8, 1)
+  NR_REFINE_CASE(16, 1)
+  NR_REFINE_CASE(48, 1)
+#undef NR_REFINE_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s) {
+  if (a.nq <= 0) return hipSuccess;
+  const int nseg = (a.row_bytes + 127) / 128;
+  const int grid = n_cu * 8;
+  return dtype == NR_U8 ? launch_refine_t<1>(a, nseg, grid, s) : launch_refine_t<0>(a, nseg, grid, s);
+}
+
+// ------------------------------------------------------------------ merge
+__global__ void __launch_bounds__(256) k_merge(MergeArgs a) {
+  const int lane = lane_id();
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (q >= a.nq) return;
+  const int k = a.k;
+  const int64_t e0 = (int64_t)a.tile_off[q] * k, e1 = (int64_t)a.tile_off[q + 1] * k;
+  TopK tk;
+  topk_init(tk);
+  for (int64_t i0 = e0; i0 < e1; i0 += WAVE) {
+    const int64_t i = i0 + lane;
+    uint32_t key = 0xffffffffu;
+    int64_t id = -1;
+    if (i < e1) {
+      key = a.pkey[i];
+      id = a.pid[i];
+    }
+    uint64_t m = ballot(id >= 0 && key <= tk.kth_key);
+    while (m) {
+      const int src = __ffsll((unsigned long long)m) - 1;
+      m &= m - 1;
+      topk_insert(tk, k, bcast_u32(key, src), (int64_t)bcast_u64((uint64_t)id, src));
+    }
+  }
+  if (lane < k) {
+    const bool have = lane < tk.cnt;
+    a.out_ids[q * k + lane] = have ? tk.id : -1;
+    a.out_dists[q * k + lane] =
+        have ? (a.is_u8 ? (float)tk.key : __uint_as_float(tk.key)) : INFINITY;
+  }
+  if (lane == 0 && a.qstats) {
+    a.qstats[q * NR_QSTATS + NR_QS_ROWS] = (int32_t)a.rtot[q];
+    a.qstats[q * NR_QSTATS + NR_QS_TILES] = a.tile_off[q + 1] - a.tile_off[q];
+  }
+}
+
+hipError_t launch_merge(const MergeArgs &a, hipStream_t s) {
+  if (a.nq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_merge, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace nr

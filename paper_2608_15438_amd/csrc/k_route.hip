@@ -1,0 +1,236 @@
+// Steps 3-4: bucket lookup in the CSR directory and the centroid stage of
+// Algorithm 2 (Sec. 3.4.2), one wavefront per query.
+//
+// Bins are visited in increasing order; every visited bin increments b_proc.
+// A probed bucket with one cluster goes straight to C_dir; the clusters of
+// multi-cluster buckets form C_z (probe order, then cluster id) and are scored
+// in batches of <= B_batch, one centroid per lane:
+//   d_c = squared L2 in logit space, acc = fmaf(t, t, acc) over dims in order;
+//   d_min tracks the best distance, theta = d_min + M(d_min) gates the heap;
+//   H <- the K_c smallest (d, cluster) of (H u batch) with d <= theta;
+//   u_heap / u_front count batch entries kept in H (and within the front
+//   d_min + alpha_front * M(d_min)); t_low counts consecutive low batches;
+//   stop once |H| = K_c, b_proc >= B_min and t_low >= T_low.
+// C(q) = C_dir (visiting order) followed by H in (d, cluster) order.
+//
+// H is a sorted array of u64 keys (d bits << 32 | cluster) in LDS.  A batch
+// is sorted across the wave (bitonic), then merged by ranks: batch element i
+// lands at i + |{h < key_i}|, a heap element moves up by |{batch < h}|; the
+// moving tail is rewritten from the top down so no element is overwritten
+// before it is read.  Probe lookups are fetched 64 at a time into LDS.
+#include "nr_internal.h"
+
+namespace nr {
+
+struct RouteLds {
+  uint32_t wc0[WAVE], wc1[WAVE];  // probe window: cluster ranges
+  int32_t wbin[WAVE];
+  uint32_t wpre[WAVE];            // exclusive prefix of multi-cluster sizes
+  uint32_t pend[WAVE];            // pending batch (cluster ids)
+  uint64_t bkey[WAVE];            // sorted batch keys
+};
+
+__device__ __forceinline__ float margin_dev(const RouteArgs &a, float x) {
+  const int m = a.m_knots;
+  if (m <= 0) return 0.0f;
+  if (m == 1 || x <= a.m_x[0]) return a.m_y[0];
+  if (x >= a.m_x[m - 1]) return a.m_y[m - 1];
+  int i = 0;
+  while (i + 1 < m - 1 && a.m_x[i + 1] <= x) ++i;
+  float v = fmaf(x - a.m_x[i], a.m_slope[i], a.m_y[i]);
+  v = v < a.m_y[i] ? a.m_y[i] : v;
+  v = v > a.m_y[i + 1] ? a.m_y[i + 1] : v;
+  return v;
+}
+
+__global__ void __launch_bounds__(64) k_route(RouteArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  RouteLds &S = *reinterpret_cast<RouteLds *>(smem_raw);
+  uint64_t *H = reinterpret_cast<uint64_t *>(smem_raw + sizeof(RouteLds));
+  const int lane = lane_id();
+  const int64_t q = blockIdx.x;
+  if (q >= a.nq) return;
+  const int b = a.b, P = a.P, k_c = a.k_c;
+  const float lg = lane < b ? a.logits[q * b + lane] : 0.0f;
+  const int cnt = a.counts[q];
+  const uint32_t *codes = a.codes + q * P;
+  const int32_t *bins = a.bins + q * P;
+  uint32_t *out = a.clus + q * a.cap;
+
+  int h = 0, ndir = 0, npend = 0;
+  float d_min = INFINITY;
+  int b_proc = 0, t_low = 0, n_scored = 0, n_batches = 0;
+  bool stop = false;
+  const int z_last = cnt > 0 ? bins[cnt - 1] : -1;
+
+  auto full_and_quiet = [&]() {
+    return a.early_stop_on && h == k_c && b_proc >= a.b_min && t_low >= a.t_low;
+  };
+
+  // score the pending batch and fold it into H
+  auto run_batch = [&]() {
+    const int nb = npend;
+    n_batches += 1;
+    n_scored += nb;
+    float d = INFINITY;
+    uint32_t cid = 0;
+    if (lane < nb) {
+      cid = S.pend[lane];
+      const float *mu = a.centroids + (int64_t)cid * b;
+      float acc = 0.0f;
+      for (int j = 0; j < b; ++j) {
+        float lj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lg), j));
+        float t = lj - mu[j];
+        acc = fmaf(t, t, acc);
+      }
+      d = acc;
+    }
+    float dm = wave_min_f32(d);
+    d_min = dm < d_min ? dm : d_min;
+    const float M = margin_dev(a, d_min);
+    const float theta = a.gate_on ? d_min + M : INFINITY;
+    const float am = a.alpha_front * M;
+    const float theta_f = d_min + am;
+    const bool valid = lane < nb && d <= theta;
+    uint64_t key = valid ? (((uint64_t)__float_as_uint(d) << 32) | cid) : ~0ull;
+    key = wave_sort_u64(key);
+    const int nv = popc64(ballot(valid));
+    // prune H to d <= theta (a prefix, as H is sorted)
+    const uint64_t cut = ((uint64_t)__float_as_uint(theta) + 1ull) << 32;
+    const int hv = lower_bound_u64(H, h, cut);
+    S.bkey[lane] = key;
+    __builtin_amdgcn_wave_barrier();
+    int pos = WAVE + lane;
+    if (lane < nv) pos = lane + lower_bound_u64(H, hv, key);
+    // move the tail of H that batch keys overtake
+    if (nv > 0) {
+      const int j0 = lower_bound_u64(H, hv, S.bkey[0]);
+      int top = hv;
+      while (top > j0) {
+        int lo = top - WAVE > j0 ? top - WAVE : j0;
+        int j = lo + lane;
+        uint64_t hk = 0;
+        int np = -1;
+        if (j < top) {
+          hk = H[j];
+          np = j + lower_bound_u64(S.bkey, nv, hk);
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (j < top && np < k_c) H[np] = hk;
+        __builtin_amdgcn_wave_barrier();
+        top = lo;
+      }
+      if (lane < nv && pos < k_c) H[pos] = key;
+      __builtin_amdgcn_wave_barrier();
+    }
+    h = hv + nv < k_c ? hv + nv : k_c;
+    const bool kept = lane < nv && pos < k_c;
+    const float dk = __uint_as_float((uint32_t)(key >> 32));
+    const int u_heap = popc64(ballot(kept));
+    const int u_front = popc64(ballot(kept && dk <= theta_f));
+    const bool low = a.lowq_or ? (u_heap < a.u_heap || u_front < a.u_front)
+                               : (u_heap < a.u_heap && u_front < a.u_front);
+    t_low = low ? t_low + 1 : 0;
+    npend = 0;
+    if (full_and_quiet()) stop = true;
+  };
+
+  int p = 0;                 // next probe of the sequence
+  int wb = 0;                // window: probes [wb, wb + WAVE), slot = lane
+  bool have_window = false;
+  for (int z = 0; z <= z_last && !stop; ++z) {
+    b_proc += 1;
+    while (p < cnt) {
+      if (!have_window || p >= wb + WAVE) {
+        wb = p;
+        have_window = true;
+        const int i = wb + lane;
+        uint32_t c0 = 0, c1 = 0;
+        int bn = 0x7fffffff;
+        if (i < cnt) {
+          const uint32_t code = codes[i];
+          c0 = a.bc_off[code];
+          c1 = a.bc_off[(uint64_t)code + 1];
+          bn = bins[i];
+        }
+        S.wc0[lane] = c0;
+        S.wc1[lane] = c1;
+        S.wbin[lane] = bn;
+        __builtin_amdgcn_wave_barrier();
+      }
+      const int off = p - wb;
+      // bins are sorted, so the probes of bin z from p are the slots [off, off + run)
+      const bool in_run = lane >= off && wb + lane < cnt && S.wbin[lane] == z;
+      const int run = popc64(ballot(in_run));
+      if (run == 0) break;
+      const uint32_t c0 = S.wc0[lane], c1 = S.wc1[lane];
+      const uint32_t sz = in_run ? c1 - c0 : 0;
+      // single-cluster buckets go to C_dir in probe order
+      const bool single = sz == 1;
+      const uint64_t sm = ballot(single);
+      if (single) out[ndir + popc64(sm & lanemask_lt())] = c0;
+      ndir += popc64(sm);
+      // clusters of multi-cluster buckets feed the batches (not after a stop)
+      if (!stop) {
+        const uint32_t msz = sz >= 2 ? sz : 0;
+        const uint32_t incl = wave_incl_scan_u32(msz);
+        const uint32_t total = __shfl(incl, WAVE - 1);
+        S.wpre[lane] = in_run ? incl - msz : 0xffffffffu;
+        __builtin_amdgcn_wave_barrier();
+        uint32_t v = 0;
+        while (v < total && !stop) {
+          uint32_t take = (uint32_t)(a.b_batch - npend);
+          if (take > total - v) take = total - v;
+          if ((uint32_t)lane < take) {
+            const uint32_t vi = v + lane;
+            // last slot of the run whose prefix is <= vi: zero-size slots share
+            // the prefix of the next non-empty one, so this is the owner
+            int lo = off, hi = off + run - 1;
+            while (lo < hi) {
+              int mid = (lo + hi + 1) >> 1;
+              if (S.wpre[mid] <= vi) lo = mid; else hi = mid - 1;
+            }
+            S.pend[npend + lane] = S.wc0[lo] + (vi - S.wpre[lo]);
+          }
+          __builtin_amdgcn_wave_barrier();
+          npend += (int)take;
+          v += take;
+          if (npend == a.b_batch) run_batch();
+        }
+      }
+      p += run;
+      if (off + run < WAVE) break;  // bin z ends inside this window
+    }
+    if (!stop && npend > 0) run_batch();
+    npend = 0;
+    if (!stop && full_and_quiet()) stop = true;
+  }
+
+  for (int i = lane; i < h; i += WAVE) out[ndir + i] = (uint32_t)H[i];
+  if (lane == 0) {
+    a.nclus[q] = ndir + h;
+    if (a.qstats) {
+      int32_t *st = a.qstats + q * NR_QSTATS;
+      st[NR_QS_PROBES] = cnt;
+      st[NR_QS_CLUSTERS] = ndir + h;
+      st[NR_QS_DIRECT] = ndir;
+      st[NR_QS_SCORED] = n_scored;
+      st[NR_QS_STOPPED] = stop ? 1 : 0;
+      st[NR_QS_BATCHES] = n_batches;
+    }
+  }
+}
+
+hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
+  if (a.nq <= 0) return hipSuccess;
+  size_t lds = sizeof(RouteLds) + sizeof(uint64_t) * (size_t)a.k_c;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)k_route,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_route, dim3((unsigned)a.nq), dim3(64), lds, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace nr

@@ -1,0 +1,704 @@
+// Host side of the C ABI declared in include/neuroute.h: argument and index
+// validation, device copies of the encoder, per-stream workspaces and the
+// launch sequence of the five search steps.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "nr_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+nr_status fail(nr_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIP_OK(call)                                                                      \
+  do {                                                                                    \
+    hipError_t e_ = (call);                                                               \
+    if (e_ != hipSuccess)                                                                 \
+      return fail(NR_EDEVICE, "%s failed: %s", #call, hipGetErrorString(e_));           \
+  } while (0)
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Carves typed sub-buffers out of one device allocation.
+struct Carver {
+  char *base;
+  size_t off = 0;
+  template <class T>
+  T *take(size_t count) {
+    off = align_up(off, 256);
+    T *p = reinterpret_cast<T *>(base ? base + off : nullptr);
+    off += sizeof(T) * count;
+    return p;
+  }
+};
+
+struct Buffers {
+  float *logits, *act0, *act1;
+  uint32_t *codes;
+  float *costs;
+  int32_t *bins, *counts;
+  uint32_t *clus;
+  int32_t *nclus;
+  uint32_t *rowpre, *rtot, *tsize;
+  int32_t *ntile, *tile_off, *tile_q, *tile_c0, *counter;
+  uint32_t *pkey;
+  int64_t *pid;
+};
+
+struct Shape {
+  int64_t nq;   // queries per chunk
+  int P, b, k, maxw;
+  int64_t cap;
+};
+
+Buffers carve(char *base, const Shape &s, size_t *bytes) {
+  Carver c{base};
+  Buffers B;
+  B.logits = c.take<float>((size_t)s.nq * s.b);
+  B.act0 = c.take<float>((size_t)s.nq * s.maxw);
+  B.act1 = c.take<float>((size_t)s.nq * s.maxw);
+  B.codes = c.take<uint32_t>((size_t)s.nq * s.P);
+  B.costs = c.take<float>((size_t)s.nq * s.P);
+  B.bins = c.take<int32_t>((size_t)s.nq * s.P);
+  B.counts = c.take<int32_t>((size_t)s.nq);
+  B.clus = c.take<uint32_t>((size_t)s.nq * s.cap);
+  B.nclus = c.take<int32_t>((size_t)s.nq);
+  B.rowpre = c.take<uint32_t>((size_t)s.nq * (s.cap + 1));
+  B.rtot = c.take<uint32_t>((size_t)s.nq);
+  B.tsize = c.take<uint32_t>((size_t)s.nq);
+  B.ntile = c.take<int32_t>((size_t)s.nq);
+  B.tile_off = c.take<int32_t>((size_t)s.nq + 1);
+  B.tile_q = c.take<int32_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY);
+  B.tile_c0 = c.take<int32_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY);
+  B.counter = c.take<int32_t>(1);
+  B.pkey = c.take<uint32_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
+  B.pid = c.take<int64_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
+  *bytes = align_up(c.off, 256);
+  return B;
+}
+
+struct Workspace {
+  hipStream_t stream = nullptr;
+  char *base = nullptr;
+  size_t bytes = 0;
+  Buffers last{};
+  int64_t last_nq = 0;
+};
+
+struct EventSet {
+  hipEvent_t ev[NR_STAGES + 1];
+};
+
+}  // namespace
+
+struct nr_index {
+  nr_index_desc d;               // scalars and borrowed device pointers
+  std::vector<int32_t> widths;
+  float *params = nullptr;       // device copy of all layers
+  std::vector<const float *> W, bias, bn_scale, bn_shift;
+  float *tau = nullptr;
+  int maxw = 0;
+  int n_cu = 0;
+  std::mutex mu;
+  std::vector<Workspace> ws;
+  bool profiling = false;
+  std::vector<EventSet> pending;
+  double stage_ms[NR_STAGES] = {0};
+  int64_t n_timed = 0;
+};
+
+namespace {
+
+nr_status workspace_for(nr_index *ix, hipStream_t stream, const Shape &s, Buffers *out,
+                        Workspace **wsp) {
+  size_t need = 0;
+  carve(nullptr, s, &need);
+  std::lock_guard<std::mutex> g(ix->mu);
+  Workspace *w = nullptr;
+  for (auto &x : ix->ws)
+    if (x.stream == stream) w = &x;
+  if (!w) {
+    ix->ws.emplace_back();
+    w = &ix->ws.back();
+    w->stream = stream;
+  }
+  if (w->bytes < need) {
+    if (w->base) {
+      HIP_OK(hipStreamSynchronize(stream));
+      HIP_OK(hipFree(w->base));
+      w->base = nullptr;
+      w->bytes = 0;
+    }
+    size_t grow = need + need / 4;
+    if (hipMalloc(&w->base, grow) != hipSuccess) {
+      (void)hipGetLastError();
+      w->base = nullptr;
+      return fail(NR_ENOMEM, "workspace allocation of %zu bytes failed", grow);
+    }
+    w->bytes = grow;
+  }
+  size_t dummy;
+  *out = carve(w->base, s, &dummy);
+  *wsp = w;
+  return NR_OK;
+}
+
+int64_t kc_eff(const nr_index *ix, const nr_params *p) {
+  int64_t k = p->k_c;
+  return k < ix->d.n_clusters ? k : ix->d.n_clusters;
+}
+
+nr_status check_params(const nr_index *ix, int32_t P, const nr_params *p) {
+  if (!p) return fail(NR_EINVAL, "params is NULL");
+  const int b = ix->d.b;
+  if (P < 1) return fail(NR_EINVAL, "probe_budget must be >= 1 (got %d)", P);
+  if (P > NR_MAX_PROBES) return fail(NR_EUNSUPPORTED, "probe_budget %d > %d", P, NR_MAX_PROBES);
+  if (p->l_sel < 0 || p->l_sel > b || p->l_sel > 32)
+    return fail(NR_EINVAL, "l_sel %d outside [0, min(b=%d, 32)]", p->l_sel, b);
+  if (p->r_max < 0) return fail(NR_EINVAL, "r_max must be >= 0");
+  if (std::isnan(p->s_max) || p->s_max < 0.f) return fail(NR_EINVAL, "s_max must be >= 0");
+  if (std::isfinite(p->s_max) && (p->n_bins < 1 || p->s_max <= 0.f))
+    return fail(NR_EINVAL, "finite s_max needs s_max > 0 and n_bins >= 1");
+  if (p->k_c < 1) return fail(NR_EINVAL, "k_c must be >= 1");
+  if (kc_eff(ix, p) > nr::MAX_KC)
+    return fail(NR_EUNSUPPORTED, "k_c %d exceeds the LDS heap limit %d", p->k_c, nr::MAX_KC);
+  if (p->b_batch < 1 || p->b_batch > 64) return fail(NR_EUNSUPPORTED, "b_batch must be in [1, 64]");
+  if (p->m_knots < 0 || p->m_knots > NR_MAX_KNOTS)
+    return fail(NR_EINVAL, "m_knots must be in [0, %d]", NR_MAX_KNOTS);
+  for (int i = 0; i < p->m_knots; ++i) {
+    if (!std::isfinite(p->m_x[i]) || !std::isfinite(p->m_y[i]))
+      return fail(NR_EINVAL, "margin knot %d is not finite", i);
+    if (i > 0 && !(p->m_x[i] > p->m_x[i - 1]))
+      return fail(NR_EINVAL, "margin knots must have strictly increasing x");
+    if (i > 0 && p->m_y[i] < p->m_y[i - 1])
+      return fail(NR_EINVAL, "margin knots must have non-decreasing y");
+  }
+  if (!std::isfinite(p->alpha_front)) return fail(NR_EINVAL, "alpha_front must be finite");
+  return NR_OK;
+}
+
+Shape shape_of(const nr_index *ix, int64_t nq, int P, int k, int64_t cap) {
+  Shape s;
+  s.nq = nq < nr::QUERY_CHUNK ? nq : nr::QUERY_CHUNK;
+  s.P = P;
+  s.b = ix->d.b;
+  s.k = k;
+  s.maxw = ix->maxw;
+  s.cap = cap;
+  return s;
+}
+
+size_t elem_size(const nr_index *ix) { return ix->d.dtype == NR_U8 ? 1 : 4; }
+
+// ----------------------------------------------------------------- stages
+hipError_t run_encode(const nr_index *ix, const void *q, int64_t nq, float *logits,
+                      const Buffers &B, hipStream_t s) {
+  const int L = (int)ix->widths.size() - 1;
+  const void *in = q;
+  int in_u8 = ix->d.dtype == NR_U8;
+  float *bufs[2] = {B.act0, B.act1};
+  for (int l = 0; l < L; ++l) {
+    nr::EncodeLayerArgs a{};
+    a.in = in;
+    a.in_u8 = in_u8;
+    a.out = l + 1 == L ? logits : bufs[l & 1];
+    a.W = ix->W[l];
+    a.bias = ix->bias[l];
+    a.bn_scale = l + 1 < L ? ix->bn_scale[l] : nullptr;
+    a.bn_shift = l + 1 < L ? ix->bn_shift[l] : nullptr;
+    a.in_scale = l == 0 ? ix->d.input_scale : 1.0f;
+    a.relu = l + 1 < L;
+    a.M = nq;
+    a.K = ix->widths[l];
+    a.N = ix->widths[l + 1];
+    hipError_t e = nr::launch_encode_layer(a, s);
+    if (e != hipSuccess) return e;
+    in = a.out;
+    in_u8 = 0;
+  }
+  return hipSuccess;
+}
+
+hipError_t run_probe(const nr_index *ix, const float *logits, int64_t nq, int P,
+                     const nr_params *p, uint32_t *codes, float *costs, int32_t *bins,
+                     int32_t *counts, hipStream_t s) {
+  nr::ProbeArgs a{};
+  a.logits = logits;
+  a.tau = ix->tau;
+  a.nq = nq;
+  a.b = ix->d.b;
+  a.l_sel = p->l_sel;
+  a.r_max = p->r_max;
+  a.P = P;
+  a.finite = std::isfinite(p->s_max) ? 1 : 0;
+  a.s_max = p->s_max;
+  a.n_bins = a.finite ? p->n_bins : 1;
+  a.bin_scale = a.finite ? (float)p->n_bins / p->s_max : 0.0f;
+  a.codes = codes;
+  a.costs = costs;
+  a.bins = bins;
+  a.counts = counts;
+  return nr::launch_probe(a, s);
+}
+
+hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
+                     const nr_params *p, const Buffers &B, uint32_t *clus, int32_t *nclus,
+                     int64_t cap, int32_t *qstats, hipStream_t s) {
+  nr::RouteArgs a{};
+  a.logits = logits;
+  a.nq = nq;
+  a.b = ix->d.b;
+  a.P = P;
+  a.codes = B.codes;
+  a.bins = B.bins;
+  a.counts = B.counts;
+  a.bc_off = ix->d.bc_off;
+  a.centroids = ix->d.centroids;
+  a.k_c = (int)kc_eff(ix, p);
+  a.b_batch = p->b_batch;
+  a.b_min = p->b_min;
+  a.t_low = p->t_low;
+  a.u_heap = p->u_heap;
+  a.u_front = p->u_front;
+  a.alpha_front = p->alpha_front;
+  a.gate_on = p->gate_on != 0;
+  a.early_stop_on = p->early_stop_on != 0;
+  a.lowq_or = p->lowq_or != 0;
+  a.finite = std::isfinite(p->s_max) ? 1 : 0;
+  a.m_knots = p->m_knots;
+  for (int i = 0; i < p->m_knots; ++i) {
+    a.m_x[i] = p->m_x[i];
+    a.m_y[i] = p->m_y[i];
+    a.m_slope[i] = i + 1 < p->m_knots ? (p->m_y[i + 1] - p->m_y[i]) / (p->m_x[i + 1] - p->m_x[i])
+                                      : 0.0f;
+  }
+  a.clus = clus;
+  a.nclus = nclus;
+  a.cap = cap;
+  a.qstats = qstats;
+  return nr::launch_route(a, s);
+}
+
+hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, const uint32_t *clus,
+                      const int32_t *nclus, int64_t cap, const Buffers &B, int64_t *out_ids,
+                      float *out_dists, int32_t *qstats, hipStream_t s, hipEvent_t *ev_plan,
+                      hipEvent_t *ev_refine) {
+  nr::PlanArgs pa{};
+  pa.nq = nq;
+  pa.clus = clus;
+  pa.nclus = nclus;
+  pa.cap = cap;
+  pa.cl_off = ix->d.cl_off;
+  pa.n_clusters = ix->d.n_clusters;
+  pa.rowpre = B.rowpre;
+  pa.rtot = B.rtot;
+  pa.tsize = B.tsize;
+  pa.ntile = B.ntile;
+  pa.tile_off = B.tile_off;
+  pa.tile_q = B.tile_q;
+  pa.tile_c0 = B.tile_c0;
+  pa.counter = B.counter;
+  hipError_t e = nr::launch_plan(pa, s);
+  if (e != hipSuccess) return e;
+  if (ev_plan) (void)hipEventRecord(*ev_plan, s);
+  nr::RefineArgs ra{};
+  ra.rows = ix->d.rows;
+  ra.row_ids = ix->d.row_ids;
+  ra.cl_off = ix->d.cl_off;
+  ra.n_clusters = ix->d.n_clusters;
+  ra.queries = q;
+  ra.nq = nq;
+  ra.d = ix->d.d;
+  ra.row_bytes = (int)(ix->d.d * elem_size(ix));
+  ra.k = k;
+  ra.clus = clus;
+  ra.nclus = nclus;
+  ra.cap = cap;
+  ra.rowpre = B.rowpre;
+  ra.rtot = B.rtot;
+  ra.tsize = B.tsize;
+  ra.tile_off = B.tile_off;
+  ra.tile_q = B.tile_q;
+  ra.tile_c0 = B.tile_c0;
+  ra.counter = B.counter;
+  ra.pkey = B.pkey;
+  ra.pid = B.pid;
+  e = nr::launch_refine(ra, ix->d.dtype, ix->n_cu, s);
+  if (e != hipSuccess) return e;
+  if (ev_refine) (void)hipEventRecord(*ev_refine, s);
+  nr::MergeArgs ma{};
+  ma.nq = nq;
+  ma.k = k;
+  ma.is_u8 = ix->d.dtype == NR_U8;
+  ma.tile_off = B.tile_off;
+  ma.pkey = B.pkey;
+  ma.pid = B.pid;
+  ma.rtot = B.rtot;
+  ma.out_ids = out_ids;
+  ma.out_dists = out_dists;
+  ma.qstats = qstats;
+  return nr::launch_merge(ma, s);
+}
+
+nr_status check_index(const nr_index *ix) {
+  if (!ix) return fail(NR_EINVAL, "index is NULL");
+  return NR_OK;
+}
+
+nr_status make_events(nr_index *ix, EventSet *es) {
+  for (int i = 0; i <= NR_STAGES; ++i) HIP_OK(hipEventCreate(&es->ev[i]));
+  return NR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *nr_status_string(nr_status s) {
+  switch (s) {
+    case NR_OK: return "ok";
+    case NR_EINVAL: return "invalid argument";
+    case NR_ENOMEM: return "out of memory";
+    case NR_EDEVICE: return "device error";
+    case NR_EUNSUPPORTED: return "unsupported";
+    case NR_ECORRUPT: return "corrupt index";
+  }
+  return "unknown status";
+}
+
+const char *nr_last_error(void) { return g_err.c_str(); }
+
+nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t stream) {
+  if (!desc || !out) return fail(NR_EINVAL, "desc and out must not be NULL");
+  *out = nullptr;
+  const nr_index_desc &d = *desc;
+  if (d.n < 1) return fail(NR_EINVAL, "n must be >= 1");
+  if (d.n >= (int64_t)1 << 32) return fail(NR_EUNSUPPORTED, "n must be < 2^32");
+  if (d.d < 1) return fail(NR_EINVAL, "d must be >= 1");
+  if (d.dtype != NR_U8 && d.dtype != NR_F32) return fail(NR_EINVAL, "dtype must be NR_U8 or NR_F32");
+  const size_t rb = (size_t)d.d * (d.dtype == NR_U8 ? 1 : 4);
+  if (rb % 16 != 0) return fail(NR_EUNSUPPORTED, "row size %zu bytes is not a multiple of 16", rb);
+  if (rb > 48 * 128) return fail(NR_EUNSUPPORTED, "row size %zu bytes exceeds 6144", rb);
+  if (d.b < 1 || d.b > 30) return fail(NR_EUNSUPPORTED, "b must be in [1, 30] (got %d)", d.b);
+  if (d.n_layers < 1 || d.n_layers > NR_MAX_LAYERS)
+    return fail(NR_EUNSUPPORTED, "n_layers must be in [1, %d]", NR_MAX_LAYERS);
+  if (!d.widths || !d.weights || !d.tau) return fail(NR_EINVAL, "widths, weights and tau are required");
+  if (d.widths[0] != d.d || d.widths[d.n_layers] != d.b)
+    return fail(NR_EINVAL, "widths[0] must equal d and widths[n_layers] must equal b");
+  for (int l = 0; l <= d.n_layers; ++l)
+    if (d.widths[l] < 1 || d.widths[l] > 4096)
+      return fail(NR_EUNSUPPORTED, "encoder width %d outside [1, 4096]", d.widths[l]);
+  for (int l = 0; l < d.n_layers; ++l)
+    if (!d.weights[l]) return fail(NR_EINVAL, "weights[%d] is NULL", l);
+  if (!std::isfinite(d.input_scale)) return fail(NR_EINVAL, "input_scale must be finite");
+  if (!d.rows || !d.row_ids || !d.bc_off || !d.cl_off || !d.centroids)
+    return fail(NR_EINVAL, "rows, row_ids, bc_off, cl_off and centroids are required");
+  if ((uintptr_t)d.rows % 16 != 0) return fail(NR_EINVAL, "rows must be 16-byte aligned");
+  if (d.n_clusters < 1 || d.n_clusters >= ((int64_t)1 << 32))
+    return fail(NR_EINVAL, "n_clusters must be in [1, 2^32)");
+
+  nr_index *ix = new (std::nothrow) nr_index();
+  if (!ix) return fail(NR_ENOMEM, "host allocation failed");
+  ix->d = d;
+  ix->widths.assign(d.widths, d.widths + d.n_layers + 1);
+  // encoder parameters: one device buffer, per layer W, bias, scale, shift
+  size_t total = 0;
+  std::vector<size_t> offW, offB, offS, offH;
+  for (int l = 0; l < d.n_layers; ++l) {
+    size_t in = d.widths[l], o = d.widths[l + 1];
+    offW.push_back(total); total += in * o;
+    offB.push_back(total); total += o;
+    offS.push_back(total); total += o;
+    offH.push_back(total); total += o;
+    ix->maxw = std::max(ix->maxw, (int)o);
+  }
+  std::vector<float> host(total, 0.0f);
+  for (int l = 0; l < d.n_layers; ++l) {
+    size_t in = d.widths[l], o = d.widths[l + 1];
+    std::memcpy(&host[offW[l]], d.weights[l], sizeof(float) * in * o);
+    if (d.biases && d.biases[l]) std::memcpy(&host[offB[l]], d.biases[l], sizeof(float) * o);
+    for (size_t i = 0; i < o; ++i) {
+      host[offS[l] + i] = (d.bn_scale && d.bn_scale[l]) ? d.bn_scale[l][i] : 1.0f;
+      host[offH[l] + i] = (d.bn_shift && d.bn_shift[l]) ? d.bn_shift[l][i] : 0.0f;
+    }
+  }
+  auto cleanup = [&](nr_status s) {
+    if (ix->params) (void)hipFree(ix->params);
+    if (ix->tau) (void)hipFree(ix->tau);
+    delete ix;
+    return s;
+  };
+  if (hipMalloc(&ix->params, sizeof(float) * total) != hipSuccess ||
+      hipMalloc(&ix->tau, sizeof(float) * d.b) != hipSuccess) {
+    (void)hipGetLastError();
+    return cleanup(fail(NR_ENOMEM, "device allocation of the encoder failed"));
+  }
+  if (hipMemcpy(ix->params, host.data(), sizeof(float) * total, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(ix->tau, d.tau, sizeof(float) * d.b, hipMemcpyHostToDevice) != hipSuccess)
+    return cleanup(fail(NR_EDEVICE, "copy of the encoder to the device failed"));
+  for (int l = 0; l < d.n_layers; ++l) {
+    ix->W.push_back(ix->params + offW[l]);
+    ix->bias.push_back(ix->params + offB[l]);
+    ix->bn_scale.push_back(ix->params + offS[l]);
+    ix->bn_shift.push_back(ix->params + offH[l]);
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ix->n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return cleanup(fail(NR_EDEVICE, "device query failed"));
+  // validate the borrowed CSR arrays and the permutation
+  uint32_t *bitmap = nullptr;
+  int32_t *flags = nullptr;
+  const size_t words = (size_t)((d.n + 31) / 32);
+  if (hipMalloc(&bitmap, words * 4) != hipSuccess || hipMalloc(&flags, 4) != hipSuccess) {
+    (void)hipGetLastError();
+    if (bitmap) (void)hipFree(bitmap);
+    return cleanup(fail(NR_ENOMEM, "validation buffers could not be allocated"));
+  }
+  int32_t hflags = 0;
+  hipError_t e = hipMemsetAsync(bitmap, 0, words * 4, stream);
+  if (e == hipSuccess) e = hipMemsetAsync(flags, 0, 4, stream);
+  if (e == hipSuccess)
+    e = nr::launch_validate(d.bc_off, (int64_t)1 << d.b, d.cl_off, d.n_clusters, d.row_ids, d.n,
+                            bitmap, flags, stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(&hflags, flags, 4, hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  (void)hipFree(bitmap);
+  (void)hipFree(flags);
+  if (e != hipSuccess) return cleanup(fail(NR_EDEVICE, "index validation failed: %s", hipGetErrorString(e)));
+  if (hflags) {
+    std::string what;
+    if (hflags & 1) what += " bucket directory (bc_off)";
+    if (hflags & 2) what += " cluster offsets (cl_off)";
+    if (hflags & 4) what += " row_ids (not a permutation of 0..n-1)";
+    return cleanup(fail(NR_ECORRUPT, "index arrays fail validation:%s", what.c_str()));
+  }
+  *out = ix;
+  return NR_OK;
+}
+
+nr_status nr_index_free(nr_index *ix) {
+  if (!ix) return NR_OK;
+  (void)hipDeviceSynchronize();
+  for (auto &w : ix->ws)
+    if (w.base) (void)hipFree(w.base);
+  for (auto &es : ix->pending)
+    for (auto &ev : es.ev) (void)hipEventDestroy(ev);
+  if (ix->params) (void)hipFree(ix->params);
+  if (ix->tau) (void)hipFree(ix->tau);
+  delete ix;
+  return NR_OK;
+}
+
+int64_t nr_route_capacity(const nr_index *ix, int32_t P, const nr_params *p) {
+  if (!ix || !p) return 0;
+  return (int64_t)P + kc_eff(ix, p);
+}
+
+nr_status nr_encode(const nr_index *cix, const void *queries, int64_t nq, float *logits,
+                    hipStream_t stream) {
+  nr_index *ix = const_cast<nr_index *>(cix);
+  if (nr_status s = check_index(ix)) return s;
+  if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
+  if (nq == 0) return NR_OK;
+  if (!queries || !logits) return fail(NR_EINVAL, "queries and logits must not be NULL");
+  Buffers B;
+  Workspace *w;
+  Shape sh = shape_of(ix, nq, 1, 1, 1);
+  if (nr_status s = workspace_for(ix, stream, sh, &B, &w)) return s;
+  for (int64_t q0 = 0; q0 < nq; q0 += sh.nq) {
+    int64_t n = nq - q0 < sh.nq ? nq - q0 : sh.nq;
+    HIP_OK(run_encode(ix, (const char *)queries + q0 * ix->d.d * elem_size(ix), n,
+                      logits + q0 * ix->d.b, B, stream));
+  }
+  return NR_OK;
+}
+
+nr_status nr_probe(const nr_index *cix, const float *logits, int64_t nq, int32_t P,
+                   const nr_params *p, uint32_t *codes, float *costs, int32_t *bins,
+                   int32_t *counts, hipStream_t stream) {
+  if (nr_status s = check_index(cix)) return s;
+  if (nr_status s = check_params(cix, P, p)) return s;
+  if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
+  if (nq == 0) return NR_OK;
+  if (!logits || !codes || !costs || !bins || !counts) return fail(NR_EINVAL, "NULL buffer");
+  HIP_OK(run_probe(cix, logits, nq, P, p, codes, costs, bins, counts, stream));
+  return NR_OK;
+}
+
+nr_status nr_route(const nr_index *cix, const float *logits, int64_t nq, int32_t P,
+                   const nr_params *p, uint32_t *clusters, int32_t *n_clusters, int64_t cap,
+                   hipStream_t stream) {
+  nr_index *ix = const_cast<nr_index *>(cix);
+  if (nr_status s = check_index(ix)) return s;
+  if (nr_status s = check_params(ix, P, p)) return s;
+  if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
+  if (nq == 0) return NR_OK;
+  if (!logits || !clusters || !n_clusters) return fail(NR_EINVAL, "NULL buffer");
+  if (cap < nr_route_capacity(ix, P, p))
+    return fail(NR_EINVAL, "cap %lld < required %lld", (long long)cap,
+                (long long)nr_route_capacity(ix, P, p));
+  Buffers B;
+  Workspace *w;
+  Shape sh = shape_of(ix, nq, P, 1, 1);
+  if (nr_status s = workspace_for(ix, stream, sh, &B, &w)) return s;
+  for (int64_t q0 = 0; q0 < nq; q0 += sh.nq) {
+    int64_t n = nq - q0 < sh.nq ? nq - q0 : sh.nq;
+    const float *lg = logits + q0 * ix->d.b;
+    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream));
+    HIP_OK(run_route(ix, lg, n, P, p, B, clusters + q0 * cap, n_clusters + q0, cap, nullptr,
+                     stream));
+  }
+  return NR_OK;
+}
+
+nr_status nr_refine(const nr_index *cix, const void *queries, int64_t nq, int32_t k,
+                    const uint32_t *clusters, const int32_t *n_clusters, int64_t cap,
+                    int64_t *out_ids, float *out_dists, hipStream_t stream) {
+  nr_index *ix = const_cast<nr_index *>(cix);
+  if (nr_status s = check_index(ix)) return s;
+  if (k < 1) return fail(NR_EINVAL, "k must be >= 1");
+  if (k > NR_MAX_K) return fail(NR_EUNSUPPORTED, "k %d > %d", k, NR_MAX_K);
+  if (nq < 0 || cap < 1) return fail(NR_EINVAL, "nq must be >= 0 and cap >= 1");
+  if (nq == 0) return NR_OK;
+  if (!queries || !clusters || !n_clusters || !out_ids || !out_dists)
+    return fail(NR_EINVAL, "NULL buffer");
+  Buffers B;
+  Workspace *w;
+  Shape sh = shape_of(ix, nq, 1, k, cap);
+  if (nr_status s = workspace_for(ix, stream, sh, &B, &w)) return s;
+  for (int64_t q0 = 0; q0 < nq; q0 += sh.nq) {
+    int64_t n = nq - q0 < sh.nq ? nq - q0 : sh.nq;
+    HIP_OK(run_refine(ix, (const char *)queries + q0 * ix->d.d * elem_size(ix), n, k,
+                      clusters + q0 * cap, n_clusters + q0, cap, B, out_ids + q0 * k,
+                      out_dists + q0 * k, nullptr, stream, nullptr, nullptr));
+  }
+  w->last = B;
+  w->last_nq = nq < sh.nq ? nq : sh.nq;
+  return NR_OK;
+}
+
+nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *logits,
+                       int64_t nq, int32_t k, int32_t P, const nr_params *p, int64_t *out_ids,
+                       float *out_dists, int32_t *qstats, hipStream_t stream) {
+  nr_index *ix = const_cast<nr_index *>(cix);
+  if (nr_status s = check_index(ix)) return s;
+  if (nr_status s = check_params(ix, P, p)) return s;
+  if (k < 1) return fail(NR_EINVAL, "k must be >= 1");
+  if (k > NR_MAX_K) return fail(NR_EUNSUPPORTED, "k %d > %d", k, NR_MAX_K);
+  if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
+  if (nq == 0) return NR_OK;
+  if (!queries || !out_ids || !out_dists) return fail(NR_EINVAL, "NULL buffer");
+  const int64_t cap = nr_route_capacity(ix, P, p);
+  Buffers B;
+  Workspace *w;
+  Shape sh = shape_of(ix, nq, P, k, cap);
+  if (nr_status s = workspace_for(ix, stream, sh, &B, &w)) return s;
+  const size_t qrow = ix->d.d * elem_size(ix);
+  for (int64_t q0 = 0; q0 < nq; q0 += sh.nq) {
+    int64_t n = nq - q0 < sh.nq ? nq - q0 : sh.nq;
+    const void *qp = (const char *)queries + q0 * qrow;
+    int32_t *qs = qstats ? qstats + q0 * NR_QSTATS : nullptr;
+    EventSet es{};
+    bool prof = ix->profiling;
+    if (prof) {
+      if (nr_status s = make_events(ix, &es)) return s;
+      HIP_OK(hipEventRecord(es.ev[0], stream));
+    }
+    const float *lg = logits ? logits + q0 * ix->d.b : B.logits;
+    if (!logits) HIP_OK(run_encode(ix, qp, n, B.logits, B, stream));
+    if (prof) HIP_OK(hipEventRecord(es.ev[1], stream));
+    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream));
+    if (prof) HIP_OK(hipEventRecord(es.ev[2], stream));
+    HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, qs, stream));
+    if (prof) HIP_OK(hipEventRecord(es.ev[3], stream));
+    HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
+                      out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr,
+                      prof ? &es.ev[5] : nullptr));
+    if (prof) {
+      HIP_OK(hipEventRecord(es.ev[6], stream));
+      std::lock_guard<std::mutex> g(ix->mu);
+      ix->pending.push_back(es);
+    }
+  }
+  w->last = B;
+  w->last_nq = nq < sh.nq ? nq : sh.nq;
+  return NR_OK;
+}
+
+nr_status nr_search(const nr_index *ix, const void *queries, int64_t nq, int32_t k, int32_t P,
+                    const nr_params *p, int64_t *out_ids, float *out_dists, hipStream_t stream) {
+  return nr_search_ex(ix, queries, nullptr, nq, k, P, p, out_ids, out_dists, nullptr, stream);
+}
+
+nr_status nr_profile_enable(nr_index *ix, int32_t on) {
+  if (nr_status s = check_index(ix)) return s;
+  ix->profiling = on != 0;
+  return NR_OK;
+}
+
+nr_status nr_profile_read(nr_index *ix, double *stage_ms, int64_t *n_searches, int32_t reset) {
+  if (nr_status s = check_index(ix)) return s;
+  std::lock_guard<std::mutex> g(ix->mu);
+  for (auto &es : ix->pending) {
+    HIP_OK(hipEventSynchronize(es.ev[NR_STAGES]));
+    for (int i = 0; i < NR_STAGES; ++i) {
+      float ms = 0.f;
+      HIP_OK(hipEventElapsedTime(&ms, es.ev[i], es.ev[i + 1]));
+      ix->stage_ms[i] += ms;
+    }
+    ix->n_timed += 1;
+    for (auto &ev : es.ev) (void)hipEventDestroy(ev);
+  }
+  ix->pending.clear();
+  if (stage_ms)
+    for (int i = 0; i < NR_STAGES; ++i) stage_ms[i] = ix->stage_ms[i];
+  if (n_searches) *n_searches = ix->n_timed;
+  if (reset) {
+    for (double &v : ix->stage_ms) v = 0.0;
+    ix->n_timed = 0;
+  }
+  return NR_OK;
+}
+
+nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *tiles, int64_t *rows) {
+  if (nr_status s = check_index(ix)) return s;
+  Workspace *w = nullptr;
+  {
+    std::lock_guard<std::mutex> g(ix->mu);
+    for (auto &x : ix->ws)
+      if (x.stream == stream) w = &x;
+  }
+  if (!w || !w->last.tile_off) return fail(NR_EINVAL, "no search has run on this stream");
+  HIP_OK(hipStreamSynchronize(stream));
+  int32_t t = 0;
+  HIP_OK(hipMemcpy(&t, w->last.tile_off + w->last_nq, 4, hipMemcpyDeviceToHost));
+  std::vector<uint32_t> r((size_t)w->last_nq);
+  HIP_OK(hipMemcpy(r.data(), w->last.rtot, 4 * r.size(), hipMemcpyDeviceToHost));
+  int64_t sum = 0;
+  for (uint32_t v : r) sum += v;
+  if (tiles) *tiles = t;
+  if (rows) *rows = sum;
+  return NR_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,201 @@
+// Internal declarations of the gfx950 search library: kernel argument
+// structs, launch wrappers and wave64 helpers.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "neuroute.h"
+
+namespace nr {
+
+constexpr int WAVE = 64;
+constexpr int MAX_TILES_PER_QUERY = 64;   // refinement tiles per query (partials slots)
+constexpr int TILE_MIN_ROWS = 512;        // smallest refinement tile
+constexpr int STAGE_CLUSTERS = 128;       // clusters staged in LDS per refinement wave
+constexpr int64_t QUERY_CHUNK = 16384;    // queries per internal launch sequence
+constexpr int MAX_KC = 16384;             // top-K_c heap held in LDS
+
+// ---------------------------------------------------------------- kernels
+struct EncodeLayerArgs {
+  const void *in;        // [M x K]: uint8 or fp32 (layer 0) / fp32 activations
+  int in_u8;
+  float *out;            // [M x N] fp32
+  const float *W;        // [N x K] row-major
+  const float *bias;     // [N]
+  const float *bn_scale; // [N] or null
+  const float *bn_shift; // [N] or null
+  float in_scale;
+  int relu;
+  int64_t M;
+  int N, K;
+};
+
+struct ProbeArgs {
+  const float *logits;   // [nq x b]
+  const float *tau;      // [b]
+  int64_t nq;
+  int b, l_sel, r_max, P, n_bins, finite;
+  float s_max, bin_scale;
+  uint32_t *codes;       // [nq x P]
+  float *costs;
+  int32_t *bins;
+  int32_t *counts;       // [nq]
+};
+
+struct RouteArgs {
+  const float *logits;
+  int64_t nq;
+  int b, P;
+  const uint32_t *codes;
+  const int32_t *bins;
+  const int32_t *counts;
+  const uint32_t *bc_off;
+  const float *centroids;
+  int k_c, b_batch, b_min, t_low, u_heap, u_front;
+  float alpha_front;
+  int gate_on, early_stop_on, lowq_or, finite;
+  int m_knots;
+  float m_x[NR_MAX_KNOTS], m_y[NR_MAX_KNOTS], m_slope[NR_MAX_KNOTS];
+  uint32_t *clus;        // [nq x cap]
+  int32_t *nclus;        // [nq]
+  int64_t cap;
+  int32_t *qstats;       // [nq x NR_QSTATS] or null
+};
+
+struct PlanArgs {
+  int64_t nq;
+  const uint32_t *clus;
+  const int32_t *nclus;
+  int64_t cap;
+  const uint64_t *cl_off;
+  int64_t n_clusters;    // cluster ids >= n_clusters count as empty
+  uint32_t *rowpre;      // [nq x (cap + 1)]
+  uint32_t *rtot;        // [nq]
+  uint32_t *tsize;       // [nq]
+  int32_t *ntile;        // [nq]
+  int32_t *tile_off;     // [nq + 1]
+  int32_t *tile_q;       // [nq x MAX_TILES_PER_QUERY]
+  int32_t *tile_c0;
+  int32_t *counter;      // work counter of the refinement kernel
+};
+
+struct RefineArgs {
+  const void *rows;      // permuted payload
+  const int64_t *row_ids;
+  const uint64_t *cl_off;
+  int64_t n_clusters;
+  const void *queries;   // [nq x d]
+  int64_t nq;
+  int d, row_bytes, k;
+  const uint32_t *clus;
+  const int32_t *nclus;
+  int64_t cap;
+  const uint32_t *rowpre;
+  const uint32_t *rtot;
+  const uint32_t *tsize;
+  const int32_t *tile_off;
+  const int32_t *tile_q;
+  const int32_t *tile_c0;
+  int32_t *counter;
+  uint32_t *pkey;        // [nq x MAX_TILES_PER_QUERY x k]
+  int64_t *pid;
+};
+
+struct MergeArgs {
+  int64_t nq;
+  int k, is_u8;
+  const int32_t *tile_off;
+  const uint32_t *pkey;
+  const int64_t *pid;
+  const uint32_t *rtot;
+  int64_t *out_ids;
+  float *out_dists;
+  int32_t *qstats;
+};
+
+hipError_t launch_encode_layer(const EncodeLayerArgs &a, hipStream_t s);
+hipError_t launch_probe(const ProbeArgs &a, hipStream_t s);
+__host__ __device__ size_t probe_lds_bytes_per_wave(int P);
+hipError_t launch_route(const RouteArgs &a, hipStream_t s);
+hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
+hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
+hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
+
+// index validation at upload; flags[0] |= error bits
+hipError_t launch_validate(const uint32_t *bc_off, int64_t n_codes, const uint64_t *cl_off,
+                           int64_t n_clusters, const int64_t *row_ids, int64_t n,
+                           uint32_t *bitmap, int32_t *flags, hipStream_t s);
+
+// ---------------------------------------------------------------- wave64 helpers
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint32_t bcast_u32(uint32_t v, int src) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, src);
+}
+__device__ __forceinline__ uint64_t bcast_u64(uint64_t v, int src) {
+  uint32_t lo = bcast_u32((uint32_t)v, src), hi = bcast_u32((uint32_t)(v >> 32), src);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+  uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
+  uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int m) {
+  uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, m);
+  uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+__device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  int l = lane_id();
+  return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+__device__ __forceinline__ float wave_min_f32(float v) {
+  for (int m = 32; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m));
+  return v;
+}
+// inclusive scan over the wave (u32)
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
+  int l = lane_id();
+  for (int o = 1; o < WAVE; o <<= 1) {
+    uint32_t t = (uint32_t)__shfl_up((int)v, o);
+    if (l >= o) v += t;
+  }
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
+  int l = lane_id();
+  for (int o = 1; o < WAVE; o <<= 1) {
+    uint64_t t = shfl_up_u64(v, o);
+    if (l >= o) v += t;
+  }
+  return v;
+}
+// ascending bitonic sort of one u64 key per lane
+__device__ __forceinline__ uint64_t wave_sort_u64(uint64_t key) {
+  int l = lane_id();
+  for (int k = 2; k <= WAVE; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      uint64_t other = shfl_xor_u64(key, j);
+      bool up = (l & k) == 0;
+      bool lower = (l & j) == 0;
+      uint64_t mn = key < other ? key : other, mx = key < other ? other : key;
+      key = (lower == up) ? mn : mx;
+    }
+  }
+  return key;
+}
+// number of entries of sorted a[0..n) strictly below key
+__device__ __forceinline__ int lower_bound_u64(const uint64_t *a, int n, uint64_t key) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if (a[mid] < key) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+}  // namespace nr

@@ -1,0 +1,337 @@
+"""Python binding of libneuroute.so (include/neuroute.h) -- argument
+marshalling only.  Device buffers are PyTorch CUDA(HIP) tensors, streams are
+torch streams; every step of the search runs in the library's HIP kernels.
+
+The library must have been built (``python -m paper_2608_15438_amd.build_lib``
+or ``__graft_entry__.build()``); importing the binding without it raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+from dataclasses import dataclass, field
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SO_PATH = os.path.join(_HERE, "libneuroute.so")
+
+NR_OK, NR_EINVAL, NR_ENOMEM, NR_EDEVICE, NR_EUNSUPPORTED, NR_ECORRUPT = range(6)
+NR_U8, NR_F32 = 0, 1
+NR_MAX_LAYERS = 8
+NR_MAX_KNOTS = 32
+NR_MAX_K = 64
+NR_MAX_PROBES = 1024
+NR_QSTATS = 8
+NR_STAGES = 6
+QS = dict(probes=0, clusters=1, direct=2, scored=3, stopped=4, rows=5, tiles=6, batches=7)
+STAGES = ("encode", "probe", "route", "plan", "refine", "merge")
+
+# every symbol include/neuroute.h declares
+EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_encode",
+           "nr_probe", "nr_route", "nr_route_capacity", "nr_refine", "nr_profile_enable",
+           "nr_profile_read", "nr_last_work", "nr_status_string", "nr_last_error")
+
+
+class NRError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: status {status} ({_status_name(status)}): {_last_error()}")
+        self.status = status
+
+
+class nr_index_desc(C.Structure):
+    _fields_ = [("n", C.c_int64), ("d", C.c_int32), ("dtype", C.c_int32), ("b", C.c_int32),
+                ("n_layers", C.c_int32), ("widths", C.POINTER(C.c_int32)),
+                ("weights", C.POINTER(C.POINTER(C.c_float))),
+                ("biases", C.POINTER(C.POINTER(C.c_float))),
+                ("bn_scale", C.POINTER(C.POINTER(C.c_float))),
+                ("bn_shift", C.POINTER(C.POINTER(C.c_float))),
+                ("input_scale", C.c_float), ("tau", C.POINTER(C.c_float)),
+                ("rows", C.c_void_p), ("row_ids", C.c_void_p), ("bc_off", C.c_void_p),
+                ("cl_off", C.c_void_p), ("centroids", C.c_void_p), ("n_clusters", C.c_int64)]
+
+
+class nr_params(C.Structure):
+    _fields_ = [("l_sel", C.c_int32), ("r_max", C.c_int32), ("s_max", C.c_float),
+                ("n_bins", C.c_int32), ("k_c", C.c_int32), ("b_batch", C.c_int32),
+                ("b_min", C.c_int32), ("t_low", C.c_int32), ("u_heap", C.c_int32),
+                ("u_front", C.c_int32), ("alpha_front", C.c_float), ("gate_on", C.c_int32),
+                ("early_stop_on", C.c_int32), ("lowq_or", C.c_int32), ("m_knots", C.c_int32),
+                ("m_x", C.c_float * NR_MAX_KNOTS), ("m_y", C.c_float * NR_MAX_KNOTS)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it was not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(SO_PATH):
+            raise RuntimeError(f"{SO_PATH} is missing: build it with "
+                               "`python -m paper_2608_15438_amd.build_lib`")
+        L = C.CDLL(SO_PATH)
+        P = C.c_void_p
+        L.nr_status_string.restype = C.c_char_p
+        L.nr_status_string.argtypes = [C.c_int]
+        L.nr_last_error.restype = C.c_char_p
+        L.nr_last_error.argtypes = []
+        L.nr_index_upload.argtypes = [C.POINTER(nr_index_desc), C.POINTER(P), P]
+        L.nr_index_free.argtypes = [P]
+        L.nr_search.argtypes = [P, P, C.c_int64, C.c_int32, C.c_int32, C.POINTER(nr_params), P, P, P]
+        L.nr_search_ex.argtypes = [P, P, P, C.c_int64, C.c_int32, C.c_int32, C.POINTER(nr_params),
+                                   P, P, P, P]
+        L.nr_encode.argtypes = [P, P, C.c_int64, P, P]
+        L.nr_probe.argtypes = [P, P, C.c_int64, C.c_int32, C.POINTER(nr_params), P, P, P, P, P]
+        L.nr_route.argtypes = [P, P, C.c_int64, C.c_int32, C.POINTER(nr_params), P, P, C.c_int64, P]
+        L.nr_route_capacity.argtypes = [P, C.c_int32, C.POINTER(nr_params)]
+        L.nr_route_capacity.restype = C.c_int64
+        L.nr_refine.argtypes = [P, P, C.c_int64, C.c_int32, P, P, C.c_int64, P, P, P]
+        L.nr_profile_enable.argtypes = [P, C.c_int32]
+        L.nr_profile_read.argtypes = [P, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.c_int32]
+        L.nr_last_work.argtypes = [P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
+        for name in EXPORTS:
+            getattr(L, name).restype = getattr(L, name).restype or C.c_int
+        L.nr_route_capacity.restype = C.c_int64
+        L.nr_status_string.restype = C.c_char_p
+        L.nr_last_error.restype = C.c_char_p
+        _lib = L
+    return _lib
+
+
+def _status_name(s: int) -> str:
+    try:
+        return lib().nr_status_string(s).decode()
+    except Exception:
+        return "?"
+
+
+def _last_error() -> str:
+    try:
+        return lib().nr_last_error().decode()
+    except Exception:
+        return ""
+
+
+def _check(status: int, what: str):
+    if status != NR_OK:
+        raise NRError(status, what)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+# --------------------------------------------------------------------------
+# search parameters
+# --------------------------------------------------------------------------
+
+@dataclass
+class Params:
+    l_sel: int = 16
+    r_max: int = 7
+    s_max: float = float("inf")
+    n_bins: int = 1
+    k_c: int = 512
+    b_batch: int = 64
+    b_min: int = 2
+    t_low: int = 3
+    u_heap: int = 1
+    u_front: int = 1
+    alpha_front: float = 0.6
+    gate_on: bool = True
+    early_stop_on: bool = True
+    lowq_or: bool = False
+    m_x: Sequence[float] = field(default_factory=list)
+    m_y: Sequence[float] = field(default_factory=list)
+
+    def c(self) -> nr_params:
+        if len(self.m_x) != len(self.m_y) or len(self.m_x) > NR_MAX_KNOTS:
+            raise ValueError("margin knots: m_x and m_y must have equal length <= 32")
+        p = nr_params()
+        p.l_sel, p.r_max, p.s_max, p.n_bins = self.l_sel, self.r_max, self.s_max, self.n_bins
+        p.k_c, p.b_batch, p.b_min, p.t_low = self.k_c, self.b_batch, self.b_min, self.t_low
+        p.u_heap, p.u_front, p.alpha_front = self.u_heap, self.u_front, self.alpha_front
+        p.gate_on, p.early_stop_on, p.lowq_or = int(self.gate_on), int(self.early_stop_on), int(self.lowq_or)
+        p.m_knots = len(self.m_x)
+        for i, (x, y) in enumerate(zip(self.m_x, self.m_y)):
+            p.m_x[i] = x
+            p.m_y[i] = y
+        return p
+
+
+# --------------------------------------------------------------------------
+# index
+# --------------------------------------------------------------------------
+
+class Index:
+    """An uploaded index.  Device arrays are kept referenced here because the
+    library borrows them."""
+
+    def __init__(self, *, n, d, dtype, b, weights, biases, input_scale, tau, rows, row_ids,
+                 bc_off, cl_off, centroids, bn_scale=None, bn_shift=None, stream=None):
+        L = len(weights)
+        self._keep = []
+        widths = np.array([weights[0].shape[1]] + [w.shape[0] for w in weights], np.int32)
+        wp = (C.POINTER(C.c_float) * L)()
+        bp = (C.POINTER(C.c_float) * L)()
+        sp = (C.POINTER(C.c_float) * L)()
+        hp = (C.POINTER(C.c_float) * L)()
+        for l in range(L):
+            w = np.ascontiguousarray(weights[l], np.float32)
+            self._keep.append(w)
+            wp[l] = w.ctypes.data_as(C.POINTER(C.c_float))
+            for src, dst in ((biases, bp), (bn_scale, sp), (bn_shift, hp)):
+                if src is not None and l < len(src) and src[l] is not None:
+                    a = np.ascontiguousarray(src[l], np.float32)
+                    self._keep.append(a)
+                    dst[l] = a.ctypes.data_as(C.POINTER(C.c_float))
+        tau = np.ascontiguousarray(tau, np.float32)
+        self._keep += [widths, tau, wp, bp, sp, hp]
+        self.dev = [_dev(rows, "rows"), _dev(row_ids, "row_ids"), _dev(bc_off, "bc_off"),
+                    _dev(cl_off, "cl_off"), _dev(centroids, "centroids")]
+        desc = nr_index_desc()
+        desc.n, desc.d, desc.dtype, desc.b, desc.n_layers = n, d, dtype, b, L
+        desc.widths = widths.ctypes.data_as(C.POINTER(C.c_int32))
+        desc.weights = wp
+        desc.biases = bp
+        desc.bn_scale = sp
+        desc.bn_shift = hp
+        desc.input_scale = input_scale
+        desc.tau = tau.ctypes.data_as(C.POINTER(C.c_float))
+        desc.rows, desc.row_ids, desc.bc_off, desc.cl_off, desc.centroids = [
+            t.data_ptr() for t in self.dev]
+        desc.n_clusters = centroids.shape[0]
+        self.n, self.d, self.dtype, self.b = n, d, dtype, b
+        self.n_clusters = int(centroids.shape[0])
+        h = C.c_void_p()
+        _check(lib().nr_index_upload(C.byref(desc), C.byref(h), _stream(stream)), "nr_index_upload")
+        self.handle = h
+
+    @classmethod
+    def from_built(cls, ix, device="cuda", stream=None):
+        """Upload an index_build.Index (host or device arrays)."""
+        def dt(a, dtype):
+            t = torch.as_tensor(a) if not isinstance(a, torch.Tensor) else a
+            return t.to(device=device, dtype=dtype).contiguous()
+        rows = ix.rows if isinstance(ix.rows, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(ix.rows))
+        rows = rows.to(device).contiguous()
+        bc = ix.bc_off
+        bc = torch.from_numpy(np.asarray(bc).astype(np.int64)) if not isinstance(bc, torch.Tensor) else bc
+        cl = ix.cl_off
+        cl = torch.from_numpy(np.asarray(cl).astype(np.int64)) if not isinstance(cl, torch.Tensor) else cl
+        e = ix.encoder
+        return cls(n=int(rows.shape[0]), d=int(rows.shape[1]),
+                   dtype=NR_U8 if rows.dtype == torch.uint8 else NR_F32, b=len(ix.tau),
+                   weights=e.weights, biases=e.biases, bn_scale=e.bn_scale, bn_shift=e.bn_shift,
+                   input_scale=e.input_scale, tau=ix.tau, rows=rows,
+                   row_ids=dt(ix.row_ids, torch.int64), bc_off=dt(bc, torch.int32),
+                   cl_off=dt(cl, torch.int64), centroids=dt(ix.centroids, torch.float32),
+                   stream=stream)
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            lib().nr_index_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---- entry points (same names as the C ABI) ----
+    def nr_search(self, queries, k, probe_budget, params: Params, logits=None, qstats=False,
+                  stream=None):
+        _dev(queries, "queries")
+        nq = queries.shape[0]
+        ids = torch.empty((nq, k), dtype=torch.int64, device=queries.device)
+        dists = torch.empty((nq, k), dtype=torch.float32, device=queries.device)
+        qs = torch.zeros((nq, NR_QSTATS), dtype=torch.int32, device=queries.device) if qstats else None
+        p = params.c()
+        if logits is None and not qstats:
+            _check(lib().nr_search(self.handle, _ptr(queries), nq, k, probe_budget, C.byref(p),
+                                   _ptr(ids), _ptr(dists), _stream(stream)), "nr_search")
+        else:
+            if logits is not None:
+                _dev(logits, "logits")
+            _check(lib().nr_search_ex(self.handle, _ptr(queries), _ptr(logits), nq, k, probe_budget,
+                                      C.byref(p), _ptr(ids), _ptr(dists), _ptr(qs), _stream(stream)),
+                   "nr_search_ex")
+        return (ids, dists, qs) if qstats else (ids, dists)
+
+    def nr_encode(self, queries, stream=None):
+        _dev(queries, "queries")
+        out = torch.empty((queries.shape[0], self.b), dtype=torch.float32, device=queries.device)
+        _check(lib().nr_encode(self.handle, _ptr(queries), queries.shape[0], _ptr(out),
+                               _stream(stream)), "nr_encode")
+        return out
+
+    def nr_probe(self, logits, probe_budget, params: Params, stream=None):
+        _dev(logits, "logits")
+        nq = logits.shape[0]
+        dev = logits.device
+        codes = torch.zeros((nq, probe_budget), dtype=torch.int32, device=dev)
+        costs = torch.zeros((nq, probe_budget), dtype=torch.float32, device=dev)
+        bins = torch.zeros((nq, probe_budget), dtype=torch.int32, device=dev)
+        counts = torch.zeros(nq, dtype=torch.int32, device=dev)
+        p = params.c()
+        _check(lib().nr_probe(self.handle, _ptr(logits), nq, probe_budget, C.byref(p), _ptr(codes),
+                              _ptr(costs), _ptr(bins), _ptr(counts), _stream(stream)), "nr_probe")
+        return codes, costs, bins, counts
+
+    def nr_route_capacity(self, probe_budget, params: Params):
+        p = params.c()
+        return int(lib().nr_route_capacity(self.handle, probe_budget, C.byref(p)))
+
+    def nr_route(self, logits, probe_budget, params: Params, stream=None):
+        _dev(logits, "logits")
+        nq = logits.shape[0]
+        cap = self.nr_route_capacity(probe_budget, params)
+        clus = torch.zeros((nq, cap), dtype=torch.int32, device=logits.device)
+        n = torch.zeros(nq, dtype=torch.int32, device=logits.device)
+        p = params.c()
+        _check(lib().nr_route(self.handle, _ptr(logits), nq, probe_budget, C.byref(p), _ptr(clus),
+                              _ptr(n), cap, _stream(stream)), "nr_route")
+        return clus, n
+
+    def nr_refine(self, queries, k, clusters, n_clusters, stream=None):
+        _dev(queries, "queries")
+        _dev(clusters, "clusters")
+        nq = queries.shape[0]
+        ids = torch.empty((nq, k), dtype=torch.int64, device=queries.device)
+        dists = torch.empty((nq, k), dtype=torch.float32, device=queries.device)
+        _check(lib().nr_refine(self.handle, _ptr(queries), nq, k, _ptr(clusters), _ptr(n_clusters),
+                               clusters.shape[1], _ptr(ids), _ptr(dists), _stream(stream)),
+               "nr_refine")
+        return ids, dists
+
+    def nr_profile_enable(self, on=True):
+        _check(lib().nr_profile_enable(self.handle, int(on)), "nr_profile_enable")
+
+    def nr_profile_read(self, reset=True):
+        ms = (C.c_double * NR_STAGES)()
+        n = C.c_int64()
+        _check(lib().nr_profile_read(self.handle, ms, C.byref(n), int(reset)), "nr_profile_read")
+        return dict(zip(STAGES, list(ms))), n.value
+
+    def nr_last_work(self, stream=None):
+        t, r = C.c_int64(), C.c_int64()
+        _check(lib().nr_last_work(self.handle, _stream(stream), C.byref(t), C.byref(r)), "nr_last_work")
+        return t.value, r.value
