@@ -1,0 +1,332 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched NeuRoute search on one MI355X.
+
+One step = one nr_search call over the whole query batch (encoder, probe
+enumeration, bucket lookup, centroid stage, exact refinement) with queries
+and index resident in HBM.  Untimed set-up: the synthetic workload and its
+index are built on the GPU (seeded generators, index construction, gate
+calibration), ground truth comes from a plain PyTorch brute force, and a
+probe-budget sweep picks the fastest point with Recall@10 >= 0.90.  Then W
+warm-up and K timed steps run at that point; HIP events around the
+refinement kernel (on its launch stream) give its average duration for the
+roofline.  The CPU oracle is timed on a bounded query sample.
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "QPS at Recall@10 ≥ 0.90 (10k-query batch); refine-stage HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=4, help="workload 1..4 (4 = 1B x 128 uint8)")
+    ap.add_argument("--n", type=int, default=0, help="override the base size (smaller instance)")
+    ap.add_argument("--probes", type=str, default="", help="comma list of probe budgets to sweep")
+    ap.add_argument("--target-recall", type=float, default=0.90)
+    ap.add_argument("--gt-queries", type=int, default=1000)
+    ap.add_argument("--calib-queries", type=int, default=300)
+    ap.add_argument("--oracle-seconds", type=float, default=10.0)
+    ap.add_argument("--oracle-stage-gb", type=float, default=8.0)
+    ap.add_argument("--oracle-threads", type=int, default=0)
+    ap.add_argument("--no-oracle", action="store_true")
+    ap.add_argument("--margin-quantile", type=float, default=0.95)
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------------------
+# ground truth: exact k-NN by plain PyTorch on the device
+# ----------------------------------------------------------------------------
+
+def ground_truth(torch, rows, row_ids, Q, k, chunk=1 << 19):
+    """Exact top-k by (squared distance, original id) for every query in Q."""
+    dev = rows.device
+    nq = Q.shape[0]
+    if rows.dtype == torch.uint8:
+        # integer distances: every fp32 step below is exact (all partial sums
+        # of byte products stay below 2^24), then (distance, id) is packed in
+        # one int64 key so ties resolve by the lower original id
+        Qf = Q.float()
+        qq = (Qf * Qf).sum(1)
+        m2q = (-2.0 * Qf).T.contiguous()
+        best = None
+        for s0 in range(0, rows.shape[0], chunk):
+            if s0 and s0 % (chunk * 256) == 0:
+                log(f"  ground truth: {s0 / rows.shape[0]:.0%} of the base")
+            X = rows[s0:s0 + chunk].float()
+            d = X @ m2q
+            d += (X * X).sum(1)[:, None]
+            d += qq[None, :]
+            key = d.to(torch.int64)
+            del d
+            key <<= 32
+            key |= row_ids[s0:s0 + chunk][:, None]
+            top = torch.topk(key, min(k, key.shape[0]), dim=0, largest=False).values
+            del key
+            best = top if best is None else torch.topk(torch.cat([best, top]), k, dim=0,
+                                                       largest=False).values
+        best = best.T.contiguous()
+        return (best & 0xFFFFFFFF).cpu().numpy(), (best >> 32).cpu().numpy().astype(np.float32)
+    Qd = Q.double()
+    qq = (Qd * Qd).sum(1)
+    bd, bi = None, None
+    for s0 in range(0, rows.shape[0], chunk):
+        if s0 and s0 % (chunk * 256) == 0:
+            log(f"  ground truth: {s0 / rows.shape[0]:.0%} of the base")
+        X = rows[s0:s0 + chunk].double()
+        d = (X * X).sum(1)[:, None] - 2 * (X @ Qd.T) + qq[None, :]
+        kk = min(k + 8, d.shape[0])
+        v, i = torch.topk(d, kk, dim=0, largest=False)
+        ids = row_ids[s0:s0 + chunk][i]
+        if bd is None:
+            bd, bi = v, ids
+        else:
+            v2, j = torch.topk(torch.cat([bd, v]), k + 8, dim=0, largest=False)
+            bi = torch.gather(torch.cat([bi, ids]), 0, j)
+            bd = v2
+    bd, bi = bd.T.cpu().numpy(), bi.T.cpu().numpy()
+    out_i = np.empty((nq, k), np.int64)
+    out_d = np.empty((nq, k), np.float32)
+    for q in range(nq):
+        o = np.lexsort((bi[q], bd[q]))[:k]
+        out_i[q], out_d[q] = bi[q][o], bd[q][o]
+    return out_i, out_d
+
+
+def recall_at_k(res, gt, k):
+    r = 0.0
+    for a, b in zip(res, gt):
+        r += len(set(a[:k].tolist()) & set(b[:k].tolist())) / k
+    return r / len(res)
+
+
+# ----------------------------------------------------------------------------
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the search shards by query batch or database, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from synth import configs as CF
+    from synth.gpu import GpuRows
+    from paper_2608_15438_amd import index_build as IB
+    from paper_2608_15438_amd import calibrate as CAL
+    from paper_2608_15438_amd import neuroute as NR
+
+    torch.backends.cuda.matmul.allow_tf32 = False
+    torch.set_float32_matmul_precision("highest")
+    dev = torch.device("cuda:0")
+    w = CF.WORKLOADS[args.config]
+    if args.n:
+        w = CF.scaled(w, args.n)
+    k = w.k
+    t_all = time.time()
+
+    # ---- workload and index (untimed)
+    log(f"building {w.name}: n={w.n} d={w.d} b={w.b}")
+    data = GpuRows(w, "data", dev)
+    t0 = time.time()
+    ix = IB.build_index(w, data, device=dev, chunk=1 << 20, keep_codes=False,
+                        payload_fn=lambda perm: data(perm), log=lambda s: log("  index:", s))
+    torch.cuda.synchronize()
+    t_build = time.time() - t0
+    log(f"index built in {t_build:.1f}s: {ix.n_clusters} clusters")
+    Q = GpuRows(w, "query", dev).range(0, w.n_queries)
+    gix = NR.Index.from_built(ix, dev)
+
+    # ---- ground truth and gate calibration (untimed)
+    t0 = time.time()
+    ng = min(args.gt_queries, w.n_queries)
+    nc = args.calib_queries
+    Qc = GpuRows(w, "calib", dev).range(0, nc)
+    gt_all, _ = ground_truth(torch, ix.rows, ix.row_ids, torch.cat([Q[:ng], Qc]), k)
+    gt_ids, gtc = gt_all[:ng], gt_all[ng:]
+    log(f"ground truth for {ng}+{nc} queries in {time.time() - t0:.1f}s")
+    fwd = IB._TorchEncoder(ix.encoder, dev)
+    row_of_id = torch.empty_like(ix.row_ids)
+    row_of_id[ix.row_ids] = torch.arange(w.n, device=dev)
+    xs, ys = CAL.margin_points(fwd(Qc), torch.from_numpy(gtc).to(dev), row_of_id, ix.cl_off,
+                               ix.bc_off, ix.centroids)
+    del row_of_id
+    m_x, m_y = CAL.fit_margin(xs, ys, args.margin_quantile)
+    params = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c,
+                       m_x=m_x.tolist(), m_y=m_y.tolist())
+
+    # ---- probe-budget sweep: recall and QPS per point
+    budgets = [int(x) for x in args.probes.split(",")] if args.probes else list(w.probe_budgets)
+    sweep = []
+    for P in budgets:
+        ids, _ = gix.nr_search(Q, k, P, params)
+        torch.cuda.synchronize()
+        t0 = time.time()
+        reps = 2
+        for _ in range(reps):
+            ids, _ = gix.nr_search(Q, k, P, params)
+        torch.cuda.synchronize()
+        dt = (time.time() - t0) / reps
+        rec = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k)
+        tiles, rows = gix.nr_last_work()
+        pt = dict(probe_budget=P, recall=round(rec, 5), qps=round(w.n_queries / dt, 1),
+                  cand_per_query=round(rows / w.n_queries, 1))
+        sweep.append(pt)
+        log("  sweep", pt)
+    ok = [p for p in sweep if p["recall"] >= args.target_recall]
+    head = max(ok, key=lambda p: p["qps"]) if ok else max(sweep, key=lambda p: p["recall"])
+    P = head["probe_budget"]
+
+    # ---- timed region: W warm-up + K steps at the chosen point
+    for _ in range(args.warmup):
+        gix.nr_search(Q, k, P, params)
+    torch.cuda.synchronize()
+    gix.nr_profile_enable(True)
+    gix.nr_profile_read(reset=True)
+    torch.cuda.synchronize()
+    t0 = time.time()
+    for _ in range(args.steps):
+        ids, dists = gix.nr_search(Q, k, P, params)
+    torch.cuda.synchronize()
+    wall = time.time() - t0
+    stage_ms, n_timed = gix.nr_profile_read(reset=True)
+    gix.nr_profile_enable(False)
+    tiles, rows = gix.nr_last_work()
+    recall = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k)
+    qps = w.n_queries * args.steps / wall
+    _, _, qs = gix.nr_search(Q, k, P, params, qstats=True)
+    qs = qs.double().mean(0).cpu().numpy()
+    per_query = {name: round(float(qs[i]), 2) for name, i in NR.QS.items()}
+    log("per-query means", per_query)
+    refine_ms = stage_ms["refine"] / max(n_timed, 1)
+    alg_bytes = rows * w.row_bytes
+    achieved = alg_bytes / (refine_ms * 1e-3) / 1e9
+    log(f"timed: {args.steps} steps, {wall * 1e3 / args.steps:.2f} ms/step, recall {recall:.4f}, "
+        f"refine {refine_ms:.3f} ms avg, {achieved:.0f} GB/s")
+
+    # ---- CPU baseline: the oracle on a bounded sample (rows staged in host memory)
+    cpu = None
+    if not args.no_oracle:
+        cpu = oracle_baseline(args, w, ix, Q, P, params, torch, dev)
+
+    out = {
+        "metric": METRIC,
+        "value": round(qps, 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "n": w.n, "d": w.d, "b": w.b, "queries": w.n_queries,
+                   "k": k, "probe_budget": P, "l_sel": params.l_sel, "r_max": params.r_max,
+                   "k_c": params.k_c, "gate": f"q{int(round(args.margin_quantile * 100))}",
+                   "early_stop": True, "parallelism": "single-gpu"},
+        "recall_at_10": round(recall, 5),
+        "recall_queries": ng,
+        "cand_per_query": round(rows / w.n_queries, 1),
+        "per_query": per_query,
+        "refine_gbs": round(achieved, 1),
+        "stage_ms_per_step": {s: round(v / max(n_timed, 1), 4) for s, v in stage_ms.items()},
+        "roofline": {"bound": "hbm", "kernel": "k_refine", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None, "alg_bytes_per_launch": int(alg_bytes),
+                     "avg_launch_ms": round(refine_ms, 4)},
+        "cpu_baseline": cpu,
+        "sweep": sweep,
+        "setup_s": {"index_build": round(t_build, 1), "total": round(time.time() - t_all, 1)},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def oracle_baseline(args, w, ix, Q, P, params, torch, dev):
+    """Time the oracle on a bounded sample: a 32-query pilot sizes the sample
+    to about `--oracle-seconds` of wall time on the host threads, capped by
+    `--oracle-stage-gb` of staged rows."""
+    import oracle as O
+    threads = args.oracle_threads or min(16, len(os.sched_getaffinity(0)))
+    e = ix.encoder
+    enc = O.Encoder(e.weights, e.biases, e.bn_scale or (), e.bn_shift or (), e.input_scale)
+    bc = ix.bc_off.cpu().numpy().astype(np.uint32)
+    cl = ix.cl_off.cpu().numpy().astype(np.uint64)
+    cent = ix.centroids.cpu().numpy()
+    prm = O.RouteParams(n_bins=params.n_bins, s_max=params.s_max, k_c=params.k_c,
+                        b_batch=params.b_batch, b_min=params.b_min, t_low=params.t_low,
+                        u_heap=params.u_heap, u_front=params.u_front,
+                        alpha_front=params.alpha_front, gate_on=params.gate_on,
+                        early_stop_on=params.early_stop_on, lowq_or=params.lowq_or,
+                        m_x=np.array(params.m_x, np.float32), m_y=np.array(params.m_y, np.float32))
+
+    def run(nqs):
+        Qh = Q[:nqs].cpu().numpy()
+        # discovery (untimed): the clusters this sample needs
+        lg = O.encode(enc, Qh)
+        codes, costs, bins, cnt = O.probes(lg, ix.tau, params.l_sel, params.r_max, P,
+                                           params.s_max, params.n_bins)
+        lists = O.route(lg, codes, bins, cnt, bc, cent, prm)
+        need = np.unique(np.concatenate(lists)).astype(np.int64)
+        sizes = (cl[need + 1] - cl[need]).astype(np.int64)
+        # stage their rows in host memory behind a cl_off in which every
+        # other cluster is empty
+        starts = torch.from_numpy(cl[need].astype(np.int64)).to(dev)
+        sz_t = torch.from_numpy(sizes).to(dev)
+        idx = torch.repeat_interleave(starts, sz_t) + (
+            torch.arange(int(sizes.sum()), device=dev) -
+            torch.repeat_interleave(torch.cumsum(sz_t, 0) - sz_t, sz_t))
+        rows_h = ix.rows[idx].cpu().numpy()
+        ids_h = ix.row_ids[idx].cpu().numpy()
+        del idx
+        cnt_all = np.zeros(ix.n_clusters, np.int64)
+        cnt_all[need] = sizes
+        cl2 = np.zeros(ix.n_clusters + 1, np.uint64)
+        cl2[1:] = np.cumsum(cnt_all)
+        t0 = time.time()
+        oi, od, ncand, secs = O.search(enc, ix.tau, rows_h, ids_h, bc, cl2, cent, Qh, w.k,
+                                       params.l_sel, params.r_max, P, prm, n_threads=threads)
+        return time.time() - t0, secs, rows_h.nbytes
+
+    pilot = min(32, w.n_queries)
+    dt, secs, nbytes = run(pilot)
+    per_q = dt / pilot
+    nqs = int(min(w.n_queries, max(pilot, args.oracle_seconds / max(per_q, 1e-9)),
+                  max(pilot, args.oracle_stage_gb * 1e9 / max(nbytes / pilot, 1.0))))
+    if nqs > pilot:
+        dt, secs, nbytes = run(nqs)
+    else:
+        nqs = pilot
+    cpu_qps = nqs / dt
+    log(f"oracle: {nqs} queries on {threads} threads in {dt:.2f}s ({cpu_qps:.1f} QPS), "
+        f"{nbytes / 1e9:.2f} GB staged")
+    return {"value": round(cpu_qps, 2), "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {nqs} queries of the batch, same index and probe budget; rows of "
+                      f"their candidate clusters ({nbytes / 1e9:.2f} GB) staged in host memory "
+                      f"before timing",
+            "seconds": round(dt, 3),
+            "stage_seconds": dict(zip(("encode", "probe", "route", "refine"),
+                                      [round(float(x), 3) for x in secs]))}
+
+
+if __name__ == "__main__":
+    main()

@@ -181,6 +181,16 @@ def _pair_argmin(X, seg_of_pt, cent, cent_start, K, chunk=1 << 22):
     return out
 
 
+def mix32(x: torch.Tensor, seed: int) -> torch.Tensor:
+    """A 32-bit integer hash of int64 values (products stay below 2^63, so it
+    is exact and identical on CPU and GPU)."""
+    m = 0xFFFFFFFF
+    h = (x ^ (seed & m)) & m
+    h = ((h >> 16) ^ h) * 0x45D9F3B & m
+    h = ((h >> 16) ^ h) * 0x45D9F3B & m
+    return (h >> 16) ^ h
+
+
 def bucket_kmeans(X: torch.Tensor, sizes: torch.Tensor, K: torch.Tensor, seed: int,
                   group_keys: torch.Tensor):
     """k-means++ on a sample then N_LLOYD Lloyd passes, independently per group.
@@ -196,9 +206,8 @@ def bucket_kmeans(X: torch.Tensor, sizes: torch.Tensor, K: torch.Tensor, seed: i
     cstart = torch.cumsum(K, 0) - K
     dim = X.shape[1]
     # seeded shuffle inside each group: the sample is the first S_g members
-    ids_np = np.arange(X.shape[0])
-    w = G._u32_words(seed, ids_np, 1, G.TAG_SAMPLE)[:, 0].astype(np.int64)
-    order = torch.as_tensor(np.lexsort((w, seg.cpu().numpy())), device=dev)
+    h = mix32(torch.arange(X.shape[0], device=dev, dtype=torch.int64), seed)
+    order = torch.sort(seg * (1 << 32) + h, stable=True).indices
     S = torch.minimum(sizes, K * SAMPLE_PER_CLUSTER)
     pos_in_group = torch.arange(X.shape[0], device=dev) - starts[seg]
     in_sample = pos_in_group < S[seg]
@@ -364,9 +373,8 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
     n_clusters = int(n_cl_bucket.sum())
     bc_off = torch.zeros(nb + 1, dtype=torch.int64, device=dev)
     bc_off[1:] = torch.cumsum(n_cl_bucket, 0)
-    # cluster sizes: global cluster id of each row in permuted order
-    row_cl = bc_off[codes[perm]] + label[perm]
-    cl_sizes = torch.bincount(row_cl, minlength=n_clusters)
+    # cluster sizes (independent of the row order)
+    cl_sizes = torch.bincount(bc_off[codes] + label, minlength=n_clusters)
     cl_off = torch.zeros(n_clusters + 1, dtype=torch.int64, device=dev)
     cl_off[1:] = torch.cumsum(cl_sizes, 0)
     # centroids: single-cluster buckets use the bucket mean, others k-means means

@@ -70,7 +70,7 @@ DEEP100M = Workload(
 SIFT1B = Workload(
     name="sift-like-1B-u8-d128-b24", cfg=4, kind="sift", n=1_000_000_000, d=128, n_centers=100_000,
     widths=(128, 256, 24), n_queries=10_000, tau_mode="median", cluster_rule="capacity",
-    capacity=4000, l_sel=16, r_max=7, k_c=3000, probe_budgets=(16, 32, 64, 128, 256, 512, 1024),
+    capacity=4000, l_sel=16, r_max=7, k_c=3000, probe_budgets=(256, 512, 640, 768, 896, 1024),
 )
 
 WORKLOADS = {w.cfg: w for w in (TINY, SIFT1M, DEEP100M, SIFT1B)}
