@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--n", type=int, default=0, help="override the base size (smaller instance)")
     ap.add_argument("--probes", type=str, default="", help="comma list of probe budgets to sweep")
     ap.add_argument("--target-recall", type=float, default=0.90)
+    ap.add_argument("--refine-steps", type=int, default=4,
+                    help="bisection steps on the probe budget around the recall target")
     ap.add_argument("--gt-queries", type=int, default=1000)
     ap.add_argument("--calib-queries", type=int, default=300)
     ap.add_argument("--oracle-seconds", type=float, default=10.0)
@@ -50,6 +52,10 @@ def parse():
     ap.add_argument("--oracle-threads", type=int, default=0)
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--margin-quantile", type=float, default=0.95)
+    ap.add_argument("--quick", action="store_true",
+                    help="no recall ground truth and no oracle (for counter passes)")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="only run a plain 4 GiB device copy (counter calibration) and exit")
     return ap.parse_args()
 
 
@@ -112,6 +118,35 @@ def ground_truth(torch, rows, row_ids, Q, k, chunk=1 << 19):
     return out_i, out_d
 
 
+def stream_read_ceiling(torch, NR, dev, gib=16, reps=5):
+    """Achievable read rate: the library's streaming-read self-check (the same
+    16-byte loads as the refinement) over a 16 GiB buffer."""
+    x = torch.ones(gib << 28, dtype=torch.float32, device=dev)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    NR.nr_stream_read(x, sink)
+    torch.cuda.synchronize()
+    t0 = time.time()
+    for _ in range(reps):
+        NR.nr_stream_read(x, sink)
+    torch.cuda.synchronize()
+    gbs = reps * x.numel() * 4 / (time.time() - t0) / 1e9
+    del x
+    torch.cuda.empty_cache()
+    log(f"streaming read of {gib} GiB: {gbs:.0f} GB/s")
+    return gbs
+
+
+def copy_calibration(torch, dev, gib=4, reps=5):
+    """A plain device copy of known size (reads and writes gib GiB per
+    launch) to scale the FETCH_SIZE / WRITE_SIZE counters."""
+    src = torch.ones(gib << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_launch": src.numel(), "launches": reps}), flush=True)
+
+
 def recall_at_k(res, gt, k):
     r = 0.0
     for a, b in zip(res, gt):
@@ -137,6 +172,10 @@ def main():
     torch.backends.cuda.matmul.allow_tf32 = False
     torch.set_float32_matmul_precision("highest")
     dev = torch.device("cuda:0")
+    if args.copy_calib:
+        copy_calibration(torch, dev)
+        return
+    stream_gbs = stream_read_ceiling(torch, NR, dev)
     w = CF.WORKLOADS[args.config]
     if args.n:
         w = CF.scaled(w, args.n)
@@ -157,7 +196,7 @@ def main():
 
     # ---- ground truth and gate calibration (untimed)
     t0 = time.time()
-    ng = min(args.gt_queries, w.n_queries)
+    ng = 0 if args.quick else min(args.gt_queries, w.n_queries)
     nc = args.calib_queries
     Qc = GpuRows(w, "calib", dev).range(0, nc)
     gt_all, _ = ground_truth(torch, ix.rows, ix.row_ids, torch.cat([Q[:ng], Qc]), k)
@@ -176,7 +215,8 @@ def main():
     # ---- probe-budget sweep: recall and QPS per point
     budgets = [int(x) for x in args.probes.split(",")] if args.probes else list(w.probe_budgets)
     sweep = []
-    for P in budgets:
+
+    def measure(P):
         ids, _ = gix.nr_search(Q, k, P, params)
         torch.cuda.synchronize()
         t0 = time.time()
@@ -185,12 +225,28 @@ def main():
             ids, _ = gix.nr_search(Q, k, P, params)
         torch.cuda.synchronize()
         dt = (time.time() - t0) / reps
-        rec = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k)
+        rec = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k) if ng else float("nan")
         tiles, rows = gix.nr_last_work()
         pt = dict(probe_budget=P, recall=round(rec, 5), qps=round(w.n_queries / dt, 1),
                   cand_per_query=round(rows / w.n_queries, 1))
         sweep.append(pt)
         log("  sweep", pt)
+        return pt
+
+    for P in budgets:
+        measure(P)
+    # bisect between the last budget below the recall target and the first above it
+    if ng and len(budgets) > 1:
+        for _ in range(args.refine_steps):
+            ok_p = sorted(p["probe_budget"] for p in sweep if p["recall"] >= args.target_recall)
+            bad_p = sorted(p["probe_budget"] for p in sweep if p["recall"] < args.target_recall)
+            if not ok_p or not bad_p:
+                break
+            hi = ok_p[0]
+            lo = max([b for b in bad_p if b < hi], default=None)
+            if lo is None or hi - lo <= 8:
+                break
+            measure((lo + hi) // 2)
     ok = [p for p in sweep if p["recall"] >= args.target_recall]
     head = max(ok, key=lambda p: p["qps"]) if ok else max(sweep, key=lambda p: p["recall"])
     P = head["probe_budget"]
@@ -210,7 +266,7 @@ def main():
     stage_ms, n_timed = gix.nr_profile_read(reset=True)
     gix.nr_profile_enable(False)
     tiles, rows = gix.nr_last_work()
-    recall = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k)
+    recall = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k) if ng else float("nan")
     qps = w.n_queries * args.steps / wall
     _, _, qs = gix.nr_search(Q, k, P, params, qstats=True)
     qs = qs.double().mean(0).cpu().numpy()
@@ -224,7 +280,7 @@ def main():
 
     # ---- CPU baseline: the oracle on a bounded sample (rows staged in host memory)
     cpu = None
-    if not args.no_oracle:
+    if not args.no_oracle and not args.quick:
         cpu = oracle_baseline(args, w, ix, Q, P, params, torch, dev)
 
     out = {
@@ -256,6 +312,7 @@ def main():
                      "avg_launch_ms": round(refine_ms, 4)},
         "cpu_baseline": cpu,
         "sweep": sweep,
+        "hbm_stream_read_gbs": round(stream_gbs, 1),
         "setup_s": {"index_build": round(t_build, 1), "total": round(time.time() - t_all, 1)},
     }
     print(json.dumps(out), flush=True)

@@ -207,6 +207,12 @@ nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches
  * (synchronises the stream). */
 nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *tiles, int64_t *rows);
 
+/* Bandwidth self-check (not part of the search): one pass of 16-byte loads
+ * over `bytes` (a multiple of 16) of the DEVICE buffer `buf`, on `stream`.
+ * `sink` is a DEVICE uint32 that the kernel may write.  Timing it gives the
+ * achievable streaming read rate of the device the index lives on. */
+nr_status nr_stream_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t stream);
+
 const char *nr_status_string(nr_status status);
 const char *nr_last_error(void);
 

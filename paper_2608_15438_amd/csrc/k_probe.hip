@@ -13,7 +13,8 @@
 // Keys are u64 (score bits << 32 | mask): scores are >= +0, so the float bit
 // pattern orders like the value.  Lists live in LDS: L, the output of the
 // merge, and the extension list E (which may need a sort when fp32 rounding
-// maps different scores to one value).
+// maps different scores to one value); each merge is a merge-path merge in
+// which every lane writes one contiguous slice of the output.
 #include "nr_internal.h"
 
 namespace nr {
@@ -121,21 +122,34 @@ __global__ void k_probe(ProbeArgs a) {
         }
       }
     }
-    // merge by ranks: keys of L and E are distinct (E's masks hold bit r)
-    for (int i0 = 0; i0 < n; i0 += WAVE) {
-      int i = i0 + lane;
-      if (i < n) {
-        uint64_t key = L[i];
-        int pos = i + lower_bound_u64(E, ne, key);
-        if (pos < P) O[pos] = key;
-      }
-    }
-    for (int i0 = 0; i0 < ne; i0 += WAVE) {
-      int i = i0 + lane;
-      if (i < ne) {
-        uint64_t key = E[i];
-        int pos = i + lower_bound_u64(L, n, key);
-        if (pos < P) O[pos] = key;
+    // merge path: lane l writes output slots [o0, o1) of the first P of
+    // L merge E; keys are distinct (only E's masks hold bit r)
+    {
+      const int nout = n + ne < P ? n + ne : P;
+      const int per = (nout + WAVE - 1) / WAVE;
+      const int o0 = lane * per;
+      const int o1 = o0 + per < nout ? o0 + per : nout;
+      if (o0 < o1) {
+        int lo = o0 - ne > 0 ? o0 - ne : 0;
+        int hi = o0 < n ? o0 : n;
+        while (lo < hi) {  // how many of the first o0 outputs come from L
+          const int mid = (lo + hi) >> 1;
+          if (L[mid] < E[o0 - mid - 1]) lo = mid + 1; else hi = mid;
+        }
+        int i = lo, j = o0 - lo;
+        uint64_t x = i < n ? L[i] : ~0ull;
+        uint64_t y = j < ne ? E[j] : ~0ull;
+        for (int o = o0; o < o1; ++o) {
+          if (x < y) {
+            O[o] = x;
+            ++i;
+            x = i < n ? L[i] : ~0ull;
+          } else {
+            O[o] = y;
+            ++j;
+            y = j < ne ? E[j] : ~0ull;
+          }
+        }
       }
     }
     __builtin_amdgcn_wave_barrier();

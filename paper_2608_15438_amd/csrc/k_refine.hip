@@ -16,7 +16,29 @@
 //  merge  (one wave per query)  the tiles' partial top-k lists are merged.
 #include "nr_internal.h"
 
+// launch shape of the refinement (tuned on MI355X)
+#ifndef NR_REFINE_BLOCKS_PER_CU
+#define NR_REFINE_BLOCKS_PER_CU 8
+#endif
+#ifndef NR_REFINE_U1
+#define NR_REFINE_U1 8          // rows in flight per lane group for 128-byte rows
+#endif
+#ifndef NR_REFINE_NT
+#define NR_REFINE_NT 1          // non-temporal payload loads (+3% on MI355X)
+#endif
+
 namespace nr {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load_payload(const uint4 *p) {
+#if NR_REFINE_NT
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+#else
+  return *p;
+#endif
+}
 
 // ------------------------------------------------------------------ plan
 // cluster counts come from the caller in nr_refine: keep them in [0, cap]
@@ -236,7 +258,8 @@ __global__ void __launch_bounds__(256) k_refine(RefineArgs a) {
 #pragma unroll
           for (int s = 0; s < NSEG; ++s) {
             const int off = 128 * s + 16 * gl;
-            xv[u][s] = (ok[u] && off < rb) ? *(const uint4 *)(rp + off) : make_uint4(0, 0, 0, 0);
+            xv[u][s] = (ok[u] && off < rb) ? load_payload((const uint4 *)(rp + off))
+                                           : make_uint4(0, 0, 0, 0);
           }
         }
         uint32_t key[U];
@@ -313,7 +336,7 @@ static hipError_t launch_refine_t(const RefineArgs &a, int nseg, int grid, hipSt
     hipLaunchKernelGGL((k_refine<IS_U8, NS, UU>), dim3(grid), dim3(256), 0, s, a); \
     return hipGetLastError();                                                      \
   }
-  NR_REFINE_CASE(1, 8)
+  NR_REFINE_CASE(1, NR_REFINE_U1)
   NR_REFINE_CASE(2, 4)
   NR_REFINE_CASE(3, 4)
   NR_REFINE_CASE(4, 2)
@@ -327,7 +350,7 @@ static hipError_t launch_refine_t(const RefineArgs &a, int nseg, int grid, hipSt
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s) {
   if (a.nq <= 0) return hipSuccess;
   const int nseg = (a.row_bytes + 127) / 128;
-  const int grid = n_cu * 8;
+  const int grid = n_cu * NR_REFINE_BLOCKS_PER_CU;
   return dtype == NR_U8 ? launch_refine_t<1>(a, nseg, grid, s) : launch_refine_t<0>(a, nseg, grid, s);
 }
 

@@ -138,72 +138,129 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   int p = 0;                 // next probe of the sequence
   int wb = 0;                // window: probes [wb, wb + WAVE), slot = lane
   bool have_window = false;
-  for (int z = 0; z <= z_last && !stop; ++z) {
-    b_proc += 1;
-    while (p < cnt) {
-      if (!have_window || p >= wb + WAVE) {
-        wb = p;
-        have_window = true;
-        const int i = wb + lane;
-        uint32_t c0 = 0, c1 = 0;
-        int bn = 0x7fffffff;
-        if (i < cnt) {
-          const uint32_t code = codes[i];
-          c0 = a.bc_off[code];
-          c1 = a.bc_off[(uint64_t)code + 1];
-          bn = bins[i];
-        }
-        S.wc0[lane] = c0;
-        S.wc1[lane] = c1;
-        S.wbin[lane] = bn;
-        __builtin_amdgcn_wave_barrier();
-      }
-      const int off = p - wb;
-      // bins are sorted, so the probes of bin z from p are the slots [off, off + run)
-      const bool in_run = lane >= off && wb + lane < cnt && S.wbin[lane] == z;
-      const int run = popc64(ballot(in_run));
-      if (run == 0) break;
-      const uint32_t c0 = S.wc0[lane], c1 = S.wc1[lane];
-      const uint32_t sz = in_run ? c1 - c0 : 0;
-      // single-cluster buckets go to C_dir in probe order
-      const bool single = sz == 1;
-      const uint64_t sm = ballot(single);
-      if (single) out[ndir + popc64(sm & lanemask_lt())] = c0;
-      ndir += popc64(sm);
-      // clusters of multi-cluster buckets feed the batches (not after a stop)
-      if (!stop) {
-        const uint32_t msz = sz >= 2 ? sz : 0;
-        const uint32_t incl = wave_incl_scan_u32(msz);
-        const uint32_t total = __shfl(incl, WAVE - 1);
-        S.wpre[lane] = in_run ? incl - msz : 0xffffffffu;
-        __builtin_amdgcn_wave_barrier();
-        uint32_t v = 0;
-        while (v < total && !stop) {
-          uint32_t take = (uint32_t)(a.b_batch - npend);
-          if (take > total - v) take = total - v;
-          if ((uint32_t)lane < take) {
-            const uint32_t vi = v + lane;
-            // last slot of the run whose prefix is <= vi: zero-size slots share
-            // the prefix of the next non-empty one, so this is the owner
-            int lo = off, hi = off + run - 1;
-            while (lo < hi) {
-              int mid = (lo + hi + 1) >> 1;
-              if (S.wpre[mid] <= vi) lo = mid; else hi = mid - 1;
-            }
-            S.pend[npend + lane] = S.wc0[lo] + (vi - S.wpre[lo]);
-          }
-          __builtin_amdgcn_wave_barrier();
-          npend += (int)take;
-          v += take;
-          if (npend == a.b_batch) run_batch();
-        }
-      }
-      p += run;
-      if (off + run < WAVE) break;  // bin z ends inside this window
+  auto load_window = [&]() {
+    wb = p;
+    have_window = true;
+    const int i = wb + lane;
+    uint32_t c0 = 0, c1 = 0;
+    int bn = 0x7fffffff;
+    if (i < cnt) {
+      const uint32_t code = codes[i];
+      c0 = a.bc_off[code];
+      c1 = a.bc_off[(uint64_t)code + 1];
+      bn = bins[i];
     }
-    if (!stop && npend > 0) run_batch();
-    npend = 0;
-    if (!stop && full_and_quiet()) stop = true;
+    S.wc0[lane] = c0;
+    S.wc1[lane] = c1;
+    S.wbin[lane] = bn;
+    __builtin_amdgcn_wave_barrier();
+  };
+
+  if (!a.finite) {
+    // S_max = +inf: every probe is its own bin.  Runs of bins without a
+    // multi-cluster bucket change neither H nor t_low, so they are taken a
+    // window at a time; the stop test after each of them can only fire
+    // where b_proc reaches B_min, which is found in closed form.
+    while (p < cnt && !stop) {
+      if (!have_window || p >= wb + WAVE) load_window();
+      const int off = p - wb;
+      const int lim = cnt - wb < WAVE ? cnt - wb : WAVE;
+      const bool valid = lane >= off && lane < lim;
+      const uint32_t c0 = S.wc0[lane], c1 = S.wc1[lane];
+      const uint32_t sz = valid ? c1 - c0 : 0;
+      const uint64_t multi = ballot(sz >= 2);
+      const int first_multi = multi ? __ffsll((unsigned long long)multi) - 1 : lim;
+      const int nbulk = first_multi - off;
+      if (nbulk > 0) {
+        int take = nbulk;
+        bool stop_here = false;
+        if (a.early_stop_on && h == k_c && t_low >= a.t_low) {
+          int j = a.b_min - b_proc - 1;
+          j = j < 0 ? 0 : j;
+          if (j < nbulk) {
+            take = j + 1;
+            stop_here = true;
+          }
+        }
+        const bool single = lane >= off && lane < off + take && sz == 1;
+        const uint64_t sm = ballot(single);
+        if (single) out[ndir + popc64(sm & lanemask_lt())] = c0;
+        ndir += popc64(sm);
+        b_proc += take;
+        p += take;
+        if (stop_here) {
+          stop = true;
+          break;
+        }
+      }
+      if (multi != 0 && p == wb + first_multi) {
+        // a multi-cluster bucket forms its bin's C_z: batches of B_batch
+        b_proc += 1;
+        const uint32_t mc0 = S.wc0[first_multi], mc1 = S.wc1[first_multi];
+        for (uint32_t v = mc0; v < mc1 && !stop;) {
+          uint32_t take = mc1 - v < (uint32_t)a.b_batch ? mc1 - v : (uint32_t)a.b_batch;
+          if ((uint32_t)lane < take) S.pend[lane] = v + lane;
+          __builtin_amdgcn_wave_barrier();
+          npend = (int)take;
+          run_batch();
+          v += take;
+        }
+        if (!stop && full_and_quiet()) stop = true;
+        p += 1;
+      }
+    }
+  } else {
+    for (int z = 0; z <= z_last && !stop; ++z) {
+      b_proc += 1;
+      while (p < cnt) {
+        if (!have_window || p >= wb + WAVE) load_window();
+        const int off = p - wb;
+        // bins are sorted, so the probes of bin z from p are the slots [off, off + run)
+        const bool in_run = lane >= off && wb + lane < cnt && S.wbin[lane] == z;
+        const int run = popc64(ballot(in_run));
+        if (run == 0) break;
+        const uint32_t c0 = S.wc0[lane], c1 = S.wc1[lane];
+        const uint32_t sz = in_run ? c1 - c0 : 0;
+        // single-cluster buckets go to C_dir in probe order
+        const bool single = sz == 1;
+        const uint64_t sm = ballot(single);
+        if (single) out[ndir + popc64(sm & lanemask_lt())] = c0;
+        ndir += popc64(sm);
+        // clusters of multi-cluster buckets feed the batches (not after a stop)
+        if (!stop) {
+          const uint32_t msz = sz >= 2 ? sz : 0;
+          const uint32_t incl = wave_incl_scan_u32(msz);
+          const uint32_t total = __shfl(incl, WAVE - 1);
+          S.wpre[lane] = in_run ? incl - msz : 0xffffffffu;
+          __builtin_amdgcn_wave_barrier();
+          uint32_t v = 0;
+          while (v < total && !stop) {
+            uint32_t take = (uint32_t)(a.b_batch - npend);
+            if (take > total - v) take = total - v;
+            if ((uint32_t)lane < take) {
+              const uint32_t vi = v + lane;
+              // last slot of the run whose prefix is <= vi: zero-size slots share
+              // the prefix of the next non-empty one, so this is the owner
+              int lo = off, hi = off + run - 1;
+              while (lo < hi) {
+                int mid = (lo + hi + 1) >> 1;
+                if (S.wpre[mid] <= vi) lo = mid; else hi = mid - 1;
+              }
+              S.pend[npend + lane] = S.wc0[lo] + (vi - S.wpre[lo]);
+            }
+            __builtin_amdgcn_wave_barrier();
+            npend += (int)take;
+            v += take;
+            if (npend == a.b_batch) run_batch();
+          }
+        }
+        p += run;
+        if (off + run < WAVE) break;  // bin z ends inside this window
+      }
+      if (!stop && npend > 0) run_batch();
+      npend = 0;
+      if (!stop && full_and_quiet()) stop = true;
+    }
   }
 
   for (int i = lane; i < h; i += WAVE) out[ndir + i] = (uint32_t)H[i];

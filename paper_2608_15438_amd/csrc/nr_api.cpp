@@ -387,6 +387,16 @@ const char *nr_status_string(nr_status s) {
 
 const char *nr_last_error(void) { return g_err.c_str(); }
 
+nr_status nr_stream_read(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t stream) {
+  if (!buf || !sink || bytes < 0 || bytes % 16 != 0)
+    return fail(NR_EINVAL, "buf and sink must be set and bytes a multiple of 16");
+  int dev = 0, n_cu = 0;
+  HIP_OK(hipGetDevice(&dev));
+  HIP_OK(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
+  HIP_OK(nr::launch_stream_read(buf, bytes, sink, n_cu, stream));
+  return NR_OK;
+}
+
 nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t stream) {
   if (!desc || !out) return fail(NR_EINVAL, "desc and out must not be NULL");
   *out = nullptr;

@@ -10,8 +10,14 @@
 namespace nr {
 
 constexpr int WAVE = 64;
-constexpr int MAX_TILES_PER_QUERY = 64;   // refinement tiles per query (partials slots)
-constexpr int TILE_MIN_ROWS = 512;        // smallest refinement tile
+#ifndef NR_MAX_TILES_PER_QUERY
+#define NR_MAX_TILES_PER_QUERY 64
+#endif
+constexpr int MAX_TILES_PER_QUERY = NR_MAX_TILES_PER_QUERY;  // refinement tiles per query
+#ifndef NR_TILE_MIN_ROWS
+#define NR_TILE_MIN_ROWS 512
+#endif
+constexpr int TILE_MIN_ROWS = NR_TILE_MIN_ROWS;  // smallest refinement tile
 constexpr int STAGE_CLUSTERS = 128;       // clusters staged in LDS per refinement wave
 constexpr int64_t QUERY_CHUNK = 16384;    // queries per internal launch sequence
 constexpr int MAX_KC = 16384;             // top-K_c heap held in LDS
@@ -121,6 +127,9 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
+
+hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, int n_cu,
+                              hipStream_t s);
 
 // index validation at upload; flags[0] |= error bits
 hipError_t launch_validate(const uint32_t *bc_off, int64_t n_codes, const uint64_t *cl_off,

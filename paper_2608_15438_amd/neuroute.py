@@ -33,7 +33,8 @@ STAGES = ("encode", "probe", "route", "plan", "refine", "merge")
 # every symbol include/neuroute.h declares
 EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_encode",
            "nr_probe", "nr_route", "nr_route_capacity", "nr_refine", "nr_profile_enable",
-           "nr_profile_read", "nr_last_work", "nr_status_string", "nr_last_error")
+           "nr_profile_read", "nr_last_work", "nr_stream_read", "nr_status_string",
+           "nr_last_error")
 
 
 class NRError(RuntimeError):
@@ -93,6 +94,7 @@ def lib():
         L.nr_profile_enable.argtypes = [P, C.c_int32]
         L.nr_profile_read.argtypes = [P, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.c_int32]
         L.nr_last_work.argtypes = [P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
+        L.nr_stream_read.argtypes = [P, C.c_int64, P, P]
         for name in EXPORTS:
             getattr(L, name).restype = getattr(L, name).restype or C.c_int
         L.nr_route_capacity.restype = C.c_int64
@@ -136,6 +138,13 @@ def _dev(t: torch.Tensor, name: str):
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return t
+
+
+def nr_stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None):
+    """One streaming pass of 16-byte loads over a device tensor."""
+    _dev(buf, "buf")
+    _check(lib().nr_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
+                                _stream(stream)), "nr_stream_read")
 
 
 # --------------------------------------------------------------------------

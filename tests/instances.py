@@ -27,3 +27,28 @@ def oracle_encoder(ix):
     import oracle as O
     e = ix.encoder
     return O.Encoder(e.weights, e.biases, e.bn_scale or (), e.bn_shift or (), e.input_scale)
+
+
+def stage_rows(ix, lists):
+    """Host copies of only the rows the given cluster lists touch, behind a
+    cl_off in which every other cluster is empty (index arrays may live on
+    the GPU).  Returns (rows, row_ids, cl_off) for the oracle."""
+    import torch
+    cl = ix.cl_off.cpu().numpy().astype(np.int64) if hasattr(ix.cl_off, "cpu") else \
+        np.asarray(ix.cl_off).astype(np.int64)
+    need = np.unique(np.concatenate([np.asarray(x, np.int64) for x in lists]))
+    sizes = cl[need + 1] - cl[need]
+    idx = np.repeat(cl[need], sizes) + (np.arange(int(sizes.sum())) -
+                                         np.repeat(np.cumsum(sizes) - sizes, sizes))
+    if isinstance(ix.rows, torch.Tensor):
+        it = torch.from_numpy(idx).to(ix.rows.device)
+        rows = ix.rows[it].cpu().numpy()
+        ids = ix.row_ids[it].cpu().numpy()
+    else:
+        rows, ids = ix.rows[idx], ix.row_ids[idx]
+    n_cl = len(cl) - 1
+    cnt = np.zeros(n_cl, np.int64)
+    cnt[need] = sizes
+    cl2 = np.zeros(n_cl + 1, np.uint64)
+    cl2[1:] = np.cumsum(cnt)
+    return rows, ids, cl2
