@@ -226,7 +226,7 @@ def main():
         torch.cuda.synchronize()
         dt = (time.time() - t0) / reps
         rec = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k) if ng else float("nan")
-        tiles, rows = gix.nr_last_work()
+        tiles, rows, rows_read = gix.nr_last_work()
         pt = dict(probe_budget=P, recall=round(rec, 5), qps=round(w.n_queries / dt, 1),
                   cand_per_query=round(rows / w.n_queries, 1))
         sweep.append(pt)
@@ -265,7 +265,7 @@ def main():
     wall = time.time() - t0
     stage_ms, n_timed = gix.nr_profile_read(reset=True)
     gix.nr_profile_enable(False)
-    tiles, rows = gix.nr_last_work()
+    tiles, rows, rows_read = gix.nr_last_work()
     recall = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k) if ng else float("nan")
     qps = w.n_queries * args.steps / wall
     _, _, qs = gix.nr_search(Q, k, P, params, qstats=True)

@@ -128,10 +128,20 @@ typedef struct {
   int32_t gate_on;
   int32_t early_stop_on;
   int32_t lowq_or;
+  int32_t refine_mode;   /* NR_REFINE_AUTO / _PER_QUERY / _SHARED (same results) */
   int32_t m_knots;
   float m_x[NR_MAX_KNOTS];
   float m_y[NR_MAX_KNOTS];
 } nr_params;
+
+/* How step 5 is scheduled; both give the same top-k.  PER_QUERY refines each
+ * query's candidate rows on their own.  SHARED refines on its own, per query,
+ * the leading clusters of the list (>= 4096 rows) and the clusters no other
+ * query of the batch lists past its own leading clusters; a cluster that
+ * several queries list there is read once for all of them, keeping the rows
+ * that rank before the query's own top-k.  AUTO picks SHARED for batches of
+ * at least 512 queries.  Rows longer than 1024 bytes always use PER_QUERY. */
+enum { NR_REFINE_AUTO = 0, NR_REFINE_PER_QUERY = 1, NR_REFINE_SHARED = 2 };
 
 /* Per-query counters written by nr_search_ex when `qstats` is not NULL. */
 #define NR_QSTATS 8
@@ -203,9 +213,14 @@ nr_status nr_refine(const nr_index *index, const void *queries, int64_t nq, int3
 nr_status nr_profile_enable(nr_index *index, int32_t on);
 nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches, int32_t reset);
 
-/* Number of refinement tiles and rows of the last search on `stream`
- * (synchronises the stream). */
-nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *tiles, int64_t *rows);
+/* Work of the last search on `stream` (its last query chunk), synchronising
+ * the stream: refinement tiles of the per-query kernel, candidate rows summed
+ * over queries, and rows the refinement had to read (equal to `rows` for the
+ * per-query schedule; for the shared one, the rows of every query's own pass,
+ * each row of a shared cluster once, and the whole list again for a query
+ * whose survivors overflowed).  Any pointer may be NULL. */
+nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *tiles, int64_t *rows,
+                       int64_t *rows_read);
 
 /* Bandwidth self-check (not part of the search): one pass of 16-byte loads
  * over `bytes` (a multiple of 16) of the DEVICE buffer `buf`, on `stream`.

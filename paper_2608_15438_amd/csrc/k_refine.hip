@@ -50,17 +50,30 @@ __global__ void __launch_bounds__(256) k_plan_rows(PlanArgs a) {
   const int lane = lane_id();
   const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (q >= a.nq) return;
+  if (a.qmask && !a.qmask[q]) {
+    if (lane == 0) {
+      a.rtot[q] = 0;
+      a.tsize[q] = TILE_MIN_ROWS;
+      a.ntile[q] = 0;
+    }
+    return;
+  }
   const int n = clamp_count(a.nclus[q], a.cap);
   const uint32_t *cl = a.clus + q * a.cap;
   uint32_t *pre = a.rowpre + q * (a.cap + 1);
   uint64_t run = 0;
+  const int own0 = a.own_hist ? a.own_cseed[q] : 0;
   if (lane == 0) pre[0] = 0;
   for (int i0 = 0; i0 < n; i0 += WAVE) {
     const int i = i0 + lane;
     uint64_t sz = 0;
     if (i < n) {
       const uint32_t c = cl[i];
-      if (c < a.n_clusters) sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
+      if (c < a.n_clusters) {
+        sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
+        // the own pass of the shared schedule leaves shared clusters to the shared scan
+        if (a.own_hist && i >= own0 && a.own_hist[c] > 1) sz = 0;
+      }
     }
     const uint64_t incl = wave_incl_scan_u64(sz);
     if (i < n) pre[i + 1] = (uint32_t)(run + incl);
@@ -75,6 +88,7 @@ __global__ void __launch_bounds__(256) k_plan_rows(PlanArgs a) {
     a.rtot[q] = tot;
     a.tsize[q] = t;
     a.ntile[q] = (int32_t)(((uint64_t)tot + t - 1) / t);
+    if (a.rfull) a.rfull[q] = tot;
   }
 }
 
@@ -359,6 +373,7 @@ __global__ void __launch_bounds__(256) k_merge(MergeArgs a) {
   const int lane = lane_id();
   const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (q >= a.nq) return;
+  if (a.qmask && !a.qmask[q]) return;
   const int k = a.k;
   const int64_t e0 = (int64_t)a.tile_off[q] * k, e1 = (int64_t)a.tile_off[q + 1] * k;
   TopK tk;

@@ -1,0 +1,581 @@
+// Batch-shared exact refinement (step 5 of the search, Sec. 3.4 intro and
+// Sec. 3.5): the same top-k over C(q) as the per-query schedule, computed so
+// that a cluster listed by several queries of the batch is read from HBM once
+// for all of them.
+//
+//  hist    per query: the leading clusters of its list that cover at least
+//          seed_min rows stay with the query; every later (cluster, query)
+//          pair is counted per cluster;
+//  own     the per-query kernels refine each query's leading clusters plus
+//          the later clusters no other query lists (count 1).  Their top-k is
+//          exact over a subset of C(q), so its k-th entry (key, id) bounds the
+//          final k-th entry: a shared row can only enter the result if it
+//          ranks before it;
+//  prep    clusters with count >= 2 are shared: they are compacted into a
+//          list, their pairs grouped by cluster, and each is cut into work
+//          units of <= g queries x <= SHARED_ROWS rows;
+//  scan    persistent waves take tiles of SHARED_TILE work from an atomic
+//          counter and walk the units of the tile in list order, staging the
+//          metadata of 64 list entries per load (one per lane).  A unit's g
+//          query slices sit in registers; each row is loaded once (8 lanes x
+//          16 bytes per 128-byte segment) and scored for all g queries; a row
+//          that ranks before its query's bound is appended to that query's
+//          survivor list;
+//  merge   own top-k + survivors -> top-k.  A query with more than
+//          SURVIVOR_CAP survivors is flagged and recomputed by the per-query
+//          schedule.
+#include <cstring>
+
+#include <rocprim/rocprim.hpp>
+
+#include "nr_internal.h"
+
+// launch shape of the shared scan (tuned on MI355X)
+#ifndef NR_SHARED_BLOCKS_PER_CU
+#define NR_SHARED_BLOCKS_PER_CU 8
+#endif
+#ifndef NR_SHARED_U1
+#define NR_SHARED_U1 4          // rows in flight per lane group for 128-byte rows
+#endif
+#ifndef NR_SHARED_TILE
+#define NR_SHARED_TILE 4096     // work (rows x query groups) per scan tile
+#endif
+
+namespace nr {
+
+constexpr uint64_t SHARED_TILE = NR_SHARED_TILE;
+
+typedef unsigned int su32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load_stream(const uint4 *p) {
+  const su32x4 v = __builtin_nontemporal_load(reinterpret_cast<const su32x4 *>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ int clamp_n(int32_t n, int64_t cap) {
+  return n < 0 ? 0 : (n > cap ? (int)cap : n);
+}
+
+// Sum over the 8 lanes of an aligned lane group with DPP moves: pairs
+// (l, l^1), then (l, l^2) inside quads, then the two quads of the group
+// (row_half_mirror pairs lane i with lane 7-i; both quads hold uniform
+// values by then).  Every lane of the group ends with the same value, added
+// in the same order as an xor-1/2/4 shuffle reduction.
+__device__ __forceinline__ int32_t group8_sum(int32_t v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm(1,0,3,2)
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm(2,3,0,1)
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  return v;
+}
+
+__device__ __forceinline__ float group8_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+  return v;
+}
+
+__global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+// queries per work unit: the g query slices of a lane take g * NSEG * 4 VGPRs
+int shared_group(int row_bytes) {
+  const int nseg = (row_bytes + 127) / 128;
+  if (nseg <= 1) return 8;
+  if (nseg <= 4) return 4;
+  return 2;
+}
+
+// ------------------------------------------------------------------ hist
+// one wave per query: full rows, leading clusters, pair counts of the rest
+__global__ void __launch_bounds__(256) k_pair_hist(SharedArgs a) {
+  const int lane = lane_id();
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (q >= a.nq) return;
+  const int n = clamp_n(a.nclus[q], a.cap);
+  const uint32_t *cl = a.clus + q * a.cap;
+  uint64_t run = 0;
+  int cs = -1;
+  for (int i0 = 0; i0 < n; i0 += WAVE) {
+    const int i = i0 + lane;
+    uint32_t c = 0xffffffffu;
+    uint64_t sz = 0;
+    if (i < n) {
+      c = cl[i];
+      if (c < a.n_clusters) sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
+    }
+    const uint64_t incl = wave_incl_scan_u64(sz);
+    if (cs < 0) {
+      const uint64_t hit = ballot(i < n && run + incl >= a.seed_min);
+      if (hit) cs = i0 + __ffsll((unsigned long long)hit);  // first position past the seed
+    }
+    if (cs >= 0 && i >= cs && c < a.n_clusters) atomicAdd(&a.hist[c], 1u);
+    run += bcast_u64(incl, WAVE - 1);
+  }
+  if (lane == 0) {
+    a.cseed[q] = cs < 0 ? n : cs;
+    a.rfull[q] = run > 0xffffffffull ? 0u : (uint32_t)run;
+  }
+}
+
+hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s) {
+  hipError_t e = launch_fill_i32((int32_t *)a.hist, a.n_clusters + 1, 0, s);
+  if (e != hipSuccess || a.nq <= 0) return e;
+  hipLaunchKernelGGL(k_pair_hist, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ prep
+// one thread per cluster: shared clusters and their pairs
+__global__ void k_shared_count(SharedArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c <= a.n_clusters; c += stride) {
+    const uint32_t h = c < a.n_clusters ? a.hist[c] : 0u;
+    a.cnt2[c] = h >= 2 ? h : 0u;
+    a.isshared[c] = h >= 2 ? 1u : 0u;
+    a.swork[c] = 0;
+  }
+}
+
+// one thread per cluster: the compacted list and the work of each entry
+__global__ void k_shared_list(SharedArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < a.n_clusters; c += stride) {
+    if (!a.isshared[c]) continue;
+    const uint32_t i = a.spos[c];
+    const uint64_t groups = (uint64_t)((a.hist[c] + a.g - 1) / a.g);
+    a.slist[i] = (uint32_t)c;
+    a.swork[i] = groups * (a.cl_off[c + 1] - a.cl_off[c]);
+  }
+}
+
+// one wave per query: the query's shared pairs into their cluster's slots
+__global__ void __launch_bounds__(256) k_pair_scatter(SharedArgs a) {
+  const int lane = lane_id();
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (q >= a.nq) return;
+  const int n = clamp_n(a.nclus[q], a.cap);
+  const uint32_t *cl = a.clus + q * a.cap;
+  for (int i = a.cseed[q] + lane; i < n; i += WAVE) {
+    const uint32_t c = cl[i];
+    if (c < a.n_clusters && a.hist[c] >= 2) {
+      const uint32_t left = atomicSub(&a.cnt2[c], 1u);
+      a.pair_q[a.hoff[c] + left - 1] = (uint32_t)q;
+    }
+  }
+}
+
+size_t shared_scan_tmp_bytes(int64_t n_clusters) {
+  size_t b32 = 0, b64 = 0;
+  const size_t n = (size_t)n_clusters + 1;
+  (void)rocprim::exclusive_scan(nullptr, b32, (const uint32_t *)nullptr, (uint32_t *)nullptr, 0u,
+                                n, rocprim::plus<uint32_t>());
+  (void)rocprim::exclusive_scan(nullptr, b64, (const uint64_t *)nullptr, (uint64_t *)nullptr,
+                                (uint64_t)0, n, rocprim::plus<uint64_t>());
+  return b32 > b64 ? b32 : b64;
+}
+
+hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
+  const int64_t nc1 = a.n_clusters + 1;
+  hipError_t e = launch_fill_i32(a.scnt, a.nq, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32(a.flag, a.nq, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
+  if (e != hipSuccess) return e;
+  int64_t blocks = (nc1 + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  hipLaunchKernelGGL(k_shared_count, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  size_t tmp = a.scan_tmp_bytes;
+  e = rocprim::exclusive_scan(a.scan_tmp, tmp, a.cnt2, a.hoff, 0u, (size_t)nc1,
+                              rocprim::plus<uint32_t>(), s);
+  if (e != hipSuccess) return e;
+  tmp = a.scan_tmp_bytes;
+  e = rocprim::exclusive_scan(a.scan_tmp, tmp, a.isshared, a.spos, 0u, (size_t)nc1,
+                              rocprim::plus<uint32_t>(), s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_shared_list, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  tmp = a.scan_tmp_bytes;
+  e = rocprim::exclusive_scan(a.scan_tmp, tmp, a.swork, a.swork_off, (uint64_t)0, (size_t)nc1,
+                              rocprim::plus<uint64_t>(), s);
+  if (e != hipSuccess) return e;
+  if (a.nq > 0)
+    hipLaunchKernelGGL(k_pair_scatter, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ scan
+// The work of shared cluster slist[i] is swork[i] = rows x query groups; a
+// unit (group gi, row chunk ch) starts at swork_off[i] + gi * rows + ch * R.
+// A tile is a SHARED_TILE-long range of that work space and takes the units
+// that start inside it, so each unit belongs to exactly one tile.
+template <int IS_U8, int NSEG, int G, int U>
+__global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
+  const int lane = lane_id();
+  const int grp = lane >> 3;  // lane group: one row at a time
+  const int gl = lane & 7;    // 16-byte slot inside a 128-byte segment
+  const int64_t NS = a.spos[a.n_clusters];
+  const uint64_t W = a.swork_off[a.n_clusters];
+  const uint64_t ntiles = (W + SHARED_TILE - 1) / SHARED_TILE;
+  const int rb = a.row_bytes;
+  const int k = a.k;
+  const unsigned char *rows = (const unsigned char *)a.rows;
+  const unsigned char *queries = (const unsigned char *)a.queries;
+
+  for (;;) {
+    unsigned long long t = 0;
+    if (lane == 0) t = atomicAdd(a.counter, 1ull);
+    t = bcast_u64(t, 0);
+    if (t >= ntiles) break;
+    const uint64_t ws = (uint64_t)t * SHARED_TILE;
+    const uint64_t we = ws + SHARED_TILE < W ? ws + SHARED_TILE : W;
+    // the list entry holding ws: the last i with swork_off[i] <= ws (64-ary search)
+    int64_t lo = 0, hi = NS;
+    while (hi - lo > 1) {
+      const int64_t step = (hi - lo + WAVE - 1) / WAVE;
+      const int64_t pos = lo + (int64_t)lane * step;
+      const bool pred = lane > 0 && pos < hi && a.swork_off[pos] <= ws;
+      const uint64_t m = ballot(pred);
+      const int last = m ? 63 - __clzll((long long)m) : 0;
+      const int64_t nlo = lo + (int64_t)last * step;
+      const int64_t nhi = nlo + step < hi ? nlo + step : hi;
+      lo = nlo;
+      hi = nhi;
+    }
+    int64_t i = lo;
+    // metadata of entries ib .. ib + 63, one per lane
+    int64_t ib = i;
+    uint64_t l_wo = 0, l_base = 0, l_sz = 0;
+    uint32_t l_hp = 0, l_m = 0;
+    auto stage = [&]() {
+      const int64_t ii = ib + lane;
+      l_wo = 0;
+      l_base = 0;
+      l_sz = 0;
+      l_hp = 0;
+      l_m = 0;
+      if (ii < NS) {
+        const uint32_t c = a.slist[ii];
+        l_wo = a.swork_off[ii];
+        l_base = a.cl_off[c];
+        l_sz = a.cl_off[(uint64_t)c + 1] - l_base;
+        l_hp = a.hoff[c];
+        l_m = a.hoff[(uint64_t)c + 1] - l_hp;
+      }
+    };
+    stage();
+    uint64_t wo = bcast_u64(l_wo, 0), base = bcast_u64(l_base, 0), sz = bcast_u64(l_sz, 0);
+    uint32_t hp = bcast_u32(l_hp, 0), mq = bcast_u32(l_m, 0);
+    uint64_t nch = (sz + SHARED_ROWS - 1) / SHARED_ROWS;
+    uint32_t ng = (mq + G - 1) / G;
+    // the first unit of entry i that starts at or after ws
+    const uint64_t rel = ws - wo;
+    uint32_t gi = (uint32_t)(rel / sz);
+    const uint64_t rr = rel - (uint64_t)gi * sz;
+    uint64_t ch = (rr + SHARED_ROWS - 1) / SHARED_ROWS;
+    bool have = true;
+    auto next_entry = [&]() {
+      do {
+        ++i;
+        if (i >= NS) {
+          have = false;
+          return;
+        }
+        if (i - ib >= WAVE) {
+          ib = i;
+          stage();
+        }
+        const int src = (int)(i - ib);
+        wo = bcast_u64(l_wo, src);
+        base = bcast_u64(l_base, src);
+        sz = bcast_u64(l_sz, src);
+        hp = bcast_u32(l_hp, src);
+        mq = bcast_u32(l_m, src);
+      } while (sz == 0);
+      nch = (sz + SHARED_ROWS - 1) / SHARED_ROWS;
+      ng = (mq + G - 1) / G;
+      gi = 0;
+      ch = 0;
+    };
+    if (ch >= nch) {
+      ch = 0;
+      if (++gi >= ng) next_entry();
+    }
+
+    while (have && wo + (uint64_t)gi * sz + ch * SHARED_ROWS < we) {
+      const uint64_t r0 = base + ch * SHARED_ROWS;
+      const uint64_t r1 = base + (ch * SHARED_ROWS + SHARED_ROWS < sz ? ch * SHARED_ROWS + SHARED_ROWS : sz);
+      const uint32_t p0 = hp + gi * G;
+      const int gm = mq - gi * G < (uint32_t)G ? (int)(mq - gi * G) : G;
+
+      // the first rows go out before the query slices, which depend on pair_q
+      bool ok[U];
+      uint4 xv[U][NSEG];
+      auto load_rows = [&](uint64_t rfirst) {
+#pragma unroll
+        for (int uu = 0; uu < U; ++uu) {
+          const uint64_t r = rfirst + 8 * uu + grp;
+          ok[uu] = r < r1;
+          const unsigned char *rp = rows + r * (uint64_t)rb;
+#pragma unroll
+          for (int s = 0; s < NSEG; ++s) {
+            const int off = 128 * s + 16 * gl;
+            xv[uu][s] = (ok[uu] && off < rb) ? load_stream((const uint4 *)(rp + off))
+                                             : make_uint4(0, 0, 0, 0);
+          }
+        }
+      };
+      load_rows(r0);
+      uint4 qv[G][NSEG];
+      uint32_t qid[G], tkey[G];
+      int64_t tid[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        qid[j] = j < gm ? a.pair_q[p0 + j] : 0u;
+        const unsigned char *qp = queries + (uint64_t)qid[j] * (uint64_t)rb;
+#pragma unroll
+        for (int s = 0; s < NSEG; ++s) {
+          const int off = 128 * s + 16 * gl;
+          qv[j][s] = (j < gm && off < rb) ? *(const uint4 *)(qp + off) : make_uint4(0, 0, 0, 0);
+        }
+        tkey[j] = 0xffffffffu;
+        tid[j] = INT64_MAX;
+        if (j < gm) {
+          const int64_t id = a.own_ids[(int64_t)qid[j] * k + k - 1];
+          const float d = a.own_dists[(int64_t)qid[j] * k + k - 1];
+          if (id >= 0) {
+            tkey[j] = a.is_u8 ? (uint32_t)d : __float_as_uint(d);
+            tid[j] = id;
+          }
+        }
+      }
+
+      for (uint64_t rb0 = r0; rb0 < r1; rb0 += 8 * U) {
+#pragma unroll
+        for (int uu = 0; uu < U; ++uu) {
+          int32_t xx = 0;
+          if (IS_U8) {
+            uint32_t acc = 0;
+#pragma unroll
+            for (int s = 0; s < NSEG; ++s) {
+              acc = __builtin_amdgcn_udot4(xv[uu][s].x, xv[uu][s].x, acc, false);
+              acc = __builtin_amdgcn_udot4(xv[uu][s].y, xv[uu][s].y, acc, false);
+              acc = __builtin_amdgcn_udot4(xv[uu][s].z, xv[uu][s].z, acc, false);
+              acc = __builtin_amdgcn_udot4(xv[uu][s].w, xv[uu][s].w, acc, false);
+            }
+            xx = (int32_t)acc;
+          }
+#pragma unroll
+          for (int j = 0; j < G; ++j) {
+            if (j >= gm) break;
+            uint32_t key;
+            if (IS_U8) {
+              // this lane's part of |x|^2 - 2 x.q + |q|^2, exact in int32
+              uint32_t xq = 0, qq = 0;
+#pragma unroll
+              for (int s = 0; s < NSEG; ++s) {
+                xq = __builtin_amdgcn_udot4(xv[uu][s].x, qv[j][s].x, xq, false);
+                xq = __builtin_amdgcn_udot4(xv[uu][s].y, qv[j][s].y, xq, false);
+                xq = __builtin_amdgcn_udot4(xv[uu][s].z, qv[j][s].z, xq, false);
+                xq = __builtin_amdgcn_udot4(xv[uu][s].w, qv[j][s].w, xq, false);
+                qq = __builtin_amdgcn_udot4(qv[j][s].x, qv[j][s].x, qq, false);
+                qq = __builtin_amdgcn_udot4(qv[j][s].y, qv[j][s].y, qq, false);
+                qq = __builtin_amdgcn_udot4(qv[j][s].z, qv[j][s].z, qq, false);
+                qq = __builtin_amdgcn_udot4(qv[j][s].w, qv[j][s].w, qq, false);
+              }
+              key = (uint32_t)group8_sum(xx - 2 * (int32_t)xq + (int32_t)qq);
+            } else {
+              float acc = 0.0f;
+#pragma unroll
+              for (int s = 0; s < NSEG; ++s) {
+                const float t0 = __uint_as_float(xv[uu][s].x) - __uint_as_float(qv[j][s].x);
+                const float t1 = __uint_as_float(xv[uu][s].y) - __uint_as_float(qv[j][s].y);
+                const float t2 = __uint_as_float(xv[uu][s].z) - __uint_as_float(qv[j][s].z);
+                const float t3 = __uint_as_float(xv[uu][s].w) - __uint_as_float(qv[j][s].w);
+                acc = fmaf(t0, t0, acc);
+                acc = fmaf(t1, t1, acc);
+                acc = fmaf(t2, t2, acc);
+                acc = fmaf(t3, t3, acc);
+              }
+              key = __float_as_uint(group8_sum(acc));
+            }
+            // the row can enter this query's result only if it ranks before the bound
+            if (ok[uu] && gl == 0 && key <= tkey[j]) {
+              const uint64_t r = rb0 + 8 * uu + grp;
+              const int64_t id = a.row_ids[r];
+              if (key < tkey[j] || id < tid[j]) {
+                const uint32_t q = qid[j];
+                const int pos = atomicAdd(&a.scnt[q], 1);
+                if (pos < SURVIVOR_CAP) {
+                  a.skey[(int64_t)q * SURVIVOR_CAP + pos] = key;
+                  a.sid[(int64_t)q * SURVIVOR_CAP + pos] = id;
+                }
+              }
+            }
+          }
+        }
+        if (rb0 + 8 * U < r1) load_rows(rb0 + 8 * U);
+      }
+      // next unit
+      if (++ch >= nch) {
+        ch = 0;
+        if (++gi >= ng) next_entry();
+      }
+    }
+  }
+}
+
+template <int IS_U8>
+static hipError_t launch_shared_t(const SharedArgs &a, int nseg, int grid, hipStream_t s) {
+#define NR_SHARED_CASE(NS, GG, UU)                                                              \
+  if (nseg <= NS) {                                                                             \
+    if (a.g != GG) return hipErrorInvalidValue;                                                 \
+    hipLaunchKernelGGL((k_shared_refine<IS_U8, NS, GG, UU>), dim3(grid), dim3(256), 0, s, a); \
+    return hipGetLastError();                                                                   \
+  }
+  NR_SHARED_CASE(1, 8, NR_SHARED_U1)
+  NR_SHARED_CASE(2, 4, 4)
+  NR_SHARED_CASE(4, 4, 2)
+  NR_SHARED_CASE(8, 2, 1)
+#undef NR_SHARED_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStream_t s) {
+  if (a.nq <= 0) return hipSuccess;
+  const int nseg = (a.row_bytes + 127) / 128;
+  if (nseg > SHARED_MAX_NSEG) return hipErrorInvalidValue;
+  const int grid = n_cu * NR_SHARED_BLOCKS_PER_CU;
+  return dtype == NR_U8 ? launch_shared_t<1>(a, nseg, grid, s) : launch_shared_t<0>(a, nseg, grid, s);
+}
+
+// ------------------------------------------------------------------ merge
+// (key, id) of a top-k list held in lanes 0..k-1
+struct SharedTopK {
+  uint32_t key;
+  int64_t id;
+  int cnt;
+  uint32_t kth_key;
+  int64_t kth_id;
+};
+
+__device__ __forceinline__ void stk_insert(SharedTopK &t, int k, uint32_t ck, int64_t cid) {
+  const int lane = lane_id();
+  if (t.cnt == k && (ck > t.kth_key || (ck == t.kth_key && cid >= t.kth_id))) return;
+  const bool less = lane < t.cnt && (t.key < ck || (t.key == ck && t.id < cid));
+  const int pos = popc64(ballot(less));
+  const uint32_t up_key = (uint32_t)__shfl_up((int)t.key, 1);
+  const int64_t up_id = (int64_t)shfl_up_u64((uint64_t)t.id, 1);
+  if (lane == pos) {
+    t.key = ck;
+    t.id = cid;
+  } else if (lane > pos && lane < k) {
+    t.key = up_key;
+    t.id = up_id;
+  }
+  t.cnt = t.cnt + 1 < k ? t.cnt + 1 : k;
+  if (t.cnt == k) {
+    t.kth_key = bcast_u32(t.key, k - 1);
+    t.kth_id = (int64_t)bcast_u64((uint64_t)t.id, k - 1);
+  }
+}
+
+__global__ void __launch_bounds__(256) k_shared_merge(SharedArgs a) {
+  const int lane = lane_id();
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (q >= a.nq) return;
+  if (lane == 0) {
+    a.own_rows[q] = a.rtot[q];
+    if (q == 0) a.wstats[1] = a.tile_off[a.nq];
+  }
+  const int k = a.k;
+  const int cnt = a.scnt[q];
+  if (cnt > SURVIVOR_CAP) {
+    if (lane == 0) a.flag[q] = 1;  // recomputed by the per-query schedule
+    return;
+  }
+  SharedTopK tk;
+  tk.key = 0xffffffffu;
+  tk.id = -1;
+  tk.cnt = 0;
+  tk.kth_key = 0xffffffffu;
+  tk.kth_id = INT64_MAX;
+  // the own-pass top-k (sorted)
+  {
+    int64_t id = -1;
+    uint32_t key = 0xffffffffu;
+    if (lane < k) {
+      id = a.own_ids[q * k + lane];
+      const float d = a.own_dists[q * k + lane];
+      key = a.is_u8 ? (uint32_t)d : __float_as_uint(d);
+    }
+    uint64_t m = ballot(lane < k && id >= 0);
+    while (m) {
+      const int src = __ffsll((unsigned long long)m) - 1;
+      m &= m - 1;
+      stk_insert(tk, k, bcast_u32(key, src), (int64_t)bcast_u64((uint64_t)id, src));
+    }
+  }
+  for (int i0 = 0; i0 < cnt; i0 += WAVE) {
+    const int i = i0 + lane;
+    uint32_t key = 0xffffffffu;
+    int64_t id = -1;
+    if (i < cnt) {
+      key = a.skey[q * SURVIVOR_CAP + i];
+      id = a.sid[q * SURVIVOR_CAP + i];
+    }
+    uint64_t m = ballot(i < cnt && key <= tk.kth_key);
+    while (m) {
+      const int src = __ffsll((unsigned long long)m) - 1;
+      m &= m - 1;
+      stk_insert(tk, k, bcast_u32(key, src), (int64_t)bcast_u64((uint64_t)id, src));
+    }
+  }
+  if (lane < k) {
+    const bool have = lane < tk.cnt;
+    a.out_ids[q * k + lane] = have ? tk.id : -1;
+    a.out_dists[q * k + lane] =
+        have ? (a.is_u8 ? (float)tk.key : __uint_as_float(tk.key)) : INFINITY;
+  }
+  if (lane == 0 && a.qstats) a.qstats[q * NR_QSTATS + NR_QS_ROWS] = (int32_t)a.rfull[q];
+}
+
+hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s) {
+  if (a.nq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_shared_merge, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ diagnostics
+// rows of the shared clusters (each read once by the scan)
+__global__ void k_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int64_t n_clusters,
+                              int64_t *out) {
+  __shared__ unsigned long long part[256];
+  unsigned long long acc = 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_clusters; c += stride)
+    if (hoff[c + 1] > hoff[c]) acc += cl_off[c + 1] - cl_off[c];
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) part[threadIdx.x] += part[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) atomicAdd((unsigned long long *)out, part[0]);
+}
+
+hipError_t launch_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int64_t n_clusters,
+                              int64_t *out, hipStream_t s) {
+  hipLaunchKernelGGL(k_unique_rows, dim3(1024), dim3(256), 0, s, hoff, cl_off, n_clusters, out);
+  return hipGetLastError();
+}
+
+}  // namespace nr

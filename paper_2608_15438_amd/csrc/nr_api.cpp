@@ -62,12 +62,29 @@ struct Buffers {
   int32_t *ntile, *tile_off, *tile_q, *tile_c0, *counter;
   uint32_t *pkey;
   int64_t *pid;
+  // shared refinement
+  int64_t *own_ids;
+  float *own_dists;
+  int32_t *cseed;
+  uint32_t *rfull, *own_rows;
+  int32_t *scnt, *flag;
+  unsigned long long *counter2;
+  uint32_t *skey;
+  int64_t *sid;
+  uint32_t *pair_q, *hist, *cnt2, *hoff, *isshared, *spos, *slist;
+  uint64_t *swork, *swork_off;
+  int64_t *wstats;
+  void *scan_tmp;
+  size_t scan_tmp_bytes;
+  bool shared;
 };
 
 struct Shape {
   int64_t nq;   // queries per chunk
   int P, b, k, maxw;
   int64_t cap;
+  bool shared = false;
+  int64_t n_clusters = 0;
 };
 
 Buffers carve(char *base, const Shape &s, size_t *bytes) {
@@ -92,6 +109,32 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
   B.counter = c.take<int32_t>(1);
   B.pkey = c.take<uint32_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
   B.pid = c.take<int64_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
+  B.shared = s.shared;
+  B.rfull = c.take<uint32_t>((size_t)s.nq);
+  B.wstats = c.take<int64_t>(2);
+  if (s.shared) {
+    const size_t nc1 = (size_t)s.n_clusters + 1;
+    B.own_ids = c.take<int64_t>((size_t)s.nq * s.k);
+    B.own_dists = c.take<float>((size_t)s.nq * s.k);
+    B.cseed = c.take<int32_t>((size_t)s.nq);
+    B.own_rows = c.take<uint32_t>((size_t)s.nq);
+    B.scnt = c.take<int32_t>((size_t)s.nq);
+    B.flag = c.take<int32_t>((size_t)s.nq);
+    B.counter2 = c.take<unsigned long long>(1);
+    B.skey = c.take<uint32_t>((size_t)s.nq * nr::SURVIVOR_CAP);
+    B.sid = c.take<int64_t>((size_t)s.nq * nr::SURVIVOR_CAP);
+    B.pair_q = c.take<uint32_t>((size_t)s.nq * s.cap);
+    B.hist = c.take<uint32_t>(nc1);
+    B.cnt2 = c.take<uint32_t>(nc1);
+    B.hoff = c.take<uint32_t>(nc1);
+    B.isshared = c.take<uint32_t>(nc1);
+    B.spos = c.take<uint32_t>(nc1);
+    B.slist = c.take<uint32_t>(nc1);
+    B.swork = c.take<uint64_t>(nc1);
+    B.swork_off = c.take<uint64_t>(nc1);
+    B.scan_tmp_bytes = nr::shared_scan_tmp_bytes(s.n_clusters);
+    B.scan_tmp = c.take<char>(B.scan_tmp_bytes);
+  }
   *bytes = align_up(c.off, 256);
   return B;
 }
@@ -102,6 +145,7 @@ struct Workspace {
   size_t bytes = 0;
   Buffers last{};
   int64_t last_nq = 0;
+  int64_t last_cap = 0;
 };
 
 struct EventSet {
@@ -193,6 +237,8 @@ nr_status check_params(const nr_index *ix, int32_t P, const nr_params *p) {
       return fail(NR_EINVAL, "margin knots must have non-decreasing y");
   }
   if (!std::isfinite(p->alpha_front)) return fail(NR_EINVAL, "alpha_front must be finite");
+  if (p->refine_mode < NR_REFINE_AUTO || p->refine_mode > NR_REFINE_SHARED)
+    return fail(NR_EINVAL, "refine_mode must be 0, 1 or 2");
   return NR_OK;
 }
 
@@ -298,10 +344,16 @@ hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
   return nr::launch_route(a, s);
 }
 
+struct RefineOpts {
+  const int32_t *qmask = nullptr;     // only these queries (the others keep their outputs)
+  const uint32_t *own_hist = nullptr; // own pass of the shared schedule
+  const int32_t *own_cseed = nullptr;
+};
+
 hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, const uint32_t *clus,
                       const int32_t *nclus, int64_t cap, const Buffers &B, int64_t *out_ids,
                       float *out_dists, int32_t *qstats, hipStream_t s, hipEvent_t *ev_plan,
-                      hipEvent_t *ev_refine) {
+                      hipEvent_t *ev_refine, const RefineOpts &o = RefineOpts()) {
   nr::PlanArgs pa{};
   pa.nq = nq;
   pa.clus = clus;
@@ -317,6 +369,10 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   pa.tile_q = B.tile_q;
   pa.tile_c0 = B.tile_c0;
   pa.counter = B.counter;
+  pa.rfull = (o.qmask || o.own_hist) ? nullptr : B.rfull;
+  pa.qmask = o.qmask;
+  pa.own_hist = o.own_hist;
+  pa.own_cseed = o.own_cseed;
   hipError_t e = nr::launch_plan(pa, s);
   if (e != hipSuccess) return e;
   if (ev_plan) (void)hipEventRecord(*ev_plan, s);
@@ -356,7 +412,87 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   ma.out_ids = out_ids;
   ma.out_dists = out_dists;
   ma.qstats = qstats;
+  ma.qmask = o.qmask;
   return nr::launch_merge(ma, s);
+}
+
+// Step 5 with the batch-shared schedule (k_shared.hip): pair counts, the own
+// pass of every query, cluster-major work units, the shared scan, the merge,
+// and the per-query schedule again for the queries whose survivors overflowed.
+hipError_t run_refine_shared(const nr_index *ix, const void *q, int64_t nq, int k,
+                             const uint32_t *clus, const int32_t *nclus, int64_t cap,
+                             const Buffers &B, int64_t *out_ids, float *out_dists,
+                             int32_t *qstats, hipStream_t s, hipEvent_t *ev_plan,
+                             hipEvent_t *ev_refine) {
+  nr::SharedArgs a{};
+  a.nq = nq;
+  a.k = k;
+  a.is_u8 = ix->d.dtype == NR_U8;
+  a.row_bytes = (int)(ix->d.d * elem_size(ix));
+  a.g = nr::shared_group(a.row_bytes);
+  a.seed_min = nr::SEED_ROWS > (uint32_t)k ? nr::SEED_ROWS : (uint32_t)k;
+  a.n_clusters = ix->d.n_clusters;
+  a.rows = ix->d.rows;
+  a.row_ids = ix->d.row_ids;
+  a.cl_off = ix->d.cl_off;
+  a.queries = q;
+  a.clus = clus;
+  a.nclus = nclus;
+  a.cap = cap;
+  a.cseed = B.cseed;
+  a.rfull = B.rfull;
+  a.rtot = B.rtot;
+  a.tile_off = B.tile_off;
+  a.own_ids = B.own_ids;
+  a.own_dists = B.own_dists;
+  a.own_rows = B.own_rows;
+  a.hist = B.hist;
+  a.cnt2 = B.cnt2;
+  a.hoff = B.hoff;
+  a.isshared = B.isshared;
+  a.spos = B.spos;
+  a.slist = B.slist;
+  a.swork = B.swork;
+  a.swork_off = B.swork_off;
+  a.pair_q = B.pair_q;
+  a.scnt = B.scnt;
+  a.skey = B.skey;
+  a.sid = B.sid;
+  a.flag = B.flag;
+  a.counter = B.counter2;
+  a.wstats = B.wstats;
+  a.scan_tmp = B.scan_tmp;
+  a.scan_tmp_bytes = B.scan_tmp_bytes;
+  a.out_ids = out_ids;
+  a.out_dists = out_dists;
+  a.qstats = qstats;
+  hipError_t e = nr::launch_shared_hist(a, s);
+  if (e != hipSuccess) return e;
+  RefineOpts own;
+  own.own_hist = B.hist;
+  own.own_cseed = B.cseed;
+  e = run_refine(ix, q, nq, k, clus, nclus, cap, B, B.own_ids, B.own_dists, qstats, s, ev_plan,
+                 nullptr, own);
+  if (e != hipSuccess) return e;
+  e = nr::launch_shared_prep(a, s);
+  if (e != hipSuccess) return e;
+  e = nr::launch_shared_refine(a, ix->d.dtype, ix->n_cu, s);
+  if (e != hipSuccess) return e;
+  if (ev_refine) (void)hipEventRecord(*ev_refine, s);
+  e = nr::launch_shared_merge(a, s);
+  if (e != hipSuccess) return e;
+  RefineOpts fb;
+  fb.qmask = B.flag;
+  return run_refine(ix, q, nq, k, clus, nclus, cap, B, out_ids, out_dists, qstats, s, nullptr,
+                    nullptr, fb);
+}
+
+bool use_shared(const nr_index *ix, const nr_params *p, int64_t nq) {
+  const int rb = (int)(ix->d.d * elem_size(ix));
+  if ((rb + 127) / 128 > nr::SHARED_MAX_NSEG) return false;
+  if (p->refine_mode == NR_REFINE_SHARED) return true;
+  if (p->refine_mode == NR_REFINE_PER_QUERY) return false;
+  return nq >= 512;
 }
 
 nr_status check_index(const nr_index *ix) {
@@ -603,7 +739,8 @@ nr_status nr_refine(const nr_index *cix, const void *queries, int64_t nq, int32_
                       out_dists + q0 * k, nullptr, stream, nullptr, nullptr));
   }
   w->last = B;
-  w->last_nq = nq < sh.nq ? nq : sh.nq;
+  w->last_nq = nq - (nq - 1) / sh.nq * sh.nq;
+  w->last_cap = cap;
   return NR_OK;
 }
 
@@ -622,6 +759,8 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
   Buffers B;
   Workspace *w;
   Shape sh = shape_of(ix, nq, P, k, cap);
+  sh.shared = use_shared(ix, p, sh.nq);
+  sh.n_clusters = ix->d.n_clusters;
   if (nr_status s = workspace_for(ix, stream, sh, &B, &w)) return s;
   const size_t qrow = ix->d.d * elem_size(ix);
   for (int64_t q0 = 0; q0 < nq; q0 += sh.nq) {
@@ -641,9 +780,14 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
     if (prof) HIP_OK(hipEventRecord(es.ev[2], stream));
     HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, qs, stream));
     if (prof) HIP_OK(hipEventRecord(es.ev[3], stream));
-    HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
-                      out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr,
-                      prof ? &es.ev[5] : nullptr));
+    if (B.shared)
+      HIP_OK(run_refine_shared(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
+                               out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr,
+                               prof ? &es.ev[5] : nullptr));
+    else
+      HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
+                        out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr,
+                        prof ? &es.ev[5] : nullptr));
     if (prof) {
       HIP_OK(hipEventRecord(es.ev[6], stream));
       std::lock_guard<std::mutex> g(ix->mu);
@@ -651,7 +795,8 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
     }
   }
   w->last = B;
-  w->last_nq = nq < sh.nq ? nq : sh.nq;
+  w->last_nq = nq - (nq - 1) / sh.nq * sh.nq;
+  w->last_cap = cap;
   return NR_OK;
 }
 
@@ -690,7 +835,8 @@ nr_status nr_profile_read(nr_index *ix, double *stage_ms, int64_t *n_searches, i
   return NR_OK;
 }
 
-nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *tiles, int64_t *rows) {
+nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *tiles, int64_t *rows,
+                       int64_t *rows_read) {
   if (nr_status s = check_index(ix)) return s;
   Workspace *w = nullptr;
   {
@@ -699,15 +845,35 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *tiles, int64_t
       if (x.stream == stream) w = &x;
   }
   if (!w || !w->last.tile_off) return fail(NR_EINVAL, "no search has run on this stream");
+  const Buffers &B = w->last;
+  const size_t nq = (size_t)w->last_nq;
+  if (B.shared) {
+    HIP_OK(nr::launch_fill_i32((int32_t *)B.wstats, 2, 0, stream));
+    HIP_OK(nr::launch_unique_rows(B.hoff, ix->d.cl_off, ix->d.n_clusters, B.wstats, stream));
+  }
   HIP_OK(hipStreamSynchronize(stream));
   int32_t t = 0;
-  HIP_OK(hipMemcpy(&t, w->last.tile_off + w->last_nq, 4, hipMemcpyDeviceToHost));
-  std::vector<uint32_t> r((size_t)w->last_nq);
-  HIP_OK(hipMemcpy(r.data(), w->last.rtot, 4 * r.size(), hipMemcpyDeviceToHost));
-  int64_t sum = 0;
-  for (uint32_t v : r) sum += v;
+  HIP_OK(hipMemcpy(&t, B.tile_off + nq, 4, hipMemcpyDeviceToHost));
+  std::vector<uint32_t> full(nq);
+  HIP_OK(hipMemcpy(full.data(), B.rfull, 4 * nq, hipMemcpyDeviceToHost));
+  int64_t sum_full = 0;
+  for (uint32_t v : full) sum_full += v;
+  int64_t read = sum_full;
+  if (B.shared) {
+    // own pass + each shared cluster once + the per-query redo of flagged queries
+    int64_t ws[2] = {0, 0};
+    HIP_OK(hipMemcpy(ws, B.wstats, sizeof(ws), hipMemcpyDeviceToHost));
+    std::vector<uint32_t> own(nq);
+    std::vector<int32_t> flag(nq);
+    HIP_OK(hipMemcpy(own.data(), B.own_rows, 4 * nq, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(flag.data(), B.flag, 4 * nq, hipMemcpyDeviceToHost));
+    read = ws[0];
+    for (size_t i = 0; i < nq; ++i) read += own[i] + (flag[i] ? full[i] : 0u);
+    t += (int32_t)ws[1];
+  }
   if (tiles) *tiles = t;
-  if (rows) *rows = sum;
+  if (rows) *rows = sum_full;
+  if (rows_read) *rows_read = read;
   return NR_OK;
 }
 

@@ -20,6 +20,11 @@ constexpr int MAX_TILES_PER_QUERY = NR_MAX_TILES_PER_QUERY;  // refinement tiles
 constexpr int TILE_MIN_ROWS = NR_TILE_MIN_ROWS;  // smallest refinement tile
 constexpr int STAGE_CLUSTERS = 128;       // clusters staged in LDS per refinement wave
 constexpr int64_t QUERY_CHUNK = 16384;    // queries per internal launch sequence
+constexpr uint32_t SEED_ROWS = 4096;      // rows of a query's first clusters refined on their own
+constexpr int SURVIVOR_CAP = 1024;        // candidates a query may keep from the shared scan
+constexpr int SHARED_G = 8;               // queries scored per shared work unit (at most)
+constexpr int SHARED_MAX_NSEG = 8;        // rows of at most 8 x 128 bytes use the shared scan
+constexpr uint32_t SHARED_ROWS = 2048;    // rows per shared work unit (at most)
 constexpr int MAX_KC = 16384;             // top-K_c heap held in LDS
 
 // ---------------------------------------------------------------- kernels
@@ -84,6 +89,10 @@ struct PlanArgs {
   int32_t *tile_q;       // [nq x MAX_TILES_PER_QUERY]
   int32_t *tile_c0;
   int32_t *counter;      // work counter of the refinement kernel
+  uint32_t *rfull;       // [nq] rows of the whole list, may be null
+  const int32_t *qmask;  // [nq] only queries with qmask[q] != 0 get tiles, may be null
+  const uint32_t *own_hist;  // with own_cseed: a cluster at list position i counts only if
+  const int32_t *own_cseed;  // i < own_cseed[q] or own_hist[cluster] <= 1
 };
 
 struct RefineArgs {
@@ -118,7 +127,53 @@ struct MergeArgs {
   int64_t *out_ids;
   float *out_dists;
   int32_t *qstats;
+  const int32_t *qmask;  // only queries with qmask[q] != 0 are written, may be null
 };
+
+// batch-shared refinement: a candidate row listed by several queries of the
+// batch is read once and scored for all of them
+struct SharedArgs {
+  int64_t nq;
+  int k, is_u8, row_bytes;
+  int g;                      // queries per work unit (<= SHARED_G)
+  uint32_t seed_min;          // rows the leading clusters of a list cover at least
+  int64_t n_clusters;
+  const void *rows;
+  const int64_t *row_ids;
+  const uint64_t *cl_off;
+  const void *queries;
+  const uint32_t *clus;
+  const int32_t *nclus;
+  int64_t cap;
+  int32_t *cseed;             // [nq] leading clusters, always scored by the query's own pass
+  uint32_t *rfull;            // [nq] rows of the whole list
+  const uint32_t *rtot;       // [nq] rows of the own pass
+  const int32_t *tile_off;    // [nq + 1] tiles of the own pass
+  const int64_t *own_ids;     // [nq x k] top-k of the own pass (sorted)
+  const float *own_dists;
+  uint32_t *own_rows;         // [nq] copy of rtot kept for diagnostics
+  uint32_t *hist;             // [n_clusters + 1] pairs per cluster past the leading clusters
+  uint32_t *cnt2;             // [n_clusters + 1] pairs of shared clusters (hist >= 2), else 0
+  uint32_t *hoff;             // [n_clusters + 1] exclusive scan of cnt2
+  uint32_t *isshared;         // [n_clusters + 1] 1 for a shared cluster
+  uint32_t *spos;             // [n_clusters + 1] exclusive scan of isshared
+  uint32_t *slist;            // [n_clusters] shared clusters in cluster order
+  uint64_t *swork;            // [n_clusters + 1] rows x query groups of slist[i], 0 past the list
+  uint64_t *swork_off;        // [n_clusters + 1] exclusive scan of swork
+  uint32_t *pair_q;           // [pairs] query of each shared pair, grouped by cluster
+  int32_t *scnt;              // [nq] survivors appended
+  uint32_t *skey;             // [nq x SURVIVOR_CAP]
+  int64_t *sid;
+  int32_t *flag;              // [nq] 1: survivors overflowed, recompute per query
+  unsigned long long *counter;  // work-unit counter
+  int64_t *wstats;            // [2] unique shared rows, own-pass tiles
+  void *scan_tmp;
+  size_t scan_tmp_bytes;
+  int64_t *out_ids;
+  float *out_dists;
+  int32_t *qstats;
+};
+
 
 hipError_t launch_encode_layer(const EncodeLayerArgs &a, hipStream_t s);
 hipError_t launch_probe(const ProbeArgs &a, hipStream_t s);
@@ -127,6 +182,15 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
+size_t shared_scan_tmp_bytes(int64_t n_clusters);
+int shared_group(int row_bytes);
+hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s);
+hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s);
+hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStream_t s);
+hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s);
+hipError_t launch_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int64_t n_clusters,
+                              int64_t *out, hipStream_t s);
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 
 hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, int n_cu,
                               hipStream_t s);

@@ -22,8 +22,9 @@ pytestmark = pytest.mark.gpu
 GATE = dict(m_x=[0.0, 1.0], m_y=[0.5, 2.0])
 
 
-@pytest.mark.parametrize("cfg,P", [(4, 640), (3, 256)])
-def test_full_size_sampled_queries(cfg, P):
+@pytest.mark.parametrize("cfg,P,mode", [(4, 640, NR.NR_REFINE_AUTO), (4, 640, NR.NR_REFINE_PER_QUERY),
+                                         (3, 256, NR.NR_REFINE_AUTO)])
+def test_full_size_sampled_queries(cfg, P, mode):
     if not torch.cuda.is_available():
         pytest.skip("no HIP device")
     dev = torch.device("cuda")
@@ -37,7 +38,7 @@ def test_full_size_sampled_queries(cfg, P):
         e = ix.encoder
         enc = O.Encoder(e.weights, e.biases, input_scale=e.input_scale)
         lg, mag = O.encode(enc, Qh, with_mag=True)
-        params = NR.Params(l_sel=16, r_max=w.r_max, k_c=w.k_c, **GATE)
+        params = NR.Params(l_sel=16, r_max=w.r_max, k_c=w.k_c, refine_mode=mode, **GATE)
         ids, dists = gix.nr_search(Q, w.k, P, params, logits=torch.from_numpy(lg).to(dev))
         ids, dists = ids.cpu().numpy(), dists.cpu().numpy()
         # a seeded sample spread over the batch

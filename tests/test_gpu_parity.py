@@ -162,12 +162,16 @@ def test_refine_given_clusters(dev, name, k):
 
 
 # ------------------------------------------------------------------ whole path
+MODES = {"per_query": NR.NR_REFINE_PER_QUERY, "shared": NR.NR_REFINE_SHARED}
+
+
+@pytest.mark.parametrize("mode", list(MODES))
 @pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("pset", ["default", "no_gate_no_stop", "small_heap_fast_stop", "binned"])
 @pytest.mark.parametrize("P", [1, 16, 256])
-def test_search_given_logits_bit_exact(dev, name, pset, P):
+def test_search_given_logits_bit_exact(dev, name, pset, P, mode):
     c = setup_case(name, dev)
-    p = default_params(c, **PARAM_SETS[pset])
+    p = default_params(c, refine_mode=MODES[mode], **PARAM_SETS[pset])
     gi, gd = c["gix"].nr_search(c["Qd"], 10, P, p, logits=c["lgd"])
     ix = c["ix"]
     oi, od, _, _ = O.search(c["enc"], ix.tau, ix.rows, ix.row_ids, ix.bc_off, ix.cl_off,
@@ -176,9 +180,11 @@ def test_search_given_logits_bit_exact(dev, name, pset, P):
     _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
 
 
-def test_full_budget_search_is_exact_knn(dev):
+@pytest.mark.parametrize("mode", list(MODES))
+def test_full_budget_search_is_exact_knn(dev, mode):
     c = setup_case("tiny", dev)
-    p = default_params(c, l_sel=8, r_max=8, gate_on=False, early_stop_on=False, k_c=10 ** 9)
+    p = default_params(c, l_sel=8, r_max=8, gate_on=False, early_stop_on=False, k_c=10 ** 9,
+                       refine_mode=MODES[mode])
     gi, gd = c["gix"].nr_search(c["Qd"], 10, 256, p)
     bi, bd = O.bruteforce(c["X"], c["Q"], 10)
     _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), bi, bd)
@@ -227,10 +233,11 @@ def test_short_lists_are_padded(dev):
         assert np.all(np.isinf(gd[q, m:]))
 
 
-def test_many_queries_span_chunks(dev):
+@pytest.mark.parametrize("mode", list(MODES))
+def test_many_queries_span_chunks(dev, mode):
     """More queries than one internal launch sequence handles."""
     c = setup_case("tiny", dev)
-    p = default_params(c)
+    p = default_params(c, refine_mode=MODES[mode])
     reps = 20000 // len(c["Q"]) + 1
     Q = np.tile(c["Q"], (reps, 1))
     lg = np.tile(c["lg"], (reps, 1))
@@ -242,9 +249,10 @@ def test_many_queries_span_chunks(dev):
         assert np.array_equal(gi[r * n0:(r + 1) * n0], gi[:n0])
 
 
-def test_deterministic(dev):
+@pytest.mark.parametrize("mode", list(MODES))
+def test_deterministic(dev, mode):
     c = setup_case("deep", dev)
-    p = default_params(c)
+    p = default_params(c, refine_mode=MODES[mode])
     a = c["gix"].nr_search(c["Qd"], 10, 256, p)
     b = c["gix"].nr_search(c["Qd"], 10, 256, p)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
@@ -290,3 +298,30 @@ def test_corrupt_index_rejected(dev, what):
                  cl_off=torch.from_numpy(cl).to(dev),
                  centroids=torch.from_numpy(ix.centroids).to(dev))
     assert err.value.status == NR.NR_ECORRUPT
+
+
+def test_shared_schedule_overflow_falls_back(dev):
+    """All rows tie and original ids fall along the rows, so after the leading
+    clusters nearly every row beats the leading top-k's last (distance, id):
+    the survivor list overflows and the query is recomputed per query."""
+    n, d, n_cl = 20000, 16, 50
+    rows = np.zeros((n, d), np.uint8)
+    row_ids = np.arange(n - 1, -1, -1, dtype=np.int64)
+    bc_off = np.array([0, 0, n_cl], np.int32)
+    cl_off = np.linspace(0, n, n_cl + 1).astype(np.int64)
+    cent = np.zeros((n_cl, 1), np.float32)
+    W = np.zeros((1, d), np.float32)
+    gix = NR.Index(n=n, d=d, dtype=NR.NR_U8, b=1, weights=[W], biases=[np.array([1.0], np.float32)],
+                   input_scale=1.0, tau=np.zeros(1, np.float32),
+                   rows=torch.from_numpy(rows).to(dev), row_ids=torch.from_numpy(row_ids).to(dev),
+                   bc_off=torch.from_numpy(bc_off).to(dev), cl_off=torch.from_numpy(cl_off).to(dev),
+                   centroids=torch.from_numpy(cent).to(dev))
+    Q = torch.zeros((600, d), dtype=torch.uint8, device=dev)
+    base = dict(l_sel=1, r_max=1, k_c=n_cl, gate_on=False, early_stop_on=False)
+    a = gix.nr_search(Q, 10, 2, NR.Params(refine_mode=NR.NR_REFINE_SHARED, **base))
+    b = gix.nr_search(Q, 10, 2, NR.Params(refine_mode=NR.NR_REFINE_PER_QUERY, **base))
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    assert a[0][0].tolist() == list(range(10))          # smallest ids, distance 0
+    tiles, rows_, read = gix.nr_last_work()
+    assert rows_ == 600 * n
+    gix.close()
