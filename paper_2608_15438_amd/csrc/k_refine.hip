@@ -63,32 +63,48 @@ __global__ void __launch_bounds__(256) k_plan_rows(PlanArgs a) {
   uint32_t *pre = a.rowpre + q * (a.cap + 1);
   uint64_t run = 0;
   const int own0 = a.own_hist ? a.own_cseed[q] : 0;
+  // own pass of the shared schedule: keep only the clusters that count, compacted
+  uint32_t *co = a.clus_out ? a.clus_out + q * a.cap : nullptr;
+  int nout = 0;
   if (lane == 0) pre[0] = 0;
   for (int i0 = 0; i0 < n; i0 += WAVE) {
     const int i = i0 + lane;
+    uint32_t c = 0;
     uint64_t sz = 0;
     if (i < n) {
-      const uint32_t c = cl[i];
+      c = cl[i];
       if (c < a.n_clusters) {
         sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
-        // the own pass of the shared schedule leaves shared clusters to the shared scan
+        // the own pass leaves shared clusters to the shared scan
         if (a.own_hist && i >= own0 && a.own_hist[c] > 1) sz = 0;
       }
     }
     const uint64_t incl = wave_incl_scan_u64(sz);
-    if (i < n) pre[i + 1] = (uint32_t)(run + incl);
+    if (co) {
+      const uint64_t keep = ballot(sz > 0);
+      const int pos = nout + popc64(keep & lanemask_lt());
+      if (sz > 0) {
+        co[pos] = c;
+        pre[pos + 1] = (uint32_t)(run + incl);
+      }
+      nout += popc64(keep);
+    } else if (i < n) {
+      pre[i + 1] = (uint32_t)(run + incl);
+    }
     run += bcast_u64(incl, WAVE - 1);
   }
   if (lane == 0) {
     // a list of more than 2^32 - 1 rows (only possible with repeated clusters
     // given to nr_refine) is refused: it returns no candidates
     const uint32_t tot = run > 0xffffffffull ? 0u : (uint32_t)run;
+    const uint32_t tmin = a.tile_min ? a.tile_min : TILE_MIN_ROWS;
     uint32_t t = (tot + MAX_TILES_PER_QUERY - 1) / MAX_TILES_PER_QUERY;
-    if (t < TILE_MIN_ROWS) t = TILE_MIN_ROWS;
+    if (t < tmin) t = tmin;
     a.rtot[q] = tot;
     a.tsize[q] = t;
     a.ntile[q] = (int32_t)(((uint64_t)tot + t - 1) / t);
     if (a.rfull) a.rfull[q] = tot;
+    if (co) a.nclus_out[q] = nout;
   }
 }
 
@@ -129,7 +145,7 @@ __global__ void __launch_bounds__(256) k_plan_tiles(PlanArgs a) {
   const uint32_t v0 = (uint32_t)t * a.tsize[q];
   const uint32_t *pre = a.rowpre + q * (a.cap + 1);
   // last cluster i with pre[i] <= v0 (clusters of zero rows are skipped)
-  int lo = 0, hi = clamp_count(a.nclus[q], a.cap) - 1;
+  int lo = 0, hi = clamp_count(a.clus_out ? a.nclus_out[q] : a.nclus[q], a.cap) - 1;
   while (lo < hi) {
     int mid = (lo + hi + 1) >> 1;
     if (pre[mid] <= v0) lo = mid; else hi = mid - 1;

@@ -88,13 +88,8 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
   return hipGetLastError();
 }
 
-// queries per work unit: the g query slices of a lane take g * NSEG * 4 VGPRs
-int shared_group(int row_bytes) {
-  const int nseg = (row_bytes + 127) / 128;
-  if (nseg <= 1) return 8;
-  if (nseg <= 4) return 4;
-  return 2;
-}
+// queries per work unit (their rows are staged in LDS)
+int shared_group(int) { return SHARED_G; }
 
 // ------------------------------------------------------------------ hist
 // one wave per query: full rows, leading clusters, pair counts of the rest
@@ -219,9 +214,17 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
 // that start inside it, so each unit belongs to exactly one tile.
 template <int IS_U8, int NSEG, int G, int U>
 __global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
+  constexpr int QCH = NSEG * 8;  // 16-byte chunks per query row (padded to 128-byte segments)
+  __shared__ uint4 s_qv[4][G * QCH];
+  __shared__ int32_t s_thr[4][G];
+  __shared__ int32_t s_qq[4][G];
   const int lane = lane_id();
+  const int w = threadIdx.x >> 6;
   const int grp = lane >> 3;  // lane group: one row at a time
   const int gl = lane & 7;    // 16-byte slot inside a 128-byte segment
+  uint4 *qs = s_qv[w];
+  int32_t *thr_s = s_thr[w];
+  int32_t *qq_s = s_qq[w];
   const int64_t NS = a.spos[a.n_clusters];
   const uint64_t W = a.swork_off[a.n_clusters];
   const uint64_t ntiles = (W + SHARED_TILE - 1) / SHARED_TILE;
@@ -276,11 +279,15 @@ __global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
     uint32_t hp = bcast_u32(l_hp, 0), mq = bcast_u32(l_m, 0);
     uint64_t nch = (sz + SHARED_ROWS - 1) / SHARED_ROWS;
     uint32_t ng = (mq + G - 1) / G;
-    // the first unit of entry i that starts at or after ws
-    const uint64_t rel = ws - wo;
-    uint32_t gi = (uint32_t)(rel / sz);
-    const uint64_t rr = rel - (uint64_t)gi * sz;
-    uint64_t ch = (rr + SHARED_ROWS - 1) / SHARED_ROWS;
+    // the first unit of entry i that starts at or after ws (the entry holding
+    // ws has work, so sz > 0; the guard keeps the division defined regardless)
+    uint32_t gi = 0;
+    uint64_t ch = 0;
+    if (sz > 0) {
+      const uint64_t rel = ws - wo;
+      gi = (uint32_t)(rel / sz);
+      ch = (rel - (uint64_t)gi * sz + SHARED_ROWS - 1) / SHARED_ROWS;
+    }
     bool have = true;
     auto next_entry = [&]() {
       do {
@@ -305,7 +312,9 @@ __global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
       gi = 0;
       ch = 0;
     };
-    if (ch >= nch) {
+    if (sz == 0) {
+      next_entry();
+    } else if (ch >= nch) {
       ch = 0;
       if (++gi >= ng) next_entry();
     }
@@ -334,34 +343,61 @@ __global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
         }
       };
       load_rows(r0);
-      uint4 qv[G][NSEG];
-      uint32_t qid[G], tkey[G];
-      int64_t tid[G];
+      // lane j < gm: query j of the unit and the k-th key of its own pass
+      uint32_t my_q = 0, my_bound = 0xffffffffu;
+      if (lane < gm) {
+        my_q = a.pair_q[p0 + lane];
+        const int64_t id = a.own_ids[(int64_t)my_q * k + k - 1];
+        const float d = a.own_dists[(int64_t)my_q * k + k - 1];
+        if (id >= 0) my_bound = a.is_u8 ? (uint32_t)d : __float_as_uint(d);
+      }
+      // the unit's query rows into LDS (zero past gm and past the row)
+      static_assert((G * QCH) % WAVE == 0, "query staging covers whole waves");
 #pragma unroll
-      for (int j = 0; j < G; ++j) {
-        qid[j] = j < gm ? a.pair_q[p0 + j] : 0u;
-        const unsigned char *qp = queries + (uint64_t)qid[j] * (uint64_t)rb;
+      for (int c0 = 0; c0 < G * QCH; c0 += WAVE) {
+        const int c = c0 + lane;
+        const int j = c / QCH;
+        const int off = (c - j * QCH) * 16;
+        const uint32_t qj = (uint32_t)__shfl((int)my_q, j);
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (j < gm && off < rb) v = *(const uint4 *)(queries + (uint64_t)qj * rb + off);
+        qs[c] = v;
+      }
+      __builtin_amdgcn_wave_barrier();
+      // per query: |q|^2 (uint8) and the bound the scan compares with:
+      // uint8 keys are |x|^2 - 2 x.q + |q|^2, compared as |x|^2 - 2 x.q <= bound - |q|^2
+      for (int j = 0; j < gm; ++j) {
+        int32_t qq = 0;
+        if (IS_U8) {
+          uint32_t acc = 0;
 #pragma unroll
-        for (int s = 0; s < NSEG; ++s) {
-          const int off = 128 * s + 16 * gl;
-          qv[j][s] = (j < gm && off < rb) ? *(const uint4 *)(qp + off) : make_uint4(0, 0, 0, 0);
-        }
-        tkey[j] = 0xffffffffu;
-        tid[j] = INT64_MAX;
-        if (j < gm) {
-          const int64_t id = a.own_ids[(int64_t)qid[j] * k + k - 1];
-          const float d = a.own_dists[(int64_t)qid[j] * k + k - 1];
-          if (id >= 0) {
-            tkey[j] = a.is_u8 ? (uint32_t)d : __float_as_uint(d);
-            tid[j] = id;
+          for (int s = 0; s < NSEG; ++s) {
+            const uint4 q4 = qs[j * QCH + s * 8 + gl];
+            acc = __builtin_amdgcn_udot4(q4.x, q4.x, acc, false);
+            acc = __builtin_amdgcn_udot4(q4.y, q4.y, acc, false);
+            acc = __builtin_amdgcn_udot4(q4.z, q4.z, acc, false);
+            acc = __builtin_amdgcn_udot4(q4.w, q4.w, acc, false);
           }
+          qq = group8_sum((int32_t)acc);
+        }
+        const uint32_t bound = bcast_u32(my_bound, j);
+        int32_t th;
+        if (IS_U8)
+          th = bound == 0xffffffffu ? INT32_MAX : (int32_t)((int64_t)bound - qq);
+        else
+          th = (int32_t)bound;
+        if (lane == 0) {
+          thr_s[j] = th;
+          qq_s[j] = qq;
         }
       }
+      __builtin_amdgcn_wave_barrier();
 
       for (uint64_t rb0 = r0; rb0 < r1; rb0 += 8 * U) {
+        int32_t xx[U];
 #pragma unroll
         for (int uu = 0; uu < U; ++uu) {
-          int32_t xx = 0;
+          xx[uu] = 0;
           if (IS_U8) {
             uint32_t acc = 0;
 #pragma unroll
@@ -371,51 +407,60 @@ __global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
               acc = __builtin_amdgcn_udot4(xv[uu][s].z, xv[uu][s].z, acc, false);
               acc = __builtin_amdgcn_udot4(xv[uu][s].w, xv[uu][s].w, acc, false);
             }
-            xx = (int32_t)acc;
+            xx[uu] = (int32_t)acc;
           }
+        }
+        for (int j = 0; j < gm; ++j) {
+          uint4 qv[NSEG];
 #pragma unroll
-          for (int j = 0; j < G; ++j) {
-            if (j >= gm) break;
-            uint32_t key;
+          for (int s = 0; s < NSEG; ++s) qv[s] = qs[j * QCH + s * 8 + gl];
+          const int32_t th = thr_s[j];
+          uint32_t key[U];    // uint8: |x|^2 - 2 x.q; fp32: the distance (bits)
+          uint32_t cand = 0;  // bit uu: row uu ranks at or before query j's bound
+#pragma unroll
+          for (int uu = 0; uu < U; ++uu) {
             if (IS_U8) {
-              // this lane's part of |x|^2 - 2 x.q + |q|^2, exact in int32
-              uint32_t xq = 0, qq = 0;
+              uint32_t xq = 0;
 #pragma unroll
               for (int s = 0; s < NSEG; ++s) {
-                xq = __builtin_amdgcn_udot4(xv[uu][s].x, qv[j][s].x, xq, false);
-                xq = __builtin_amdgcn_udot4(xv[uu][s].y, qv[j][s].y, xq, false);
-                xq = __builtin_amdgcn_udot4(xv[uu][s].z, qv[j][s].z, xq, false);
-                xq = __builtin_amdgcn_udot4(xv[uu][s].w, qv[j][s].w, xq, false);
-                qq = __builtin_amdgcn_udot4(qv[j][s].x, qv[j][s].x, qq, false);
-                qq = __builtin_amdgcn_udot4(qv[j][s].y, qv[j][s].y, qq, false);
-                qq = __builtin_amdgcn_udot4(qv[j][s].z, qv[j][s].z, qq, false);
-                qq = __builtin_amdgcn_udot4(qv[j][s].w, qv[j][s].w, qq, false);
+                xq = __builtin_amdgcn_udot4(xv[uu][s].x, qv[s].x, xq, false);
+                xq = __builtin_amdgcn_udot4(xv[uu][s].y, qv[s].y, xq, false);
+                xq = __builtin_amdgcn_udot4(xv[uu][s].z, qv[s].z, xq, false);
+                xq = __builtin_amdgcn_udot4(xv[uu][s].w, qv[s].w, xq, false);
               }
-              key = (uint32_t)group8_sum(xx - 2 * (int32_t)xq + (int32_t)qq);
+              const int32_t part = group8_sum(xx[uu] - 2 * (int32_t)xq);
+              key[uu] = (uint32_t)part;
+              cand |= (ok[uu] && part <= th ? 1u : 0u) << uu;
             } else {
               float acc = 0.0f;
 #pragma unroll
               for (int s = 0; s < NSEG; ++s) {
-                const float t0 = __uint_as_float(xv[uu][s].x) - __uint_as_float(qv[j][s].x);
-                const float t1 = __uint_as_float(xv[uu][s].y) - __uint_as_float(qv[j][s].y);
-                const float t2 = __uint_as_float(xv[uu][s].z) - __uint_as_float(qv[j][s].z);
-                const float t3 = __uint_as_float(xv[uu][s].w) - __uint_as_float(qv[j][s].w);
+                const float t0 = __uint_as_float(xv[uu][s].x) - __uint_as_float(qv[s].x);
+                const float t1 = __uint_as_float(xv[uu][s].y) - __uint_as_float(qv[s].y);
+                const float t2 = __uint_as_float(xv[uu][s].z) - __uint_as_float(qv[s].z);
+                const float t3 = __uint_as_float(xv[uu][s].w) - __uint_as_float(qv[s].w);
                 acc = fmaf(t0, t0, acc);
                 acc = fmaf(t1, t1, acc);
                 acc = fmaf(t2, t2, acc);
                 acc = fmaf(t3, t3, acc);
               }
-              key = __float_as_uint(group8_sum(acc));
+              key[uu] = __float_as_uint(group8_sum(acc));
+              cand |= (ok[uu] && key[uu] <= (uint32_t)th ? 1u : 0u) << uu;
             }
-            // the row can enter this query's result only if it ranks before the bound
-            if (ok[uu] && gl == 0 && key <= tkey[j]) {
-              const uint64_t r = rb0 + 8 * uu + grp;
-              const int64_t id = a.row_ids[r];
-              if (key < tkey[j] || id < tid[j]) {
-                const uint32_t q = qid[j];
+          }
+          if (gl != 0) cand = 0;
+          // rare: survivors (ties at the bound included; the merge orders them)
+          if (cand) {
+            const uint32_t q = (uint32_t)__builtin_amdgcn_readlane((int)my_q, j);
+            const int32_t qq = qq_s[j];
+#pragma unroll
+            for (int uu = 0; uu < U; ++uu) {
+              if ((cand >> uu) & 1u) {
+                const int64_t id = a.row_ids[rb0 + 8 * uu + grp];
                 const int pos = atomicAdd(&a.scnt[q], 1);
                 if (pos < SURVIVOR_CAP) {
-                  a.skey[(int64_t)q * SURVIVOR_CAP + pos] = key;
+                  a.skey[(int64_t)q * SURVIVOR_CAP + pos] =
+                      IS_U8 ? (uint32_t)((int32_t)key[uu] + qq) : key[uu];
                   a.sid[(int64_t)q * SURVIVOR_CAP + pos] = id;
                 }
               }
@@ -424,6 +469,7 @@ __global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
         }
         if (rb0 + 8 * U < r1) load_rows(rb0 + 8 * U);
       }
+      __builtin_amdgcn_wave_barrier();
       // next unit
       if (++ch >= nch) {
         ch = 0;
@@ -442,9 +488,9 @@ static hipError_t launch_shared_t(const SharedArgs &a, int nseg, int grid, hipSt
     return hipGetLastError();                                                                   \
   }
   NR_SHARED_CASE(1, 8, NR_SHARED_U1)
-  NR_SHARED_CASE(2, 4, 4)
-  NR_SHARED_CASE(4, 4, 2)
-  NR_SHARED_CASE(8, 2, 1)
+  NR_SHARED_CASE(2, 8, 4)
+  NR_SHARED_CASE(4, 8, 2)
+  NR_SHARED_CASE(8, 8, 1)
 #undef NR_SHARED_CASE
   return hipErrorInvalidValue;
 }

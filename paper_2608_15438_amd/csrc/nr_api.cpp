@@ -65,6 +65,8 @@ struct Buffers {
   // shared refinement
   int64_t *own_ids;
   float *own_dists;
+  uint32_t *clus_own;
+  int32_t *nclus_own;
   int32_t *cseed;
   uint32_t *rfull, *own_rows;
   int32_t *scnt, *flag;
@@ -116,6 +118,8 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     const size_t nc1 = (size_t)s.n_clusters + 1;
     B.own_ids = c.take<int64_t>((size_t)s.nq * s.k);
     B.own_dists = c.take<float>((size_t)s.nq * s.k);
+    B.clus_own = c.take<uint32_t>((size_t)s.nq * s.cap);
+    B.nclus_own = c.take<int32_t>((size_t)s.nq);
     B.cseed = c.take<int32_t>((size_t)s.nq);
     B.own_rows = c.take<uint32_t>((size_t)s.nq);
     B.scnt = c.take<int32_t>((size_t)s.nq);
@@ -373,6 +377,11 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   pa.qmask = o.qmask;
   pa.own_hist = o.own_hist;
   pa.own_cseed = o.own_cseed;
+  if (o.own_hist) {
+    pa.clus_out = B.clus_own;
+    pa.nclus_out = B.nclus_own;
+    pa.tile_min = nr::OWN_TILE_MIN_ROWS;
+  }
   hipError_t e = nr::launch_plan(pa, s);
   if (e != hipSuccess) return e;
   if (ev_plan) (void)hipEventRecord(*ev_plan, s);
@@ -386,8 +395,8 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   ra.d = ix->d.d;
   ra.row_bytes = (int)(ix->d.d * elem_size(ix));
   ra.k = k;
-  ra.clus = clus;
-  ra.nclus = nclus;
+  ra.clus = o.own_hist ? B.clus_own : clus;
+  ra.nclus = o.own_hist ? B.nclus_own : nclus;
   ra.cap = cap;
   ra.rowpre = B.rowpre;
   ra.rtot = B.rtot;

@@ -20,8 +20,15 @@ constexpr int MAX_TILES_PER_QUERY = NR_MAX_TILES_PER_QUERY;  // refinement tiles
 constexpr int TILE_MIN_ROWS = NR_TILE_MIN_ROWS;  // smallest refinement tile
 constexpr int STAGE_CLUSTERS = 128;       // clusters staged in LDS per refinement wave
 constexpr int64_t QUERY_CHUNK = 16384;    // queries per internal launch sequence
+#ifndef NR_OWN_TILE_MIN_ROWS
+#define NR_OWN_TILE_MIN_ROWS 2048
+#endif
+constexpr uint32_t OWN_TILE_MIN_ROWS = NR_OWN_TILE_MIN_ROWS;  // smallest tile of the own pass
 constexpr uint32_t SEED_ROWS = 4096;      // rows of a query's first clusters refined on their own
-constexpr int SURVIVOR_CAP = 1024;        // candidates a query may keep from the shared scan
+#ifndef NR_SURVIVOR_CAP
+#define NR_SURVIVOR_CAP 2048
+#endif
+constexpr int SURVIVOR_CAP = NR_SURVIVOR_CAP;  // candidates a query may keep from the shared scan
 constexpr int SHARED_G = 8;               // queries scored per shared work unit (at most)
 constexpr int SHARED_MAX_NSEG = 8;        // rows of at most 8 x 128 bytes use the shared scan
 constexpr uint32_t SHARED_ROWS = 2048;    // rows per shared work unit (at most)
@@ -93,6 +100,9 @@ struct PlanArgs {
   const int32_t *qmask;  // [nq] only queries with qmask[q] != 0 get tiles, may be null
   const uint32_t *own_hist;  // with own_cseed: a cluster at list position i counts only if
   const int32_t *own_cseed;  // i < own_cseed[q] or own_hist[cluster] <= 1
+  uint32_t *clus_out;        // with own_hist: [nq x cap] the clusters that count, compacted
+  int32_t *nclus_out;        // [nq]
+  uint32_t tile_min;         // smallest tile (rows); 0: TILE_MIN_ROWS
 };
 
 struct RefineArgs {
