@@ -147,6 +147,22 @@ def copy_calibration(torch, dev, gib=4, reps=5):
     print(json.dumps({"copy_bytes_per_launch": src.numel(), "launches": reps}), flush=True)
 
 
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed counter record
+    (FETCH_SIZE + WRITE_SIZE, each scaled by a copy of known size), or None
+    when there is none or the kernel's sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    from paper_2608_15438_amd.counters import source_digest
+    if rec.get("source_sha256") != source_digest(kernel):
+        log(f"traffic record {os.path.basename(path)} is stale (kernel sources changed)")
+        return None
+    return int(rec["hbm_bytes_per_launch"])
+
+
 def recall_at_k(res, gt, k):
     r = 0.0
     for a, b in zip(res, gt):
@@ -226,7 +242,7 @@ def main():
         torch.cuda.synchronize()
         dt = (time.time() - t0) / reps
         rec = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k) if ng else float("nan")
-        tiles, rows, rows_read = gix.nr_last_work()
+        rows = gix.nr_last_work()["rows"]
         pt = dict(probe_budget=P, recall=round(rec, 5), qps=round(w.n_queries / dt, 1),
                   cand_per_query=round(rows / w.n_queries, 1))
         sweep.append(pt)
@@ -265,18 +281,40 @@ def main():
     wall = time.time() - t0
     stage_ms, n_timed = gix.nr_profile_read(reset=True)
     gix.nr_profile_enable(False)
-    tiles, rows, rows_read = gix.nr_last_work()
+    work = gix.nr_last_work()
+    rows = work["rows"]
     recall = recall_at_k(ids[:ng].cpu().numpy(), gt_ids, k) if ng else float("nan")
     qps = w.n_queries * args.steps / wall
     _, _, qs = gix.nr_search(Q, k, P, params, qstats=True)
     qs = qs.double().mean(0).cpu().numpy()
     per_query = {name: round(float(qs[i]), 2) for name, i in NR.QS.items()}
-    log("per-query means", per_query)
-    refine_ms = stage_ms["refine"] / max(n_timed, 1)
-    alg_bytes = rows * w.row_bytes
-    achieved = alg_bytes / (refine_ms * 1e-3) / 1e9
+    log("per-query means", per_query, "work", work)
+    # the two refinement kernels: algorithmic bytes = rows each reads x row bytes
+    # (one launch of each per search: the batch fits one query chunk)
+    nt = max(n_timed, 1)
+    kernels = {}
+    for kname, stage, nrows in (("k_refine", "refine", work["own_rows"]),
+                                ("k_shared_refine", "shared_scan", work["shared_rows"])):
+        ms = stage_ms[stage] / nt
+        if ms <= 0 or nrows <= 0:
+            continue
+        ab = nrows * w.row_bytes
+        kernels[kname] = {"avg_launch_ms": round(ms, 4), "alg_bytes_per_launch": int(ab),
+                          "rows_per_launch": int(nrows), "achieved_gbs": round(ab / (ms * 1e-3) / 1e9, 1)}
+    dom = max(kernels, key=lambda n: kernels[n]["avg_launch_ms"])
+    refine_ms = kernels[dom]["avg_launch_ms"]
+    alg_bytes = kernels[dom]["alg_bytes_per_launch"]
+    achieved = kernels[dom]["achieved_gbs"]
+    traffic = measured_traffic(dom, w.name)
+    # the whole refinement stage (step 5): every launch from the plan to the merge
+    st5 = sum(stage_ms[x] for x in ("plan", "refine", "merge", "shared_prep", "shared_scan",
+                                    "shared_merge")) / nt
+    b5 = work["rows_read"] * w.row_bytes
+    refine_stage = {"ms": round(st5, 4), "bytes_read": int(b5),
+                    "gbs": round(b5 / (st5 * 1e-3) / 1e9, 1),
+                    "frac_of_peak": round(b5 / (st5 * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     log(f"timed: {args.steps} steps, {wall * 1e3 / args.steps:.2f} ms/step, recall {recall:.4f}, "
-        f"refine {refine_ms:.3f} ms avg, {achieved:.0f} GB/s")
+        f"kernels {kernels}, dominant {dom}")
 
     # ---- CPU baseline: the oracle on a bounded sample (rows staged in host memory)
     cpu = None
@@ -304,12 +342,15 @@ def main():
         "recall_queries": ng,
         "cand_per_query": round(rows / w.n_queries, 1),
         "per_query": per_query,
-        "refine_gbs": round(achieved, 1),
+        "rows_read_per_query": round(work["rows_read"] / w.n_queries, 1),
+        "work": work,
         "stage_ms_per_step": {s: round(v / max(n_timed, 1), 4) for s, v in stage_ms.items()},
-        "roofline": {"bound": "hbm", "kernel": "k_refine", "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "alg_bytes_per_launch": int(alg_bytes),
+                     "traffic": traffic, "alg_bytes_per_launch": int(alg_bytes),
                      "avg_launch_ms": round(refine_ms, 4)},
+        "kernels": kernels,
+        "refine_stage": refine_stage,
         "cpu_baseline": cpu,
         "sweep": sweep,
         "hbm_stream_read_gbs": round(stream_gbs, 1),
@@ -336,7 +377,7 @@ def oracle_baseline(args, w, ix, Q, P, params, torch, dev):
                         early_stop_on=params.early_stop_on, lowq_or=params.lowq_or,
                         m_x=np.array(params.m_x, np.float32), m_y=np.array(params.m_y, np.float32))
 
-    def run(nqs):
+    def run(nqs, min_seconds):
         Qh = Q[:nqs].cpu().numpy()
         # discovery (untimed): the clusters this sample needs
         lg = O.encode(enc, Qh)
@@ -359,30 +400,33 @@ def oracle_baseline(args, w, ix, Q, P, params, torch, dev):
         cnt_all[need] = sizes
         cl2 = np.zeros(ix.n_clusters + 1, np.uint64)
         cl2[1:] = np.cumsum(cnt_all)
-        t0 = time.time()
-        oi, od, ncand, secs = O.search(enc, ix.tau, rows_h, ids_h, bc, cl2, cent, Qh, w.k,
-                                       params.l_sel, params.r_max, P, prm, n_threads=threads)
-        return time.time() - t0, secs, rows_h.nbytes
+        # timed: whole passes over the staged sample until min_seconds have
+        # elapsed (at least one pass)
+        passes, t0 = 0, time.time()
+        while True:
+            oi, od, ncand, secs = O.search(enc, ix.tau, rows_h, ids_h, bc, cl2, cent, Qh, w.k,
+                                           params.l_sel, params.r_max, P, prm, n_threads=threads)
+            passes += 1
+            if time.time() - t0 >= min_seconds:
+                break
+        return (time.time() - t0) / passes, passes, secs, rows_h.nbytes
 
     pilot = min(32, w.n_queries)
-    dt, secs, nbytes = run(pilot)
+    dt, _, secs, nbytes = run(pilot, 0.0)
     per_q = dt / pilot
     nqs = int(min(w.n_queries, max(pilot, args.oracle_seconds / max(per_q, 1e-9)),
                   max(pilot, args.oracle_stage_gb * 1e9 / max(nbytes / pilot, 1.0))))
-    if nqs > pilot:
-        dt, secs, nbytes = run(nqs)
-    else:
-        nqs = pilot
+    dt, passes, secs, nbytes = run(nqs, args.oracle_seconds)
     cpu_qps = nqs / dt
-    log(f"oracle: {nqs} queries on {threads} threads in {dt:.2f}s ({cpu_qps:.1f} QPS), "
-        f"{nbytes / 1e9:.2f} GB staged")
+    log(f"oracle: {nqs} queries x {passes} passes on {threads} threads, {dt:.2f}s per pass "
+        f"({cpu_qps:.1f} QPS), {nbytes / 1e9:.2f} GB staged")
     return {"value": round(cpu_qps, 2), "unit": "queries/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {nqs} queries of the batch, same index and probe budget; rows of "
-                      f"their candidate clusters ({nbytes / 1e9:.2f} GB) staged in host memory "
-                      f"before timing",
-            "seconds": round(dt, 3),
-            "stage_seconds": dict(zip(("encode", "probe", "route", "refine"),
-                                      [round(float(x), 3) for x in secs]))}
+            "sample": f"first {nqs} queries of the batch, same index and probe budget, timed over "
+                      f"{passes} whole passes; rows of their candidate clusters "
+                      f"({nbytes / 1e9:.2f} GB) staged in host memory before timing",
+            "seconds": round(dt * passes, 3),
+            "stage_seconds_last_pass": dict(zip(("encode", "probe", "route", "refine"),
+                                                [round(float(x), 3) for x in secs]))}
 
 
 if __name__ == "__main__":

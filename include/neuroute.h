@@ -129,6 +129,8 @@ typedef struct {
   int32_t early_stop_on;
   int32_t lowq_or;
   int32_t refine_mode;   /* NR_REFINE_AUTO / _PER_QUERY / _SHARED (same results) */
+  int32_t shared_seed_rows; /* shared schedule: rows of each list's leading clusters
+                               kept for the query's own pass (>= k); 0: 4096 */
   int32_t m_knots;
   float m_x[NR_MAX_KNOTS];
   float m_y[NR_MAX_KNOTS];
@@ -207,20 +209,47 @@ nr_status nr_refine(const nr_index *index, const void *queries, int64_t nq, int3
 
 /* Stage timing with HIP events on the launch stream (off by default).
  * nr_profile_read synchronises the recorded events and returns the summed
- * milliseconds per stage {encode, probe, route, plan, refine, merge} and the
- * number of timed searches since the last reset. */
-#define NR_STAGES 6
+ * milliseconds per stage and the number of timed searches since the last
+ * reset.  Stages, in launch order:
+ *   encode, probe, route,
+ *   plan    (per-query tiles; shared schedule: pair counts + own-pass tiles),
+ *   refine  (the per-query refinement kernel; shared schedule: own pass),
+ *   merge   (per-query merge; shared schedule: own-pass merge),
+ *   shared_prep, shared_scan, shared_merge (shared schedule only; the last
+ *   includes the per-query redo of queries whose survivors overflowed). */
+#define NR_STAGES 9
 nr_status nr_profile_enable(nr_index *index, int32_t on);
 nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches, int32_t reset);
 
 /* Work of the last search on `stream` (its last query chunk), synchronising
- * the stream: refinement tiles of the per-query kernel, candidate rows summed
- * over queries, and rows the refinement had to read (equal to `rows` for the
- * per-query schedule; for the shared one, the rows of every query's own pass,
- * each row of a shared cluster once, and the whole list again for a query
- * whose survivors overflowed).  Any pointer may be NULL. */
-nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *tiles, int64_t *rows,
-                       int64_t *rows_read);
+ * the stream.  Writes min(n_work, NR_WORK) counters into `work` (host):
+ *   NR_WORK_TILES          tiles of the per-query refinement kernel
+ *   NR_WORK_ROWS           candidate rows summed over queries (sum of |rows of C(q)|)
+ *   NR_WORK_ROWS_READ      rows the refinement read from the index
+ *   NR_WORK_OWN_ROWS       rows refined by the per-query kernel (all of them for
+ *                          the per-query schedule; the own pass for the shared one)
+ *   NR_WORK_SHARED_ROWS    rows of shared clusters, each read once by the scan
+ *   NR_WORK_SHARED_PAIRS   (query, shared cluster) pairs scored by the scan
+ *   NR_WORK_SURVIVORS      rows the scan kept for the merge (before capping)
+ *   NR_WORK_FLAGGED        queries recomputed after their survivors overflowed
+ *   NR_WORK_FALLBACK_ROWS  rows read by that recomputation
+ *   NR_WORK_SHARED_PAIR_ROWS rows scored by the scan, summed over its pairs
+ * ROWS_READ = OWN_ROWS + SHARED_ROWS + FALLBACK_ROWS and
+ * ROWS = OWN_ROWS + SHARED_PAIR_ROWS. */
+enum {
+  NR_WORK_TILES = 0,
+  NR_WORK_ROWS = 1,
+  NR_WORK_ROWS_READ = 2,
+  NR_WORK_OWN_ROWS = 3,
+  NR_WORK_SHARED_ROWS = 4,
+  NR_WORK_SHARED_PAIRS = 5,
+  NR_WORK_SURVIVORS = 6,
+  NR_WORK_FLAGGED = 7,
+  NR_WORK_FALLBACK_ROWS = 8,
+  NR_WORK_SHARED_PAIR_ROWS = 9,
+  NR_WORK = 10
+};
+nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *work, int32_t n_work);
 
 /* Bandwidth self-check (not part of the search): one pass of 16-byte loads
  * over `bytes` (a multiple of 16) of the DEVICE buffer `buf`, on `stream`.

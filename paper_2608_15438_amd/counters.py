@@ -1,0 +1,123 @@
+"""Summaries of rocprofv3 output for the refinement kernels.
+
+    python -m paper_2608_15438_amd.counters stats TRACE_STATS.csv
+        markdown table of the search kernels from a --kernel-trace --stats run
+
+    python -m paper_2608_15438_amd.counters traffic --kernel NAME --workload W \\
+        --fetch F.csv --write W.csv --copy-fetch CF.csv --copy-write CW.csv \\
+        --copy-bytes N [--command TEXT]
+        HBM traffic record (JSON) of one kernel from two --pmc passes
+        (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by what the
+        same counter reads for a device copy of N bytes per launch.
+
+The record carries the sha256 of the kernel's sources, so a reader can tell
+when the kernel changed after the counters were taken.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+KERNEL_SOURCES = {"k_refine": ["k_refine.hip", "nr_internal.h"],
+                  "k_shared_refine": ["k_shared.hip", "nr_internal.h"]}
+
+
+def source_digest(kernel: str) -> str:
+    """sha256 over the sources a refinement kernel is built from."""
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(HERE, "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _rows(path):
+    with open(path, newline="") as fh:
+        return list(csv.DictReader(fh))
+
+
+def per_dispatch(path: str, name_part: str, counter: str) -> list[float]:
+    """Counter value of every dispatch whose kernel name contains name_part."""
+    out = {}
+    for r in _rows(path):
+        if r.get("Counter_Name") != counter or name_part not in r.get("Kernel_Name", ""):
+            continue
+        key = r.get("Dispatch_Id") or r.get("Correlation_Id")
+        out[key] = out.get(key, 0.0) + float(r["Counter_Value"])
+    return list(out.values())
+
+
+def _mean(v):
+    return sum(v) / len(v) if v else float("nan")
+
+
+def traffic(a) -> dict:
+    fetch = per_dispatch(a.fetch, a.kernel, "FETCH_SIZE")
+    write = per_dispatch(a.write, a.kernel, "WRITE_SIZE")
+    cf = per_dispatch(a.copy_fetch, a.copy_kernel, "FETCH_SIZE")
+    cw = per_dispatch(a.copy_write, a.copy_kernel, "WRITE_SIZE")
+    if not (fetch and write and cf and cw):
+        raise SystemExit("a counter pass has no dispatch of the named kernel")
+    kib = 1024.0
+    f_scale = a.copy_bytes / (max(cf) * kib)
+    w_scale = a.copy_bytes / (max(cw) * kib)
+    fb = _mean(fetch) * kib * f_scale
+    wb = _mean(write) * kib * w_scale
+    return {"kernel": a.kernel, "workload": a.workload,
+            "source_sha256": source_digest(a.kernel),
+            "dispatches": {"fetch": len(fetch), "write": len(write)},
+            "fetch_kib_per_launch": round(_mean(fetch), 1),
+            "write_kib_per_launch": round(_mean(write), 1),
+            "copy_bytes_per_launch": a.copy_bytes,
+            "copy_fetch_kib": round(max(cf), 1), "copy_write_kib": round(max(cw), 1),
+            "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+            "hbm_fetch_bytes_per_launch": int(fb), "hbm_write_bytes_per_launch": int(wb),
+            "hbm_bytes_per_launch": int(fb + wb),
+            "command": a.command}
+
+
+def stats(path: str) -> str:
+    keep = ("nr::", "synth", "rocprim")
+    lines = ["| kernel | calls | avg us | min us | max us | total ms |",
+             "|---|---:|---:|---:|---:|---:|"]
+    for r in _rows(path):
+        name = r["Name"]
+        if not any(k in name for k in keep):
+            continue
+        short = name.split("(")[0].replace("void ", "")[:60]
+        lines.append(f"| `{short}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.2f} |")
+    return "\n".join(lines)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("csv")
+    t = sub.add_parser("traffic")
+    t.add_argument("--kernel", required=True, choices=sorted(KERNEL_SOURCES))
+    t.add_argument("--workload", required=True)
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--copy-fetch", required=True)
+    t.add_argument("--copy-write", required=True)
+    t.add_argument("--copy-bytes", type=int, required=True)
+    t.add_argument("--copy-kernel", default="copy")
+    t.add_argument("--command", default="")
+    a = ap.parse_args(argv)
+    if a.cmd == "stats":
+        print(stats(a.csv))
+    else:
+        print(json.dumps(traffic(a), indent=1))
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -601,21 +601,33 @@ hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s) {
 }
 
 // ------------------------------------------------------------------ diagnostics
-// rows of the shared clusters (each read once by the scan)
+// rows of the shared clusters (each read once by the scan) -> out[0] and
+// rows scored by the scan summed over pairs -> out[2]
 __global__ void k_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int64_t n_clusters,
                               int64_t *out) {
-  __shared__ unsigned long long part[256];
-  unsigned long long acc = 0;
+  __shared__ unsigned long long part[2][256];
+  unsigned long long acc = 0, accp = 0;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_clusters; c += stride)
-    if (hoff[c + 1] > hoff[c]) acc += cl_off[c + 1] - cl_off[c];
-  part[threadIdx.x] = acc;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_clusters; c += stride) {
+    const uint32_t m = hoff[c + 1] - hoff[c];
+    const uint64_t sz = cl_off[c + 1] - cl_off[c];
+    if (m > 0) acc += sz;
+    accp += (uint64_t)m * sz;
+  }
+  part[0][threadIdx.x] = acc;
+  part[1][threadIdx.x] = accp;
   __syncthreads();
   for (int o = 128; o > 0; o >>= 1) {
-    if ((int)threadIdx.x < o) part[threadIdx.x] += part[threadIdx.x + o];
+    if ((int)threadIdx.x < o) {
+      part[0][threadIdx.x] += part[0][threadIdx.x + o];
+      part[1][threadIdx.x] += part[1][threadIdx.x + o];
+    }
     __syncthreads();
   }
-  if (threadIdx.x == 0) atomicAdd((unsigned long long *)out, part[0]);
+  if (threadIdx.x == 0) {
+    atomicAdd((unsigned long long *)out, part[0][0]);
+    atomicAdd((unsigned long long *)(out + 2), part[1][0]);
+  }
 }
 
 hipError_t launch_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int64_t n_clusters,

@@ -113,7 +113,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
   B.pid = c.take<int64_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
   B.shared = s.shared;
   B.rfull = c.take<uint32_t>((size_t)s.nq);
-  B.wstats = c.take<int64_t>(2);
+  B.wstats = c.take<int64_t>(3);
   if (s.shared) {
     const size_t nc1 = (size_t)s.n_clusters + 1;
     B.own_ids = c.take<int64_t>((size_t)s.nq * s.k);
@@ -243,6 +243,7 @@ nr_status check_params(const nr_index *ix, int32_t P, const nr_params *p) {
   if (!std::isfinite(p->alpha_front)) return fail(NR_EINVAL, "alpha_front must be finite");
   if (p->refine_mode < NR_REFINE_AUTO || p->refine_mode > NR_REFINE_SHARED)
     return fail(NR_EINVAL, "refine_mode must be 0, 1 or 2");
+  if (p->shared_seed_rows < 0) return fail(NR_EINVAL, "shared_seed_rows must be >= 0");
   return NR_OK;
 }
 
@@ -354,10 +355,11 @@ struct RefineOpts {
   const int32_t *own_cseed = nullptr;
 };
 
+// ev (may be null): events recorded after the plan, the refinement and the merge
 hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, const uint32_t *clus,
                       const int32_t *nclus, int64_t cap, const Buffers &B, int64_t *out_ids,
-                      float *out_dists, int32_t *qstats, hipStream_t s, hipEvent_t *ev_plan,
-                      hipEvent_t *ev_refine, const RefineOpts &o = RefineOpts()) {
+                      float *out_dists, int32_t *qstats, hipStream_t s, hipEvent_t *ev,
+                      const RefineOpts &o = RefineOpts()) {
   nr::PlanArgs pa{};
   pa.nq = nq;
   pa.clus = clus;
@@ -384,7 +386,7 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   }
   hipError_t e = nr::launch_plan(pa, s);
   if (e != hipSuccess) return e;
-  if (ev_plan) (void)hipEventRecord(*ev_plan, s);
+  if (ev) (void)hipEventRecord(ev[0], s);
   nr::RefineArgs ra{};
   ra.rows = ix->d.rows;
   ra.row_ids = ix->d.row_ids;
@@ -409,7 +411,7 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   ra.pid = B.pid;
   e = nr::launch_refine(ra, ix->d.dtype, ix->n_cu, s);
   if (e != hipSuccess) return e;
-  if (ev_refine) (void)hipEventRecord(*ev_refine, s);
+  if (ev) (void)hipEventRecord(ev[1], s);
   nr::MergeArgs ma{};
   ma.nq = nq;
   ma.k = k;
@@ -422,24 +424,28 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   ma.out_dists = out_dists;
   ma.qstats = qstats;
   ma.qmask = o.qmask;
-  return nr::launch_merge(ma, s);
+  e = nr::launch_merge(ma, s);
+  if (e == hipSuccess && ev) (void)hipEventRecord(ev[2], s);
+  return e;
 }
 
 // Step 5 with the batch-shared schedule (k_shared.hip): pair counts, the own
 // pass of every query, cluster-major work units, the shared scan, the merge,
 // and the per-query schedule again for the queries whose survivors overflowed.
-hipError_t run_refine_shared(const nr_index *ix, const void *q, int64_t nq, int k,
-                             const uint32_t *clus, const int32_t *nclus, int64_t cap,
+// ev (may be null): after the own plan, own refinement, own merge, shared
+// prep, shared scan, shared merge.
+hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void *q, int64_t nq,
+                             int k, const uint32_t *clus, const int32_t *nclus, int64_t cap,
                              const Buffers &B, int64_t *out_ids, float *out_dists,
-                             int32_t *qstats, hipStream_t s, hipEvent_t *ev_plan,
-                             hipEvent_t *ev_refine) {
+                             int32_t *qstats, hipStream_t s, hipEvent_t *ev) {
   nr::SharedArgs a{};
   a.nq = nq;
   a.k = k;
   a.is_u8 = ix->d.dtype == NR_U8;
   a.row_bytes = (int)(ix->d.d * elem_size(ix));
   a.g = nr::shared_group(a.row_bytes);
-  a.seed_min = nr::SEED_ROWS > (uint32_t)k ? nr::SEED_ROWS : (uint32_t)k;
+  const uint32_t seed = p->shared_seed_rows > 0 ? (uint32_t)p->shared_seed_rows : nr::SEED_ROWS;
+  a.seed_min = seed > (uint32_t)k ? seed : (uint32_t)k;
   a.n_clusters = ix->d.n_clusters;
   a.rows = ix->d.rows;
   a.row_ids = ix->d.row_ids;
@@ -480,20 +486,21 @@ hipError_t run_refine_shared(const nr_index *ix, const void *q, int64_t nq, int 
   RefineOpts own;
   own.own_hist = B.hist;
   own.own_cseed = B.cseed;
-  e = run_refine(ix, q, nq, k, clus, nclus, cap, B, B.own_ids, B.own_dists, qstats, s, ev_plan,
-                 nullptr, own);
+  e = run_refine(ix, q, nq, k, clus, nclus, cap, B, B.own_ids, B.own_dists, qstats, s, ev, own);
   if (e != hipSuccess) return e;
   e = nr::launch_shared_prep(a, s);
   if (e != hipSuccess) return e;
+  if (ev) (void)hipEventRecord(ev[3], s);
   e = nr::launch_shared_refine(a, ix->d.dtype, ix->n_cu, s);
   if (e != hipSuccess) return e;
-  if (ev_refine) (void)hipEventRecord(*ev_refine, s);
+  if (ev) (void)hipEventRecord(ev[4], s);
   e = nr::launch_shared_merge(a, s);
   if (e != hipSuccess) return e;
   RefineOpts fb;
   fb.qmask = B.flag;
-  return run_refine(ix, q, nq, k, clus, nclus, cap, B, out_ids, out_dists, qstats, s, nullptr,
-                    nullptr, fb);
+  e = run_refine(ix, q, nq, k, clus, nclus, cap, B, out_ids, out_dists, qstats, s, nullptr, fb);
+  if (e == hipSuccess && ev) (void)hipEventRecord(ev[5], s);
+  return e;
 }
 
 bool use_shared(const nr_index *ix, const nr_params *p, int64_t nq) {
@@ -745,7 +752,7 @@ nr_status nr_refine(const nr_index *cix, const void *queries, int64_t nq, int32_
     int64_t n = nq - q0 < sh.nq ? nq - q0 : sh.nq;
     HIP_OK(run_refine(ix, (const char *)queries + q0 * ix->d.d * elem_size(ix), n, k,
                       clusters + q0 * cap, n_clusters + q0, cap, B, out_ids + q0 * k,
-                      out_dists + q0 * k, nullptr, stream, nullptr, nullptr));
+                      out_dists + q0 * k, nullptr, stream, nullptr));
   }
   w->last = B;
   w->last_nq = nq - (nq - 1) / sh.nq * sh.nq;
@@ -789,16 +796,16 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
     if (prof) HIP_OK(hipEventRecord(es.ev[2], stream));
     HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, qs, stream));
     if (prof) HIP_OK(hipEventRecord(es.ev[3], stream));
-    if (B.shared)
-      HIP_OK(run_refine_shared(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
-                               out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr,
-                               prof ? &es.ev[5] : nullptr));
-    else
+    if (B.shared) {
+      HIP_OK(run_refine_shared(ix, p, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
+                               out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr));
+    } else {
       HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
-                        out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr,
-                        prof ? &es.ev[5] : nullptr));
+                        out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr));
+      if (prof)
+        for (int i = 7; i <= NR_STAGES; ++i) HIP_OK(hipEventRecord(es.ev[i], stream));
+    }
     if (prof) {
-      HIP_OK(hipEventRecord(es.ev[6], stream));
       std::lock_guard<std::mutex> g(ix->mu);
       ix->pending.push_back(es);
     }
@@ -844,9 +851,9 @@ nr_status nr_profile_read(nr_index *ix, double *stage_ms, int64_t *n_searches, i
   return NR_OK;
 }
 
-nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *tiles, int64_t *rows,
-                       int64_t *rows_read) {
+nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t n_work) {
   if (nr_status s = check_index(ix)) return s;
+  if (!work || n_work < 0) return fail(NR_EINVAL, "work must be a host array");
   Workspace *w = nullptr;
   {
     std::lock_guard<std::mutex> g(ix->mu);
@@ -857,32 +864,45 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *tiles, int64_t
   const Buffers &B = w->last;
   const size_t nq = (size_t)w->last_nq;
   if (B.shared) {
-    HIP_OK(nr::launch_fill_i32((int32_t *)B.wstats, 2, 0, stream));
+    HIP_OK(nr::launch_fill_i32((int32_t *)B.wstats, 2, 0, stream));      // wstats[0]
+    HIP_OK(nr::launch_fill_i32((int32_t *)(B.wstats + 2), 2, 0, stream));  // wstats[2]
     HIP_OK(nr::launch_unique_rows(B.hoff, ix->d.cl_off, ix->d.n_clusters, B.wstats, stream));
   }
   HIP_OK(hipStreamSynchronize(stream));
+  int64_t v[NR_WORK] = {0};
   int32_t t = 0;
   HIP_OK(hipMemcpy(&t, B.tile_off + nq, 4, hipMemcpyDeviceToHost));
   std::vector<uint32_t> full(nq);
   HIP_OK(hipMemcpy(full.data(), B.rfull, 4 * nq, hipMemcpyDeviceToHost));
-  int64_t sum_full = 0;
-  for (uint32_t v : full) sum_full += v;
-  int64_t read = sum_full;
+  for (uint32_t x : full) v[NR_WORK_ROWS] += x;
+  v[NR_WORK_TILES] = t;
+  v[NR_WORK_OWN_ROWS] = v[NR_WORK_ROWS];
   if (B.shared) {
-    // own pass + each shared cluster once + the per-query redo of flagged queries
-    int64_t ws[2] = {0, 0};
+    int64_t ws[3] = {0, 0, 0};
+    uint32_t pairs = 0;
     HIP_OK(hipMemcpy(ws, B.wstats, sizeof(ws), hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(&pairs, B.hoff + ix->d.n_clusters, 4, hipMemcpyDeviceToHost));
     std::vector<uint32_t> own(nq);
-    std::vector<int32_t> flag(nq);
+    std::vector<int32_t> flag(nq), scnt(nq);
     HIP_OK(hipMemcpy(own.data(), B.own_rows, 4 * nq, hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(flag.data(), B.flag, 4 * nq, hipMemcpyDeviceToHost));
-    read = ws[0];
-    for (size_t i = 0; i < nq; ++i) read += own[i] + (flag[i] ? full[i] : 0u);
-    t += (int32_t)ws[1];
+    HIP_OK(hipMemcpy(scnt.data(), B.scnt, 4 * nq, hipMemcpyDeviceToHost));
+    v[NR_WORK_TILES] += ws[1];
+    v[NR_WORK_OWN_ROWS] = 0;
+    for (size_t i = 0; i < nq; ++i) {
+      v[NR_WORK_OWN_ROWS] += own[i];
+      v[NR_WORK_SURVIVORS] += scnt[i];
+      if (flag[i]) {
+        v[NR_WORK_FLAGGED] += 1;
+        v[NR_WORK_FALLBACK_ROWS] += full[i];
+      }
+    }
+    v[NR_WORK_SHARED_ROWS] = ws[0];
+    v[NR_WORK_SHARED_PAIRS] = pairs;
+    v[NR_WORK_SHARED_PAIR_ROWS] = ws[2];
   }
-  if (tiles) *tiles = t;
-  if (rows) *rows = sum_full;
-  if (rows_read) *rows_read = read;
+  v[NR_WORK_ROWS_READ] = v[NR_WORK_OWN_ROWS] + v[NR_WORK_SHARED_ROWS] + v[NR_WORK_FALLBACK_ROWS];
+  for (int i = 0; i < n_work && i < NR_WORK; ++i) work[i] = v[i];
   return NR_OK;
 }
 

@@ -24,9 +24,12 @@ constexpr int64_t QUERY_CHUNK = 16384;    // queries per internal launch sequenc
 #define NR_OWN_TILE_MIN_ROWS 2048
 #endif
 constexpr uint32_t OWN_TILE_MIN_ROWS = NR_OWN_TILE_MIN_ROWS;  // smallest tile of the own pass
-constexpr uint32_t SEED_ROWS = 4096;      // rows of a query's first clusters refined on their own
+#ifndef NR_SEED_ROWS
+#define NR_SEED_ROWS 4096
+#endif
+constexpr uint32_t SEED_ROWS = NR_SEED_ROWS;      // rows of a query's first clusters refined on their own
 #ifndef NR_SURVIVOR_CAP
-#define NR_SURVIVOR_CAP 2048
+#define NR_SURVIVOR_CAP 8192
 #endif
 constexpr int SURVIVOR_CAP = NR_SURVIVOR_CAP;  // candidates a query may keep from the shared scan
 constexpr int SHARED_G = 8;               // queries scored per shared work unit (at most)

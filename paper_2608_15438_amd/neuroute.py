@@ -27,9 +27,12 @@ NR_MAX_K = 64
 NR_MAX_PROBES = 1024
 NR_QSTATS = 8
 NR_REFINE_AUTO, NR_REFINE_PER_QUERY, NR_REFINE_SHARED = 0, 1, 2
-NR_STAGES = 6
+NR_STAGES = 9
 QS = dict(probes=0, clusters=1, direct=2, scored=3, stopped=4, rows=5, tiles=6, batches=7)
-STAGES = ("encode", "probe", "route", "plan", "refine", "merge")
+STAGES = ("encode", "probe", "route", "plan", "refine", "merge", "shared_prep", "shared_scan",
+          "shared_merge")
+WORK = ("tiles", "rows", "rows_read", "own_rows", "shared_rows", "shared_pairs", "survivors",
+        "flagged", "fallback_rows", "shared_pair_rows")
 
 # every symbol include/neuroute.h declares
 EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_encode",
@@ -62,6 +65,7 @@ class nr_params(C.Structure):
                 ("b_min", C.c_int32), ("t_low", C.c_int32), ("u_heap", C.c_int32),
                 ("u_front", C.c_int32), ("alpha_front", C.c_float), ("gate_on", C.c_int32),
                 ("early_stop_on", C.c_int32), ("lowq_or", C.c_int32), ("refine_mode", C.c_int32),
+                ("shared_seed_rows", C.c_int32),
                 ("m_knots", C.c_int32),
                 ("m_x", C.c_float * NR_MAX_KNOTS), ("m_y", C.c_float * NR_MAX_KNOTS)]
 
@@ -95,8 +99,7 @@ def lib():
         L.nr_refine.argtypes = [P, P, C.c_int64, C.c_int32, P, P, C.c_int64, P, P, P]
         L.nr_profile_enable.argtypes = [P, C.c_int32]
         L.nr_profile_read.argtypes = [P, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.c_int32]
-        L.nr_last_work.argtypes = [P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int64),
-                                   C.POINTER(C.c_int64)]
+        L.nr_last_work.argtypes = [P, P, C.POINTER(C.c_int64), C.c_int32]
         L.nr_stream_read.argtypes = [P, C.c_int64, P, P]
         for name in EXPORTS:
             getattr(L, name).restype = getattr(L, name).restype or C.c_int
@@ -171,6 +174,7 @@ class Params:
     early_stop_on: bool = True
     lowq_or: bool = False
     refine_mode: int = NR_REFINE_AUTO
+    shared_seed_rows: int = 0
     m_x: Sequence[float] = field(default_factory=list)
     m_y: Sequence[float] = field(default_factory=list)
 
@@ -183,6 +187,7 @@ class Params:
         p.u_heap, p.u_front, p.alpha_front = self.u_heap, self.u_front, self.alpha_front
         p.gate_on, p.early_stop_on, p.lowq_or = int(self.gate_on), int(self.early_stop_on), int(self.lowq_or)
         p.refine_mode = int(self.refine_mode)
+        p.shared_seed_rows = int(self.shared_seed_rows)
         p.m_knots = len(self.m_x)
         for i, (x, y) in enumerate(zip(self.m_x, self.m_y)):
             p.m_x[i] = x
@@ -346,8 +351,7 @@ class Index:
         return dict(zip(STAGES, list(ms))), n.value
 
     def nr_last_work(self, stream=None):
-        """(tiles, candidate rows, rows read) of the last search's last chunk."""
-        t, r, u = C.c_int64(), C.c_int64(), C.c_int64()
-        _check(lib().nr_last_work(self.handle, _stream(stream), C.byref(t), C.byref(r), C.byref(u)),
-               "nr_last_work")
-        return t.value, r.value, u.value
+        """Work counters of the last search's last chunk, keyed by WORK."""
+        v = (C.c_int64 * len(WORK))()
+        _check(lib().nr_last_work(self.handle, _stream(stream), v, len(WORK)), "nr_last_work")
+        return dict(zip(WORK, list(v)))

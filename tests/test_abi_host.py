@@ -101,3 +101,12 @@ def test_null_arguments(L):
     assert L.nr_search(None, None, 1, 10, 4, C.byref(p), None, None, None) == NR.NR_EINVAL
     assert L.nr_route_capacity(None, 4, C.byref(p)) == 0
     assert L.nr_index_free(None) == NR.NR_OK
+
+
+def test_counter_enums_match_header():
+    txt = open(HEADER).read()
+    assert int(re.search(r"#define NR_STAGES (\d+)", txt).group(1)) == NR.NR_STAGES == len(NR.STAGES)
+    work = dict((m.group(1).lower(), int(m.group(2)))
+                for m in re.finditer(r"NR_WORK_([A-Z_]+) = (\d+)", txt))
+    assert int(re.search(r"\bNR_WORK = (\d+)", txt).group(1)) == len(NR.WORK)
+    assert [work[n] for n in NR.WORK] == list(range(len(NR.WORK)))

@@ -162,7 +162,11 @@ def test_refine_given_clusters(dev, name, k):
 
 
 # ------------------------------------------------------------------ whole path
-MODES = {"per_query": NR.NR_REFINE_PER_QUERY, "shared": NR.NR_REFINE_SHARED}
+# the shared schedule with a tiny seed sends nearly every cluster a query
+# shares with another query through the shared scan, even on small cases
+MODES = {"per_query": dict(refine_mode=NR.NR_REFINE_PER_QUERY),
+         "shared": dict(refine_mode=NR.NR_REFINE_SHARED),
+         "shared_seed64": dict(refine_mode=NR.NR_REFINE_SHARED, shared_seed_rows=64)}
 
 
 @pytest.mark.parametrize("mode", list(MODES))
@@ -171,7 +175,7 @@ MODES = {"per_query": NR.NR_REFINE_PER_QUERY, "shared": NR.NR_REFINE_SHARED}
 @pytest.mark.parametrize("P", [1, 16, 256])
 def test_search_given_logits_bit_exact(dev, name, pset, P, mode):
     c = setup_case(name, dev)
-    p = default_params(c, refine_mode=MODES[mode], **PARAM_SETS[pset])
+    p = default_params(c, **MODES[mode], **PARAM_SETS[pset])
     gi, gd = c["gix"].nr_search(c["Qd"], 10, P, p, logits=c["lgd"])
     ix = c["ix"]
     oi, od, _, _ = O.search(c["enc"], ix.tau, ix.rows, ix.row_ids, ix.bc_off, ix.cl_off,
@@ -184,7 +188,7 @@ def test_search_given_logits_bit_exact(dev, name, pset, P, mode):
 def test_full_budget_search_is_exact_knn(dev, mode):
     c = setup_case("tiny", dev)
     p = default_params(c, l_sel=8, r_max=8, gate_on=False, early_stop_on=False, k_c=10 ** 9,
-                       refine_mode=MODES[mode])
+                       **MODES[mode])
     gi, gd = c["gix"].nr_search(c["Qd"], 10, 256, p)
     bi, bd = O.bruteforce(c["X"], c["Q"], 10)
     _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), bi, bd)
@@ -237,7 +241,7 @@ def test_short_lists_are_padded(dev):
 def test_many_queries_span_chunks(dev, mode):
     """More queries than one internal launch sequence handles."""
     c = setup_case("tiny", dev)
-    p = default_params(c, refine_mode=MODES[mode])
+    p = default_params(c, **MODES[mode])
     reps = 20000 // len(c["Q"]) + 1
     Q = np.tile(c["Q"], (reps, 1))
     lg = np.tile(c["lg"], (reps, 1))
@@ -252,7 +256,7 @@ def test_many_queries_span_chunks(dev, mode):
 @pytest.mark.parametrize("mode", list(MODES))
 def test_deterministic(dev, mode):
     c = setup_case("deep", dev)
-    p = default_params(c, refine_mode=MODES[mode])
+    p = default_params(c, **MODES[mode])
     a = c["gix"].nr_search(c["Qd"], 10, 256, p)
     b = c["gix"].nr_search(c["Qd"], 10, 256, p)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
@@ -300,6 +304,26 @@ def test_corrupt_index_rejected(dev, what):
     assert err.value.status == NR.NR_ECORRUPT
 
 
+@pytest.mark.parametrize("name", list(CASES))
+def test_shared_schedule_work_counters(dev, name):
+    """The shared scan really runs on these cases (pairs and survivors), and
+    its counters add up: every (query, cluster) pair is scored either by the
+    query's own pass or by the scan."""
+    c = setup_case(name, dev)
+    p = default_params(c, **MODES["shared_seed64"])
+    gi, gd = c["gix"].nr_search(c["Qd"], 10, 256, p, logits=c["lgd"])
+    w = c["gix"].nr_last_work()
+    assert w["shared_pairs"] > 0 and w["survivors"] > 0
+    assert w["rows"] == w["own_rows"] + w["shared_pair_rows"]
+    assert w["rows_read"] == w["own_rows"] + w["shared_rows"] + w["fallback_rows"]
+    assert w["shared_rows"] <= w["shared_pair_rows"] and w["flagged"] == 0
+    pi, pd = c["gix"].nr_search(c["Qd"], 10, 256, default_params(c, **MODES["per_query"]),
+                                logits=c["lgd"])
+    assert torch.equal(gi, pi) and torch.equal(gd, pd)
+    w1 = c["gix"].nr_last_work()
+    assert w1["rows"] == w["rows"] == w1["rows_read"] == w1["own_rows"]
+
+
 def test_shared_schedule_overflow_falls_back(dev):
     """All rows tie and original ids fall along the rows, so after the leading
     clusters nearly every row beats the leading top-k's last (distance, id):
@@ -318,10 +342,13 @@ def test_shared_schedule_overflow_falls_back(dev):
                    centroids=torch.from_numpy(cent).to(dev))
     Q = torch.zeros((600, d), dtype=torch.uint8, device=dev)
     base = dict(l_sel=1, r_max=1, k_c=n_cl, gate_on=False, early_stop_on=False)
-    a = gix.nr_search(Q, 10, 2, NR.Params(refine_mode=NR.NR_REFINE_SHARED, **base))
-    b = gix.nr_search(Q, 10, 2, NR.Params(refine_mode=NR.NR_REFINE_PER_QUERY, **base))
+    a = gix.nr_search(Q, 10, 2, NR.Params(refine_mode=NR.NR_REFINE_PER_QUERY, **base))
+    b = gix.nr_search(Q, 10, 2, NR.Params(refine_mode=NR.NR_REFINE_SHARED, **base))
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
-    assert a[0][0].tolist() == list(range(10))          # smallest ids, distance 0
-    tiles, rows_, read = gix.nr_last_work()
-    assert rows_ == 600 * n
+    assert b[0][0].tolist() == list(range(10))          # smallest ids, distance 0
+    w = gix.nr_last_work()
+    assert w["rows"] == 600 * n
+    assert w["flagged"] == 600 and w["fallback_rows"] == 600 * n
+    assert w["rows_read"] == w["own_rows"] + w["shared_rows"] + w["fallback_rows"]
+    assert w["rows"] == w["own_rows"] + w["shared_pair_rows"]
     gix.close()
