@@ -57,9 +57,21 @@ def _mean(v):
     return sum(v) / len(v) if v else float("nan")
 
 
+def working(v: list[float]) -> list[float]:
+    """Dispatches that did work: the shared schedule also launches the
+    per-query kernel for queries whose survivors overflowed, usually with
+    none, and such empty launches read next to nothing."""
+    top = max(v) if v else 0.0
+    return [x for x in v if x >= 0.01 * top]
+
+
 def traffic(a) -> dict:
-    fetch = per_dispatch(a.fetch, a.kernel, "FETCH_SIZE")
-    write = per_dispatch(a.write, a.kernel, "WRITE_SIZE")
+    fetch_all = per_dispatch(a.fetch, a.kernel, "FETCH_SIZE")
+    fetch = working(fetch_all)
+    # the write pass is a second run of the same program: keep the same launches
+    write_all = per_dispatch(a.write, a.kernel, "WRITE_SIZE")
+    keep = [i for i, x in enumerate(fetch_all) if x >= 0.01 * max(fetch_all)] if fetch_all else []
+    write = [write_all[i] for i in keep if i < len(write_all)]
     cf = per_dispatch(a.copy_fetch, a.copy_kernel, "FETCH_SIZE")
     cw = per_dispatch(a.copy_write, a.copy_kernel, "WRITE_SIZE")
     if not (fetch and write and cf and cw):
