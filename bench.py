@@ -56,6 +56,12 @@ def parse():
                     help="no recall ground truth and no oracle (for counter passes)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a plain 4 GiB device copy (counter calibration) and exit")
+    ap.add_argument("--grid", action="store_true",
+                    help="parameter grid instead of the headline: probe budget x gate margin "
+                         "quantile x early stop x batch size, one JSON line per point")
+    ap.add_argument("--grid-probes", type=str, default="", help="default: the workload's budgets")
+    ap.add_argument("--grid-gates", type=str, default="0.99,0.95,0.80")
+    ap.add_argument("--grid-batches", type=str, default="1,256,10000")
     return ap.parse_args()
 
 
@@ -227,6 +233,9 @@ def main():
     m_x, m_y = CAL.fit_margin(xs, ys, args.margin_quantile)
     params = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c,
                        m_x=m_x.tolist(), m_y=m_y.tolist())
+    if args.grid:
+        grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch)
+        return
 
     # ---- probe-budget sweep: recall and QPS per point
     budgets = [int(x) for x in args.probes.split(",")] if args.probes else list(w.probe_budgets)
@@ -357,6 +366,76 @@ def main():
         "setup_s": {"index_build": round(t_build, 1), "total": round(time.time() - t_all, 1)},
     }
     print(json.dumps(out), flush=True)
+
+
+def grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch):
+    """Probe budget x gate (margin quantile of M) x early stop x batch size.
+    Batch 1 runs the first 1,000 queries one call each; larger batches run the
+    whole query set in consecutive calls of that size.  Per point: QPS of an
+    unprofiled pass, Recall@10 on the ground-truth queries it covers, stage
+    milliseconds of a second (profiled) pass, per-query counters of a third."""
+    k = w.k
+    probes = [int(x) for x in args.grid_probes.split(",")] if args.grid_probes \
+        else list(w.probe_budgets)
+    gates = [float(x) for x in args.grid_gates.split(",")]
+    batches = [int(x) for x in args.grid_batches.split(",")]
+    step5 = ("plan", "refine", "merge", "shared_prep", "shared_scan", "shared_merge")
+
+    def run_all(Qr, B, P, params, qstats=False):
+        outs = []
+        for s0 in range(0, len(Qr), B):
+            outs.append(gix.nr_search(Qr[s0:s0 + B], k, P, params, qstats=qstats))
+        return outs
+
+    for gq in gates:
+        m_x, m_y = CAL.fit_margin(xs, ys, gq)
+        for es in (True, False):
+            params = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c,
+                               m_x=m_x.tolist(), m_y=m_y.tolist(), early_stop_on=es)
+            for P in probes:
+                for B in batches:
+                    nq = min(1000, w.n_queries) if B == 1 else w.n_queries
+                    Qr = Q[:nq]
+                    run_all(Qr[:min(nq, 2 * B)], B, P, params)          # warm-up
+                    torch.cuda.synchronize()
+                    t0 = time.time()
+                    outs = run_all(Qr, B, P, params)
+                    torch.cuda.synchronize()
+                    wall = time.time() - t0
+                    ids = torch.cat([o[0] for o in outs])
+                    nr = min(ng, nq)
+                    rec = recall_at_k(ids[:nr].cpu().numpy(), gt_ids[:nr], k) if nr else float("nan")
+                    # profiled pass: stage times, and rows read by the last call
+                    gix.nr_profile_enable(True)
+                    gix.nr_profile_read(reset=True)
+                    run_all(Qr, B, P, params)
+                    torch.cuda.synchronize()
+                    st, ncalls = gix.nr_profile_read(reset=True)
+                    gix.nr_profile_enable(False)
+                    work = gix.nr_last_work()
+                    qs = torch.cat([o[2] for o in run_all(Qr, B, P, params, qstats=True)])
+                    qm = qs.double().mean(0).cpu().numpy()
+                    rows = float(qs[:, NR.QS["rows"]].double().sum())
+                    # rows read: the shared schedule (one call) reports them; the
+                    # per-query schedule reads every candidate row
+                    read = work["rows_read"] if B >= nq and work["shared_pairs"] else rows
+                    t5 = sum(st[x] for x in step5)
+                    pt = {"workload": w.name, "probe_budget": P, "gate": f"q{int(round(gq * 100))}",
+                          "early_stop": es, "batch": B, "queries": nq,
+                          "qps": round(nq / wall, 1), "recall_at_10": round(rec, 5),
+                          "recall_queries": nr,
+                          "cand_per_query": round(rows / nq, 1),
+                          "rows_read_per_query": round(read / nq, 1),
+                          "clusters_per_query": round(float(qm[NR.QS["clusters"]]), 1),
+                          "centroids_scored_per_query": round(float(qm[NR.QS["scored"]]), 2),
+                          "centroid_batches_per_query": round(float(qm[NR.QS["batches"]]), 2),
+                          "stopped_frac": round(float(qm[NR.QS["stopped"]]), 3),
+                          "refine_gbs": round(read * w.row_bytes / (t5 * 1e-3) / 1e9, 1) if t5 else None,
+                          "stage_ms_per_call": {x: round(v / max(ncalls, 1), 4) for x, v in st.items()},
+                          "calls": ncalls}
+                    print(json.dumps(pt), flush=True)
+                    log("grid", {x: pt[x] for x in ("probe_budget", "gate", "early_stop", "batch",
+                                                     "qps", "recall_at_10", "refine_gbs")})
 
 
 def oracle_baseline(args, w, ix, Q, P, params, torch, dev):

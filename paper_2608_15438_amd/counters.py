@@ -3,6 +3,9 @@
     python -m paper_2608_15438_amd.counters stats TRACE_STATS.csv
         markdown table of the search kernels from a --kernel-trace --stats run
 
+    python -m paper_2608_15438_amd.counters grid GRID.jsonl
+        markdown table of a `bench.py --grid` run (one JSON object per line)
+
     python -m paper_2608_15438_amd.counters traffic --kernel NAME --workload W \\
         --fetch F.csv --write W.csv --copy-fetch CF.csv --copy-write CW.csv \\
         --copy-bytes N [--command TEXT]
@@ -109,11 +112,30 @@ def stats(path: str) -> str:
     return "\n".join(lines)
 
 
+def grid_table(path: str) -> str:
+    pts = [json.loads(x) for x in open(path) if x.strip().startswith("{")]
+    lines = ["| P | gate | early stop | batch | QPS | Recall@10 | cand/q | read/q | clusters/q | "
+             "centroids/q | stopped | refine GB/s | refine ms/call |",
+             "|---:|---|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for p in pts:
+        st = p["stage_ms_per_call"]
+        t5 = sum(st.get(x, 0.0) for x in ("plan", "refine", "merge", "shared_prep", "shared_scan",
+                                          "shared_merge"))
+        lines.append(f"| {p['probe_budget']} | {p['gate']} | {'on' if p['early_stop'] else 'off'} | "
+                     f"{p['batch']} | {p['qps']:.0f} | {p['recall_at_10']:.4f} | "
+                     f"{p['cand_per_query']:.0f} | {p['rows_read_per_query']:.0f} | "
+                     f"{p['clusters_per_query']:.1f} | {p['centroids_scored_per_query']:.1f} | "
+                     f"{p['stopped_frac']:.2f} | {p['refine_gbs']} | {t5:.3f} |")
+    return "\n".join(lines)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
     s = sub.add_parser("stats")
     s.add_argument("csv")
+    g = sub.add_parser("grid")
+    g.add_argument("jsonl")
     t = sub.add_parser("traffic")
     t.add_argument("--kernel", required=True, choices=sorted(KERNEL_SOURCES))
     t.add_argument("--workload", required=True)
@@ -127,6 +149,8 @@ def main(argv=None):
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         print(stats(a.csv))
+    elif a.cmd == "grid":
+        print(grid_table(a.jsonl))
     else:
         print(json.dumps(traffic(a), indent=1))
 
