@@ -3,6 +3,9 @@
     python -m paper_2608_15438_amd.counters stats TRACE_STATS.csv
         markdown table of the search kernels from a --kernel-trace --stats run
 
+    python -m paper_2608_15438_amd.counters bench BENCH.json
+        markdown summary of a headline `bench.py` line
+
     python -m paper_2608_15438_amd.counters grid GRID.jsonl
         markdown table of a `bench.py --grid` run (one JSON object per line)
 
@@ -129,6 +132,35 @@ def grid_table(path: str) -> str:
     return "\n".join(lines)
 
 
+def bench_summary(path: str) -> str:
+    d = json.loads(open(path).read().strip().splitlines()[-1])
+    c = d["config"]
+    out = [f"Workload `{c['workload']}`: n = {c['n']}, d = {d['config']['d']}, b = {c['b']}, "
+           f"{c['queries']} queries, k = {c['k']}, dtype {d['dtype']}.", "",
+           "| P | Recall@10 | QPS | candidates/query |", "|---:|---:|---:|---:|"]
+    for p in sorted(d["sweep"], key=lambda p: p["probe_budget"]):
+        out.append(f"| {p['probe_budget']} | {p['recall']:.4f} | {p['qps']:.0f} | "
+                   f"{p['cand_per_query']:.0f} |")
+    out += ["", f"Timed point P = {c['probe_budget']}: {d['value']:.0f} QPS ({d['ms_per_step']:.3f} ms "
+            f"per search of {c['queries']} queries), Recall@10 = {d['recall_at_10']:.4f} on "
+            f"{d['recall_queries']} queries.", ""]
+    out.append("| kernel | avg launch ms (HIP events) | algorithmic GB / launch | GB/s | % of 8 TB/s |")
+    out.append("|---|---:|---:|---:|---:|")
+    for k, v in d.get("kernels", {}).items():
+        out.append(f"| `{k}` | {v['avg_launch_ms']:.3f} | {v['alg_bytes_per_launch'] / 1e9:.2f} | "
+                   f"{v['achieved_gbs']:.0f} | {100 * v['achieved_gbs'] / 8000:.1f} |")
+    r = d["roofline"]
+    out += ["", f"Roofline object: kernel `{r['kernel']}`, {r['achieved']:.0f} {r['unit']} of "
+            f"{r['peak']:.0f} ({100 * r['frac']:.1f} %), traffic {r['traffic']} bytes per launch.",
+            f"Whole refinement stage: {json.dumps(d.get('refine_stage'))}.",
+            f"Stage ms per search: {json.dumps(d['stage_ms_per_step'])}.",
+            f"Work of one search: {json.dumps(d.get('work'))}.",
+            f"Streaming-read self-check: {d.get('hbm_stream_read_gbs')} GB/s.",
+            f"CPU baseline (oracle): {json.dumps(d.get('cpu_baseline'))}.", "",
+            "JSON line:", "", "```", json.dumps(d), "```"]
+    return "\n".join(out)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -136,6 +168,8 @@ def main(argv=None):
     s.add_argument("csv")
     g = sub.add_parser("grid")
     g.add_argument("jsonl")
+    b = sub.add_parser("bench")
+    b.add_argument("json")
     t = sub.add_parser("traffic")
     t.add_argument("--kernel", required=True, choices=sorted(KERNEL_SOURCES))
     t.add_argument("--workload", required=True)
@@ -151,6 +185,8 @@ def main(argv=None):
         print(stats(a.csv))
     elif a.cmd == "grid":
         print(grid_table(a.jsonl))
+    elif a.cmd == "bench":
+        print(bench_summary(a.json))
     else:
         print(json.dumps(traffic(a), indent=1))
 
