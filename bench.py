@@ -56,6 +56,9 @@ def parse():
                     help="no recall ground truth and no oracle (for counter passes)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a plain 4 GiB device copy (counter calibration) and exit")
+    ap.add_argument("--head-bytes", type=int, default=-1,
+                    help="payload layout: 0 row-major, else head plane of this many bytes "
+                         "(default: the first 16 dimensions)")
     ap.add_argument("--grid", action="store_true",
                     help="parameter grid instead of the headline: probe budget x gate margin "
                          "quantile x early stop x batch size, one JSON line per point")
@@ -69,11 +72,11 @@ def parse():
 # ground truth: exact k-NN by plain PyTorch on the device
 # ----------------------------------------------------------------------------
 
-def ground_truth(torch, rows, row_ids, Q, k, chunk=1 << 19):
-    """Exact top-k by (squared distance, original id) for every query in Q."""
-    dev = rows.device
+def ground_truth(torch, rows_range, n, is_u8, row_ids, Q, k, chunk=1 << 19):
+    """Exact top-k by (squared distance, original id) for every query in Q;
+    rows_range(s0, s1) returns payload rows [s0, s1) row-major."""
     nq = Q.shape[0]
-    if rows.dtype == torch.uint8:
+    if is_u8:
         # integer distances: every fp32 step below is exact (all partial sums
         # of byte products stay below 2^24), then (distance, id) is packed in
         # one int64 key so ties resolve by the lower original id
@@ -81,10 +84,10 @@ def ground_truth(torch, rows, row_ids, Q, k, chunk=1 << 19):
         qq = (Qf * Qf).sum(1)
         m2q = (-2.0 * Qf).T.contiguous()
         best = None
-        for s0 in range(0, rows.shape[0], chunk):
+        for s0 in range(0, n, chunk):
             if s0 and s0 % (chunk * 256) == 0:
-                log(f"  ground truth: {s0 / rows.shape[0]:.0%} of the base")
-            X = rows[s0:s0 + chunk].float()
+                log(f"  ground truth: {s0 / n:.0%} of the base")
+            X = rows_range(s0, min(n, s0 + chunk)).float()
             d = X @ m2q
             d += (X * X).sum(1)[:, None]
             d += qq[None, :]
@@ -101,10 +104,10 @@ def ground_truth(torch, rows, row_ids, Q, k, chunk=1 << 19):
     Qd = Q.double()
     qq = (Qd * Qd).sum(1)
     bd, bi = None, None
-    for s0 in range(0, rows.shape[0], chunk):
+    for s0 in range(0, n, chunk):
         if s0 and s0 % (chunk * 256) == 0:
-            log(f"  ground truth: {s0 / rows.shape[0]:.0%} of the base")
-        X = rows[s0:s0 + chunk].double()
+            log(f"  ground truth: {s0 / n:.0%} of the base")
+        X = rows_range(s0, min(n, s0 + chunk)).double()
         d = (X * X).sum(1)[:, None] - 2 * (X @ Qd.T) + qq[None, :]
         kk = min(k + 8, d.shape[0])
         v, i = torch.topk(d, kk, dim=0, largest=False)
@@ -208,8 +211,10 @@ def main():
     log(f"building {w.name}: n={w.n} d={w.d} b={w.b}")
     data = GpuRows(w, "data", dev)
     t0 = time.time()
+    hb = args.head_bytes if args.head_bytes >= 0 else 16 * (1 if w.dtype == "u8" else 4)
     ix = IB.build_index(w, data, device=dev, chunk=1 << 20, keep_codes=False,
-                        payload_fn=lambda perm: data(perm), log=lambda s: log("  index:", s))
+                        payload_fn=lambda perm: data(perm), log=lambda s: log("  index:", s),
+                        head_bytes=hb)
     torch.cuda.synchronize()
     t_build = time.time() - t0
     log(f"index built in {t_build:.1f}s: {ix.n_clusters} clusters")
@@ -221,7 +226,8 @@ def main():
     ng = 0 if args.quick else min(args.gt_queries, w.n_queries)
     nc = args.calib_queries
     Qc = GpuRows(w, "calib", dev).range(0, nc)
-    gt_all, _ = ground_truth(torch, ix.rows, ix.row_ids, torch.cat([Q[:ng], Qc]), k)
+    gt_all, _ = ground_truth(torch, lambda a, b: IB.payload_range(ix, a, b), w.n, w.dtype == "u8",
+                             ix.row_ids, torch.cat([Q[:ng], Qc]), k)
     gt_ids, gtc = gt_all[:ng], gt_all[ng:]
     log(f"ground truth for {ng}+{nc} queries in {time.time() - t0:.1f}s")
     fwd = IB._TorchEncoder(ix.encoder, dev)
@@ -298,16 +304,19 @@ def main():
     qs = qs.double().mean(0).cpu().numpy()
     per_query = {name: round(float(qs[i]), 2) for name, i in NR.QS.items()}
     log("per-query means", per_query, "work", work)
-    # the two refinement kernels: algorithmic bytes = rows each reads x row bytes
-    # (one launch of each per search: the batch fits one query chunk)
+    # the two refinement kernels.  Algorithmic bytes: k_refine reads whole rows;
+    # k_scan reads the head of every scanned row and the rest of the rows it
+    # reads whole (one launch of each per search: the batch fits one chunk)
     nt = max(n_timed, 1)
     kernels = {}
-    for kname, stage, nrows in (("k_refine", "refine", work["own_rows"]),
-                                ("k_shared_refine", "shared_scan", work["shared_rows"])):
+    hb = work["head_bytes"]
+    for kname, stage, nrows, ab in (
+            ("k_refine", "refine", work["own_rows"], work["own_rows"] * w.row_bytes),
+            ("k_scan", "shared_scan", work["shared_rows"],
+             work["shared_rows"] * hb + work["full_rows"] * (w.row_bytes - hb))):
         ms = stage_ms[stage] / nt
         if ms <= 0 or nrows <= 0:
             continue
-        ab = nrows * w.row_bytes
         kernels[kname] = {"avg_launch_ms": round(ms, 4), "alg_bytes_per_launch": int(ab),
                           "rows_per_launch": int(nrows), "achieved_gbs": round(ab / (ms * 1e-3) / 1e9, 1)}
     dom = max(kernels, key=lambda n: kernels[n]["avg_launch_ms"])
@@ -318,8 +327,11 @@ def main():
     # the whole refinement stage (step 5): every launch from the plan to the merge
     st5 = sum(stage_ms[x] for x in ("plan", "refine", "merge", "shared_prep", "shared_scan",
                                     "shared_merge")) / nt
-    b5 = work["rows_read"] * w.row_bytes
-    refine_stage = {"ms": round(st5, 4), "bytes_read": int(b5),
+    b5 = ((work["own_rows"] + work["fallback_rows"]) * w.row_bytes + work["shared_rows"] * hb
+          + work["full_rows"] * (w.row_bytes - hb))
+    cand_bytes = rows * w.row_bytes
+    refine_stage = {"ms": round(st5, 4), "bytes_read": int(b5), "candidate_bytes": int(cand_bytes),
+                    "candidate_gbs": round(cand_bytes / (st5 * 1e-3) / 1e9, 1),
                     "gbs": round(b5 / (st5 * 1e-3) / 1e9, 1),
                     "frac_of_peak": round(b5 / (st5 * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     log(f"timed: {args.steps} steps, {wall * 1e3 / args.steps:.2f} ms/step, recall {recall:.4f}, "
@@ -344,6 +356,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "d": w.d, "b": w.b, "queries": w.n_queries,
+                   "layout": f"head{ix.head_bytes}+tail" if ix.head_bytes else "row-major",
                    "k": k, "probe_budget": P, "l_sel": params.l_sel, "r_max": params.r_max,
                    "k_c": params.k_c, "gate": f"q{int(round(args.margin_quantile * 100))}",
                    "early_stop": True, "parallelism": "single-gpu"},
@@ -443,6 +456,7 @@ def oracle_baseline(args, w, ix, Q, P, params, torch, dev):
     to about `--oracle-seconds` of wall time on the host threads, capped by
     `--oracle-stage-gb` of staged rows."""
     import oracle as O
+    from paper_2608_15438_amd import index_build as IB
     threads = args.oracle_threads or min(16, len(os.sched_getaffinity(0)))
     e = ix.encoder
     enc = O.Encoder(e.weights, e.biases, e.bn_scale or (), e.bn_shift or (), e.input_scale)
@@ -472,7 +486,7 @@ def oracle_baseline(args, w, ix, Q, P, params, torch, dev):
         idx = torch.repeat_interleave(starts, sz_t) + (
             torch.arange(int(sizes.sum()), device=dev) -
             torch.repeat_interleave(torch.cumsum(sz_t, 0) - sz_t, sz_t))
-        rows_h = ix.rows[idx].cpu().numpy()
+        rows_h = IB.payload_rows(ix, idx).cpu().numpy()
         ids_h = ix.row_ids[idx].cpu().numpy()
         del idx
         cnt_all = np.zeros(ix.n_clusters, np.int64)

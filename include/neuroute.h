@@ -96,6 +96,13 @@ typedef struct {
   const uint64_t *cl_off;         /* [n_clusters + 1] non-decreasing, cl_off[0] = 0, cl_off[n_clusters] = n */
   const float *centroids;         /* [n_clusters x b] cluster centroids in latent space */
   int64_t n_clusters;             /* >= 1, < 2^32 */
+  /* Payload layout.  0: `rows` is row-major [n x row_bytes].  Otherwise the
+   * split layout: `rows` holds a head plane [n x head_bytes] (the first
+   * head_bytes bytes of every permuted row) followed by a tail plane
+   * [n x (row_bytes - head_bytes)].  head_bytes is 16, 32, 64 or 128 and at
+   * most row_bytes - 16.  The shared refinement reads only the heads of the
+   * candidate rows that cannot enter a top-k (see NR_REFINE_SHARED). */
+  int32_t head_bytes;
 } nr_index_desc;
 
 /*
@@ -137,12 +144,15 @@ typedef struct {
 } nr_params;
 
 /* How step 5 is scheduled; both give the same top-k.  PER_QUERY refines each
- * query's candidate rows on their own.  SHARED refines on its own, per query,
- * the leading clusters of the list (>= 4096 rows) and the clusters no other
- * query of the batch lists past its own leading clusters; a cluster that
- * several queries list there is read once for all of them, keeping the rows
- * that rank before the query's own top-k.  AUTO picks SHARED for batches of
- * at least 512 queries.  Rows longer than 1024 bytes always use PER_QUERY. */
+ * query's candidate rows on their own.  SHARED refines, per query, only the
+ * leading clusters of its list (at least shared_seed_rows rows); the exact
+ * top-k of those rows bounds the final k-th entry.  Every later (cluster,
+ * query) pair goes to one scan over the batch, grouped by cluster: each row's
+ * head (the first NR_WORK_HEAD_BYTES bytes) is read once and compared with
+ * the bounds of all queries listing its cluster; only rows whose head leaves
+ * some query open are read whole, and those at or before the bound are merged
+ * into the query's result.  AUTO picks SHARED for batches of at least 512
+ * queries.  Rows longer than 1024 bytes always use PER_QUERY. */
 enum { NR_REFINE_AUTO = 0, NR_REFINE_PER_QUERY = 1, NR_REFINE_SHARED = 2 };
 
 /* Per-query counters written by nr_search_ex when `qstats` is not NULL. */
@@ -234,6 +244,8 @@ nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches
  *   NR_WORK_FLAGGED        queries recomputed after their survivors overflowed
  *   NR_WORK_FALLBACK_ROWS  rows read by that recomputation
  *   NR_WORK_SHARED_PAIR_ROWS rows scored by the scan, summed over its pairs
+ *   NR_WORK_FULL_ROWS      rows the scan read whole (their head left a query open)
+ *   NR_WORK_HEAD_BYTES     bytes of a row the scan reads for every row (its head)
  * ROWS_READ = OWN_ROWS + SHARED_ROWS + FALLBACK_ROWS and
  * ROWS = OWN_ROWS + SHARED_PAIR_ROWS. */
 enum {
@@ -247,7 +259,9 @@ enum {
   NR_WORK_FLAGGED = 7,
   NR_WORK_FALLBACK_ROWS = 8,
   NR_WORK_SHARED_PAIR_ROWS = 9,
-  NR_WORK = 10
+  NR_WORK_FULL_ROWS = 10,
+  NR_WORK_HEAD_BYTES = 11,
+  NR_WORK = 12
 };
 nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *work, int32_t n_work);
 

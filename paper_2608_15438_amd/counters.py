@@ -31,7 +31,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 KERNEL_SOURCES = {"k_refine": ["k_refine.hip", "nr_internal.h"],
-                  "k_shared_refine": ["k_shared.hip", "nr_internal.h"]}
+                  "k_scan": ["k_shared.hip", "nr_internal.h"]}
 
 
 def source_digest(kernel: str) -> str:

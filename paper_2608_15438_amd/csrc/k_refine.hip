@@ -62,8 +62,8 @@ __global__ void __launch_bounds__(256) k_plan_rows(PlanArgs a) {
   const uint32_t *cl = a.clus + q * a.cap;
   uint32_t *pre = a.rowpre + q * (a.cap + 1);
   uint64_t run = 0;
-  const int own0 = a.own_hist ? a.own_cseed[q] : 0;
-  // own pass of the shared schedule: keep only the clusters that count, compacted
+  const int own0 = a.own_cseed ? a.own_cseed[q] : 0;
+  // own (seed) pass of the shared schedule: only the leading clusters, compacted
   uint32_t *co = a.clus_out ? a.clus_out + q * a.cap : nullptr;
   int nout = 0;
   if (lane == 0) pre[0] = 0;
@@ -75,8 +75,8 @@ __global__ void __launch_bounds__(256) k_plan_rows(PlanArgs a) {
       c = cl[i];
       if (c < a.n_clusters) {
         sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
-        // the own pass leaves shared clusters to the shared scan
-        if (a.own_hist && i >= own0 && a.own_hist[c] > 1) sz = 0;
+        // the seed pass leaves every later cluster to the scan
+        if (a.own_cseed && i >= own0) sz = 0;
       }
     }
     const uint64_t incl = wave_incl_scan_u64(sz);
@@ -212,7 +212,6 @@ __global__ void __launch_bounds__(256) k_refine(RefineArgs a) {
   const int total = a.tile_off[a.nq];
   const int rb = a.row_bytes;
   const int k = a.k;
-  const unsigned char *rows = (const unsigned char *)a.rows;
 
   for (;;) {
     int t = 0;
@@ -284,11 +283,10 @@ __global__ void __launch_bounds__(256) k_refine(RefineArgs a) {
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-          const unsigned char *rp = rows + phys[u] * (uint64_t)rb;
 #pragma unroll
           for (int s = 0; s < NSEG; ++s) {
             const int off = 128 * s + 16 * gl;
-            xv[u][s] = (ok[u] && off < rb) ? load_payload((const uint4 *)(rp + off))
+            xv[u][s] = (ok[u] && off < rb) ? load_payload(a.ra.seg(phys[u], off))
                                            : make_uint4(0, 0, 0, 0);
           }
         }

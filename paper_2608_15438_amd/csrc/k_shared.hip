@@ -34,9 +34,6 @@
 #ifndef NR_SHARED_BLOCKS_PER_CU
 #define NR_SHARED_BLOCKS_PER_CU 8
 #endif
-#ifndef NR_SHARED_U1
-#define NR_SHARED_U1 4          // rows in flight per lane group for 128-byte rows
-#endif
 #ifndef NR_SHARED_TILE
 #define NR_SHARED_TILE 4096     // work (rows x query groups) per scan tile
 #endif
@@ -88,8 +85,6 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
   return hipGetLastError();
 }
 
-// queries per work unit (their rows are staged in LDS)
-int shared_group(int) { return SHARED_G; }
 
 // ------------------------------------------------------------------ hist
 // one wave per query: full rows, leading clusters, pair counts of the rest
@@ -136,8 +131,8 @@ __global__ void k_shared_count(SharedArgs a) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c <= a.n_clusters; c += stride) {
     const uint32_t h = c < a.n_clusters ? a.hist[c] : 0u;
-    a.cnt2[c] = h >= 2 ? h : 0u;
-    a.isshared[c] = h >= 2 ? 1u : 0u;
+    a.cnt2[c] = h;
+    a.isshared[c] = h >= 1 ? 1u : 0u;
     a.swork[c] = 0;
   }
 }
@@ -163,7 +158,7 @@ __global__ void __launch_bounds__(256) k_pair_scatter(SharedArgs a) {
   const uint32_t *cl = a.clus + q * a.cap;
   for (int i = a.cseed[q] + lane; i < n; i += WAVE) {
     const uint32_t c = cl[i];
-    if (c < a.n_clusters && a.hist[c] >= 2) {
+    if (c < a.n_clusters) {
       const uint32_t left = atomicSub(&a.cnt2[c], 1u);
       a.pair_q[a.hoff[c] + left - 1] = (uint32_t)q;
     }
@@ -184,6 +179,7 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   const int64_t nc1 = a.n_clusters + 1;
   hipError_t e = launch_fill_i32(a.scnt, a.nq, 0, s);
   if (e == hipSuccess) e = launch_fill_i32(a.flag, a.nq, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t *)(a.wstats + 3), 2, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
   if (e != hipSuccess) return e;
   int64_t blocks = (nc1 + 255) / 256;
@@ -208,30 +204,111 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
 }
 
 // ------------------------------------------------------------------ scan
-// The work of shared cluster slist[i] is swork[i] = rows x query groups; a
-// unit (group gi, row chunk ch) starts at swork_off[i] + gi * rows + ch * R.
-// A tile is a SHARED_TILE-long range of that work space and takes the units
-// that start inside it, so each unit belongs to exactly one tile.
-template <int IS_U8, int NSEG, int G, int U>
-__global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
-  constexpr int QCH = NSEG * 8;  // 16-byte chunks per query row (padded to 128-byte segments)
-  __shared__ uint4 s_qv[4][G * QCH];
-  __shared__ int32_t s_thr[4][G];
-  __shared__ int32_t s_qq[4][G];
+// The work of scan-list entry i (cluster slist[i]) is swork[i] = rows x query
+// groups; a unit (group gi, row chunk ch) starts at swork_off[i] + gi * rows +
+// ch * R.  A tile is a SHARED_TILE-long range of that work space and takes the
+// units that start inside it, so each unit belongs to exactly one tile.  A
+// wave gathers up to SCAN_UMAX consecutive units of its tile (with up to 32
+// query slots for 128-byte rows, fewer for longer ones) into a batch whose
+// rows form one virtual row range; the batch's query rows sit in LDS:
+//   phase A  HL lanes read the head of one virtual row (16 B each) and test it
+//            against every query of its unit: the head's part of the squared
+//            distance only grows with the rest of the row, so a row whose head
+//            part already exceeds the query's bound cannot enter its top-k
+//            (fp32 keeps a relative margin of 1e-4 for rounding); rows with any
+//            query left go to an LDS list as (unit, row, query mask);
+//   phase B  8 lanes per listed row (several rows in flight per lane group)
+//            load the whole row and compute the exact distance for the listed
+//            queries in the same arithmetic and order as k_refine; rows at or
+//            before the query's bound become survivors.
+constexpr int SCAN_UMAX = 64;    // units per batch
+
+template <int HL>
+__device__ __forceinline__ int32_t head_sum(int32_t v) {
+  if (HL >= 2) v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  if (HL >= 4) v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  if (HL >= 8) v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+  return v;
+}
+
+template <int HL>
+__device__ __forceinline__ float head_sum(float v) {
+  if (HL >= 2) v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+  if (HL >= 4) v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+  if (HL >= 8) v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+  return v;
+}
+
+// exact key of one (row, query) pair from 8 lanes' 16-byte slices: the same
+// arithmetic and reduction order as k_refine
+template <int IS_U8, int NSEG>
+__device__ __forceinline__ uint32_t pair_key(const uint4 *xv, const uint4 *qv, int32_t xx,
+                                             int32_t qq) {
+  if (IS_U8) {
+    uint32_t xq = 0;
+#pragma unroll
+    for (int s = 0; s < NSEG; ++s) {
+      xq = __builtin_amdgcn_udot4(xv[s].x, qv[s].x, xq, false);
+      xq = __builtin_amdgcn_udot4(xv[s].y, qv[s].y, xq, false);
+      xq = __builtin_amdgcn_udot4(xv[s].z, qv[s].z, xq, false);
+      xq = __builtin_amdgcn_udot4(xv[s].w, qv[s].w, xq, false);
+    }
+    return (uint32_t)(group8_sum(xx - 2 * (int32_t)xq) + qq);
+  }
+  float acc = 0.0f;
+#pragma unroll
+  for (int s = 0; s < NSEG; ++s) {
+    const float t0 = __uint_as_float(xv[s].x) - __uint_as_float(qv[s].x);
+    const float t1 = __uint_as_float(xv[s].y) - __uint_as_float(qv[s].y);
+    const float t2 = __uint_as_float(xv[s].z) - __uint_as_float(qv[s].z);
+    const float t3 = __uint_as_float(xv[s].w) - __uint_as_float(qv[s].w);
+    acc = fmaf(t0, t0, acc);
+    acc = fmaf(t1, t1, acc);
+    acc = fmaf(t2, t2, acc);
+    acc = fmaf(t3, t3, acc);
+  }
+  return __float_as_uint(group8_sum(acc));
+}
+
+template <int IS_U8, int NSEG, int HL, int U>
+__global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
+  constexpr int RPW = WAVE / HL;             // virtual rows per phase-A load
+  constexpr int STEP = RPW * U;              // virtual rows per phase-A pass
+  constexpr int SCAP = STEP + 128;           // listed rows before phase B runs
+  constexpr int G = SHARED_G;
+  constexpr int QCH = NSEG * 8;              // 16-byte chunks of a (padded) query row
+  constexpr int QMAX = NSEG <= 1 ? 32 : (NSEG <= 2 ? 16 : 8);  // query slots per batch
+  constexpr int UB = NSEG <= 1 ? 4 : (NSEG <= 2 ? 2 : 1);      // phase-B rows per lane group
+  __shared__ uint64_t s_ub[4][SCAN_UMAX];        // unit: first payload row
+  __shared__ uint32_t s_uv[4][SCAN_UMAX + 1];    // unit: first virtual row
+  __shared__ uint32_t s_uq[4][SCAN_UMAX];        // unit: first query slot | queries << 16
+  __shared__ uint4 s_q[4][QMAX * QCH];           // the batch's query rows (zero padded)
+  __shared__ int32_t s_th[4][QMAX];              // phase-A bound (int32 or fp32 bits)
+  __shared__ uint32_t s_tk[4][QMAX];             // k-th key of the query's own pass
+  __shared__ uint32_t s_qi[4][QMAX];             // query id
+  __shared__ int32_t s_qq[4][QMAX];              // |q|^2 (uint8)
+  __shared__ uint32_t s_sv[4][SCAP];             // listed rows: unit << 20 | row << 8 | mask
   const int lane = lane_id();
   const int w = threadIdx.x >> 6;
-  const int grp = lane >> 3;  // lane group: one row at a time
-  const int gl = lane & 7;    // 16-byte slot inside a 128-byte segment
-  uint4 *qs = s_qv[w];
-  int32_t *thr_s = s_thr[w];
-  int32_t *qq_s = s_qq[w];
+  const int grp = lane >> 3;  // phase B: 8 lanes per row
+  const int gl = lane & 7;
+  const int hl = lane % HL;   // phase A: HL lanes per row
+  uint64_t *ub = s_ub[w];
+  uint32_t *uv = s_uv[w];
+  uint32_t *uq = s_uq[w];
+  uint4 *qs = s_q[w];
+  int32_t *th = s_th[w];
+  uint32_t *tk = s_tk[w];
+  uint32_t *qi = s_qi[w];
+  int32_t *qqs = s_qq[w];
+  uint32_t *sv = s_sv[w];
   const int64_t NS = a.spos[a.n_clusters];
   const uint64_t W = a.swork_off[a.n_clusters];
   const uint64_t ntiles = (W + SHARED_TILE - 1) / SHARED_TILE;
   const int rb = a.row_bytes;
   const int k = a.k;
-  const unsigned char *rows = (const unsigned char *)a.rows;
   const unsigned char *queries = (const unsigned char *)a.queries;
+  unsigned long long full_rows = 0;
 
   for (;;) {
     unsigned long long t = 0;
@@ -312,6 +389,12 @@ __global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
       gi = 0;
       ch = 0;
     };
+    auto next_unit = [&]() {
+      if (++ch >= nch) {
+        ch = 0;
+        if (++gi >= ng) next_entry();
+      }
+    };
     if (sz == 0) {
       next_entry();
     } else if (ch >= nch) {
@@ -320,187 +403,236 @@ __global__ void __launch_bounds__(256) k_shared_refine(SharedArgs a) {
     }
 
     while (have && wo + (uint64_t)gi * sz + ch * SHARED_ROWS < we) {
-      const uint64_t r0 = base + ch * SHARED_ROWS;
-      const uint64_t r1 = base + (ch * SHARED_ROWS + SHARED_ROWS < sz ? ch * SHARED_ROWS + SHARED_ROWS : sz);
-      const uint32_t p0 = hp + gi * G;
-      const int gm = mq - gi * G < (uint32_t)G ? (int)(mq - gi * G) : G;
-
-      // the first rows go out before the query slices, which depend on pair_q
-      bool ok[U];
-      uint4 xv[U][NSEG];
-      auto load_rows = [&](uint64_t rfirst) {
-#pragma unroll
-        for (int uu = 0; uu < U; ++uu) {
-          const uint64_t r = rfirst + 8 * uu + grp;
-          ok[uu] = r < r1;
-          const unsigned char *rp = rows + r * (uint64_t)rb;
-#pragma unroll
-          for (int s = 0; s < NSEG; ++s) {
-            const int off = 128 * s + 16 * gl;
-            xv[uu][s] = (ok[uu] && off < rb) ? load_stream((const uint4 *)(rp + off))
-                                             : make_uint4(0, 0, 0, 0);
-          }
+      // ---- a batch of consecutive units of this tile
+      int nu = 0, nqs = 0, gmax = 0;
+      uint32_t vtot = 0;
+      while (have && nu < SCAN_UMAX && wo + (uint64_t)gi * sz + ch * SHARED_ROWS < we) {
+        const int gm = mq - gi * G < (uint32_t)G ? (int)(mq - gi * G) : G;
+        if (nqs + gm > QMAX) break;
+        const uint64_t r0 = ch * SHARED_ROWS;
+        const uint32_t nrows = (uint32_t)(r0 + SHARED_ROWS < sz ? SHARED_ROWS : sz - r0);
+        if (lane == 0) {
+          ub[nu] = base + r0;
+          uv[nu] = vtot;
+          uq[nu] = (uint32_t)nqs | ((uint32_t)gm << 16);
         }
-      };
-      load_rows(r0);
-      // lane j < gm: query j of the unit and the k-th key of its own pass
-      uint32_t my_q = 0, my_bound = 0xffffffffu;
-      if (lane < gm) {
-        my_q = a.pair_q[p0 + lane];
-        const int64_t id = a.own_ids[(int64_t)my_q * k + k - 1];
-        const float d = a.own_dists[(int64_t)my_q * k + k - 1];
-        if (id >= 0) my_bound = a.is_u8 ? (uint32_t)d : __float_as_uint(d);
+        if (lane < gm) qi[nqs + lane] = a.pair_q[hp + gi * G + lane];
+        ++nu;
+        nqs += gm;
+        vtot += nrows;
+        gmax = gm > gmax ? gm : gmax;
+        next_unit();
       }
-      // the unit's query rows into LDS (zero past gm and past the row)
-      static_assert((G * QCH) % WAVE == 0, "query staging covers whole waves");
+      if (lane == 0) uv[nu] = vtot;
+      __builtin_amdgcn_wave_barrier();
+      // ---- the batch's queries: rows into LDS, bounds, |q|^2
 #pragma unroll
-      for (int c0 = 0; c0 < G * QCH; c0 += WAVE) {
+      for (int c0 = 0; c0 < QMAX * QCH; c0 += WAVE) {
         const int c = c0 + lane;
-        const int j = c / QCH;
-        const int off = (c - j * QCH) * 16;
-        const uint32_t qj = (uint32_t)__shfl((int)my_q, j);
+        const int sl = c / QCH;
+        const int off = (c - sl * QCH) * 16;
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (j < gm && off < rb) v = *(const uint4 *)(queries + (uint64_t)qj * rb + off);
+        if (sl < nqs && off < rb) v = *(const uint4 *)(queries + (uint64_t)qi[sl] * rb + off);
         qs[c] = v;
       }
-      __builtin_amdgcn_wave_barrier();
-      // per query: |q|^2 (uint8) and the bound the scan compares with:
-      // uint8 keys are |x|^2 - 2 x.q + |q|^2, compared as |x|^2 - 2 x.q <= bound - |q|^2
-      for (int j = 0; j < gm; ++j) {
-        int32_t qq = 0;
+      for (int sl = lane; sl < nqs; sl += WAVE) {
+        const uint32_t q = qi[sl];
+        const int64_t id = a.own_ids[(int64_t)q * k + k - 1];
+        const float d = a.own_dists[(int64_t)q * k + k - 1];
+        const uint32_t bound = id < 0 ? 0xffffffffu : (a.is_u8 ? (uint32_t)d : __float_as_uint(d));
+        tk[sl] = bound;
         if (IS_U8) {
-          uint32_t acc = 0;
-#pragma unroll
-          for (int s = 0; s < NSEG; ++s) {
-            const uint4 q4 = qs[j * QCH + s * 8 + gl];
-            acc = __builtin_amdgcn_udot4(q4.x, q4.x, acc, false);
-            acc = __builtin_amdgcn_udot4(q4.y, q4.y, acc, false);
-            acc = __builtin_amdgcn_udot4(q4.z, q4.z, acc, false);
-            acc = __builtin_amdgcn_udot4(q4.w, q4.w, acc, false);
+          const uint4 *qp = reinterpret_cast<const uint4 *>(queries + (uint64_t)q * rb);
+          uint32_t full = 0, head = 0;
+          for (int c = 0; c < rb / 16; ++c) {
+            const uint4 v = qp[c];
+            uint32_t p = 0;
+            p = __builtin_amdgcn_udot4(v.x, v.x, p, false);
+            p = __builtin_amdgcn_udot4(v.y, v.y, p, false);
+            p = __builtin_amdgcn_udot4(v.z, v.z, p, false);
+            p = __builtin_amdgcn_udot4(v.w, v.w, p, false);
+            full += p;
+            if (c < HL) head += p;
           }
-          qq = group8_sum((int32_t)acc);
-        }
-        const uint32_t bound = bcast_u32(my_bound, j);
-        int32_t th;
-        if (IS_U8)
-          th = bound == 0xffffffffu ? INT32_MAX : (int32_t)((int64_t)bound - qq);
-        else
-          th = (int32_t)bound;
-        if (lane == 0) {
-          thr_s[j] = th;
-          qq_s[j] = qq;
+          qqs[sl] = (int32_t)full;
+          th[sl] = bound == 0xffffffffu ? INT32_MAX : (int32_t)((int64_t)bound - (int64_t)head);
+        } else {
+          qqs[sl] = 0;
+          th[sl] = bound == 0xffffffffu ? (int32_t)__float_as_uint(INFINITY)
+                                        : (int32_t)__float_as_uint(__uint_as_float(bound) * 1.0001f);
         }
       }
       __builtin_amdgcn_wave_barrier();
 
-      for (uint64_t rb0 = r0; rb0 < r1; rb0 += 8 * U) {
-        int32_t xx[U];
+      // ---- phase B: whole rows of the listed (row, queries), UB rows per lane group
+      auto phase_b = [&](int nsv) {
+        for (int e0 = 0; e0 < nsv; e0 += 8 * UB) {
+          uint32_t ent[UB];
+          uint64_t row[UB];
+          uint4 xv[UB][NSEG];
 #pragma unroll
-        for (int uu = 0; uu < U; ++uu) {
-          xx[uu] = 0;
-          if (IS_U8) {
-            uint32_t acc = 0;
+          for (int b = 0; b < UB; ++b) {
+            const int e = e0 + 8 * b + grp;
+            ent[b] = e < nsv ? sv[e] : 0u;
+            row[b] = ub[ent[b] >> 20] + ((ent[b] >> 8) & 0xfffu);
 #pragma unroll
             for (int s = 0; s < NSEG; ++s) {
-              acc = __builtin_amdgcn_udot4(xv[uu][s].x, xv[uu][s].x, acc, false);
-              acc = __builtin_amdgcn_udot4(xv[uu][s].y, xv[uu][s].y, acc, false);
-              acc = __builtin_amdgcn_udot4(xv[uu][s].z, xv[uu][s].z, acc, false);
-              acc = __builtin_amdgcn_udot4(xv[uu][s].w, xv[uu][s].w, acc, false);
+              const int off = 128 * s + 16 * gl;
+              xv[b][s] = ((ent[b] & 0xffu) && off < rb) ? load_stream(a.ra.seg(row[b], off))
+                                                       : make_uint4(0, 0, 0, 0);
             }
-            xx[uu] = (int32_t)acc;
           }
-        }
-        for (int j = 0; j < gm; ++j) {
-          uint4 qv[NSEG];
 #pragma unroll
-          for (int s = 0; s < NSEG; ++s) qv[s] = qs[j * QCH + s * 8 + gl];
-          const int32_t th = thr_s[j];
-          uint32_t key[U];    // uint8: |x|^2 - 2 x.q; fp32: the distance (bits)
-          uint32_t cand = 0;  // bit uu: row uu ranks at or before query j's bound
-#pragma unroll
-          for (int uu = 0; uu < U; ++uu) {
+          for (int b = 0; b < UB; ++b) {
+            const uint32_t mask = ent[b] & 0xffu;
+            if (!ballot(mask != 0)) continue;
+            int32_t xx = 0;
             if (IS_U8) {
-              uint32_t xq = 0;
+              uint32_t acc = 0;
 #pragma unroll
               for (int s = 0; s < NSEG; ++s) {
-                xq = __builtin_amdgcn_udot4(xv[uu][s].x, qv[s].x, xq, false);
-                xq = __builtin_amdgcn_udot4(xv[uu][s].y, qv[s].y, xq, false);
-                xq = __builtin_amdgcn_udot4(xv[uu][s].z, qv[s].z, xq, false);
-                xq = __builtin_amdgcn_udot4(xv[uu][s].w, qv[s].w, xq, false);
+                acc = __builtin_amdgcn_udot4(xv[b][s].x, xv[b][s].x, acc, false);
+                acc = __builtin_amdgcn_udot4(xv[b][s].y, xv[b][s].y, acc, false);
+                acc = __builtin_amdgcn_udot4(xv[b][s].z, xv[b][s].z, acc, false);
+                acc = __builtin_amdgcn_udot4(xv[b][s].w, xv[b][s].w, acc, false);
               }
-              const int32_t part = group8_sum(xx[uu] - 2 * (int32_t)xq);
-              key[uu] = (uint32_t)part;
-              cand |= (ok[uu] && part <= th ? 1u : 0u) << uu;
-            } else {
-              float acc = 0.0f;
-#pragma unroll
-              for (int s = 0; s < NSEG; ++s) {
-                const float t0 = __uint_as_float(xv[uu][s].x) - __uint_as_float(qv[s].x);
-                const float t1 = __uint_as_float(xv[uu][s].y) - __uint_as_float(qv[s].y);
-                const float t2 = __uint_as_float(xv[uu][s].z) - __uint_as_float(qv[s].z);
-                const float t3 = __uint_as_float(xv[uu][s].w) - __uint_as_float(qv[s].w);
-                acc = fmaf(t0, t0, acc);
-                acc = fmaf(t1, t1, acc);
-                acc = fmaf(t2, t2, acc);
-                acc = fmaf(t3, t3, acc);
-              }
-              key[uu] = __float_as_uint(group8_sum(acc));
-              cand |= (ok[uu] && key[uu] <= (uint32_t)th ? 1u : 0u) << uu;
+              xx = (int32_t)acc;
             }
-          }
-          if (gl != 0) cand = 0;
-          // rare: survivors (ties at the bound included; the merge orders them)
-          if (cand) {
-            const uint32_t q = (uint32_t)__builtin_amdgcn_readlane((int)my_q, j);
-            const int32_t qq = qq_s[j];
+            const int slot0 = (int)(uq[ent[b] >> 20] & 0xffffu);
+            for (int j = 0; j < gmax; ++j) {
+              const bool bit = ((mask >> j) & 1u) != 0;
+              if (!ballot(bit)) continue;
+              const int slot = slot0 + (bit ? j : 0);
+              uint4 qv[NSEG];
 #pragma unroll
-            for (int uu = 0; uu < U; ++uu) {
-              if ((cand >> uu) & 1u) {
-                const int64_t id = a.row_ids[rb0 + 8 * uu + grp];
+              for (int s = 0; s < NSEG; ++s) qv[s] = qs[slot * QCH + 8 * s + gl];
+              const uint32_t key = pair_key<IS_U8, NSEG>(xv[b], qv, xx, qqs[slot]);
+              // at or before the bound: a survivor (ties included; the merge orders them)
+              if (bit && gl == 0 && key <= tk[slot]) {
+                const uint32_t q = qi[slot];
                 const int pos = atomicAdd(&a.scnt[q], 1);
                 if (pos < SURVIVOR_CAP) {
-                  a.skey[(int64_t)q * SURVIVOR_CAP + pos] =
-                      IS_U8 ? (uint32_t)((int32_t)key[uu] + qq) : key[uu];
-                  a.sid[(int64_t)q * SURVIVOR_CAP + pos] = id;
+                  a.skey[(int64_t)q * SURVIVOR_CAP + pos] = key;
+                  a.sid[(int64_t)q * SURVIVOR_CAP + pos] = a.row_ids[row[b]];
                 }
               }
             }
           }
         }
-        if (rb0 + 8 * U < r1) load_rows(rb0 + 8 * U);
+        full_rows += (unsigned long long)nsv;
+      };
+
+      // ---- phase A: heads of the batch's virtual rows
+      int nsv = 0;
+      int cur = 0;  // per lane; its virtual rows only increase
+      for (uint32_t v0 = 0; v0 < vtot; v0 += STEP) {
+        if (nsv > SCAP - STEP) {
+          phase_b(nsv);
+          nsv = 0;
+        }
+        uint4 hv[U];
+        bool ok[U];
+        int cus[U];
+        uint32_t vv[U];
+#pragma unroll
+        for (int uu = 0; uu < U; ++uu) {
+          const uint32_t v = v0 + uu * RPW + lane / HL;
+          ok[uu] = v < vtot;
+          vv[uu] = v;
+          if (ok[uu])
+            while (uv[cur + 1] <= v) ++cur;
+          cus[uu] = cur;
+          const uint64_t row = ub[cur] + (v - uv[cur]);
+          hv[uu] = ok[uu] ? load_stream(a.ra.seg(row, 16 * hl)) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int uu = 0; uu < U; ++uu) {
+          int32_t xx = 0;
+          if (IS_U8) {
+            uint32_t acc = 0;
+            acc = __builtin_amdgcn_udot4(hv[uu].x, hv[uu].x, acc, false);
+            acc = __builtin_amdgcn_udot4(hv[uu].y, hv[uu].y, acc, false);
+            acc = __builtin_amdgcn_udot4(hv[uu].z, hv[uu].z, acc, false);
+            acc = __builtin_amdgcn_udot4(hv[uu].w, hv[uu].w, acc, false);
+            xx = (int32_t)acc;
+          }
+          const uint32_t uqv = uq[cus[uu]];
+          const int slot0 = (int)(uqv & 0xffffu);
+          const int gmu = (int)(uqv >> 16);
+          uint32_t mask = 0;
+          for (int j = 0; j < gmax; ++j) {
+            const bool valid = ok[uu] && j < gmu;
+            if (!ballot(valid)) break;  // no row of this load has a j-th query
+            const int slot = slot0 + (valid ? j : 0);
+            const uint4 q4 = qs[slot * QCH + hl];
+            bool keep;
+            if (IS_U8) {
+              uint32_t xq = 0;
+              xq = __builtin_amdgcn_udot4(hv[uu].x, q4.x, xq, false);
+              xq = __builtin_amdgcn_udot4(hv[uu].y, q4.y, xq, false);
+              xq = __builtin_amdgcn_udot4(hv[uu].z, q4.z, xq, false);
+              xq = __builtin_amdgcn_udot4(hv[uu].w, q4.w, xq, false);
+              keep = head_sum<HL>(xx - 2 * (int32_t)xq) <= th[slot];
+            } else {
+              const float t0 = __uint_as_float(hv[uu].x) - __uint_as_float(q4.x);
+              const float t1 = __uint_as_float(hv[uu].y) - __uint_as_float(q4.y);
+              const float t2 = __uint_as_float(hv[uu].z) - __uint_as_float(q4.z);
+              const float t3 = __uint_as_float(hv[uu].w) - __uint_as_float(q4.w);
+              float acc = 0.0f;
+              acc = fmaf(t0, t0, acc);
+              acc = fmaf(t1, t1, acc);
+              acc = fmaf(t2, t2, acc);
+              acc = fmaf(t3, t3, acc);
+              keep = head_sum<HL>(acc) <= __uint_as_float((uint32_t)th[slot]);
+            }
+            mask |= (valid && keep ? 1u : 0u) << j;
+          }
+          const bool lead = hl == 0 && mask != 0;
+          const uint64_t m = ballot(lead);
+          if (lead) {
+            const int cu = cus[uu];
+            sv[nsv + popc64(m & lanemask_lt())] =
+                ((uint32_t)cu << 20) | ((vv[uu] - uv[cu]) << 8) | mask;
+          }
+          nsv += popc64(m);
+        }
       }
+      phase_b(nsv);
       __builtin_amdgcn_wave_barrier();
-      // next unit
-      if (++ch >= nch) {
-        ch = 0;
-        if (++gi >= ng) next_entry();
-      }
     }
   }
+  if (lane == 0 && full_rows) atomicAdd((unsigned long long *)&a.wstats[3], full_rows);
+}
+
+template <int IS_U8, int NSEG>
+static hipError_t launch_scan_h(const SharedArgs &a, int hl, int grid, hipStream_t s) {
+  switch (hl) {
+    case 1: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 1, 8>), dim3(grid), dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 2, 4>), dim3(grid), dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 4, 4>), dim3(grid), dim3(256), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 8, 2>), dim3(grid), dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 template <int IS_U8>
-static hipError_t launch_shared_t(const SharedArgs &a, int nseg, int grid, hipStream_t s) {
-#define NR_SHARED_CASE(NS, GG, UU)                                                              \
-  if (nseg <= NS) {                                                                             \
-    if (a.g != GG) return hipErrorInvalidValue;                                                 \
-    hipLaunchKernelGGL((k_shared_refine<IS_U8, NS, GG, UU>), dim3(grid), dim3(256), 0, s, a); \
-    return hipGetLastError();                                                                   \
-  }
-  NR_SHARED_CASE(1, 8, NR_SHARED_U1)
-  NR_SHARED_CASE(2, 8, 4)
-  NR_SHARED_CASE(4, 8, 2)
-  NR_SHARED_CASE(8, 8, 1)
-#undef NR_SHARED_CASE
+static hipError_t launch_scan_t(const SharedArgs &a, int nseg, int hl, int grid, hipStream_t s) {
+  if (nseg <= 1) return launch_scan_h<IS_U8, 1>(a, hl, grid, s);
+  if (nseg <= 2) return launch_scan_h<IS_U8, 2>(a, hl, grid, s);
+  if (nseg <= 4) return launch_scan_h<IS_U8, 4>(a, hl, grid, s);
+  if (nseg <= 8) return launch_scan_h<IS_U8, 8>(a, hl, grid, s);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStream_t s) {
   if (a.nq <= 0) return hipSuccess;
   const int nseg = (a.row_bytes + 127) / 128;
-  if (nseg > SHARED_MAX_NSEG) return hipErrorInvalidValue;
+  const int hl = a.scan_head / 16;
+  if (nseg > SHARED_MAX_NSEG || a.scan_head % 16 != 0 || a.scan_head > a.ra.h) return hipErrorInvalidValue;
   const int grid = n_cu * NR_SHARED_BLOCKS_PER_CU;
-  return dtype == NR_U8 ? launch_shared_t<1>(a, nseg, grid, s) : launch_shared_t<0>(a, nseg, grid, s);
+  return dtype == NR_U8 ? launch_scan_t<1>(a, nseg, hl, grid, s)
+                        : launch_scan_t<0>(a, nseg, hl, grid, s);
 }
 
 // ------------------------------------------------------------------ merge

@@ -113,7 +113,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
   B.pid = c.take<int64_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
   B.shared = s.shared;
   B.rfull = c.take<uint32_t>((size_t)s.nq);
-  B.wstats = c.take<int64_t>(3);
+  B.wstats = c.take<int64_t>(4);
   if (s.shared) {
     const size_t nc1 = (size_t)s.n_clusters + 1;
     B.own_ids = c.take<int64_t>((size_t)s.nq * s.k);
@@ -260,6 +260,36 @@ Shape shape_of(const nr_index *ix, int64_t nq, int P, int k, int64_t cap) {
 
 size_t elem_size(const nr_index *ix) { return ix->d.dtype == NR_U8 ? 1 : 4; }
 
+// bytes of each row the shared scan's filter reads: the head plane of the
+// split layout, else the first 16 dimensions of the row-major row
+int scan_head(const nr_index *ix) {
+  if (ix->d.head_bytes > 0) return ix->d.head_bytes;
+  const int rb = (int)(ix->d.d * (ix->d.dtype == NR_U8 ? 1 : 4));
+  const int h = ix->d.dtype == NR_U8 ? 16 : 64;
+  return h < rb ? h : rb;
+}
+
+// payload addressing for the kernels (row-major or head/tail planes)
+nr::RowAddr row_addr(const nr_index *ix) {
+  const uint64_t rb = (uint64_t)ix->d.d * elem_size(ix);
+  const unsigned char *base = (const unsigned char *)ix->d.rows;
+  nr::RowAddr r;
+  if (ix->d.head_bytes > 0) {
+    r.h = ix->d.head_bytes;
+    r.hb = base;
+    r.hs = (uint64_t)ix->d.head_bytes;
+    r.tb = base + (uint64_t)ix->d.n * (uint64_t)ix->d.head_bytes;
+    r.ts = rb - (uint64_t)ix->d.head_bytes;
+  } else {
+    r.h = (int)rb;
+    r.hb = base;
+    r.hs = rb;
+    r.tb = base;  // unused: every offset is below h
+    r.ts = rb;
+  }
+  return r;
+}
+
 // ----------------------------------------------------------------- stages
 hipError_t run_encode(const nr_index *ix, const void *q, int64_t nq, float *logits,
                       const Buffers &B, hipStream_t s) {
@@ -350,9 +380,8 @@ hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
 }
 
 struct RefineOpts {
-  const int32_t *qmask = nullptr;     // only these queries (the others keep their outputs)
-  const uint32_t *own_hist = nullptr; // own pass of the shared schedule
-  const int32_t *own_cseed = nullptr;
+  const int32_t *qmask = nullptr;      // only these queries (the others keep their outputs)
+  const int32_t *own_cseed = nullptr;  // seed pass of the shared schedule: leading clusters only
 };
 
 // ev (may be null): events recorded after the plan, the refinement and the merge
@@ -375,11 +404,10 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   pa.tile_q = B.tile_q;
   pa.tile_c0 = B.tile_c0;
   pa.counter = B.counter;
-  pa.rfull = (o.qmask || o.own_hist) ? nullptr : B.rfull;
+  pa.rfull = (o.qmask || o.own_cseed) ? nullptr : B.rfull;
   pa.qmask = o.qmask;
-  pa.own_hist = o.own_hist;
   pa.own_cseed = o.own_cseed;
-  if (o.own_hist) {
+  if (o.own_cseed) {
     pa.clus_out = B.clus_own;
     pa.nclus_out = B.nclus_own;
     pa.tile_min = nr::OWN_TILE_MIN_ROWS;
@@ -388,7 +416,7 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[0], s);
   nr::RefineArgs ra{};
-  ra.rows = ix->d.rows;
+  ra.ra = row_addr(ix);
   ra.row_ids = ix->d.row_ids;
   ra.cl_off = ix->d.cl_off;
   ra.n_clusters = ix->d.n_clusters;
@@ -397,8 +425,8 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   ra.d = ix->d.d;
   ra.row_bytes = (int)(ix->d.d * elem_size(ix));
   ra.k = k;
-  ra.clus = o.own_hist ? B.clus_own : clus;
-  ra.nclus = o.own_hist ? B.nclus_own : nclus;
+  ra.clus = o.own_cseed ? B.clus_own : clus;
+  ra.nclus = o.own_cseed ? B.nclus_own : nclus;
   ra.cap = cap;
   ra.rowpre = B.rowpre;
   ra.rtot = B.rtot;
@@ -443,11 +471,12 @@ hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void 
   a.k = k;
   a.is_u8 = ix->d.dtype == NR_U8;
   a.row_bytes = (int)(ix->d.d * elem_size(ix));
-  a.g = nr::shared_group(a.row_bytes);
+  a.g = nr::SHARED_G;
+  a.scan_head = scan_head(ix);
   const uint32_t seed = p->shared_seed_rows > 0 ? (uint32_t)p->shared_seed_rows : nr::SEED_ROWS;
   a.seed_min = seed > (uint32_t)k ? seed : (uint32_t)k;
   a.n_clusters = ix->d.n_clusters;
-  a.rows = ix->d.rows;
+  a.ra = row_addr(ix);
   a.row_ids = ix->d.row_ids;
   a.cl_off = ix->d.cl_off;
   a.queries = q;
@@ -484,7 +513,6 @@ hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void 
   hipError_t e = nr::launch_shared_hist(a, s);
   if (e != hipSuccess) return e;
   RefineOpts own;
-  own.own_hist = B.hist;
   own.own_cseed = B.cseed;
   e = run_refine(ix, q, nq, k, clus, nclus, cap, B, B.own_ids, B.own_dists, qstats, s, ev, own);
   if (e != hipSuccess) return e;
@@ -575,6 +603,10 @@ nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t
   if (!d.rows || !d.row_ids || !d.bc_off || !d.cl_off || !d.centroids)
     return fail(NR_EINVAL, "rows, row_ids, bc_off, cl_off and centroids are required");
   if ((uintptr_t)d.rows % 16 != 0) return fail(NR_EINVAL, "rows must be 16-byte aligned");
+  if (d.head_bytes != 0 &&
+      ((d.head_bytes != 16 && d.head_bytes != 32 && d.head_bytes != 64 && d.head_bytes != 128) ||
+       (size_t)d.head_bytes > rb - 16))
+    return fail(NR_EINVAL, "head_bytes must be 0, 16, 32, 64 or 128 and leave a tail of >= 16 bytes");
   if (d.n_clusters < 1 || d.n_clusters >= ((int64_t)1 << 32))
     return fail(NR_EINVAL, "n_clusters must be in [1, 2^32)");
 
@@ -878,7 +910,7 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
   v[NR_WORK_TILES] = t;
   v[NR_WORK_OWN_ROWS] = v[NR_WORK_ROWS];
   if (B.shared) {
-    int64_t ws[3] = {0, 0, 0};
+    int64_t ws[4] = {0, 0, 0, 0};
     uint32_t pairs = 0;
     HIP_OK(hipMemcpy(ws, B.wstats, sizeof(ws), hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(&pairs, B.hoff + ix->d.n_clusters, 4, hipMemcpyDeviceToHost));
@@ -900,6 +932,8 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
     v[NR_WORK_SHARED_ROWS] = ws[0];
     v[NR_WORK_SHARED_PAIRS] = pairs;
     v[NR_WORK_SHARED_PAIR_ROWS] = ws[2];
+    v[NR_WORK_FULL_ROWS] = ws[3];
+    v[NR_WORK_HEAD_BYTES] = scan_head(ix);
   }
   v[NR_WORK_ROWS_READ] = v[NR_WORK_OWN_ROWS] + v[NR_WORK_SHARED_ROWS] + v[NR_WORK_FALLBACK_ROWS];
   for (int i = 0; i < n_work && i < NR_WORK; ++i) work[i] = v[i];

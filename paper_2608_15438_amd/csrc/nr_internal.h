@@ -38,6 +38,20 @@ constexpr uint32_t SHARED_ROWS = 2048;    // rows per shared work unit (at most)
 constexpr int MAX_KC = 16384;             // top-K_c heap held in LDS
 
 // ---------------------------------------------------------------- kernels
+// Addressing of the permuted payload: bytes [0, h) of row r at hb + r * hs,
+// bytes [h, row_bytes) at tb + r * ts.  Row-major: hb = tb - h = rows,
+// hs = ts = row_bytes.  Split layout: a head plane then a tail plane.
+struct RowAddr {
+  const unsigned char *hb;
+  const unsigned char *tb;
+  uint64_t hs, ts;
+  int h;
+  __device__ __forceinline__ const uint4 *seg(uint64_t r, int off) const {
+    return off < h ? reinterpret_cast<const uint4 *>(hb + r * hs + off)
+                   : reinterpret_cast<const uint4 *>(tb + r * ts + (off - h));
+  }
+};
+
 struct EncodeLayerArgs {
   const void *in;        // [M x K]: uint8 or fp32 (layer 0) / fp32 activations
   int in_u8;
@@ -101,15 +115,14 @@ struct PlanArgs {
   int32_t *counter;      // work counter of the refinement kernel
   uint32_t *rfull;       // [nq] rows of the whole list, may be null
   const int32_t *qmask;  // [nq] only queries with qmask[q] != 0 get tiles, may be null
-  const uint32_t *own_hist;  // with own_cseed: a cluster at list position i counts only if
-  const int32_t *own_cseed;  // i < own_cseed[q] or own_hist[cluster] <= 1
-  uint32_t *clus_out;        // with own_hist: [nq x cap] the clusters that count, compacted
+  const int32_t *own_cseed;  // [nq] may be null; else only list positions i < own_cseed[q] count
+  uint32_t *clus_out;        // with own_cseed: [nq x cap] the clusters that count, compacted
   int32_t *nclus_out;        // [nq]
   uint32_t tile_min;         // smallest tile (rows); 0: TILE_MIN_ROWS
 };
 
 struct RefineArgs {
-  const void *rows;      // permuted payload
+  RowAddr ra;            // permuted payload
   const int64_t *row_ids;
   const uint64_t *cl_off;
   int64_t n_clusters;
@@ -148,17 +161,18 @@ struct MergeArgs {
 struct SharedArgs {
   int64_t nq;
   int k, is_u8, row_bytes;
-  int g;                      // queries per work unit (<= SHARED_G)
+  int g;                      // queries per work unit (SHARED_G)
   uint32_t seed_min;          // rows the leading clusters of a list cover at least
   int64_t n_clusters;
-  const void *rows;
+  RowAddr ra;                 // permuted payload
+  int scan_head;              // bytes of each row the scan's filter reads (its head)
   const int64_t *row_ids;
   const uint64_t *cl_off;
   const void *queries;
   const uint32_t *clus;
   const int32_t *nclus;
   int64_t cap;
-  int32_t *cseed;             // [nq] leading clusters, always scored by the query's own pass
+  int32_t *cseed;             // [nq] leading clusters, scored by the query's own (seed) pass
   uint32_t *rfull;            // [nq] rows of the whole list
   const uint32_t *rtot;       // [nq] rows of the own pass
   const int32_t *tile_off;    // [nq + 1] tiles of the own pass
@@ -166,20 +180,20 @@ struct SharedArgs {
   const float *own_dists;
   uint32_t *own_rows;         // [nq] copy of rtot kept for diagnostics
   uint32_t *hist;             // [n_clusters + 1] pairs per cluster past the leading clusters
-  uint32_t *cnt2;             // [n_clusters + 1] pairs of shared clusters (hist >= 2), else 0
+  uint32_t *cnt2;             // [n_clusters + 1] copy of hist consumed by the pair scatter
   uint32_t *hoff;             // [n_clusters + 1] exclusive scan of cnt2
-  uint32_t *isshared;         // [n_clusters + 1] 1 for a shared cluster
+  uint32_t *isshared;         // [n_clusters + 1] 1 for a cluster the scan reads (hist >= 1)
   uint32_t *spos;             // [n_clusters + 1] exclusive scan of isshared
-  uint32_t *slist;            // [n_clusters] shared clusters in cluster order
+  uint32_t *slist;            // [n_clusters] scanned clusters in cluster order
   uint64_t *swork;            // [n_clusters + 1] rows x query groups of slist[i], 0 past the list
   uint64_t *swork_off;        // [n_clusters + 1] exclusive scan of swork
-  uint32_t *pair_q;           // [pairs] query of each shared pair, grouped by cluster
+  uint32_t *pair_q;           // [pairs] query of each scanned pair, grouped by cluster
   int32_t *scnt;              // [nq] survivors appended
   uint32_t *skey;             // [nq x SURVIVOR_CAP]
   int64_t *sid;
   int32_t *flag;              // [nq] 1: survivors overflowed, recompute per query
   unsigned long long *counter;  // work-unit counter
-  int64_t *wstats;            // [2] unique shared rows, own-pass tiles
+  int64_t *wstats;            // [4] scanned rows, own-pass tiles, scanned pair rows, rows re-read whole
   void *scan_tmp;
   size_t scan_tmp_bytes;
   int64_t *out_ids;
@@ -196,7 +210,6 @@ hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
 size_t shared_scan_tmp_bytes(int64_t n_clusters);
-int shared_group(int row_bytes);
 hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s);
 hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s);
 hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStream_t s);

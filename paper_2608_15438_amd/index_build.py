@@ -61,10 +61,61 @@ class Index:
     cl_off: object             # uint64 [n_clusters + 1]
     centroids: object          # fp32 [n_clusters, b]
     codes: Optional[object] = None   # uint32 code of each permuted row (diagnostics)
+    head_bytes: int = 0        # 0: rows is [n, d]; else the split layout (see split_payload)
 
     @property
     def n_clusters(self) -> int:
         return int(self.centroids.shape[0])
+
+    @property
+    def row_bytes(self) -> int:
+        return self.workload.row_bytes
+
+
+def _row_dtype(w: Workload):
+    return torch.uint8 if w.dtype == "u8" else torch.float32
+
+
+def payload_rows(ix: Index, idx) -> torch.Tensor:
+    """Row-major payload rows at permuted positions ``idx`` (a torch index
+    tensor on the payload's device), whatever the layout."""
+    if not ix.head_bytes:
+        return ix.rows[idx]
+    n, R, H = ix.workload.n, ix.row_bytes, ix.head_bytes
+    head = ix.rows[:n * H].view(n, H)
+    tail = ix.rows[n * H:n * R].view(n, R - H)
+    by = torch.cat([head[idx], tail[idx]], dim=1).contiguous()
+    return by.view(_row_dtype(ix.workload)).view(-1, ix.workload.d)
+
+
+def payload_range(ix: Index, s0: int, s1: int) -> torch.Tensor:
+    """Row-major payload rows [s0, s1), whatever the layout."""
+    if not ix.head_bytes:
+        return ix.rows[s0:s1]
+    n, R, H = ix.workload.n, ix.row_bytes, ix.head_bytes
+    head = ix.rows[:n * H].view(n, H)[s0:s1]
+    tail = ix.rows[n * H:n * R].view(n, R - H)[s0:s1]
+    by = torch.cat([head, tail], dim=1).contiguous()
+    return by.view(_row_dtype(ix.workload)).view(-1, ix.workload.d)
+
+
+def split_payload(rows_chunks, n: int, row_bytes: int, head_bytes: int, device) -> torch.Tensor:
+    """Split layout of a payload given as consecutive row-major chunks: one
+    uint8 buffer holding the head plane [n x head_bytes] (the first head_bytes
+    of every row) followed by the tail plane [n x (row_bytes - head_bytes)]."""
+    H, R = head_bytes, row_bytes
+    out = torch.empty(n * R, dtype=torch.uint8, device=device)
+    head = out[:n * H].view(n, H)
+    tail = out[n * H:].view(n, R - H)
+    s0 = 0
+    for r in rows_chunks:
+        by = r.contiguous().view(torch.uint8).view(r.shape[0], R)
+        m = by.shape[0]
+        head[s0:s0 + m] = by[:, :H]
+        tail[s0:s0 + m] = by[:, H:]
+        s0 += m
+    assert s0 == n
+    return out
 
 
 def seeded_encoder(w: Workload) -> Encoder:
@@ -285,12 +336,14 @@ def _clusters_per_bucket(w: Workload, sizes: torch.Tensor) -> torch.Tensor:
 
 def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 20,
                 encoder: Optional[Encoder] = None, keep_codes: bool = True,
-                payload_fn: Optional[Callable] = None, log=None) -> Index:
+                payload_fn: Optional[Callable] = None, log=None,
+                head_bytes: int = 0) -> Index:
     """Build the index of workload ``w`` from ``rows_fn(ids) -> rows``.
 
     ``rows_fn`` returns numpy or torch rows for an int64 id array.  With
     ``payload_fn(perm) -> rows`` the permuted payload is produced directly
     (e.g. regenerated on the GPU) instead of gathered from ``rows_fn``.
+    With ``head_bytes`` > 0 the payload is stored in the split layout.
     """
     dev = torch.device(device)
     enc = encoder or seeded_encoder(w)
@@ -390,7 +443,15 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
         centroids[first[seg] + within] = cm
     say("directory done")
     # payload
-    if payload_fn is not None:
+    if head_bytes:
+        big = max(chunk, 1 << 24)
+        if payload_fn is not None:
+            gen = (payload_fn(perm[s0:s0 + big]) for s0 in range(0, n, big))
+        else:
+            pn = perm.cpu().numpy()
+            gen = (rows_t(pn[s0:s0 + big]) for s0 in range(0, n, big))
+        rows = split_payload(gen, n, w.row_bytes, head_bytes, dev)
+    elif payload_fn is not None:
         rows = payload_fn(perm)
     else:
         pn = perm.cpu().numpy()
@@ -401,7 +462,7 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
         workload=w, encoder=enc, tau=tau.cpu().numpy().astype(np.float32),
         rows=rows, row_ids=perm,
         bc_off=bc_off.to(torch.int64), cl_off=cl_off, centroids=centroids.to(torch.float32),
-        codes=codes[perm] if keep_codes else None,
+        codes=codes[perm] if keep_codes else None, head_bytes=head_bytes,
     )
 
 
@@ -416,4 +477,5 @@ def to_numpy(ix: Index) -> Index:
         cl_off=np.ascontiguousarray(f(ix.cl_off)).astype(np.uint64),
         centroids=np.ascontiguousarray(f(ix.centroids)).astype(np.float32),
         codes=None if ix.codes is None else np.ascontiguousarray(f(ix.codes)).astype(np.uint32),
+        head_bytes=ix.head_bytes,
     )

@@ -32,7 +32,7 @@ QS = dict(probes=0, clusters=1, direct=2, scored=3, stopped=4, rows=5, tiles=6, 
 STAGES = ("encode", "probe", "route", "plan", "refine", "merge", "shared_prep", "shared_scan",
           "shared_merge")
 WORK = ("tiles", "rows", "rows_read", "own_rows", "shared_rows", "shared_pairs", "survivors",
-        "flagged", "fallback_rows", "shared_pair_rows")
+        "flagged", "fallback_rows", "shared_pair_rows", "full_rows", "head_bytes")
 
 # every symbol include/neuroute.h declares
 EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_encode",
@@ -56,7 +56,8 @@ class nr_index_desc(C.Structure):
                 ("bn_shift", C.POINTER(C.POINTER(C.c_float))),
                 ("input_scale", C.c_float), ("tau", C.POINTER(C.c_float)),
                 ("rows", C.c_void_p), ("row_ids", C.c_void_p), ("bc_off", C.c_void_p),
-                ("cl_off", C.c_void_p), ("centroids", C.c_void_p), ("n_clusters", C.c_int64)]
+                ("cl_off", C.c_void_p), ("centroids", C.c_void_p), ("n_clusters", C.c_int64),
+                ("head_bytes", C.c_int32)]
 
 
 class nr_params(C.Structure):
@@ -204,7 +205,8 @@ class Index:
     library borrows them."""
 
     def __init__(self, *, n, d, dtype, b, weights, biases, input_scale, tau, rows, row_ids,
-                 bc_off, cl_off, centroids, bn_scale=None, bn_shift=None, stream=None):
+                 bc_off, cl_off, centroids, bn_scale=None, bn_shift=None, head_bytes=0,
+                 stream=None):
         L = len(weights)
         self._keep = []
         widths = np.array([weights[0].shape[1]] + [w.shape[0] for w in weights], np.int32)
@@ -237,6 +239,7 @@ class Index:
         desc.rows, desc.row_ids, desc.bc_off, desc.cl_off, desc.centroids = [
             t.data_ptr() for t in self.dev]
         desc.n_clusters = centroids.shape[0]
+        desc.head_bytes = int(head_bytes)
         self.n, self.d, self.dtype, self.b = n, d, dtype, b
         self.n_clusters = int(centroids.shape[0])
         h = C.c_void_p()
@@ -245,24 +248,30 @@ class Index:
 
     @classmethod
     def from_built(cls, ix, device="cuda", stream=None):
-        """Upload an index_build.Index (host or device arrays)."""
+        """Upload an index_build.Index (host or device arrays, either layout)."""
         def dt(a, dtype):
             t = torch.as_tensor(a) if not isinstance(a, torch.Tensor) else a
             return t.to(device=device, dtype=dtype).contiguous()
         rows = ix.rows if isinstance(ix.rows, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(ix.rows))
         rows = rows.to(device).contiguous()
+        w = ix.workload
+        hb = int(getattr(ix, "head_bytes", 0) or 0)
+        if hb:
+            n, d, dtype = int(w.n), int(w.d), NR_U8 if w.dtype == "u8" else NR_F32
+        else:
+            n, d = int(rows.shape[0]), int(rows.shape[1])
+            dtype = NR_U8 if rows.dtype == torch.uint8 else NR_F32
         bc = ix.bc_off
         bc = torch.from_numpy(np.asarray(bc).astype(np.int64)) if not isinstance(bc, torch.Tensor) else bc
         cl = ix.cl_off
         cl = torch.from_numpy(np.asarray(cl).astype(np.int64)) if not isinstance(cl, torch.Tensor) else cl
         e = ix.encoder
-        return cls(n=int(rows.shape[0]), d=int(rows.shape[1]),
-                   dtype=NR_U8 if rows.dtype == torch.uint8 else NR_F32, b=len(ix.tau),
+        return cls(n=n, d=d, dtype=dtype, b=len(ix.tau),
                    weights=e.weights, biases=e.biases, bn_scale=e.bn_scale, bn_shift=e.bn_shift,
                    input_scale=e.input_scale, tau=ix.tau, rows=rows,
                    row_ids=dt(ix.row_ids, torch.int64), bc_off=dt(bc, torch.int32),
                    cl_off=dt(cl, torch.int64), centroids=dt(ix.centroids, torch.float32),
-                   stream=stream)
+                   head_bytes=hb, stream=stream)
 
     def close(self):
         if getattr(self, "handle", None) is not None and self.handle.value:

@@ -23,6 +23,22 @@ def instance(cfg: int, n: int = 0, n_queries: int = 0, **overrides):
     return w, ix, X, Q
 
 
+def head_bytes_for(w) -> int:
+    """Head size of the split layout used by the tests and the benchmark:
+    the first 16 dimensions of a row."""
+    return 16 * (1 if w.dtype == "u8" else 4)
+
+
+def split_index(ix, dev):
+    """A device copy of a row-major host index in the split layout."""
+    import torch
+    from dataclasses import replace as dc_replace
+    w = ix.workload
+    H = head_bytes_for(w)
+    rows = torch.from_numpy(np.ascontiguousarray(ix.rows)).to(dev)
+    return dc_replace(ix, rows=IB.split_payload([rows], w.n, w.row_bytes, H, dev), head_bytes=H)
+
+
 def oracle_encoder(ix):
     import oracle as O
     e = ix.encoder
@@ -42,7 +58,7 @@ def stage_rows(ix, lists):
                                          np.repeat(np.cumsum(sizes) - sizes, sizes))
     if isinstance(ix.rows, torch.Tensor):
         it = torch.from_numpy(idx).to(ix.rows.device)
-        rows = ix.rows[it].cpu().numpy()
+        rows = IB.payload_rows(ix, it).cpu().numpy()
         ids = ix.row_ids[it].cpu().numpy()
     else:
         rows, ids = ix.rows[idx], ix.row_ids[idx]

@@ -46,9 +46,10 @@ def test_struct_layout_matches_header(tmp_path):
 #include <stdio.h>
 #include "neuroute.h"
 int main(void) {
-  printf("%zu %zu %zu %zu %zu %zu\n", sizeof(nr_index_desc), offsetof(nr_index_desc, rows),
-         offsetof(nr_index_desc, n_clusters), sizeof(nr_params), offsetof(nr_params, m_x),
-         offsetof(nr_params, m_y));
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu\n", sizeof(nr_index_desc),
+         offsetof(nr_index_desc, rows), offsetof(nr_index_desc, n_clusters),
+         offsetof(nr_index_desc, head_bytes), sizeof(nr_params), offsetof(nr_params, refine_mode),
+         offsetof(nr_params, shared_seed_rows), offsetof(nr_params, m_x), offsetof(nr_params, m_y));
   return 0;
 }
 ''')
@@ -58,8 +59,9 @@ int main(void) {
     got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
                                           check=True).stdout.split()]
     exp = [C.sizeof(NR.nr_index_desc), NR.nr_index_desc.rows.offset,
-           NR.nr_index_desc.n_clusters.offset, C.sizeof(NR.nr_params), NR.nr_params.m_x.offset,
-           NR.nr_params.m_y.offset]
+           NR.nr_index_desc.n_clusters.offset, NR.nr_index_desc.head_bytes.offset,
+           C.sizeof(NR.nr_params), NR.nr_params.refine_mode.offset,
+           NR.nr_params.shared_seed_rows.offset, NR.nr_params.m_x.offset, NR.nr_params.m_y.offset]
     assert got == exp
 
 

@@ -15,22 +15,25 @@ from paper_2608_15438_amd import neuroute as NR
 from synth import configs as CF
 from synth import generators as G
 from synth.gpu import GpuRows
-from tests.instances import stage_rows
+from tests.instances import head_bytes_for, stage_rows
 
 pytestmark = pytest.mark.gpu
 
 GATE = dict(m_x=[0.0, 1.0], m_y=[0.5, 2.0])
 
 
-@pytest.mark.parametrize("cfg,P,mode", [(4, 640, NR.NR_REFINE_AUTO), (4, 640, NR.NR_REFINE_PER_QUERY),
-                                         (3, 256, NR.NR_REFINE_AUTO)])
-def test_full_size_sampled_queries(cfg, P, mode):
+@pytest.mark.parametrize("cfg,P,mode,split", [(4, 640, NR.NR_REFINE_AUTO, True),
+                                               (4, 640, NR.NR_REFINE_PER_QUERY, True),
+                                               (3, 256, NR.NR_REFINE_AUTO, True),
+                                               (3, 256, NR.NR_REFINE_AUTO, False)])
+def test_full_size_sampled_queries(cfg, P, mode, split):
     if not torch.cuda.is_available():
         pytest.skip("no HIP device")
     dev = torch.device("cuda")
     w = CF.WORKLOADS[cfg]
     data = GpuRows(w, "data", dev)
-    ix = IB.build_index(w, data, device=dev, keep_codes=False, payload_fn=lambda p: data(p))
+    ix = IB.build_index(w, data, device=dev, keep_codes=False, payload_fn=lambda p: data(p),
+                        head_bytes=head_bytes_for(w) if split else 0)
     try:
         gix = NR.Index.from_built(ix, dev)
         Q = GpuRows(w, "query", dev).range(0, w.n_queries)

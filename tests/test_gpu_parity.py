@@ -9,7 +9,7 @@ import torch
 
 import oracle as O
 from paper_2608_15438_amd import neuroute as NR
-from tests.instances import instance, oracle_encoder
+from tests.instances import instance, oracle_encoder, split_index
 
 pytestmark = pytest.mark.gpu
 
@@ -35,9 +35,11 @@ def setup_case(name, dev):
         cfg, n, nq, ov = CASES[name]
         w, ix, X, Q = instance(cfg, n, nq, **dict(ov))
         gix = NR.Index.from_built(ix, dev)
+        gix_split = NR.Index.from_built(split_index(ix, dev), dev)
         enc = oracle_encoder(ix)
         lg, mag = O.encode(enc, Q, with_mag=True)
-        _cache[name] = dict(w=w, ix=ix, X=X, Q=Q, gix=gix, enc=enc, lg=lg, mag=mag,
+        _cache[name] = dict(w=w, ix=ix, X=X, Q=Q, gix=gix, gix_split=gix_split, enc=enc, lg=lg,
+                            mag=mag,
                             Qd=torch.from_numpy(Q).to(dev), lgd=torch.from_numpy(lg).to(dev))
     return _cache[name]
 
@@ -141,9 +143,10 @@ def _assert_topk(c, gi, gd, oi, od):
         assert np.allclose(gd[q][: len(ids)], true, rtol=1e-5, atol=1e-6), q
 
 
+@pytest.mark.parametrize("layout", ["gix", "gix_split"])
 @pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("k", [1, 10, 64])
-def test_refine_given_clusters(dev, name, k):
+def test_refine_given_clusters(dev, name, k, layout):
     c = setup_case(name, dev)
     p = default_params(c)
     P = 128
@@ -155,18 +158,21 @@ def test_refine_given_clusters(dev, name, k):
     for q, L in enumerate(lists):
         cl[q, :len(L)] = L
         n[q] = len(L)
-    gi, gd = c["gix"].nr_refine(c["Qd"], k, torch.from_numpy(cl.view(np.int32)).to(dev),
-                                torch.from_numpy(n).to(dev))
+    gi, gd = c[layout].nr_refine(c["Qd"], k, torch.from_numpy(cl.view(np.int32)).to(dev),
+                                 torch.from_numpy(n).to(dev))
     oi, od, _ = O.refine(c["ix"].rows, c["ix"].row_ids, c["ix"].cl_off, c["Q"], lists, k)
     _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
 
 
 # ------------------------------------------------------------------ whole path
-# the shared schedule with a tiny seed sends nearly every cluster a query
-# shares with another query through the shared scan, even on small cases
-MODES = {"per_query": dict(refine_mode=NR.NR_REFINE_PER_QUERY),
-         "shared": dict(refine_mode=NR.NR_REFINE_SHARED),
-         "shared_seed64": dict(refine_mode=NR.NR_REFINE_SHARED, shared_seed_rows=64)}
+# refinement schedule x payload layout; the shared schedule with a tiny seed
+# sends nearly every candidate cluster through the scan, even on small cases
+MODES = {"per_query": ("gix", dict(refine_mode=NR.NR_REFINE_PER_QUERY)),
+         "shared": ("gix", dict(refine_mode=NR.NR_REFINE_SHARED)),
+         "shared_seed64": ("gix", dict(refine_mode=NR.NR_REFINE_SHARED, shared_seed_rows=64)),
+         "split_per_query": ("gix_split", dict(refine_mode=NR.NR_REFINE_PER_QUERY)),
+         "split_shared_seed64": ("gix_split", dict(refine_mode=NR.NR_REFINE_SHARED,
+                                                   shared_seed_rows=64))}
 
 
 @pytest.mark.parametrize("mode", list(MODES))
@@ -175,8 +181,8 @@ MODES = {"per_query": dict(refine_mode=NR.NR_REFINE_PER_QUERY),
 @pytest.mark.parametrize("P", [1, 16, 256])
 def test_search_given_logits_bit_exact(dev, name, pset, P, mode):
     c = setup_case(name, dev)
-    p = default_params(c, **MODES[mode], **PARAM_SETS[pset])
-    gi, gd = c["gix"].nr_search(c["Qd"], 10, P, p, logits=c["lgd"])
+    p = default_params(c, **MODES[mode][1], **PARAM_SETS[pset])
+    gi, gd = c[MODES[mode][0]].nr_search(c["Qd"], 10, P, p, logits=c["lgd"])
     ix = c["ix"]
     oi, od, _, _ = O.search(c["enc"], ix.tau, ix.rows, ix.row_ids, ix.bc_off, ix.cl_off,
                             ix.centroids, c["Q"], 10, p.l_sel, p.r_max, P, oracle_params(p),
@@ -188,8 +194,8 @@ def test_search_given_logits_bit_exact(dev, name, pset, P, mode):
 def test_full_budget_search_is_exact_knn(dev, mode):
     c = setup_case("tiny", dev)
     p = default_params(c, l_sel=8, r_max=8, gate_on=False, early_stop_on=False, k_c=10 ** 9,
-                       **MODES[mode])
-    gi, gd = c["gix"].nr_search(c["Qd"], 10, 256, p)
+                       **MODES[mode][1])
+    gi, gd = c[MODES[mode][0]].nr_search(c["Qd"], 10, 256, p)
     bi, bd = O.bruteforce(c["X"], c["Q"], 10)
     _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), bi, bd)
 
@@ -241,11 +247,11 @@ def test_short_lists_are_padded(dev):
 def test_many_queries_span_chunks(dev, mode):
     """More queries than one internal launch sequence handles."""
     c = setup_case("tiny", dev)
-    p = default_params(c, **MODES[mode])
+    p = default_params(c, **MODES[mode][1])
     reps = 20000 // len(c["Q"]) + 1
     Q = np.tile(c["Q"], (reps, 1))
     lg = np.tile(c["lg"], (reps, 1))
-    gi, gd = c["gix"].nr_search(torch.from_numpy(Q).to(dev), 10, 8, p,
+    gi, gd = c[MODES[mode][0]].nr_search(torch.from_numpy(Q).to(dev), 10, 8, p,
                                 logits=torch.from_numpy(lg).to(dev))
     gi = gi.cpu().numpy()
     n0 = len(c["Q"])
@@ -256,9 +262,9 @@ def test_many_queries_span_chunks(dev, mode):
 @pytest.mark.parametrize("mode", list(MODES))
 def test_deterministic(dev, mode):
     c = setup_case("deep", dev)
-    p = default_params(c, **MODES[mode])
-    a = c["gix"].nr_search(c["Qd"], 10, 256, p)
-    b = c["gix"].nr_search(c["Qd"], 10, 256, p)
+    p = default_params(c, **MODES[mode][1])
+    a = c[MODES[mode][0]].nr_search(c["Qd"], 10, 256, p)
+    b = c[MODES[mode][0]].nr_search(c["Qd"], 10, 256, p)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
 
 
@@ -304,24 +310,41 @@ def test_corrupt_index_rejected(dev, what):
     assert err.value.status == NR.NR_ECORRUPT
 
 
+@pytest.mark.parametrize("layout", ["gix", "gix_split"])
 @pytest.mark.parametrize("name", list(CASES))
-def test_shared_schedule_work_counters(dev, name):
-    """The shared scan really runs on these cases (pairs and survivors), and
-    its counters add up: every (query, cluster) pair is scored either by the
-    query's own pass or by the scan."""
+def test_shared_schedule_work_counters(dev, name, layout):
+    """The scan really runs on these cases (pairs, rows read whole,
+    survivors), and its counters add up: every (query, cluster) pair is
+    scored either by the query's seed pass or by the scan."""
     c = setup_case(name, dev)
-    p = default_params(c, **MODES["shared_seed64"])
-    gi, gd = c["gix"].nr_search(c["Qd"], 10, 256, p, logits=c["lgd"])
-    w = c["gix"].nr_last_work()
-    assert w["shared_pairs"] > 0 and w["survivors"] > 0
+    p = default_params(c, **MODES["shared_seed64"][1])
+    gi, gd = c[layout].nr_search(c["Qd"], 10, 256, p, logits=c["lgd"])
+    w = c[layout].nr_last_work()
+    assert w["shared_pairs"] > 0 and w["survivors"] > 0 and w["full_rows"] > 0
     assert w["rows"] == w["own_rows"] + w["shared_pair_rows"]
     assert w["rows_read"] == w["own_rows"] + w["shared_rows"] + w["fallback_rows"]
     assert w["shared_rows"] <= w["shared_pair_rows"] and w["flagged"] == 0
-    pi, pd = c["gix"].nr_search(c["Qd"], 10, 256, default_params(c, **MODES["per_query"]),
-                                logits=c["lgd"])
+    assert w["full_rows"] <= w["shared_pair_rows"]
+    assert w["head_bytes"] == 16 * (1 if c["w"].dtype == "u8" else 4)
+    pi, pd = c[layout].nr_search(c["Qd"], 10, 256, default_params(c, **MODES["per_query"][1]),
+                                 logits=c["lgd"])
     assert torch.equal(gi, pi) and torch.equal(gd, pd)
-    w1 = c["gix"].nr_last_work()
+    w1 = c[layout].nr_last_work()
     assert w1["rows"] == w["rows"] == w1["rows_read"] == w1["own_rows"]
+
+
+def test_split_layout_rejects_bad_head(dev):
+    c = setup_case("sift", dev)
+    ix = c["ix"]
+    e = ix.encoder
+    for hb in (8, 48, 128):
+        with pytest.raises(NR.NRError) as err:
+            NR.Index(n=ix.workload.n, d=ix.workload.d, dtype=NR.NR_U8, b=len(ix.tau),
+                     weights=e.weights, biases=e.biases, input_scale=e.input_scale, tau=ix.tau,
+                     rows=c["gix_split"].dev[0], row_ids=c["gix_split"].dev[1],
+                     bc_off=c["gix_split"].dev[2], cl_off=c["gix_split"].dev[3],
+                     centroids=c["gix_split"].dev[4], head_bytes=hb)
+        assert err.value.status == NR.NR_EINVAL
 
 
 def test_shared_schedule_overflow_falls_back(dev):
