@@ -212,6 +212,7 @@ __global__ void __launch_bounds__(256) k_refine(RefineArgs a) {
   const int total = a.tile_off[a.nq];
   const int rb = a.row_bytes;
   const int k = a.k;
+  if (total == 0) return;  // nothing to do: skip the counter (an empty redo launch)
 
   for (;;) {
     int t = 0;

@@ -180,6 +180,7 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   hipError_t e = launch_fill_i32(a.scnt, a.nq, 0, s);
   if (e == hipSuccess) e = launch_fill_i32(a.flag, a.nq, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)(a.wstats + 3), 2, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.pool_cnt, 2, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
   if (e != hipSuccess) return e;
   int64_t blocks = (nc1 + 255) / 256;
@@ -201,6 +202,28 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   if (a.nq > 0)
     hipLaunchKernelGGL(k_pair_scatter, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ survivors
+// one survivor of query q: its own slots first, then the shared pool; a
+// survivor that finds the pool full is lost, so its query is flagged and
+// recomputed by the per-query schedule
+__device__ __forceinline__ void add_survivor(const SharedArgs &a, uint32_t q, uint32_t key,
+                                             int64_t id) {
+  const int pos = atomicAdd(&a.scnt[q], 1);
+  if (pos < SURVIVOR_CAP) {
+    a.skey[(int64_t)q * SURVIVOR_CAP + pos] = key;
+    a.sid[(int64_t)q * SURVIVOR_CAP + pos] = id;
+    return;
+  }
+  const unsigned long long pp = atomicAdd(a.pool_cnt, 1ull);
+  if (pp < SURVIVOR_POOL) {
+    a.pool_q[pp] = q;
+    a.pool_key[pp] = key;
+    a.pool_id[pp] = id;
+  } else {
+    a.flag[q] = 1;
+  }
 }
 
 // ------------------------------------------------------------------ scan
@@ -309,6 +332,7 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
   const int k = a.k;
   const unsigned char *queries = (const unsigned char *)a.queries;
   unsigned long long full_rows = 0;
+  if (ntiles == 0) return;
 
   for (;;) {
     unsigned long long t = 0;
@@ -509,12 +533,7 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
               const uint32_t key = pair_key<IS_U8, NSEG>(xv[b], qv, xx, qqs[slot]);
               // at or before the bound: a survivor (ties included; the merge orders them)
               if (bit && gl == 0 && key <= tk[slot]) {
-                const uint32_t q = qi[slot];
-                const int pos = atomicAdd(&a.scnt[q], 1);
-                if (pos < SURVIVOR_CAP) {
-                  a.skey[(int64_t)q * SURVIVOR_CAP + pos] = key;
-                  a.sid[(int64_t)q * SURVIVOR_CAP + pos] = a.row_ids[row[b]];
-                }
+                add_survivor(a, qi[slot], key, a.row_ids[row[b]]);
               }
             }
           }
@@ -666,6 +685,68 @@ __device__ __forceinline__ void stk_insert(SharedTopK &t, int k, uint32_t ck, in
   }
 }
 
+// pooled survivors per query: offsets (one block scans the per-query counts)
+__global__ void __launch_bounds__(1024) k_pool_offsets(SharedArgs a) {
+  __shared__ uint32_t part[1024];
+  const int tid = threadIdx.x;
+  const int64_t per = (a.nq + 1023) / 1024;
+  const int64_t s0 = tid * per;
+  uint32_t sum = 0;
+  // a flagged query lost survivors and is recomputed: it takes no pool2 space,
+  // so the offsets stay within the survivors actually pooled
+  for (int64_t q = s0; q < s0 + per && q < a.nq; ++q) {
+    const int c = a.flag[q] ? 0 : a.scnt[q];
+    sum += c > SURVIVOR_CAP ? (uint32_t)(c - SURVIVOR_CAP) : 0u;
+  }
+  part[tid] = sum;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const uint32_t v = tid >= o ? part[tid - o] : 0u;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  uint32_t run = part[tid] - sum;
+  for (int64_t q = s0; q < s0 + per && q < a.nq; ++q) {
+    const int c = a.flag[q] ? 0 : a.scnt[q];
+    a.poff[q] = run;
+    a.pcur[q] = 0;
+    run += c > SURVIVOR_CAP ? (uint32_t)(c - SURVIVOR_CAP) : 0u;
+  }
+  if (tid == 1023) a.poff[a.nq] = part[1023];
+}
+
+// pooled survivors grouped by query (order inside a query is arbitrary)
+// (pooled entries of one query tend to be adjacent: the lanes of a wave that
+// share a query take their positions with one atomic)
+__global__ void k_pool_scatter(SharedArgs a) {
+  const unsigned long long used = *a.pool_cnt;
+  const uint64_t n = used < SURVIVOR_POOL ? used : SURVIVOR_POOL;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  const uint64_t first = (uint64_t)blockIdx.x * blockDim.x + (threadIdx.x & ~63u);
+  for (uint64_t e0 = first; e0 < n; e0 += stride) {
+    const uint64_t e = e0 + lane_id();
+    const bool in = e < n;
+    const uint32_t q = in ? a.pool_q[e] : 0xffffffffu;
+    const bool live = in && !a.flag[q];
+    uint64_t todo = ballot(live);
+    while (todo) {
+      const uint32_t lq = bcast_u32(q, __ffsll((unsigned long long)todo) - 1);
+      const uint64_t same = ballot(live && q == lq);
+      todo &= ~same;
+      uint32_t base = 0;
+      if (live && q == lq && (same & lanemask_lt()) == 0)
+        base = atomicAdd(&a.pcur[lq], (uint32_t)popc64(same));
+      base = bcast_u32(base, __ffsll((unsigned long long)same) - 1);
+      if (live && q == lq) {
+        const uint32_t pos = a.poff[lq] + base + (uint32_t)popc64(same & lanemask_lt());
+        a.pool2_key[pos] = a.pool_key[e];
+        a.pool2_id[pos] = a.pool_id[e];
+      }
+    }
+  }
+}
+
 __global__ void __launch_bounds__(256) k_shared_merge(SharedArgs a) {
   const int lane = lane_id();
   const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
@@ -675,18 +756,17 @@ __global__ void __launch_bounds__(256) k_shared_merge(SharedArgs a) {
     if (q == 0) a.wstats[1] = a.tile_off[a.nq];
   }
   const int k = a.k;
+  if (a.flag[q]) return;  // a survivor was lost: recomputed by the per-query schedule
   const int cnt = a.scnt[q];
-  if (cnt > SURVIVOR_CAP) {
-    if (lane == 0) a.flag[q] = 1;  // recomputed by the per-query schedule
-    return;
-  }
+  const int own = cnt < SURVIVOR_CAP ? cnt : SURVIVOR_CAP;
+  const uint32_t p0 = a.poff[q];
   SharedTopK tk;
   tk.key = 0xffffffffu;
   tk.id = -1;
   tk.cnt = 0;
   tk.kth_key = 0xffffffffu;
   tk.kth_id = INT64_MAX;
-  // the own-pass top-k (sorted)
+  // the seed top-k (sorted)
   {
     int64_t id = -1;
     uint32_t key = 0xffffffffu;
@@ -702,13 +782,17 @@ __global__ void __launch_bounds__(256) k_shared_merge(SharedArgs a) {
       stk_insert(tk, k, bcast_u32(key, src), (int64_t)bcast_u64((uint64_t)id, src));
     }
   }
+  // survivors: the query's own slots, then its pooled ones
   for (int i0 = 0; i0 < cnt; i0 += WAVE) {
     const int i = i0 + lane;
     uint32_t key = 0xffffffffu;
     int64_t id = -1;
-    if (i < cnt) {
+    if (i < own) {
       key = a.skey[q * SURVIVOR_CAP + i];
       id = a.sid[q * SURVIVOR_CAP + i];
+    } else if (i < cnt) {
+      key = a.pool2_key[p0 + (uint32_t)(i - SURVIVOR_CAP)];
+      id = a.pool2_id[p0 + (uint32_t)(i - SURVIVOR_CAP)];
     }
     uint64_t m = ballot(i < cnt && key <= tk.kth_key);
     while (m) {
@@ -728,6 +812,8 @@ __global__ void __launch_bounds__(256) k_shared_merge(SharedArgs a) {
 
 hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s) {
   if (a.nq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_pool_offsets, dim3(1), dim3(1024), 0, s, a);
+  hipLaunchKernelGGL(k_pool_scatter, dim3(1024), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_shared_merge, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }

@@ -70,6 +70,9 @@ struct Buffers {
   int32_t *cseed;
   uint32_t *rfull, *own_rows;
   int32_t *scnt, *flag;
+  unsigned long long *pool_cnt;
+  uint32_t *pool_q, *pool_key, *poff, *pcur, *pool2_key;
+  int64_t *pool_id, *pool2_id;
   unsigned long long *counter2;
   uint32_t *skey;
   int64_t *sid;
@@ -127,6 +130,14 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.counter2 = c.take<unsigned long long>(1);
     B.skey = c.take<uint32_t>((size_t)s.nq * nr::SURVIVOR_CAP);
     B.sid = c.take<int64_t>((size_t)s.nq * nr::SURVIVOR_CAP);
+    B.pool_cnt = c.take<unsigned long long>(1);
+    B.pool_q = c.take<uint32_t>(nr::SURVIVOR_POOL);
+    B.pool_key = c.take<uint32_t>(nr::SURVIVOR_POOL);
+    B.pool_id = c.take<int64_t>(nr::SURVIVOR_POOL);
+    B.poff = c.take<uint32_t>((size_t)s.nq + 1);
+    B.pcur = c.take<uint32_t>((size_t)s.nq);
+    B.pool2_key = c.take<uint32_t>(nr::SURVIVOR_POOL);
+    B.pool2_id = c.take<int64_t>(nr::SURVIVOR_POOL);
     B.pair_q = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.hist = c.take<uint32_t>(nc1);
     B.cnt2 = c.take<uint32_t>(nc1);
@@ -503,6 +514,14 @@ hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void 
   a.skey = B.skey;
   a.sid = B.sid;
   a.flag = B.flag;
+  a.pool_cnt = B.pool_cnt;
+  a.pool_q = B.pool_q;
+  a.pool_key = B.pool_key;
+  a.pool_id = B.pool_id;
+  a.poff = B.poff;
+  a.pcur = B.pcur;
+  a.pool2_key = B.pool2_key;
+  a.pool2_id = B.pool2_id;
   a.counter = B.counter2;
   a.wstats = B.wstats;
   a.scan_tmp = B.scan_tmp;

@@ -29,9 +29,13 @@ constexpr uint32_t OWN_TILE_MIN_ROWS = NR_OWN_TILE_MIN_ROWS;  // smallest tile o
 #endif
 constexpr uint32_t SEED_ROWS = NR_SEED_ROWS;      // rows of a query's first clusters refined on their own
 #ifndef NR_SURVIVOR_CAP
-#define NR_SURVIVOR_CAP 8192
+#define NR_SURVIVOR_CAP 2048
 #endif
-constexpr int SURVIVOR_CAP = NR_SURVIVOR_CAP;  // candidates a query may keep from the shared scan
+constexpr int SURVIVOR_CAP = NR_SURVIVOR_CAP;  // survivors a query keeps in its own slots
+#ifndef NR_SURVIVOR_POOL
+#define NR_SURVIVOR_POOL (1u << 22)
+#endif
+constexpr uint32_t SURVIVOR_POOL = NR_SURVIVOR_POOL;  // survivors past SURVIVOR_CAP, all queries
 constexpr int SHARED_G = 8;               // queries scored per shared work unit (at most)
 constexpr int SHARED_MAX_NSEG = 8;        // rows of at most 8 x 128 bytes use the shared scan
 constexpr uint32_t SHARED_ROWS = 2048;    // rows per shared work unit (at most)
@@ -191,7 +195,14 @@ struct SharedArgs {
   int32_t *scnt;              // [nq] survivors appended
   uint32_t *skey;             // [nq x SURVIVOR_CAP]
   int64_t *sid;
-  int32_t *flag;              // [nq] 1: survivors overflowed, recompute per query
+  int32_t *flag;              // [nq] 1: survivors lost (pool full), recompute per query
+  unsigned long long *pool_cnt;  // survivors appended to the pool
+  uint32_t *pool_q, *pool_key;   // [SURVIVOR_POOL] query and key of pooled survivors
+  int64_t *pool_id;
+  uint32_t *poff;             // [nq + 1] per-query start of its pooled survivors in pool2
+  uint32_t *pcur;             // [nq] scatter cursors
+  uint32_t *pool2_key;        // [SURVIVOR_POOL] pooled survivors grouped by query
+  int64_t *pool2_id;
   unsigned long long *counter;  // work-unit counter
   int64_t *wstats;            // [4] scanned rows, own-pass tiles, scanned pair rows, rows re-read whole
   void *scan_tmp;
