@@ -57,8 +57,10 @@ def parse():
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a plain 4 GiB device copy (counter calibration) and exit")
     ap.add_argument("--head-bytes", type=int, default=-1,
-                    help="payload layout: 0 row-major, else head plane of this many bytes "
+                    help="payload layout: 0 row-major, else a head plane of this many bytes "
                          "(default: the first 16 dimensions)")
+    ap.add_argument("--head-split", action="store_true",
+                    help="store tails after the head plane instead of whole rows (less memory)")
     ap.add_argument("--grid", action="store_true",
                     help="parameter grid instead of the headline: probe budget x gate margin "
                          "quantile x early stop x batch size, one JSON line per point")
@@ -214,7 +216,7 @@ def main():
     hb = args.head_bytes if args.head_bytes >= 0 else 16 * (1 if w.dtype == "u8" else 4)
     ix = IB.build_index(w, data, device=dev, chunk=1 << 20, keep_codes=False,
                         payload_fn=lambda perm: data(perm), log=lambda s: log("  index:", s),
-                        head_bytes=hb)
+                        head_bytes=hb, head_copy=not args.head_split)
     torch.cuda.synchronize()
     t_build = time.time() - t0
     log(f"index built in {t_build:.1f}s: {ix.n_clusters} clusters")
@@ -356,7 +358,8 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "d": w.d, "b": w.b, "queries": w.n_queries,
-                   "layout": f"head{ix.head_bytes}+tail" if ix.head_bytes else "row-major",
+                   "layout": (f"head{ix.head_bytes}+" + ("rows" if ix.head_copy else "tail"))
+                   if ix.head_bytes else "row-major",
                    "k": k, "probe_budget": P, "l_sel": params.l_sel, "r_max": params.r_max,
                    "k_c": params.k_c, "gate": f"q{int(round(args.margin_quantile * 100))}",
                    "early_stop": True, "parallelism": "single-gpu"},

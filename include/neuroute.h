@@ -96,13 +96,18 @@ typedef struct {
   const uint64_t *cl_off;         /* [n_clusters + 1] non-decreasing, cl_off[0] = 0, cl_off[n_clusters] = n */
   const float *centroids;         /* [n_clusters x b] cluster centroids in latent space */
   int64_t n_clusters;             /* >= 1, < 2^32 */
-  /* Payload layout.  0: `rows` is row-major [n x row_bytes].  Otherwise the
-   * split layout: `rows` holds a head plane [n x head_bytes] (the first
-   * head_bytes bytes of every permuted row) followed by a tail plane
-   * [n x (row_bytes - head_bytes)].  head_bytes is 16, 32, 64 or 128 and at
-   * most row_bytes - 16.  The shared refinement reads only the heads of the
+  /* Payload layout.  head_bytes = 0: `rows` is row-major [n x row_bytes].
+   * Otherwise `rows` starts with a head plane [n x head_bytes] holding the
+   * first head_bytes bytes of every permuted row, followed by
+   *   head_copy = 0: a tail plane [n x (row_bytes - head_bytes)] (the rest of
+   *                  every row; no byte is stored twice), or
+   *   head_copy = 1: the whole row-major payload [n x row_bytes] (the heads
+   *                  are stored twice; whole rows stay aligned to their size).
+   * head_bytes is 16, 32, 64 or 128 and, with head_copy = 0, at most
+   * row_bytes - 16.  The shared refinement reads only the heads of the
    * candidate rows that cannot enter a top-k (see NR_REFINE_SHARED). */
   int32_t head_bytes;
+  int32_t head_copy;
 } nr_index_desc;
 
 /*

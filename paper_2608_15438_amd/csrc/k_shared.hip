@@ -37,6 +37,18 @@
 #ifndef NR_SHARED_TILE
 #define NR_SHARED_TILE 4096     // work (rows x query groups) per scan tile
 #endif
+#ifndef NR_SCAN_U1
+#define NR_SCAN_U1 8            // head loads in flight per lane (16-byte heads)
+#endif
+#ifndef NR_SCAN_UB1
+#define NR_SCAN_UB1 4           // whole rows in flight per lane group (128-byte rows)
+#endif
+#ifndef NR_SCAN_SLACK
+#define NR_SCAN_SLACK 128       // listed rows beyond one pass before whole rows are read
+#endif
+#ifndef NR_SCAN_QMAX1
+#define NR_SCAN_QMAX1 32        // query slots per batch (128-byte rows)
+#endif
 
 namespace nr {
 
@@ -297,11 +309,11 @@ template <int IS_U8, int NSEG, int HL, int U>
 __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
   constexpr int RPW = WAVE / HL;             // virtual rows per phase-A load
   constexpr int STEP = RPW * U;              // virtual rows per phase-A pass
-  constexpr int SCAP = STEP + 128;           // listed rows before phase B runs
+  constexpr int SCAP = STEP + NR_SCAN_SLACK;  // listed rows before phase B runs
   constexpr int G = SHARED_G;
   constexpr int QCH = NSEG * 8;              // 16-byte chunks of a (padded) query row
-  constexpr int QMAX = NSEG <= 1 ? 32 : (NSEG <= 2 ? 16 : 8);  // query slots per batch
-  constexpr int UB = NSEG <= 1 ? 4 : (NSEG <= 2 ? 2 : 1);      // phase-B rows per lane group
+  constexpr int QMAX = NSEG <= 1 ? NR_SCAN_QMAX1 : (NSEG <= 2 ? 16 : 8);  // query slots per batch
+  constexpr int UB = NSEG <= 1 ? NR_SCAN_UB1 : (NSEG <= 2 ? 2 : 1);      // phase-B rows per lane group
   __shared__ uint64_t s_ub[4][SCAN_UMAX];        // unit: first payload row
   __shared__ uint32_t s_uv[4][SCAN_UMAX + 1];    // unit: first virtual row
   __shared__ uint32_t s_uq[4][SCAN_UMAX];        // unit: first query slot | queries << 16
@@ -562,7 +574,9 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
             while (uv[cur + 1] <= v) ++cur;
           cus[uu] = cur;
           const uint64_t row = ub[cur] + (v - uv[cur]);
-          hv[uu] = ok[uu] ? load_stream(a.ra.seg(row, 16 * hl)) : make_uint4(0, 0, 0, 0);
+          hv[uu] = ok[uu] ? load_stream(reinterpret_cast<const uint4 *>(a.scan_hb + row * a.scan_hs +
+                                                                        16 * hl))
+                          : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int uu = 0; uu < U; ++uu) {
@@ -626,7 +640,7 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
 template <int IS_U8, int NSEG>
 static hipError_t launch_scan_h(const SharedArgs &a, int hl, int grid, hipStream_t s) {
   switch (hl) {
-    case 1: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 1, 8>), dim3(grid), dim3(256), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 1, NR_SCAN_U1>), dim3(grid), dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 2, 4>), dim3(grid), dim3(256), 0, s, a); break;
     case 4: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 4, 4>), dim3(grid), dim3(256), 0, s, a); break;
     case 8: hipLaunchKernelGGL((k_scan<IS_U8, NSEG, 8, 2>), dim3(grid), dim3(256), 0, s, a); break;
@@ -648,7 +662,8 @@ hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStr
   if (a.nq <= 0) return hipSuccess;
   const int nseg = (a.row_bytes + 127) / 128;
   const int hl = a.scan_head / 16;
-  if (nseg > SHARED_MAX_NSEG || a.scan_head % 16 != 0 || a.scan_head > a.ra.h) return hipErrorInvalidValue;
+  if (nseg > SHARED_MAX_NSEG || a.scan_head % 16 != 0 || a.scan_head > a.row_bytes)
+    return hipErrorInvalidValue;
   const int grid = n_cu * NR_SHARED_BLOCKS_PER_CU;
   return dtype == NR_U8 ? launch_scan_t<1>(a, nseg, hl, grid, s)
                         : launch_scan_t<0>(a, nseg, hl, grid, s);

@@ -283,19 +283,20 @@ int scan_head(const nr_index *ix) {
 // payload addressing for the kernels (row-major or head/tail planes)
 nr::RowAddr row_addr(const nr_index *ix) {
   const uint64_t rb = (uint64_t)ix->d.d * elem_size(ix);
+  const uint64_t H = ix->d.head_bytes > 0 ? (uint64_t)ix->d.head_bytes : 0;
   const unsigned char *base = (const unsigned char *)ix->d.rows;
   nr::RowAddr r;
-  if (ix->d.head_bytes > 0) {
-    r.h = ix->d.head_bytes;
+  if (H > 0 && !ix->d.head_copy) {  // head plane, then tail plane
+    r.h = (int)H;
     r.hb = base;
-    r.hs = (uint64_t)ix->d.head_bytes;
-    r.tb = base + (uint64_t)ix->d.n * (uint64_t)ix->d.head_bytes;
-    r.ts = rb - (uint64_t)ix->d.head_bytes;
-  } else {
+    r.hs = H;
+    r.tb = base + (uint64_t)ix->d.n * H;
+    r.ts = rb - H;
+  } else {  // row-major rows (after the head plane when it is a copy)
     r.h = (int)rb;
-    r.hb = base;
+    r.hb = base + (uint64_t)ix->d.n * H;
     r.hs = rb;
-    r.tb = base;  // unused: every offset is below h
+    r.tb = r.hb;  // unused: every offset is below h
     r.ts = rb;
   }
   return r;
@@ -484,6 +485,8 @@ hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void 
   a.row_bytes = (int)(ix->d.d * elem_size(ix));
   a.g = nr::SHARED_G;
   a.scan_head = scan_head(ix);
+  a.scan_hb = (const unsigned char *)ix->d.rows;  // the head plane, or the rows themselves
+  a.scan_hs = ix->d.head_bytes > 0 ? (uint64_t)ix->d.head_bytes : (uint64_t)a.row_bytes;
   const uint32_t seed = p->shared_seed_rows > 0 ? (uint32_t)p->shared_seed_rows : nr::SEED_ROWS;
   a.seed_min = seed > (uint32_t)k ? seed : (uint32_t)k;
   a.n_clusters = ix->d.n_clusters;
@@ -624,8 +627,10 @@ nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t
   if ((uintptr_t)d.rows % 16 != 0) return fail(NR_EINVAL, "rows must be 16-byte aligned");
   if (d.head_bytes != 0 &&
       ((d.head_bytes != 16 && d.head_bytes != 32 && d.head_bytes != 64 && d.head_bytes != 128) ||
-       (size_t)d.head_bytes > rb - 16))
-    return fail(NR_EINVAL, "head_bytes must be 0, 16, 32, 64 or 128 and leave a tail of >= 16 bytes");
+       (size_t)d.head_bytes > (d.head_copy ? rb : rb - 16)))
+    return fail(NR_EINVAL, "head_bytes must be 0, 16, 32, 64 or 128, at most the row size "
+                           "(row size - 16 without head_copy)");
+  if (d.head_copy != 0 && d.head_copy != 1) return fail(NR_EINVAL, "head_copy must be 0 or 1");
   if (d.n_clusters < 1 || d.n_clusters >= ((int64_t)1 << 32))
     return fail(NR_EINVAL, "n_clusters must be in [1, 2^32)");
 

@@ -170,6 +170,8 @@ struct SharedArgs {
   int64_t n_clusters;
   RowAddr ra;                 // permuted payload
   int scan_head;              // bytes of each row the scan's filter reads (its head)
+  const unsigned char *scan_hb;  // head of row r at scan_hb + r * scan_hs
+  uint64_t scan_hs;
   const int64_t *row_ids;
   const uint64_t *cl_off;
   const void *queries;

@@ -61,7 +61,8 @@ class Index:
     cl_off: object             # uint64 [n_clusters + 1]
     centroids: object          # fp32 [n_clusters, b]
     codes: Optional[object] = None   # uint32 code of each permuted row (diagnostics)
-    head_bytes: int = 0        # 0: rows is [n, d]; else the split layout (see split_payload)
+    head_bytes: int = 0        # 0: rows is [n, d]; else a head plane first (see split_payload)
+    head_copy: int = 0         # with head_bytes: 1 = whole rows follow the heads, 0 = tails
 
     @property
     def n_clusters(self) -> int:
@@ -82,6 +83,9 @@ def payload_rows(ix: Index, idx) -> torch.Tensor:
     if not ix.head_bytes:
         return ix.rows[idx]
     n, R, H = ix.workload.n, ix.row_bytes, ix.head_bytes
+    if ix.head_copy:
+        full = ix.rows[n * H:n * H + n * R].view(n, R)
+        return full[idx].contiguous().view(_row_dtype(ix.workload)).view(-1, ix.workload.d)
     head = ix.rows[:n * H].view(n, H)
     tail = ix.rows[n * H:n * R].view(n, R - H)
     by = torch.cat([head[idx], tail[idx]], dim=1).contiguous()
@@ -93,26 +97,32 @@ def payload_range(ix: Index, s0: int, s1: int) -> torch.Tensor:
     if not ix.head_bytes:
         return ix.rows[s0:s1]
     n, R, H = ix.workload.n, ix.row_bytes, ix.head_bytes
+    if ix.head_copy:
+        full = ix.rows[n * H:n * H + n * R].view(n, R)[s0:s1]
+        return full.contiguous().view(_row_dtype(ix.workload)).view(-1, ix.workload.d)
     head = ix.rows[:n * H].view(n, H)[s0:s1]
     tail = ix.rows[n * H:n * R].view(n, R - H)[s0:s1]
     by = torch.cat([head, tail], dim=1).contiguous()
     return by.view(_row_dtype(ix.workload)).view(-1, ix.workload.d)
 
 
-def split_payload(rows_chunks, n: int, row_bytes: int, head_bytes: int, device) -> torch.Tensor:
-    """Split layout of a payload given as consecutive row-major chunks: one
-    uint8 buffer holding the head plane [n x head_bytes] (the first head_bytes
-    of every row) followed by the tail plane [n x (row_bytes - head_bytes)]."""
+def split_payload(rows_chunks, n: int, row_bytes: int, head_bytes: int, device,
+                  copy: bool = False) -> torch.Tensor:
+    """Head-plane layout of a payload given as consecutive row-major chunks:
+    one uint8 buffer holding the head plane [n x head_bytes] (the first
+    head_bytes of every row) followed by the tail plane [n x (row_bytes -
+    head_bytes)], or with ``copy`` by the whole row-major payload."""
     H, R = head_bytes, row_bytes
-    out = torch.empty(n * R, dtype=torch.uint8, device=device)
+    rest = R if copy else R - H
+    out = torch.empty(n * (H + rest), dtype=torch.uint8, device=device)
     head = out[:n * H].view(n, H)
-    tail = out[n * H:].view(n, R - H)
+    tail = out[n * H:].view(n, rest)
     s0 = 0
     for r in rows_chunks:
         by = r.contiguous().view(torch.uint8).view(r.shape[0], R)
         m = by.shape[0]
         head[s0:s0 + m] = by[:, :H]
-        tail[s0:s0 + m] = by[:, H:]
+        tail[s0:s0 + m] = by if copy else by[:, H:]
         s0 += m
     assert s0 == n
     return out
@@ -337,13 +347,14 @@ def _clusters_per_bucket(w: Workload, sizes: torch.Tensor) -> torch.Tensor:
 def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 20,
                 encoder: Optional[Encoder] = None, keep_codes: bool = True,
                 payload_fn: Optional[Callable] = None, log=None,
-                head_bytes: int = 0) -> Index:
+                head_bytes: int = 0, head_copy: bool = False) -> Index:
     """Build the index of workload ``w`` from ``rows_fn(ids) -> rows``.
 
     ``rows_fn`` returns numpy or torch rows for an int64 id array.  With
     ``payload_fn(perm) -> rows`` the permuted payload is produced directly
     (e.g. regenerated on the GPU) instead of gathered from ``rows_fn``.
-    With ``head_bytes`` > 0 the payload is stored in the split layout.
+    With ``head_bytes`` > 0 the payload starts with a head plane, followed by
+    the tails or (``head_copy``) by the whole rows.
     """
     dev = torch.device(device)
     enc = encoder or seeded_encoder(w)
@@ -450,7 +461,7 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
         else:
             pn = perm.cpu().numpy()
             gen = (rows_t(pn[s0:s0 + big]) for s0 in range(0, n, big))
-        rows = split_payload(gen, n, w.row_bytes, head_bytes, dev)
+        rows = split_payload(gen, n, w.row_bytes, head_bytes, dev, copy=head_copy)
     elif payload_fn is not None:
         rows = payload_fn(perm)
     else:
@@ -463,6 +474,7 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
         rows=rows, row_ids=perm,
         bc_off=bc_off.to(torch.int64), cl_off=cl_off, centroids=centroids.to(torch.float32),
         codes=codes[perm] if keep_codes else None, head_bytes=head_bytes,
+        head_copy=int(bool(head_copy and head_bytes)),
     )
 
 
@@ -477,5 +489,5 @@ def to_numpy(ix: Index) -> Index:
         cl_off=np.ascontiguousarray(f(ix.cl_off)).astype(np.uint64),
         centroids=np.ascontiguousarray(f(ix.centroids)).astype(np.float32),
         codes=None if ix.codes is None else np.ascontiguousarray(f(ix.codes)).astype(np.uint32),
-        head_bytes=ix.head_bytes,
+        head_bytes=ix.head_bytes, head_copy=ix.head_copy,
     )

@@ -57,7 +57,7 @@ class nr_index_desc(C.Structure):
                 ("input_scale", C.c_float), ("tau", C.POINTER(C.c_float)),
                 ("rows", C.c_void_p), ("row_ids", C.c_void_p), ("bc_off", C.c_void_p),
                 ("cl_off", C.c_void_p), ("centroids", C.c_void_p), ("n_clusters", C.c_int64),
-                ("head_bytes", C.c_int32)]
+                ("head_bytes", C.c_int32), ("head_copy", C.c_int32)]
 
 
 class nr_params(C.Structure):
@@ -206,7 +206,7 @@ class Index:
 
     def __init__(self, *, n, d, dtype, b, weights, biases, input_scale, tau, rows, row_ids,
                  bc_off, cl_off, centroids, bn_scale=None, bn_shift=None, head_bytes=0,
-                 stream=None):
+                 head_copy=0, stream=None):
         L = len(weights)
         self._keep = []
         widths = np.array([weights[0].shape[1]] + [w.shape[0] for w in weights], np.int32)
@@ -240,6 +240,7 @@ class Index:
             t.data_ptr() for t in self.dev]
         desc.n_clusters = centroids.shape[0]
         desc.head_bytes = int(head_bytes)
+        desc.head_copy = int(head_copy)
         self.n, self.d, self.dtype, self.b = n, d, dtype, b
         self.n_clusters = int(centroids.shape[0])
         h = C.c_void_p()
@@ -271,7 +272,7 @@ class Index:
                    input_scale=e.input_scale, tau=ix.tau, rows=rows,
                    row_ids=dt(ix.row_ids, torch.int64), bc_off=dt(bc, torch.int32),
                    cl_off=dt(cl, torch.int64), centroids=dt(ix.centroids, torch.float32),
-                   head_bytes=hb, stream=stream)
+                   head_bytes=hb, head_copy=int(getattr(ix, "head_copy", 0) or 0), stream=stream)
 
     def close(self):
         if getattr(self, "handle", None) is not None and self.handle.value:

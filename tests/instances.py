@@ -29,14 +29,16 @@ def head_bytes_for(w) -> int:
     return 16 * (1 if w.dtype == "u8" else 4)
 
 
-def split_index(ix, dev):
-    """A device copy of a row-major host index in the split layout."""
+def split_index(ix, dev, copy=False):
+    """A device copy of a row-major host index with a head plane, followed by
+    the tails or (copy) by the whole rows."""
     import torch
     from dataclasses import replace as dc_replace
     w = ix.workload
     H = head_bytes_for(w)
     rows = torch.from_numpy(np.ascontiguousarray(ix.rows)).to(dev)
-    return dc_replace(ix, rows=IB.split_payload([rows], w.n, w.row_bytes, H, dev), head_bytes=H)
+    return dc_replace(ix, rows=IB.split_payload([rows], w.n, w.row_bytes, H, dev, copy=copy),
+                      head_bytes=H, head_copy=int(copy))
 
 
 def oracle_encoder(ix):

@@ -22,18 +22,22 @@ pytestmark = pytest.mark.gpu
 GATE = dict(m_x=[0.0, 1.0], m_y=[0.5, 2.0])
 
 
-@pytest.mark.parametrize("cfg,P,mode,split", [(4, 640, NR.NR_REFINE_AUTO, True),
-                                               (4, 640, NR.NR_REFINE_PER_QUERY, True),
-                                               (3, 256, NR.NR_REFINE_AUTO, True),
-                                               (3, 256, NR.NR_REFINE_AUTO, False)])
-def test_full_size_sampled_queries(cfg, P, mode, split):
+# layout: "copy" = head plane + whole rows (the benchmark's), "split" = head
+# plane + tails, "rows" = row-major
+@pytest.mark.parametrize("cfg,P,mode,layout", [(4, 640, NR.NR_REFINE_AUTO, "copy"),
+                                                (4, 640, NR.NR_REFINE_PER_QUERY, "copy"),
+                                                (4, 520, NR.NR_REFINE_AUTO, "split"),
+                                                (3, 256, NR.NR_REFINE_AUTO, "copy"),
+                                                (3, 256, NR.NR_REFINE_AUTO, "rows")])
+def test_full_size_sampled_queries(cfg, P, mode, layout):
     if not torch.cuda.is_available():
         pytest.skip("no HIP device")
     dev = torch.device("cuda")
     w = CF.WORKLOADS[cfg]
     data = GpuRows(w, "data", dev)
     ix = IB.build_index(w, data, device=dev, keep_codes=False, payload_fn=lambda p: data(p),
-                        head_bytes=head_bytes_for(w) if split else 0)
+                        head_bytes=0 if layout == "rows" else head_bytes_for(w),
+                        head_copy=layout == "copy")
     try:
         gix = NR.Index.from_built(ix, dev)
         Q = GpuRows(w, "query", dev).range(0, w.n_queries)

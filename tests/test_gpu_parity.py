@@ -36,10 +36,11 @@ def setup_case(name, dev):
         w, ix, X, Q = instance(cfg, n, nq, **dict(ov))
         gix = NR.Index.from_built(ix, dev)
         gix_split = NR.Index.from_built(split_index(ix, dev), dev)
+        gix_copy = NR.Index.from_built(split_index(ix, dev, copy=True), dev)
         enc = oracle_encoder(ix)
         lg, mag = O.encode(enc, Q, with_mag=True)
-        _cache[name] = dict(w=w, ix=ix, X=X, Q=Q, gix=gix, gix_split=gix_split, enc=enc, lg=lg,
-                            mag=mag,
+        _cache[name] = dict(w=w, ix=ix, X=X, Q=Q, gix=gix, gix_split=gix_split,
+                            gix_copy=gix_copy, enc=enc, lg=lg, mag=mag,
                             Qd=torch.from_numpy(Q).to(dev), lgd=torch.from_numpy(lg).to(dev))
     return _cache[name]
 
@@ -143,7 +144,7 @@ def _assert_topk(c, gi, gd, oi, od):
         assert np.allclose(gd[q][: len(ids)], true, rtol=1e-5, atol=1e-6), q
 
 
-@pytest.mark.parametrize("layout", ["gix", "gix_split"])
+@pytest.mark.parametrize("layout", ["gix", "gix_split", "gix_copy"])
 @pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("k", [1, 10, 64])
 def test_refine_given_clusters(dev, name, k, layout):
@@ -172,7 +173,10 @@ MODES = {"per_query": ("gix", dict(refine_mode=NR.NR_REFINE_PER_QUERY)),
          "shared_seed64": ("gix", dict(refine_mode=NR.NR_REFINE_SHARED, shared_seed_rows=64)),
          "split_per_query": ("gix_split", dict(refine_mode=NR.NR_REFINE_PER_QUERY)),
          "split_shared_seed64": ("gix_split", dict(refine_mode=NR.NR_REFINE_SHARED,
-                                                   shared_seed_rows=64))}
+                                                   shared_seed_rows=64)),
+         "copy_per_query": ("gix_copy", dict(refine_mode=NR.NR_REFINE_PER_QUERY)),
+         "copy_shared_seed64": ("gix_copy", dict(refine_mode=NR.NR_REFINE_SHARED,
+                                                 shared_seed_rows=64))}
 
 
 @pytest.mark.parametrize("mode", list(MODES))
@@ -310,7 +314,7 @@ def test_corrupt_index_rejected(dev, what):
     assert err.value.status == NR.NR_ECORRUPT
 
 
-@pytest.mark.parametrize("layout", ["gix", "gix_split"])
+@pytest.mark.parametrize("layout", ["gix", "gix_split", "gix_copy"])
 @pytest.mark.parametrize("name", list(CASES))
 def test_shared_schedule_work_counters(dev, name, layout):
     """The scan really runs on these cases (pairs, rows read whole,
@@ -337,13 +341,13 @@ def test_split_layout_rejects_bad_head(dev):
     c = setup_case("sift", dev)
     ix = c["ix"]
     e = ix.encoder
-    for hb in (8, 48, 128):
+    for hb, copy in ((8, 0), (48, 0), (128, 0), (256, 1), (16, 2)):
         with pytest.raises(NR.NRError) as err:
             NR.Index(n=ix.workload.n, d=ix.workload.d, dtype=NR.NR_U8, b=len(ix.tau),
                      weights=e.weights, biases=e.biases, input_scale=e.input_scale, tau=ix.tau,
                      rows=c["gix_split"].dev[0], row_ids=c["gix_split"].dev[1],
                      bc_off=c["gix_split"].dev[2], cl_off=c["gix_split"].dev[3],
-                     centroids=c["gix_split"].dev[4], head_bytes=hb)
+                     centroids=c["gix_split"].dev[4], head_bytes=hb, head_copy=copy)
         assert err.value.status == NR.NR_EINVAL
 
 
