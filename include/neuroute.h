@@ -230,8 +230,10 @@ nr_status nr_refine(const nr_index *index, const void *queries, int64_t nq, int3
  *   plan    (per-query tiles; shared schedule: pair counts + own-pass tiles),
  *   refine  (the per-query refinement kernel; shared schedule: own pass),
  *   merge   (per-query merge; shared schedule: own-pass merge),
- *   shared_prep, shared_scan, shared_merge (shared schedule only; the last
- *   includes the per-query redo of queries whose survivors overflowed). */
+ *   shared_prep, shared_scan, shared_merge (shared schedule only).  The
+ *   scan's preparation runs on a second stream of the library's, beside the
+ *   seed pass, so shared_prep counts only the part the seed pass did not hide;
+ *   shared_merge includes the per-query redo of queries that lost survivors. */
 #define NR_STAGES 9
 nr_status nr_profile_enable(nr_index *index, int32_t on);
 nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches, int32_t reset);

@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <deque>
 #include <mutex>
 #include <new>
 #include <string>
@@ -82,6 +83,8 @@ struct Buffers {
   void *scan_tmp;
   size_t scan_tmp_bytes;
   bool shared;
+  hipStream_t aux;   // from the workspace
+  hipEvent_t fork, join;
 };
 
 struct Shape {
@@ -158,6 +161,9 @@ struct Workspace {
   hipStream_t stream = nullptr;
   char *base = nullptr;
   size_t bytes = 0;
+  // the shared schedule's second stream (default priority) and its fork/join events
+  hipStream_t aux = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   Buffers last{};
   int64_t last_nq = 0;
   int64_t last_cap = 0;
@@ -178,7 +184,7 @@ struct nr_index {
   int maxw = 0;
   int n_cu = 0;
   std::mutex mu;
-  std::vector<Workspace> ws;
+  std::deque<Workspace> ws;     // stable addresses: callers keep Workspace pointers
   bool profiling = false;
   std::vector<EventSet> pending;
   double stage_ms[NR_STAGES] = {0};
@@ -215,8 +221,16 @@ nr_status workspace_for(nr_index *ix, hipStream_t stream, const Shape &s, Buffer
     }
     w->bytes = grow;
   }
+  if (s.shared && !w->aux) {
+    HIP_OK(hipStreamCreateWithFlags(&w->aux, hipStreamNonBlocking));
+    HIP_OK(hipEventCreateWithFlags(&w->fork, hipEventDisableTiming));
+    HIP_OK(hipEventCreateWithFlags(&w->join, hipEventDisableTiming));
+  }
   size_t dummy;
   *out = carve(w->base, s, &dummy);
+  out->aux = w->aux;
+  out->fork = w->fork;
+  out->join = w->join;
   *wsp = w;
   return NR_OK;
 }
@@ -534,13 +548,20 @@ hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void 
   a.qstats = qstats;
   hipError_t e = nr::launch_shared_hist(a, s);
   if (e != hipSuccess) return e;
+  // the scan's prep needs only the pair counts: it runs on the second stream
+  // while the seed pass runs here
+  e = hipEventRecord(B.fork, s);
+  if (e == hipSuccess) e = hipStreamWaitEvent(B.aux, B.fork, 0);
+  if (e == hipSuccess) e = nr::launch_shared_prep(a, B.aux);
+  if (e == hipSuccess) e = hipEventRecord(B.join, B.aux);
+  if (e != hipSuccess) return e;
   RefineOpts own;
   own.own_cseed = B.cseed;
   e = run_refine(ix, q, nq, k, clus, nclus, cap, B, B.own_ids, B.own_dists, qstats, s, ev, own);
   if (e != hipSuccess) return e;
-  e = nr::launch_shared_prep(a, s);
+  e = hipStreamWaitEvent(s, B.join, 0);
   if (e != hipSuccess) return e;
-  if (ev) (void)hipEventRecord(ev[3], s);
+  if (ev) (void)hipEventRecord(ev[3], s);  // the part of the prep the seed pass did not hide
   e = nr::launch_shared_refine(a, ix->d.dtype, ix->n_cu, s);
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[4], s);
@@ -717,8 +738,12 @@ nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t
 nr_status nr_index_free(nr_index *ix) {
   if (!ix) return NR_OK;
   (void)hipDeviceSynchronize();
-  for (auto &w : ix->ws)
+  for (auto &w : ix->ws) {
     if (w.base) (void)hipFree(w.base);
+    if (w.fork) (void)hipEventDestroy(w.fork);
+    if (w.join) (void)hipEventDestroy(w.join);
+    if (w.aux) (void)hipStreamDestroy(w.aux);
+  }
   for (auto &es : ix->pending)
     for (auto &ev : es.ev) (void)hipEventDestroy(ev);
   if (ix->params) (void)hipFree(ix->params);
