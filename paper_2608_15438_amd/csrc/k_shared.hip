@@ -313,7 +313,7 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
   constexpr int G = SHARED_G;
   constexpr int QCH = NSEG * 8;              // 16-byte chunks of a (padded) query row
   constexpr int QMAX = NSEG <= 1 ? NR_SCAN_QMAX1 : (NSEG <= 2 ? 16 : 8);  // query slots per batch
-  constexpr int UB = NSEG <= 1 ? NR_SCAN_UB1 : (NSEG <= 2 ? 2 : 1);      // phase-B rows per lane group
+  constexpr int UB = NSEG <= 1 ? NR_SCAN_UB1 : (NSEG <= 4 ? 2 : 1);      // phase-B rows per lane group
   __shared__ uint64_t s_ub[4][SCAN_UMAX];        // unit: first payload row
   __shared__ uint32_t s_uv[4][SCAN_UMAX + 1];    // unit: first virtual row
   __shared__ uint32_t s_uq[4][SCAN_UMAX];        // unit: first query slot | queries << 16
@@ -344,6 +344,8 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
   const int k = a.k;
   const unsigned char *queries = (const unsigned char *)a.queries;
   unsigned long long full_rows = 0;
+  uint32_t nbatch = 0, tested_batches = 0;  // direct batches: see below
+  uint64_t tested_rows = 0, open_rows = 0;
   if (ntiles == 0) return;
 
   for (;;) {
@@ -553,8 +555,41 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
         full_rows += (unsigned long long)nsv;
       };
 
+      // ---- direct batches: when the heads this wave has tested so far (at
+      // least 16 batches, drawn from across the work) left more than two
+      // thirds of the rows open, list every row with all its unit's queries
+      // (the head test only ever drops rows, so skipping it changes no
+      // result); every 8th batch still tests
+      ++nbatch;
+      const bool direct = (nbatch & 7) != 0 && tested_batches >= 16 && 3 * open_rows > 2 * tested_rows;
+      if (direct) {
+        int nsv = 0;
+        int cur = 0;
+        for (uint32_t v0 = 0; v0 < vtot; v0 += WAVE) {
+          if (nsv > SCAP - WAVE) {
+            phase_b(nsv);
+            nsv = 0;
+          }
+          const uint32_t v = v0 + lane;
+          const bool ok = v < vtot;
+          if (ok)
+            while (uv[cur + 1] <= v) ++cur;
+          const uint64_t m = ballot(ok);
+          if (ok) {
+            const uint32_t gmu = uq[cur] >> 16;
+            sv[nsv + popc64(m & lanemask_lt())] =
+                ((uint32_t)cur << 20) | ((v - uv[cur]) << 8) | ((1u << gmu) - 1u);
+          }
+          nsv += popc64(m);
+        }
+        phase_b(nsv);
+        __builtin_amdgcn_wave_barrier();
+        continue;
+      }
+
       // ---- phase A: heads of the batch's virtual rows
       int nsv = 0;
+      uint32_t listed = 0;  // rows left open by their heads
       int cur = 0;  // per lane; its virtual rows only increase
       for (uint32_t v0 = 0; v0 < vtot; v0 += STEP) {
         if (nsv > SCAP - STEP) {
@@ -628,9 +663,13 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
                 ((uint32_t)cu << 20) | ((vv[uu] - uv[cu]) << 8) | mask;
           }
           nsv += popc64(m);
+          listed += popc64(m);
         }
       }
       phase_b(nsv);
+      ++tested_batches;
+      tested_rows += vtot;
+      open_rows += listed;
       __builtin_amdgcn_wave_barrier();
     }
   }
@@ -653,6 +692,7 @@ template <int IS_U8>
 static hipError_t launch_scan_t(const SharedArgs &a, int nseg, int hl, int grid, hipStream_t s) {
   if (nseg <= 1) return launch_scan_h<IS_U8, 1>(a, hl, grid, s);
   if (nseg <= 2) return launch_scan_h<IS_U8, 2>(a, hl, grid, s);
+  if (nseg <= 3) return launch_scan_h<IS_U8, 3>(a, hl, grid, s);
   if (nseg <= 4) return launch_scan_h<IS_U8, 4>(a, hl, grid, s);
   if (nseg <= 8) return launch_scan_h<IS_U8, 8>(a, hl, grid, s);
   return hipErrorInvalidValue;

@@ -206,7 +206,7 @@ struct SharedArgs {
   uint32_t *pool2_key;        // [SURVIVOR_POOL] pooled survivors grouped by query
   int64_t *pool2_id;
   unsigned long long *counter;  // work-unit counter
-  int64_t *wstats;            // [4] scanned rows, own-pass tiles, scanned pair rows, rows re-read whole
+  int64_t *wstats;            // [4] scanned rows, seed tiles, scanned pair rows, rows read whole
   void *scan_tmp;
   size_t scan_tmp_bytes;
   int64_t *out_ids;
