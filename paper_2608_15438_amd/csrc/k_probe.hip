@@ -11,39 +11,103 @@
 // the global first-P has its parent in the previous first-P; the recursion is
 // therefore exact, and adding delta_r last reproduces the rank-order sum.
 // Keys are u64 (score bits << 32 | mask): scores are >= +0, so the float bit
-// pattern orders like the value.  Lists live in LDS: L, the output of the
-// merge, and the extension list E (which may need a sort when fp32 rounding
-// maps different scores to one value); each merge is a merge-path merge in
-// which every lane writes one contiguous slice of the output.
+// pattern orders like the value.  The lists live in registers: element
+// i = 64 j + lane of a list of PE = 64 K slots (PE the power of two >= P) is
+// register j of that lane, unused slots hold all ones.  Each step keeps the
+// PE smallest of L and E as min(L[i], E[PE-1-i]) -- a bitonic sequence --
+// and sorts it with a bitonic merge (register pairs for distances >= 64,
+// lane shuffles below).  E is compacted through LDS (one write and one read
+// per step).  E keeps L's order except where fp32 rounding mapped different
+// scores of L to one value and left equal scores out of mask order; such
+// short runs are repaired by odd-even transposition rounds before the merge,
+// and a list that is still unsorted after eight rounds is fully sorted.
 #include "nr_internal.h"
 
 namespace nr {
 
-static __host__ __device__ inline int pow2_ceil(int v) {
-  int p = 1;
-  while (p < v) p <<= 1;
-  return p;
+__device__ __forceinline__ uint64_t xor_u64(uint64_t v, int m) {
+  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
+  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
 }
 
-__host__ __device__ size_t probe_lds_bytes_per_wave(int P) {
-  return sizeof(uint64_t) * (size_t)(2 * P + pow2_ceil(P)) + 32 * (sizeof(int) + sizeof(float));
+__device__ __forceinline__ uint64_t from_lane_u64(uint64_t v, int src) {
+  const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src);
+  const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src);
+  return ((uint64_t)hi << 32) | lo;
 }
 
-__global__ void k_probe(ProbeArgs a) {
-  extern __shared__ __align__(16) unsigned char smem_raw[];
+__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a < b ? b : a; }
+
+// sort a bitonic list ascending
+template <int K>
+__device__ __forceinline__ void bitonic_merge(uint64_t (&v)[K]) {
   const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
-  const int wpb = blockDim.x >> 6;
-  const int64_t q = (int64_t)blockIdx.x * wpb + wave;
+#pragma unroll
+  for (int dj = K / 2; dj >= 1; dj >>= 1) {
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      if ((j & dj) == 0) {
+        const uint64_t x = v[j], y = v[j | dj];
+        v[j] = umin64(x, y);
+        v[j | dj] = umax64(x, y);
+      }
+    }
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) {
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      const uint64_t o = xor_u64(v[j], d);
+      v[j] = (lane & d) ? umax64(v[j], o) : umin64(v[j], o);
+    }
+  }
+}
+
+// sort any list ascending (bitonic sorting network)
+template <int K>
+__device__ __forceinline__ void bitonic_sort(uint64_t (&v)[K]) {
+  const int lane = lane_id();
+  constexpr int PE = 64 * K;
+#pragma unroll
+  for (int kk = 2; kk <= PE; kk <<= 1) {
+#pragma unroll
+    for (int d = kk >> 1; d >= 1; d >>= 1) {
+      if (d >= 64) {
+        const int dj = d >> 6;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+          if ((j & dj) == 0) {
+            const bool asc = ((j * 64) & kk) == 0;
+            const uint64_t x = v[j], y = v[j | dj];
+            v[j] = asc ? umin64(x, y) : umax64(x, y);
+            v[j | dj] = asc ? umax64(x, y) : umin64(x, y);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+          const int i = j * 64 + lane;
+          const uint64_t o = xor_u64(v[j], d);
+          const bool asc = (i & kk) == 0;
+          const bool lower = (lane & d) == 0;
+          v[j] = (lower == asc) ? umin64(v[j], o) : umax64(v[j], o);
+        }
+      }
+    }
+  }
+}
+
+template <int K>
+__global__ void __launch_bounds__(256) k_probe(ProbeArgs a) {
+  constexpr int PE = 64 * K;
+  __shared__ uint64_t s_e[4][PE];
+  const int lane = lane_id();
+  uint64_t *es = s_e[threadIdx.x >> 6];
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (q >= a.nq) return;
   const int P = a.P, b = a.b, l_sel = a.l_sel;
-  const int Pe = pow2_ceil(P);
-  unsigned char *base = smem_raw + (size_t)wave * probe_lds_bytes_per_wave(P);
-  uint64_t *L = reinterpret_cast<uint64_t *>(base);
-  uint64_t *O = L + P;
-  uint64_t *E = O + P;
-  int *sel_dim = reinterpret_cast<int *>(E + Pe);
-  float *sel_dlt = reinterpret_cast<float *>(sel_dim + 32);
 
   // a_j, b0 and delta_j, one dimension per lane
   float l = 0.f, t = 0.f;
@@ -57,122 +121,140 @@ __global__ void k_probe(ProbeArgs a) {
   // rank of each dimension by (delta, dim): SmallestKIndices
   int rank = 0;
   for (int i = 0; i < b; ++i) {
-    float di = __shfl(dl, i);
+    const float di = __shfl(dl, i);
     rank += (di < dl) || (di == dl && i < lane);
   }
-  if (lane < b && rank < l_sel) {
-    sel_dim[rank] = lane;
-    sel_dlt[rank] = dl;
+  // lane r < l_sel: the dimension of rank r and its delta
+  int sel_dim = 0;
+  float sel_dlt = 0.f;
+  for (int i = 0; i < b; ++i) {
+    const int ri = __shfl(rank, i);
+    const float di = __shfl(dl, i);
+    if (lane == ri) {
+      sel_dim = i;
+      sel_dlt = di;
+    }
   }
-  __builtin_amdgcn_wave_barrier();
 
+  uint64_t L[K];
+#pragma unroll
+  for (int j = 0; j < K; ++j) L[j] = ~0ull;
   if (lane == 0) L[0] = 0ull;  // the base address, score 0
   int n = 1;
   for (int r = 0; r < l_sel; ++r) {
-    const float dr = sel_dlt[r];
+    const float dr = __shfl(sel_dlt, r);
     const uint32_t rbit = 1u << r;
-    // extension list E
+    // extension list E: every kept flip set plus rank r, compacted in L's
+    // order through LDS (flip sets at r_max or past s_max drop out)
+    uint64_t E[K];
     int ne = 0;
-    for (int i0 = 0; i0 < n; i0 += WAVE) {
-      int i = i0 + lane;
-      bool ok = false;
-      uint64_t key = 0;
-      if (i < n) {
-        uint64_t k0 = L[i];
-        uint32_t m = (uint32_t)k0;
-        float c = __uint_as_float((uint32_t)(k0 >> 32));
-        float c2 = c + dr;
-        ok = __popc(m) < a.r_max && c2 <= a.s_max;
-        key = ((uint64_t)__float_as_uint(c2) << 32) | (m | rbit);
-      }
-      uint64_t bm = ballot(ok);
-      if (ok) E[ne + popc64(bm & lanemask_lt())] = key;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      const uint64_t k0 = L[j];
+      const uint32_t m = (uint32_t)k0;
+      const float c2 = __uint_as_float((uint32_t)(k0 >> 32)) + dr;
+      const bool ok = k0 != ~0ull && __popc(m) < a.r_max && c2 <= a.s_max;
+      const uint64_t bm = ballot(ok);
+      if (ok) es[ne + popc64(bm & lanemask_lt())] = ((uint64_t)__float_as_uint(c2) << 32) | (m | rbit);
       ne += popc64(bm);
     }
     if (ne == 0) continue;
     __builtin_amdgcn_wave_barrier();
-    // nothing of E can enter a full list whose last score is below E's first
-    if (n == P) {
-      float c_last = __uint_as_float((uint32_t)(L[n - 1] >> 32));
-      float c_e = __uint_as_float((uint32_t)(E[0] >> 32));
-      if (c_e > c_last) continue;
-    }
-    // E is ordered by score; equal scores may be out of mask order
-    bool unsorted = false;
-    for (int i0 = 0; i0 + 1 < ne; i0 += WAVE) {
-      int i = i0 + lane;
-      unsorted |= (i + 1 < ne) && E[i] > E[i + 1];
-    }
-    if (ballot(unsorted)) {
-      int m2 = pow2_ceil(ne);
-      for (int i = ne + lane; i < m2; i += WAVE) E[i] = ~0ull;
-      __builtin_amdgcn_wave_barrier();
-      for (int kk = 2; kk <= m2; kk <<= 1) {
-        for (int j = kk >> 1; j > 0; j >>= 1) {
-          for (int i0 = 0; i0 < m2; i0 += WAVE) {
-            int i = i0 + lane;
-            int ixj = i ^ j;
-            if (i < m2 && ixj > i) {
-              uint64_t x = E[i], y = E[ixj];
-              bool asc = (i & kk) == 0;
-              if ((x > y) == asc) { E[i] = y; E[ixj] = x; }
-            }
-          }
-          __builtin_amdgcn_wave_barrier();
-        }
-      }
-    }
-    // merge path: lane l writes output slots [o0, o1) of the first P of
-    // L merge E; keys are distinct (only E's masks hold bit r)
-    {
-      const int nout = n + ne < P ? n + ne : P;
-      const int per = (nout + WAVE - 1) / WAVE;
-      const int o0 = lane * per;
-      const int o1 = o0 + per < nout ? o0 + per : nout;
-      if (o0 < o1) {
-        int lo = o0 - ne > 0 ? o0 - ne : 0;
-        int hi = o0 < n ? o0 : n;
-        while (lo < hi) {  // how many of the first o0 outputs come from L
-          const int mid = (lo + hi) >> 1;
-          if (L[mid] < E[o0 - mid - 1]) lo = mid + 1; else hi = mid;
-        }
-        int i = lo, j = o0 - lo;
-        uint64_t x = i < n ? L[i] : ~0ull;
-        uint64_t y = j < ne ? E[j] : ~0ull;
-        for (int o = o0; o < o1; ++o) {
-          if (x < y) {
-            O[o] = x;
-            ++i;
-            x = i < n ? L[i] : ~0ull;
-          } else {
-            O[o] = y;
-            ++j;
-            y = j < ne ? E[j] : ~0ull;
-          }
-        }
-      }
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      const int i = j * 64 + lane;
+      E[j] = i < ne ? es[i] : ~0ull;
     }
     __builtin_amdgcn_wave_barrier();
+    // E follows L's order except inside runs of scores that rounding made
+    // equal: odd-even transposition rounds repair such short runs; a list
+    // still unsorted after 8 rounds gets the full sorting network.  Lane j of
+    // bn / bp holds element 64 (j + 1) / 64 j - 1 (the neighbours across
+    // register boundaries), taken before a round changes anything.
+    for (int round = 0;; ++round) {
+      uint64_t bn = ~0ull, bp = 0ull;
+#pragma unroll
+      for (int j = 0; j < K; ++j) {
+        if (j + 1 < K) {
+          const uint64_t v = bcast_u64(E[j + 1 < K ? j + 1 : j], 0);
+          if (lane == j) bn = v;
+        }
+        if (j > 0) {
+          const uint64_t v = bcast_u64(E[j > 0 ? j - 1 : j], 63);
+          if (lane == j) bp = v;
+        }
+      }
+      bool inv = false;
+#pragma unroll
+      for (int j = 0; j < K; ++j) {
+        // every lane takes part in both exchanges before the select
+        const uint64_t up = from_lane_u64(E[j], lane < 63 ? lane + 1 : lane);
+        const uint64_t bj = bcast_u64(bn, j);
+        const uint64_t nx = lane == 63 ? bj : up;
+        inv |= E[j] > nx;
+      }
+      if (!ballot(inv)) break;
+      if (round == 8) {
+        bitonic_sort<K>(E);
+        break;
+      }
+#pragma unroll
+      for (int parity = 0; parity < 2; ++parity) {
+        if (parity == 1) {  // the even round moved values: new boundary neighbours
+          bn = ~0ull;
+          bp = 0ull;
+#pragma unroll
+          for (int j = 0; j < K; ++j) {
+            if (j + 1 < K) {
+              const uint64_t v = bcast_u64(E[j + 1 < K ? j + 1 : j], 0);
+              if (lane == j) bn = v;
+            }
+            if (j > 0) {
+              const uint64_t v = bcast_u64(E[j > 0 ? j - 1 : j], 63);
+              if (lane == j) bp = v;
+            }
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+          // pairs (i, i + 1) with i of this parity; 64 is even, so the pair
+          // of lane 63 and the next register's lane 0 has odd parity
+          const uint64_t up = from_lane_u64(E[j], lane < 63 ? lane + 1 : lane);
+          const uint64_t dn = from_lane_u64(E[j], lane > 0 ? lane - 1 : lane);
+          const uint64_t bnj = bcast_u64(bn, j), bpj = bcast_u64(bp, j);
+          const uint64_t nx = lane == 63 ? bnj : up;
+          const uint64_t pv = lane == 0 ? bpj : dn;
+          const bool first = (lane & 1) == parity;
+          E[j] = first ? umin64(E[j], nx) : umax64(E[j], pv);
+        }
+      }
+    }
+    // the PE smallest of L and E, then sorted
+#pragma unroll
+    for (int j = 0; j < K; ++j) L[j] = umin64(L[j], from_lane_u64(E[K - 1 - j], 63 - lane));
+    bitonic_merge<K>(L);
     n = n + ne < P ? n + ne : P;
-    uint64_t *tmp = L; L = O; O = tmp;
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+      if (j * 64 + lane >= P) L[j] = ~0ull;
   }
 
   // codes, scores and bins of the sequence
-  for (int i0 = 0; i0 < n; i0 += WAVE) {
-    int i = i0 + lane;
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    const int i = j * 64 + lane;
+    const uint64_t key = L[j];
+    const uint32_t m = (uint32_t)key;
+    uint32_t code = code0;
+    for (int r = 0; r < l_sel; ++r) {
+      const int dim = __shfl(sel_dim, r);
+      if ((m >> r) & 1u) code ^= 1u << dim;
+    }
     if (i < n) {
-      uint64_t key = L[i];
-      uint32_t m = (uint32_t)key;
-      float c = __uint_as_float((uint32_t)(key >> 32));
-      uint32_t code = code0;
-      while (m) {
-        int rr = __ffs(m) - 1;
-        m &= m - 1;
-        code ^= 1u << sel_dim[rr];
-      }
+      const float c = __uint_as_float((uint32_t)(key >> 32));
       int bin = i;
       if (a.finite) {
-        int z = (int)floorf(c * a.bin_scale);
+        const int z = (int)floorf(c * a.bin_scale);
         bin = z < a.n_bins - 1 ? z : a.n_bins - 1;
       }
       a.codes[q * P + i] = code;
@@ -185,18 +267,20 @@ __global__ void k_probe(ProbeArgs a) {
 
 hipError_t launch_probe(const ProbeArgs &a, hipStream_t s) {
   if (a.nq <= 0) return hipSuccess;
-  size_t per = probe_lds_bytes_per_wave(a.P);
-  int wpb = 4;
-  while (wpb > 1 && per * wpb > 64 * 1024) wpb >>= 1;
-  int64_t blocks = (a.nq + wpb - 1) / wpb;
-  size_t lds = per * wpb;
-  if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void *)k_probe,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
+  const unsigned blocks = (unsigned)((a.nq + 3) / 4);
+  const int P = a.P;
+#define NR_PROBE_CASE(KK)                                                          \
+  if (P <= 64 * KK) {                                                              \
+    hipLaunchKernelGGL(k_probe<KK>, dim3(blocks), dim3(256), 0, s, a);             \
+    return hipGetLastError();                                                      \
   }
-  hipLaunchKernelGGL(k_probe, dim3((unsigned)blocks), dim3(64 * wpb), lds, s, a);
-  return hipGetLastError();
+  NR_PROBE_CASE(1)
+  NR_PROBE_CASE(2)
+  NR_PROBE_CASE(4)
+  NR_PROBE_CASE(8)
+  NR_PROBE_CASE(16)
+#undef NR_PROBE_CASE
+  return hipErrorInvalidValue;
 }
 
 }  // namespace nr

@@ -217,7 +217,6 @@ struct SharedArgs {
 
 hipError_t launch_encode_layer(const EncodeLayerArgs &a, hipStream_t s);
 hipError_t launch_probe(const ProbeArgs &a, hipStream_t s);
-__host__ __device__ size_t probe_lds_bytes_per_wave(int P);
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
