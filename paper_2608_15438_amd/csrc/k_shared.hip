@@ -128,6 +128,23 @@ __global__ void __launch_bounds__(256) k_pair_hist(SharedArgs a) {
     a.cseed[q] = cs < 0 ? n : cs;
     a.rfull[q] = run > 0xffffffffull ? 0u : (uint32_t)run;
   }
+  // uint8 rows: |q|^2 and the part of it over the scan's head, one 16-byte
+  // chunk per lane (rows are at most 64 chunks); integer sums, so the order
+  // of the additions does not matter
+  if (a.is_u8) {
+    uint32_t p = 0;
+    if (16 * lane < a.row_bytes) {
+      const uint4 v = *reinterpret_cast<const uint4 *>((const unsigned char *)a.queries +
+                                                       (uint64_t)q * a.row_bytes + 16 * lane);
+      p = __builtin_amdgcn_udot4(v.x, v.x, p, false);
+      p = __builtin_amdgcn_udot4(v.y, v.y, p, false);
+      p = __builtin_amdgcn_udot4(v.z, v.z, p, false);
+      p = __builtin_amdgcn_udot4(v.w, v.w, p, false);
+    }
+    const uint32_t full = wave_sum_u32(p);
+    const uint32_t head = wave_sum_u32(16 * lane < a.scan_head ? p : 0u);
+    if (lane == 0) a.qnorm[q] = make_uint2(full, head);
+  }
 }
 
 hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s) {
@@ -314,6 +331,7 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
   constexpr int QCH = NSEG * 8;              // 16-byte chunks of a (padded) query row
   constexpr int QMAX = NSEG <= 1 ? NR_SCAN_QMAX1 : (NSEG <= 2 ? 16 : 8);  // query slots per batch
   constexpr int UB = NSEG <= 1 ? NR_SCAN_UB1 : (NSEG <= 4 ? 2 : 1);      // phase-B rows per lane group
+  static_assert(QMAX <= WAVE, "one query slot per lane");
   __shared__ uint64_t s_ub[4][SCAN_UMAX];        // unit: first payload row
   __shared__ uint32_t s_uv[4][SCAN_UMAX + 1];    // unit: first virtual row
   __shared__ uint32_t s_uq[4][SCAN_UMAX];        // unit: first query slot | queries << 16
@@ -441,9 +459,12 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
     }
 
     while (have && wo + (uint64_t)gi * sz + ch * SHARED_ROWS < we) {
-      // ---- a batch of consecutive units of this tile
+      // ---- a batch of consecutive units of this tile; lane s fetches the
+      // query of slot s as its unit joins, and nothing waits for those loads
+      // until the batch is complete
       int nu = 0, nqs = 0, gmax = 0;
       uint32_t vtot = 0;
+      uint32_t myq = 0;
       while (have && nu < SCAN_UMAX && wo + (uint64_t)gi * sz + ch * SHARED_ROWS < we) {
         const int gm = mq - gi * G < (uint32_t)G ? (int)(mq - gi * G) : G;
         if (nqs + gm > QMAX) break;
@@ -454,7 +475,7 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
           uv[nu] = vtot;
           uq[nu] = (uint32_t)nqs | ((uint32_t)gm << 16);
         }
-        if (lane < gm) qi[nqs + lane] = a.pair_q[hp + gi * G + lane];
+        if (lane >= nqs && lane < nqs + gm) myq = a.pair_q[hp + gi * G + (lane - nqs)];
         ++nu;
         nqs += gm;
         vtot += nrows;
@@ -462,42 +483,43 @@ __global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
         next_unit();
       }
       if (lane == 0) uv[nu] = vtot;
-      __builtin_amdgcn_wave_barrier();
-      // ---- the batch's queries: rows into LDS, bounds, |q|^2
+      // ---- the batch's queries: rows into LDS, bounds, |q|^2 (one slot per
+      // lane).  myq is a valid query id in every lane (0 in lanes without a
+      // slot), so all loads go out unconditionally and together; what lies
+      // past the batch's slots or the row is replaced by zeros afterwards
+      constexpr int QL = QMAX * QCH / WAVE;
+      static_assert(QMAX * QCH % WAVE == 0, "whole loads of query chunks");
+      uint4 qload[QL];
 #pragma unroll
-      for (int c0 = 0; c0 < QMAX * QCH; c0 += WAVE) {
-        const int c = c0 + lane;
+      for (int t = 0; t < QL; ++t) {
+        const int c = t * WAVE + lane;
         const int sl = c / QCH;
         const int off = (c - sl * QCH) * 16;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (sl < nqs && off < rb) v = *(const uint4 *)(queries + (uint64_t)qi[sl] * rb + off);
-        qs[c] = v;
+        const uint32_t qsl = (uint32_t)__shfl((int)myq, sl);
+        qload[t] = *(const uint4 *)(queries + (uint64_t)qsl * rb + (off < rb ? off : 0));
       }
-      for (int sl = lane; sl < nqs; sl += WAVE) {
-        const uint32_t q = qi[sl];
-        const int64_t id = a.own_ids[(int64_t)q * k + k - 1];
-        const float d = a.own_dists[(int64_t)q * k + k - 1];
-        const uint32_t bound = id < 0 ? 0xffffffffu : (a.is_u8 ? (uint32_t)d : __float_as_uint(d));
-        tk[sl] = bound;
+      const int64_t own_id = a.own_ids[(int64_t)myq * k + k - 1];
+      const float own_d = a.own_dists[(int64_t)myq * k + k - 1];
+      const uint2 qn = IS_U8 ? a.qnorm[myq] : make_uint2(0, 0);
+#pragma unroll
+      for (int t = 0; t < QL; ++t) {
+        const int c = t * WAVE + lane;
+        const int sl = c / QCH;
+        const int off = (c - sl * QCH) * 16;
+        qs[c] = sl < nqs && off < rb ? qload[t] : make_uint4(0, 0, 0, 0);
+      }
+      if (lane < nqs) {
+        const uint32_t bound =
+            own_id < 0 ? 0xffffffffu : (a.is_u8 ? (uint32_t)own_d : __float_as_uint(own_d));
+        qi[lane] = myq;
+        tk[lane] = bound;
         if (IS_U8) {
-          const uint4 *qp = reinterpret_cast<const uint4 *>(queries + (uint64_t)q * rb);
-          uint32_t full = 0, head = 0;
-          for (int c = 0; c < rb / 16; ++c) {
-            const uint4 v = qp[c];
-            uint32_t p = 0;
-            p = __builtin_amdgcn_udot4(v.x, v.x, p, false);
-            p = __builtin_amdgcn_udot4(v.y, v.y, p, false);
-            p = __builtin_amdgcn_udot4(v.z, v.z, p, false);
-            p = __builtin_amdgcn_udot4(v.w, v.w, p, false);
-            full += p;
-            if (c < HL) head += p;
-          }
-          qqs[sl] = (int32_t)full;
-          th[sl] = bound == 0xffffffffu ? INT32_MAX : (int32_t)((int64_t)bound - (int64_t)head);
+          qqs[lane] = (int32_t)qn.x;
+          th[lane] = bound == 0xffffffffu ? INT32_MAX : (int32_t)((int64_t)bound - (int64_t)qn.y);
         } else {
-          qqs[sl] = 0;
-          th[sl] = bound == 0xffffffffu ? (int32_t)__float_as_uint(INFINITY)
-                                        : (int32_t)__float_as_uint(__uint_as_float(bound) * 1.0001f);
+          qqs[lane] = 0;
+          th[lane] = bound == 0xffffffffu ? (int32_t)__float_as_uint(INFINITY)
+                                          : (int32_t)__float_as_uint(__uint_as_float(bound) * 1.0001f);
         }
       }
       __builtin_amdgcn_wave_barrier();

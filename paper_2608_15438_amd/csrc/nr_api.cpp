@@ -78,6 +78,7 @@ struct Buffers {
   uint32_t *skey;
   int64_t *sid;
   uint32_t *pair_q, *hist, *cnt2, *hoff, *isshared, *spos, *slist;
+  uint2 *qnorm;
   uint64_t *swork, *swork_off;
   int64_t *wstats;
   void *scan_tmp;
@@ -142,6 +143,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.pool2_key = c.take<uint32_t>(nr::SURVIVOR_POOL);
     B.pool2_id = c.take<int64_t>(nr::SURVIVOR_POOL);
     B.pair_q = c.take<uint32_t>((size_t)s.nq * s.cap);
+    B.qnorm = c.take<uint2>((size_t)s.nq);
     B.hist = c.take<uint32_t>(nc1);
     B.cnt2 = c.take<uint32_t>(nc1);
     B.hoff = c.take<uint32_t>(nc1);
@@ -527,6 +529,7 @@ hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void 
   a.swork = B.swork;
   a.swork_off = B.swork_off;
   a.pair_q = B.pair_q;
+  a.qnorm = B.qnorm;
   a.scnt = B.scnt;
   a.skey = B.skey;
   a.sid = B.sid;

@@ -194,6 +194,7 @@ struct SharedArgs {
   uint64_t *swork;            // [n_clusters + 1] rows x query groups of slist[i], 0 past the list
   uint64_t *swork_off;        // [n_clusters + 1] exclusive scan of swork
   uint32_t *pair_q;           // [pairs] query of each scanned pair, grouped by cluster
+  uint2 *qnorm;               // [nq] uint8 rows: (|q|^2, |q head|^2 over scan_head bytes)
   int32_t *scnt;              // [nq] survivors appended
   uint32_t *skey;             // [nq x SURVIVOR_CAP]
   int64_t *sid;
@@ -266,6 +267,10 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 }
 __device__ __forceinline__ float wave_min_f32(float v) {
   for (int m = 32; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m));
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+  for (int m = 32; m >= 1; m >>= 1) v += (uint32_t)__shfl_xor((int)v, m);
   return v;
 }
 // inclusive scan over the wave (u32)
