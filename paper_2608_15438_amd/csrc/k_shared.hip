@@ -38,16 +38,22 @@
 #define NR_SHARED_TILE 4096     // work (rows x query groups) per scan tile
 #endif
 #ifndef NR_SCAN_U1
-#define NR_SCAN_U1 8            // head loads in flight per lane (16-byte heads)
+#define NR_SCAN_U1 6            // head loads in flight per lane (16-byte heads)
 #endif
 #ifndef NR_SCAN_UB1
 #define NR_SCAN_UB1 4           // whole rows in flight per lane group (128-byte rows)
 #endif
 #ifndef NR_SCAN_SLACK
-#define NR_SCAN_SLACK 128       // listed rows beyond one pass before whole rows are read
+#define NR_SCAN_SLACK 124       // listed rows beyond one pass before whole rows are read
 #endif
 #ifndef NR_SCAN_QMAX1
 #define NR_SCAN_QMAX1 32        // query slots per batch (128-byte rows)
+#endif
+// waves per SIMD the register budget is sized for, rows of one 128-byte
+// segment (five blocks of four waves per CU also need at most 32 KiB of LDS
+// per block); longer rows keep what their registers allow
+#ifndef NR_SCAN_WAVES1
+#define NR_SCAN_WAVES1 5
 #endif
 
 namespace nr {
@@ -323,7 +329,7 @@ __device__ __forceinline__ uint32_t pair_key(const uint4 *xv, const uint4 *qv, i
 }
 
 template <int IS_U8, int NSEG, int HL, int U>
-__global__ void __launch_bounds__(256) k_scan(SharedArgs a) {
+__global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(SharedArgs a) {
   constexpr int RPW = WAVE / HL;             // virtual rows per phase-A load
   constexpr int STEP = RPW * U;              // virtual rows per phase-A pass
   constexpr int SCAP = STEP + NR_SCAN_SLACK;  // listed rows before phase B runs
