@@ -17,7 +17,10 @@
 // is sorted across the wave (bitonic), then merged by ranks: batch element i
 // lands at i + |{h < key_i}|, a heap element moves up by |{batch < h}|; the
 // moving tail is rewritten from the top down so no element is overwritten
-// before it is read.  Probe lookups are fetched 64 at a time into LDS.
+// before it is read.  A first pass looks up every probe's bucket in the
+// directory (one thread per probe); the per-query pass stages the ranges of
+// its first pst probes in LDS with one round of loads and walks them 64 at a
+// time.
 #include "nr_internal.h"
 
 namespace nr {
@@ -47,13 +50,15 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   RouteLds &S = *reinterpret_cast<RouteLds *>(smem_raw);
   uint64_t *H = reinterpret_cast<uint64_t *>(smem_raw + sizeof(RouteLds));
+  uint32_t *st_c0 = reinterpret_cast<uint32_t *>(H + a.k_c);
+  uint32_t *st_c1 = st_c0 + a.pst;
+  int32_t *st_bin = reinterpret_cast<int32_t *>(st_c1 + a.pst);
   const int lane = lane_id();
   const int64_t q = blockIdx.x;
   if (q >= a.nq) return;
   const int b = a.b, P = a.P, k_c = a.k_c;
   const float lg = lane < b ? a.logits[q * b + lane] : 0.0f;
   const int cnt = a.counts[q];
-  const uint32_t *codes = a.codes + q * P;
   const int32_t *bins = a.bins + q * P;
   uint32_t *out = a.clus + q * a.cap;
 
@@ -77,11 +82,19 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     if (lane < nb) {
       cid = S.pend[lane];
       const float *mu = a.centroids + (int64_t)cid * b;
+      // the whole centroid row is loaded at once (b <= 30; unused slots read
+      // coordinate 0), then accumulated in dimension order
+      float m[32];
+#pragma unroll
+      for (int j = 0; j < 32; ++j) m[j] = mu[j < b ? j : 0];
       float acc = 0.0f;
-      for (int j = 0; j < b; ++j) {
-        float lj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lg), j));
-        float t = lj - mu[j];
-        acc = fmaf(t, t, acc);
+#pragma unroll
+      for (int j = 0; j < 32; ++j) {
+        if (j < b) {
+          const float lj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lg), j));
+          const float t = lj - m[j];
+          acc = fmaf(t, t, acc);
+        }
       }
       d = acc;
     }
@@ -93,7 +106,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     const float theta_f = d_min + am;
     const bool valid = lane < nb && d <= theta;
     uint64_t key = valid ? (((uint64_t)__float_as_uint(d) << 32) | cid) : ~0ull;
-    key = wave_sort_u64(key);
+    key = wave_sort_u64(key, nb);
     const int nv = popc64(ballot(valid));
     // prune H to d <= theta (a prefix, as H is sorted)
     const uint64_t cut = ((uint64_t)__float_as_uint(theta) + 1ull) << 32;
@@ -138,16 +151,47 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   int p = 0;                 // next probe of the sequence
   int wb = 0;                // window: probes [wb, wb + WAVE), slot = lane
   bool have_window = false;
+  // the window after the current one is fetched ahead: it usually starts
+  // where the current one ends
+  // the query's first nst probe ranges are staged in LDS at once; windows
+  // copy from there (and read the global ranges only past nst)
+  const uint2 *lk = a.lk + q * P;
+  const int nst = cnt < a.pst ? cnt : a.pst;
+  for (int base = 0; base < nst; base += 8 * WAVE) {
+    uint2 v[8];
+    int bv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = base + u * WAVE + lane;
+      const int ii = i < nst ? i : 0;
+      v[u] = lk[ii];
+      bv[u] = bins[ii];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = base + u * WAVE + lane;
+      if (i < nst) {
+        st_c0[i] = v[u].x;
+        st_c1[i] = v[u].y;
+        st_bin[i] = bv[u];
+      }
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
   auto load_window = [&]() {
     wb = p;
     have_window = true;
     const int i = wb + lane;
     uint32_t c0 = 0, c1 = 0;
     int bn = 0x7fffffff;
-    if (i < cnt) {
-      const uint32_t code = codes[i];
-      c0 = a.bc_off[code];
-      c1 = a.bc_off[(uint64_t)code + 1];
+    if (i < nst) {
+      c0 = st_c0[i];
+      c1 = st_c1[i];
+      bn = st_bin[i];
+    } else if (i < cnt) {
+      const uint2 cc = lk[i];
+      c0 = cc.x;
+      c1 = cc.y;
       bn = bins[i];
     }
     S.wc0[lane] = c0;
@@ -278,9 +322,30 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   }
 }
 
+// one thread per probe: the cluster range [c0, c1) of its bucket
+__global__ void k_route_lookup(RouteArgs a) {
+  const int64_t n = a.nq * a.P;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += stride) {
+    const int64_t q = t / a.P;
+    if (t - q * a.P >= a.counts[q]) continue;
+    const uint32_t code = a.codes[t];
+    a.lk[t] = make_uint2(a.bc_off[code], a.bc_off[(uint64_t)code + 1]);
+  }
+}
+
+size_t route_lds_bytes(int k_c, int pst) {
+  return sizeof(RouteLds) + sizeof(uint64_t) * (size_t)k_c + 3 * sizeof(uint32_t) * (size_t)pst;
+}
+
 hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
   if (a.nq <= 0) return hipSuccess;
-  size_t lds = sizeof(RouteLds) + sizeof(uint64_t) * (size_t)a.k_c;
+  {
+    int64_t blocks = (a.nq * a.P + 255) / 256;
+    if (blocks > 16384) blocks = 16384;
+    hipLaunchKernelGGL(k_route_lookup, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  }
+  size_t lds = route_lds_bytes(a.k_c, a.pst);
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void *)k_route,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -90,6 +90,8 @@ struct RouteArgs {
   const int32_t *bins;
   const int32_t *counts;
   const uint32_t *bc_off;
+  uint2 *lk;             // [nq x P] scratch: cluster range of each probe's bucket
+  int pst;               // probes per query whose ranges are staged in LDS
   const float *centroids;
   int k_c, b_batch, b_min, t_low, u_heap, u_front;
   float alpha_front;
@@ -218,6 +220,7 @@ struct SharedArgs {
 
 hipError_t launch_encode_layer(const EncodeLayerArgs &a, hipStream_t s);
 hipError_t launch_probe(const ProbeArgs &a, hipStream_t s);
+size_t route_lds_bytes(int k_c, int pst);
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
@@ -290,10 +293,13 @@ __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
   }
   return v;
 }
-// ascending bitonic sort of one u64 key per lane
-__device__ __forceinline__ uint64_t wave_sort_u64(uint64_t key) {
+// ascending bitonic sort of one u64 key per lane, where every lane from n on
+// holds ~0: only the first power of two >= n lanes need the network
+__device__ __forceinline__ uint64_t wave_sort_u64(uint64_t key, int n = WAVE) {
   int l = lane_id();
-  for (int k = 2; k <= WAVE; k <<= 1) {
+  int top = 2;
+  while (top < n && top < WAVE) top <<= 1;
+  for (int k = 2; k <= top; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
       uint64_t other = shfl_xor_u64(key, j);
       bool up = (l & k) == 0;
