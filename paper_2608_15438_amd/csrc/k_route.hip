@@ -31,6 +31,7 @@ struct RouteLds {
   uint32_t wpre[WAVE];            // exclusive prefix of multi-cluster sizes
   uint32_t pend[WAVE];            // pending batch (cluster ids)
   uint64_t bkey[WAVE];            // sorted batch keys
+  float wd[WAVE];                 // distances of the window's first multi-bucket clusters
 };
 
 __device__ __forceinline__ float margin_dev(const RouteArgs &a, float x) {
@@ -72,8 +73,30 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     return a.early_stop_on && h == k_c && b_proc >= a.b_min && t_low >= a.t_low;
   };
 
-  // score the pending batch and fold it into H
-  auto run_batch = [&]() {
+  // distance of one centroid to the query's logits, dimensions in order
+  auto centroid_dist = [&](uint32_t cid) {
+    const float *mu = a.centroids + (int64_t)cid * b;
+    // the whole centroid row is loaded at once (b <= 30; unused slots read
+    // coordinate 0), then accumulated in dimension order
+    float m[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) m[j] = mu[j < b ? j : 0];
+    float acc = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      if (j < b) {
+        const float lj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lg), j));
+        const float t = lj - m[j];
+        acc = fmaf(t, t, acc);
+      }
+    }
+    return acc;
+  };
+  int npre = 0;  // S.wd holds the distances of window clusters [0, npre)
+
+  // score the pending batch and fold it into H; with pre >= 0 the batch is
+  // window clusters pre, pre + 1, ... whose distances may already be in S.wd
+  auto run_batch = [&](int pre) {
     const int nb = npend;
     n_batches += 1;
     n_scored += nb;
@@ -81,22 +104,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     uint32_t cid = 0;
     if (lane < nb) {
       cid = S.pend[lane];
-      const float *mu = a.centroids + (int64_t)cid * b;
-      // the whole centroid row is loaded at once (b <= 30; unused slots read
-      // coordinate 0), then accumulated in dimension order
-      float m[32];
-#pragma unroll
-      for (int j = 0; j < 32; ++j) m[j] = mu[j < b ? j : 0];
-      float acc = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 32; ++j) {
-        if (j < b) {
-          const float lj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lg), j));
-          const float t = lj - m[j];
-          acc = fmaf(t, t, acc);
-        }
-      }
-      d = acc;
+      d = pre >= 0 && pre + lane < npre ? S.wd[pre + lane] : centroid_dist(cid);
     }
     float dm = wave_min_f32(d);
     d_min = dm < d_min ? dm : d_min;
@@ -206,7 +214,33 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     // window at a time; the stop test after each of them can only fire
     // where b_proc reaches B_min, which is found in closed form.
     while (p < cnt && !stop) {
-      if (!have_window || p >= wb + WAVE) load_window();
+      if (!have_window || p >= wb + WAVE) {
+        load_window();
+        // the window's multi-bucket clusters, numbered in slot order: the
+        // first 64 are scored here at once, so their batches need no loads
+        const int limw = cnt - wb < WAVE ? cnt - wb : WAVE;
+        const uint32_t wsz = lane < limw ? S.wc1[lane] - S.wc0[lane] : 0u;
+        const uint32_t msz = wsz >= 2 ? wsz : 0u;
+        const uint32_t incl = wave_incl_scan_u32(msz);
+        const uint32_t total = (uint32_t)__shfl((int)incl, WAVE - 1);
+        S.wpre[lane] = incl - msz;
+        __builtin_amdgcn_wave_barrier();
+        npre = total < (uint32_t)WAVE ? (int)total : WAVE;
+        if (npre > 0) {
+          float dw = 0.0f;
+          if (lane < npre) {
+            // the slot owning number lane: the last slot whose prefix is <= lane
+            int lo = 0, hi = limw - 1;
+            while (lo < hi) {
+              const int mid = (lo + hi + 1) >> 1;
+              if (S.wpre[mid] <= (uint32_t)lane) lo = mid; else hi = mid - 1;
+            }
+            dw = centroid_dist(S.wc0[lo] + ((uint32_t)lane - S.wpre[lo]));
+          }
+          S.wd[lane] = dw;
+          __builtin_amdgcn_wave_barrier();
+        }
+      }
       const int off = p - wb;
       const int lim = cnt - wb < WAVE ? cnt - wb : WAVE;
       const bool valid = lane >= off && lane < lim;
@@ -246,7 +280,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
           if ((uint32_t)lane < take) S.pend[lane] = v + lane;
           __builtin_amdgcn_wave_barrier();
           npend = (int)take;
-          run_batch();
+          run_batch((int)(S.wpre[first_multi] + (v - mc0)));
           v += take;
         }
         if (!stop && full_and_quiet()) stop = true;
@@ -295,13 +329,13 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
             __builtin_amdgcn_wave_barrier();
             npend += (int)take;
             v += take;
-            if (npend == a.b_batch) run_batch();
+            if (npend == a.b_batch) run_batch(-1);
           }
         }
         p += run;
         if (off + run < WAVE) break;  // bin z ends inside this window
       }
-      if (!stop && npend > 0) run_batch();
+      if (!stop && npend > 0) run_batch(-1);
       npend = 0;
       if (!stop && full_and_quiet()) stop = true;
     }
