@@ -67,11 +67,13 @@ __global__ void __launch_bounds__(256) k_plan_rows(PlanArgs a) {
   uint32_t *co = a.clus_out ? a.clus_out + q * a.cap : nullptr;
   int nout = 0;
   if (lane == 0) pre[0] = 0;
-  for (int i0 = 0; i0 < n; i0 += WAVE) {
+  // the compacted seed pass needs only the leading clusters
+  const int nw = co && a.own_cseed && own0 < n ? own0 : n;
+  for (int i0 = 0; i0 < nw; i0 += WAVE) {
     const int i = i0 + lane;
     uint32_t c = 0;
     uint64_t sz = 0;
-    if (i < n) {
+    if (i < nw) {
       c = cl[i];
       if (c < a.n_clusters) {
         sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];

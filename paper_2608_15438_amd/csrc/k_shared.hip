@@ -112,23 +112,33 @@ __global__ void __launch_bounds__(256) k_pair_hist(SharedArgs a) {
   if (q >= a.nq) return;
   const int n = clamp_n(a.nclus[q], a.cap);
   const uint32_t *cl = a.clus + q * a.cap;
+  // rows of the leading clusters, and of the whole list when eager_rows is
+  // set (otherwise the sizes of the later clusters are not needed here)
+  const bool all = a.eager_rows != 0;
   uint64_t run = 0;
   int cs = -1;
   for (int i0 = 0; i0 < n; i0 += WAVE) {
     const int i = i0 + lane;
+    const bool sizes = cs < 0 || all;
     uint32_t c = 0xffffffffu;
     uint64_t sz = 0;
     if (i < n) {
       c = cl[i];
-      if (c < a.n_clusters) sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
+      if (sizes && c < a.n_clusters) sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
     }
-    const uint64_t incl = wave_incl_scan_u64(sz);
-    if (cs < 0) {
-      const uint64_t hit = ballot(i < n && run + incl >= a.seed_min);
-      if (hit) cs = i0 + __ffsll((unsigned long long)hit);  // first position past the seed
+    if (sizes) {
+      const uint64_t incl = wave_incl_scan_u64(sz);
+      int upto = WAVE - 1;
+      if (cs < 0) {
+        const uint64_t hit = ballot(i < n && run + incl >= a.seed_min);
+        if (hit) {
+          cs = i0 + __ffsll((unsigned long long)hit);  // first position past the seed
+          if (!all) upto = cs - 1 - i0;
+        }
+      }
+      run += bcast_u64(incl, upto);
     }
     if (cs >= 0 && i >= cs && c < a.n_clusters) atomicAdd(&a.hist[c], 1u);
-    run += bcast_u64(incl, WAVE - 1);
   }
   if (lane == 0) {
     a.cseed[q] = cs < 0 ? n : cs;
@@ -161,30 +171,43 @@ hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s) {
 }
 
 // ------------------------------------------------------------------ prep
-// one thread per cluster: shared clusters and their pairs
-__global__ void k_shared_count(SharedArgs a) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c <= a.n_clusters; c += stride) {
-    const uint32_t h = c < a.n_clusters ? a.hist[c] : 0u;
-    a.cnt2[c] = h;
-    a.isshared[c] = h >= 1 ? 1u : 0u;
-    a.swork[c] = 0;
+// One scan over the clusters gives both where each cluster's pairs start in
+// pair_q (low half) and its position in the scan list (high half): a
+// cluster with h pairs adds h to the first and 1 to the second when h > 0.
+struct HistPack {
+  const uint32_t *hist;
+  __device__ uint64_t operator()(uint32_t h) const {
+    return (uint64_t)h | ((uint64_t)(h > 0 ? 1u : 0u) << 32);
   }
-}
+};
 
-// one thread per cluster: the compacted list and the work of each entry
+// the work of scan-list entry i, 0 past the list
+struct ListWork {
+  const uint64_t *swork;
+  const uint64_t *total;  // hpos[n_clusters]: list length in the high half
+  __device__ uint64_t operator()(int64_t i) const {
+    return i < (int64_t)(*total >> 32) ? swork[i] : 0ull;
+  }
+};
+
+typedef rocprim::transform_iterator<const uint32_t *, HistPack, uint64_t> HistPackInput;
+typedef rocprim::transform_iterator<rocprim::counting_iterator<int64_t>, ListWork, uint64_t>
+    ListWorkInput;
+
+// one thread per cluster with pairs: its list entry and the entry's work
 __global__ void k_shared_list(SharedArgs a) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < a.n_clusters; c += stride) {
-    if (!a.isshared[c]) continue;
-    const uint32_t i = a.spos[c];
-    const uint64_t groups = (uint64_t)((a.hist[c] + a.g - 1) / a.g);
+    const uint32_t h = a.hist[c];
+    if (h == 0) continue;
+    const uint32_t i = (uint32_t)(a.hpos[c] >> 32);
     a.slist[i] = (uint32_t)c;
-    a.swork[i] = groups * (a.cl_off[c + 1] - a.cl_off[c]);
+    a.swork[i] = (uint64_t)((h + a.g - 1) / a.g) * (a.cl_off[c + 1] - a.cl_off[c]);
   }
 }
 
-// one wave per query: the query's shared pairs into their cluster's slots
+// one wave per query: the query's pairs into their cluster's slots; the
+// pair counts, no longer needed, are counted back down to hand out the slots
 __global__ void __launch_bounds__(256) k_pair_scatter(SharedArgs a) {
   const int lane = lane_id();
   const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
@@ -194,20 +217,27 @@ __global__ void __launch_bounds__(256) k_pair_scatter(SharedArgs a) {
   for (int i = a.cseed[q] + lane; i < n; i += WAVE) {
     const uint32_t c = cl[i];
     if (c < a.n_clusters) {
-      const uint32_t left = atomicSub(&a.cnt2[c], 1u);
-      a.pair_q[a.hoff[c] + left - 1] = (uint32_t)q;
+      const uint32_t left = atomicSub(&a.hist[c], 1u);
+      a.pair_q[(uint32_t)a.hpos[c] + left - 1] = (uint32_t)q;
     }
   }
 }
 
-size_t shared_scan_tmp_bytes(int64_t n_clusters) {
-  size_t b32 = 0, b64 = 0;
-  const size_t n = (size_t)n_clusters + 1;
-  (void)rocprim::exclusive_scan(nullptr, b32, (const uint32_t *)nullptr, (uint32_t *)nullptr, 0u,
-                                n, rocprim::plus<uint32_t>());
-  (void)rocprim::exclusive_scan(nullptr, b64, (const uint64_t *)nullptr, (uint64_t *)nullptr,
-                                (uint64_t)0, n, rocprim::plus<uint64_t>());
-  return b32 > b64 ? b32 : b64;
+// entries of the work scan: the list is at most one entry per cluster and
+// per pair slot
+static size_t work_scan_size(int64_t n_clusters, int64_t pair_slots) {
+  return (size_t)(pair_slots < n_clusters ? pair_slots : n_clusters) + 1;
+}
+
+size_t shared_scan_tmp_bytes(int64_t n_clusters, int64_t pair_slots) {
+  size_t b1 = 0, b2 = 0;
+  const HistPackInput hin((const uint32_t *)nullptr, HistPack{nullptr});
+  (void)rocprim::exclusive_scan(nullptr, b1, hin, (uint64_t *)nullptr, (uint64_t)0,
+                                (size_t)n_clusters + 1, rocprim::plus<uint64_t>());
+  const ListWorkInput win(rocprim::counting_iterator<int64_t>(0), ListWork{nullptr, nullptr});
+  (void)rocprim::exclusive_scan(nullptr, b2, win, (uint64_t *)nullptr, (uint64_t)0,
+                                work_scan_size(n_clusters, pair_slots), rocprim::plus<uint64_t>());
+  return b1 > b2 ? b1 : b2;
 }
 
 hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
@@ -218,24 +248,49 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.pool_cnt, 2, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
   if (e != hipSuccess) return e;
+  size_t tmp = a.scan_tmp_bytes;
+  const HistPackInput hin(a.hist, HistPack{a.hist});
+  e = rocprim::exclusive_scan(a.scan_tmp, tmp, hin, a.hpos, (uint64_t)0, (size_t)nc1,
+                              rocprim::plus<uint64_t>(), s);
+  if (e != hipSuccess) return e;
   int64_t blocks = (nc1 + 255) / 256;
   if (blocks > 16384) blocks = 16384;
-  hipLaunchKernelGGL(k_shared_count, dim3((unsigned)blocks), dim3(256), 0, s, a);
-  size_t tmp = a.scan_tmp_bytes;
-  e = rocprim::exclusive_scan(a.scan_tmp, tmp, a.cnt2, a.hoff, 0u, (size_t)nc1,
-                              rocprim::plus<uint32_t>(), s);
-  if (e != hipSuccess) return e;
-  tmp = a.scan_tmp_bytes;
-  e = rocprim::exclusive_scan(a.scan_tmp, tmp, a.isshared, a.spos, 0u, (size_t)nc1,
-                              rocprim::plus<uint32_t>(), s);
-  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_shared_list, dim3((unsigned)blocks), dim3(256), 0, s, a);
   tmp = a.scan_tmp_bytes;
-  e = rocprim::exclusive_scan(a.scan_tmp, tmp, a.swork, a.swork_off, (uint64_t)0, (size_t)nc1,
+  const ListWorkInput win(rocprim::counting_iterator<int64_t>(0),
+                          ListWork{a.swork, a.hpos + a.n_clusters});
+  e = rocprim::exclusive_scan(a.scan_tmp, tmp, win, a.swork_off, (uint64_t)0,
+                              work_scan_size(a.n_clusters, a.nq * a.cap),
                               rocprim::plus<uint64_t>(), s);
   if (e != hipSuccess) return e;
   if (a.nq > 0)
     hipLaunchKernelGGL(k_pair_scatter, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// one wave per query: rows of its whole list (diagnostics)
+__global__ void __launch_bounds__(256) k_list_rows(const uint32_t *clus, const int32_t *nclus,
+                                                   int64_t cap, int64_t nq, const uint64_t *cl_off,
+                                                   int64_t n_clusters, uint32_t *rows) {
+  const int lane = lane_id();
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (q >= nq) return;
+  const int n = clamp_n(nclus[q], cap);
+  uint64_t sum = 0;
+  for (int i = lane; i < n; i += WAVE) {
+    const uint32_t c = clus[q * cap + i];
+    if (c < n_clusters) sum += cl_off[(uint64_t)c + 1] - cl_off[c];
+  }
+  for (int m = 32; m >= 1; m >>= 1) sum += shfl_xor_u64(sum, m);
+  if (lane == 0) rows[q] = sum > 0xffffffffull ? 0u : (uint32_t)sum;
+}
+
+hipError_t launch_list_rows(const uint32_t *clus, const int32_t *nclus, int64_t cap, int64_t nq,
+                            const uint64_t *cl_off, int64_t n_clusters, uint32_t *rows,
+                            hipStream_t s) {
+  if (nq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_list_rows, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, s, clus, nclus,
+                     cap, nq, cl_off, n_clusters, rows);
   return hipGetLastError();
 }
 
@@ -361,8 +416,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
   uint32_t *qi = s_qi[w];
   int32_t *qqs = s_qq[w];
   uint32_t *sv = s_sv[w];
-  const int64_t NS = a.spos[a.n_clusters];
-  const uint64_t W = a.swork_off[a.n_clusters];
+  const int64_t NS = (int64_t)(a.hpos[a.n_clusters] >> 32);
+  const uint64_t W = a.swork_off[NS];
   const uint64_t ntiles = (W + SHARED_TILE - 1) / SHARED_TILE;
   const int rb = a.row_bytes;
   const int k = a.k;
@@ -409,8 +464,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
         l_wo = a.swork_off[ii];
         l_base = a.cl_off[c];
         l_sz = a.cl_off[(uint64_t)c + 1] - l_base;
-        l_hp = a.hoff[c];
-        l_m = a.hoff[(uint64_t)c + 1] - l_hp;
+        l_hp = (uint32_t)a.hpos[c];
+        l_m = (uint32_t)a.hpos[(uint64_t)c + 1] - l_hp;
       }
     };
     stage();
@@ -904,13 +959,13 @@ hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s) {
 // ------------------------------------------------------------------ diagnostics
 // rows of the shared clusters (each read once by the scan) -> out[0] and
 // rows scored by the scan summed over pairs -> out[2]
-__global__ void k_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int64_t n_clusters,
+__global__ void k_unique_rows(const uint64_t *hpos, const uint64_t *cl_off, int64_t n_clusters,
                               int64_t *out) {
   __shared__ unsigned long long part[2][256];
   unsigned long long acc = 0, accp = 0;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_clusters; c += stride) {
-    const uint32_t m = hoff[c + 1] - hoff[c];
+    const uint32_t m = (uint32_t)hpos[c + 1] - (uint32_t)hpos[c];
     const uint64_t sz = cl_off[c + 1] - cl_off[c];
     if (m > 0) acc += sz;
     accp += (uint64_t)m * sz;
@@ -931,9 +986,9 @@ __global__ void k_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int6
   }
 }
 
-hipError_t launch_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int64_t n_clusters,
+hipError_t launch_unique_rows(const uint64_t *hpos, const uint64_t *cl_off, int64_t n_clusters,
                               int64_t *out, hipStream_t s) {
-  hipLaunchKernelGGL(k_unique_rows, dim3(1024), dim3(256), 0, s, hoff, cl_off, n_clusters, out);
+  hipLaunchKernelGGL(k_unique_rows, dim3(1024), dim3(256), 0, s, hpos, cl_off, n_clusters, out);
   return hipGetLastError();
 }
 

@@ -78,7 +78,8 @@ struct Buffers {
   unsigned long long *counter2;
   uint32_t *skey;
   int64_t *sid;
-  uint32_t *pair_q, *hist, *cnt2, *hoff, *isshared, *spos, *slist;
+  uint32_t *pair_q, *hist, *slist;
+  uint64_t *hpos;
   uint2 *qnorm;
   uint64_t *swork, *swork_off;
   int64_t *wstats;
@@ -147,14 +148,11 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.pair_q = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.qnorm = c.take<uint2>((size_t)s.nq);
     B.hist = c.take<uint32_t>(nc1);
-    B.cnt2 = c.take<uint32_t>(nc1);
-    B.hoff = c.take<uint32_t>(nc1);
-    B.isshared = c.take<uint32_t>(nc1);
-    B.spos = c.take<uint32_t>(nc1);
+    B.hpos = c.take<uint64_t>(nc1);
     B.slist = c.take<uint32_t>(nc1);
     B.swork = c.take<uint64_t>(nc1);
     B.swork_off = c.take<uint64_t>(nc1);
-    B.scan_tmp_bytes = nr::shared_scan_tmp_bytes(s.n_clusters);
+    B.scan_tmp_bytes = nr::shared_scan_tmp_bytes(s.n_clusters, s.nq * s.cap);
     B.scan_tmp = c.take<char>(B.scan_tmp_bytes);
   }
   *bytes = align_up(c.off, 256);
@@ -532,11 +530,11 @@ hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void 
   a.own_dists = B.own_dists;
   a.own_rows = B.own_rows;
   a.hist = B.hist;
-  a.cnt2 = B.cnt2;
-  a.hoff = B.hoff;
-  a.isshared = B.isshared;
-  a.spos = B.spos;
+  a.hpos = B.hpos;
   a.slist = B.slist;
+  // the per-query rows of the whole list are diagnostics: taken here only
+  // when the caller asked for per-query statistics
+  a.eager_rows = qstats != nullptr;
   a.swork = B.swork;
   a.swork_off = B.swork_off;
   a.pair_q = B.pair_q;
@@ -961,7 +959,9 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
   if (B.shared) {
     HIP_OK(nr::launch_fill_i32((int32_t *)B.wstats, 2, 0, stream));      // wstats[0]
     HIP_OK(nr::launch_fill_i32((int32_t *)(B.wstats + 2), 2, 0, stream));  // wstats[2]
-    HIP_OK(nr::launch_unique_rows(B.hoff, ix->d.cl_off, ix->d.n_clusters, B.wstats, stream));
+    HIP_OK(nr::launch_unique_rows(B.hpos, ix->d.cl_off, ix->d.n_clusters, B.wstats, stream));
+    HIP_OK(nr::launch_list_rows(B.clus, B.nclus, w->last_cap, (int64_t)nq, ix->d.cl_off,
+                                ix->d.n_clusters, B.rfull, stream));
   }
   HIP_OK(hipStreamSynchronize(stream));
   int64_t v[NR_WORK] = {0};
@@ -976,7 +976,7 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
     int64_t ws[4] = {0, 0, 0, 0};
     uint32_t pairs = 0;
     HIP_OK(hipMemcpy(ws, B.wstats, sizeof(ws), hipMemcpyDeviceToHost));
-    HIP_OK(hipMemcpy(&pairs, B.hoff + ix->d.n_clusters, 4, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(&pairs, B.hpos + ix->d.n_clusters, 4, hipMemcpyDeviceToHost));
     std::vector<uint32_t> own(nq);
     std::vector<int32_t> flag(nq), scnt(nq);
     HIP_OK(hipMemcpy(own.data(), B.own_rows, 4 * nq, hipMemcpyDeviceToHost));

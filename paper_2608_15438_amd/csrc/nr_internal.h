@@ -188,13 +188,14 @@ struct SharedArgs {
   const float *own_dists;
   uint32_t *own_rows;         // [nq] copy of rtot kept for diagnostics
   uint32_t *hist;             // [n_clusters + 1] pairs per cluster past the leading clusters
-  uint32_t *cnt2;             // [n_clusters + 1] copy of hist consumed by the pair scatter
-  uint32_t *hoff;             // [n_clusters + 1] exclusive scan of cnt2
-  uint32_t *isshared;         // [n_clusters + 1] 1 for a cluster the scan reads (hist >= 1)
-  uint32_t *spos;             // [n_clusters + 1] exclusive scan of isshared
-  uint32_t *slist;            // [n_clusters] scanned clusters in cluster order
-  uint64_t *swork;            // [n_clusters + 1] rows x query groups of slist[i], 0 past the list
-  uint64_t *swork_off;        // [n_clusters + 1] exclusive scan of swork
+                              // (counted back to zero by the pair scatter)
+  uint64_t *hpos;             // [n_clusters + 1] exclusive scan over clusters: pairs before
+                              // (low half, the cluster's start in pair_q) and clusters with
+                              // pairs before (high half, its scan-list position)
+  uint32_t *slist;            // [n_clusters] scanned clusters (those with pairs) in cluster order
+  uint64_t *swork;            // [list] rows x query groups of slist[i]
+  uint64_t *swork_off;        // [list + 1] exclusive scan of swork
+  int eager_rows;             // 1: rfull gets the rows of the whole list (else the leading ones)
   uint32_t *pair_q;           // [pairs] query of each scanned pair, grouped by cluster
   uint2 *qnorm;               // [nq] uint8 rows: (|q|^2, |q head|^2 over scan_head bytes)
   int32_t *scnt;              // [nq] survivors appended
@@ -225,13 +226,16 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
-size_t shared_scan_tmp_bytes(int64_t n_clusters);
+size_t shared_scan_tmp_bytes(int64_t n_clusters, int64_t pair_slots);
 hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s);
 hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s);
 hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s);
-hipError_t launch_unique_rows(const uint32_t *hoff, const uint64_t *cl_off, int64_t n_clusters,
+hipError_t launch_unique_rows(const uint64_t *hpos, const uint64_t *cl_off, int64_t n_clusters,
                               int64_t *out, hipStream_t s);
+hipError_t launch_list_rows(const uint32_t *clus, const int32_t *nclus, int64_t cap, int64_t nq,
+                            const uint64_t *cl_off, int64_t n_clusters, uint32_t *rows,
+                            hipStream_t s);
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 
 hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, int n_cu,
