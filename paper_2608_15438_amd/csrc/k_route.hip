@@ -34,17 +34,39 @@ struct RouteLds {
   float wd[WAVE];                 // distances of the window's first multi-bucket clusters
 };
 
-__device__ __forceinline__ float margin_dev(const RouteArgs &a, float x) {
-  const int m = a.m_knots;
+// M(x): piecewise linear through the knots, constant outside them.  Knot j
+// sits in lane j (kx, ky, ks); the segment is the last i whose next knot is
+// not above x, found with one ballot
+__device__ __forceinline__ float margin_dev(int m, float kx, float ky, float ks, float x) {
+  const int lane = lane_id();
   if (m <= 0) return 0.0f;
-  if (m == 1 || x <= a.m_x[0]) return a.m_y[0];
-  if (x >= a.m_x[m - 1]) return a.m_y[m - 1];
-  int i = 0;
-  while (i + 1 < m - 1 && a.m_x[i + 1] <= x) ++i;
-  float v = fmaf(x - a.m_x[i], a.m_slope[i], a.m_y[i]);
-  v = v < a.m_y[i] ? a.m_y[i] : v;
-  v = v > a.m_y[i + 1] ? a.m_y[i + 1] : v;
+  const float x0 = bcast_f32(kx, 0), y0 = bcast_f32(ky, 0);
+  if (m == 1 || x <= x0) return y0;
+  if (x >= bcast_f32(kx, m - 1)) return bcast_f32(ky, m - 1);
+  const uint64_t above = ballot(lane >= 1 && lane <= m - 2 && !(kx <= x));
+  const int i = (above ? __ffsll((unsigned long long)above) - 1 : m - 1) - 1;
+  const float yi = bcast_f32(ky, i), yn = bcast_f32(ky, i + 1);
+  float v = fmaf(x - bcast_f32(kx, i), bcast_f32(ks, i), yi);
+  v = v < yi ? yi : v;
+  v = v > yn ? yn : v;
   return v;
+}
+
+// entries of sorted a[0..n) below key, the same key in every lane: each round
+// samples 64 evenly spaced entries and keeps the gap the key falls in
+__device__ __forceinline__ int wave_lower_bound_u64(const uint64_t *a, int n, uint64_t key) {
+  const int lane = lane_id();
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int chunk = (hi - lo + WAVE - 1) / WAVE;
+    const int p = lo + lane * chunk;
+    const int c = popc64(ballot(p < hi && a[p] < key));
+    if (c == 0) break;
+    const int top = lo + c * chunk;
+    hi = top < hi ? top : hi;
+    lo = lo + (c - 1) * chunk + 1;
+  }
+  return lo;
 }
 
 __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
@@ -58,6 +80,9 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   const int64_t q = blockIdx.x;
   if (q >= a.nq) return;
   const int b = a.b, P = a.P, k_c = a.k_c;
+  const float kx = lane < a.m_knots ? a.m_x[lane] : 0.0f;
+  const float ky = lane < a.m_knots ? a.m_y[lane] : 0.0f;
+  const float ks = lane < a.m_knots ? a.m_slope[lane] : 0.0f;
   const float lg = lane < b ? a.logits[q * b + lane] : 0.0f;
   const int cnt = a.counts[q];
   const int32_t *bins = a.bins + q * P;
@@ -108,7 +133,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     }
     float dm = wave_min_f32(d);
     d_min = dm < d_min ? dm : d_min;
-    const float M = margin_dev(a, d_min);
+    const float M = margin_dev(a.m_knots, kx, ky, ks, d_min);
     const float theta = a.gate_on ? d_min + M : INFINITY;
     const float am = a.alpha_front * M;
     const float theta_f = d_min + am;
@@ -118,14 +143,14 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     const int nv = popc64(ballot(valid));
     // prune H to d <= theta (a prefix, as H is sorted)
     const uint64_t cut = ((uint64_t)__float_as_uint(theta) + 1ull) << 32;
-    const int hv = lower_bound_u64(H, h, cut);
+    const int hv = wave_lower_bound_u64(H, h, cut);
     S.bkey[lane] = key;
     __builtin_amdgcn_wave_barrier();
     int pos = WAVE + lane;
     if (lane < nv) pos = lane + lower_bound_u64(H, hv, key);
     // move the tail of H that batch keys overtake
     if (nv > 0) {
-      const int j0 = lower_bound_u64(H, hv, S.bkey[0]);
+      const int j0 = wave_lower_bound_u64(H, hv, S.bkey[0]);
       int top = hv;
       while (top > j0) {
         int lo = top - WAVE > j0 ? top - WAVE : j0;

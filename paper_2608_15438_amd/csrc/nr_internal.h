@@ -252,6 +252,9 @@ __device__ __forceinline__ int lane_id() { return __lane_id(); }
 __device__ __forceinline__ uint32_t bcast_u32(uint32_t v, int src) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, src);
 }
+__device__ __forceinline__ float bcast_f32(float v, int src) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src));
+}
 __device__ __forceinline__ uint64_t bcast_u64(uint64_t v, int src) {
   uint32_t lo = bcast_u32((uint32_t)v, src), hi = bcast_u32((uint32_t)(v >> 32), src);
   return ((uint64_t)hi << 32) | lo;
