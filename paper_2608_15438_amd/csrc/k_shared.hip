@@ -920,23 +920,31 @@ __global__ void __launch_bounds__(256) k_shared_merge(SharedArgs a) {
       stk_insert(tk, k, bcast_u32(key, src), (int64_t)bcast_u64((uint64_t)id, src));
     }
   }
-  // survivors: the query's own slots, then its pooled ones
-  for (int i0 = 0; i0 < cnt; i0 += WAVE) {
-    const int i = i0 + lane;
-    uint32_t key = 0xffffffffu;
-    int64_t id = -1;
-    if (i < own) {
-      key = a.skey[q * SURVIVOR_CAP + i];
-      id = a.sid[q * SURVIVOR_CAP + i];
-    } else if (i < cnt) {
-      key = a.pool2_key[p0 + (uint32_t)(i - SURVIVOR_CAP)];
-      id = a.pool2_id[p0 + (uint32_t)(i - SURVIVOR_CAP)];
+  // survivors: the query's own slots, then its pooled ones; four chunks of
+  // 64 are loaded per round, ids only for keys that can still enter
+  constexpr int RC = 4;
+  for (int r0 = 0; r0 < cnt; r0 += RC * WAVE) {
+    uint32_t key[RC];
+#pragma unroll
+    for (int u = 0; u < RC; ++u) {
+      const int i = r0 + u * WAVE + lane;
+      key[u] = 0xffffffffu;
+      if (i < own) key[u] = a.skey[q * SURVIVOR_CAP + i];
+      else if (i < cnt) key[u] = a.pool2_key[p0 + (uint32_t)(i - SURVIVOR_CAP)];
     }
-    uint64_t m = ballot(i < cnt && key <= tk.kth_key);
-    while (m) {
-      const int src = __ffsll((unsigned long long)m) - 1;
-      m &= m - 1;
-      stk_insert(tk, k, bcast_u32(key, src), (int64_t)bcast_u64((uint64_t)id, src));
+#pragma unroll
+    for (int u = 0; u < RC; ++u) {
+      const int i = r0 + u * WAVE + lane;
+      uint64_t m = ballot(i < cnt && key[u] <= tk.kth_key);
+      if (!m) continue;
+      int64_t id = -1;
+      if ((m >> lane) & 1ull)
+        id = i < own ? a.sid[q * SURVIVOR_CAP + i] : a.pool2_id[p0 + (uint32_t)(i - SURVIVOR_CAP)];
+      while (m) {
+        const int src = __ffsll((unsigned long long)m) - 1;
+        m &= m - 1;
+        stk_insert(tk, k, bcast_u32(key[u], src), (int64_t)bcast_u64((uint64_t)id, src));
+      }
     }
   }
   if (lane < k) {
