@@ -67,6 +67,9 @@ PARAM_SETS = {
     "or_reading": dict(k_c=8, b_batch=7, b_min=1, t_low=2, lowq_or=True),
     "binned": dict(s_max=1.5, n_bins=6),
     "one_per_batch": dict(b_batch=1, k_c=16),
+    # margins through several knots: the segment search and both clamps
+    "many_knots": dict(m_x=[0.0, 0.5, 1.5, 3.0, 6.0], m_y=[0.2, 0.8, 1.5, 2.2, 3.0]),
+    "knots_flat": dict(m_x=[0.0, 0.3, 0.9, 2.0], m_y=[0.4, 1.2, 1.2, 2.5], k_c=12, b_batch=5),
 }
 
 
