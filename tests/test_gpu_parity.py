@@ -70,6 +70,9 @@ PARAM_SETS = {
     # margins through several knots: the segment search and both clamps
     "many_knots": dict(m_x=[0.0, 0.5, 1.5, 3.0, 6.0], m_y=[0.2, 0.8, 1.5, 2.2, 3.0]),
     "knots_flat": dict(m_x=[0.0, 0.3, 0.9, 2.0], m_y=[0.4, 1.2, 1.2, 2.5], k_c=12, b_batch=5),
+    # a heap this large leaves LDS for only the first ~600 probe ranges of a
+    # query: the rest of a 1024-probe sequence is read from HBM
+    "big_heap": dict(k_c=5000, gate_on=False, early_stop_on=False),
 }
 
 
