@@ -379,6 +379,12 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
       st[NR_QS_BATCHES] = n_batches;
     }
   }
+  if (a.ph_on) {
+    // the shared schedule's pair counts for this query, now that its list is
+    // final (the wave reads back what it wrote above)
+    __threadfence_block();
+    pair_hist_wave(a.ph, q, out, ndir + h);
+  }
 }
 
 // one thread per probe: the cluster range [c0, c1) of its bucket

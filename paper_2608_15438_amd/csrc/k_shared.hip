@@ -105,69 +105,29 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
 
 
 // ------------------------------------------------------------------ hist
-// one wave per query: full rows, leading clusters, pair counts of the rest
-__global__ void __launch_bounds__(256) k_pair_hist(SharedArgs a) {
-  const int lane = lane_id();
-  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (q >= a.nq) return;
-  const int n = clamp_n(a.nclus[q], a.cap);
-  const uint32_t *cl = a.clus + q * a.cap;
-  // rows of the leading clusters, and of the whole list when eager_rows is
-  // set (otherwise the sizes of the later clusters are not needed here)
-  const bool all = a.eager_rows != 0;
-  uint64_t run = 0;
-  int cs = -1;
-  for (int i0 = 0; i0 < n; i0 += WAVE) {
-    const int i = i0 + lane;
-    const bool sizes = cs < 0 || all;
-    uint32_t c = 0xffffffffu;
-    uint64_t sz = 0;
-    if (i < n) {
-      c = cl[i];
-      if (sizes && c < a.n_clusters) sz = a.cl_off[(uint64_t)c + 1] - a.cl_off[c];
-    }
-    if (sizes) {
-      const uint64_t incl = wave_incl_scan_u64(sz);
-      int upto = WAVE - 1;
-      if (cs < 0) {
-        const uint64_t hit = ballot(i < n && run + incl >= a.seed_min);
-        if (hit) {
-          cs = i0 + __ffsll((unsigned long long)hit);  // first position past the seed
-          if (!all) upto = cs - 1 - i0;
-        }
-      }
-      run += bcast_u64(incl, upto);
-    }
-    if (cs >= 0 && i >= cs && c < a.n_clusters) atomicAdd(&a.hist[c], 1u);
-  }
-  if (lane == 0) {
-    a.cseed[q] = cs < 0 ? n : cs;
-    a.rfull[q] = run > 0xffffffffull ? 0u : (uint32_t)run;
-  }
-  // uint8 rows: |q|^2 and the part of it over the scan's head, one 16-byte
-  // chunk per lane (rows are at most 64 chunks); integer sums, so the order
-  // of the additions does not matter
-  if (a.is_u8) {
-    uint32_t p = 0;
-    if (16 * lane < a.row_bytes) {
-      const uint4 v = *reinterpret_cast<const uint4 *>((const unsigned char *)a.queries +
-                                                       (uint64_t)q * a.row_bytes + 16 * lane);
-      p = __builtin_amdgcn_udot4(v.x, v.x, p, false);
-      p = __builtin_amdgcn_udot4(v.y, v.y, p, false);
-      p = __builtin_amdgcn_udot4(v.z, v.z, p, false);
-      p = __builtin_amdgcn_udot4(v.w, v.w, p, false);
-    }
-    const uint32_t full = wave_sum_u32(p);
-    const uint32_t head = wave_sum_u32(16 * lane < a.scan_head ? p : 0u);
-    if (lane == 0) a.qnorm[q] = make_uint2(full, head);
-  }
+
+// ------------------------------------------------------------------ hist
+// The pair counts are taken at the end of the route kernel, per query, once
+// its list is final (pair_hist_wave); the counts start from zero.
+hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s) {
+  return launch_fill_i32((int32_t *)a.hist, a.n_clusters + 1, 0, s);
 }
 
-hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s) {
-  hipError_t e = launch_fill_i32((int32_t *)a.hist, a.n_clusters + 1, 0, s);
-  if (e != hipSuccess || a.nq <= 0) return e;
-  hipLaunchKernelGGL(k_pair_hist, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
-  return hipGetLastError();
+PairHistArgs pair_hist_args(const SharedArgs &a) {
+  PairHistArgs h;
+  h.hist = a.hist;
+  h.cl_off = a.cl_off;
+  h.n_clusters = a.n_clusters;
+  h.seed_min = a.seed_min;
+  h.cseed = a.cseed;
+  h.rfull = a.rfull;
+  h.qnorm = a.qnorm;
+  h.queries = (const unsigned char *)a.queries;
+  h.row_bytes = a.row_bytes;
+  h.scan_head = a.scan_head;
+  h.is_u8 = a.is_u8;
+  h.eager_rows = a.eager_rows;
+  return h;
 }
 
 // ------------------------------------------------------------------ prep

@@ -371,7 +371,8 @@ hipError_t run_probe(const nr_index *ix, const float *logits, int64_t nq, int P,
 
 hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
                      const nr_params *p, const Buffers &B, uint32_t *clus, int32_t *nclus,
-                     int64_t cap, int32_t *qstats, hipStream_t s) {
+                     int64_t cap, int32_t *qstats, hipStream_t s,
+                     const nr::PairHistArgs *ph = nullptr) {
   nr::RouteArgs a{};
   a.logits = logits;
   a.nq = nq;
@@ -413,6 +414,10 @@ hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
   a.nclus = nclus;
   a.cap = cap;
   a.qstats = qstats;
+  if (ph) {
+    a.ph = *ph;
+    a.ph_on = 1;
+  }
   return nr::launch_route(a, s);
 }
 
@@ -499,10 +504,10 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
 // and the per-query schedule again for the queries whose survivors overflowed.
 // ev (may be null): after the own plan, own refinement, own merge, shared
 // prep, shared scan, shared merge.
-hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void *q, int64_t nq,
-                             int k, const uint32_t *clus, const int32_t *nclus, int64_t cap,
-                             const Buffers &B, int64_t *out_ids, float *out_dists,
-                             int32_t *qstats, hipStream_t s, hipEvent_t *ev) {
+nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q, int64_t nq,
+                           int k, const uint32_t *clus, const int32_t *nclus, int64_t cap,
+                           const Buffers &B, int64_t *out_ids, float *out_dists,
+                           int32_t *qstats) {
   nr::SharedArgs a{};
   a.nq = nq;
   a.k = k;
@@ -558,11 +563,18 @@ hipError_t run_refine_shared(const nr_index *ix, const nr_params *p, const void 
   a.out_ids = out_ids;
   a.out_dists = out_dists;
   a.qstats = qstats;
-  hipError_t e = nr::launch_shared_hist(a, s);
-  if (e != hipSuccess) return e;
+  return a;
+}
+
+// The shared schedule after routing; the route kernel has counted the pairs
+// (its pair_hist_wave epilogue, on counts zeroed before it ran).
+hipError_t run_refine_shared(const nr_index *ix, const nr::SharedArgs &a, const void *q,
+                             int64_t nq, int k, const uint32_t *clus, const int32_t *nclus,
+                             int64_t cap, const Buffers &B, int64_t *out_ids, float *out_dists,
+                             int32_t *qstats, hipStream_t s, hipEvent_t *ev) {
   // the scan's prep needs only the pair counts: it runs on the second stream
   // while the seed pass runs here
-  e = hipEventRecord(B.fork, s);
+  hipError_t e = hipEventRecord(B.fork, s);
   if (e == hipSuccess) e = hipStreamWaitEvent(B.aux, B.fork, 0);
   if (e == hipSuccess) e = nr::launch_shared_prep(a, B.aux);
   if (e == hipSuccess) e = hipEventRecord(B.join, B.aux);
@@ -887,10 +899,19 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
     if (prof) HIP_OK(hipEventRecord(es.ev[1], stream));
     HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream));
     if (prof) HIP_OK(hipEventRecord(es.ev[2], stream));
-    HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, qs, stream));
+    nr::SharedArgs sa{};
+    nr::PairHistArgs ph{};
+    if (B.shared) {
+      sa = shared_args(ix, p, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
+                       out_dists + q0 * k, qs);
+      ph = nr::pair_hist_args(sa);
+      HIP_OK(nr::launch_shared_hist(sa, stream));  // zero the pair counts
+    }
+    HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, qs, stream,
+                     B.shared ? &ph : nullptr));
     if (prof) HIP_OK(hipEventRecord(es.ev[3], stream));
     if (B.shared) {
-      HIP_OK(run_refine_shared(ix, p, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
+      HIP_OK(run_refine_shared(ix, sa, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
                                out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr));
     } else {
       HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,

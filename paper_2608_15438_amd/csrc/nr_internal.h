@@ -82,6 +82,19 @@ struct ProbeArgs {
   int32_t *counts;       // [nq]
 };
 
+// per-query pair counting of the shared schedule (see pair_hist_wave)
+struct PairHistArgs {
+  uint32_t *hist;               // [n_clusters + 1] pairs per cluster past the leading clusters
+  const uint64_t *cl_off;
+  int64_t n_clusters;
+  uint32_t seed_min;            // rows the leading clusters cover at least
+  int32_t *cseed;               // [nq] leading clusters
+  uint32_t *rfull;              // [nq] rows of the leading clusters (whole list: eager_rows)
+  uint2 *qnorm;                 // [nq] uint8 rows: |q|^2 and its head part
+  const unsigned char *queries;
+  int row_bytes, scan_head, is_u8, eager_rows;
+};
+
 struct RouteArgs {
   const float *logits;
   int64_t nq;
@@ -102,6 +115,8 @@ struct RouteArgs {
   int32_t *nclus;        // [nq]
   int64_t cap;
   int32_t *qstats;       // [nq x NR_QSTATS] or null
+  PairHistArgs ph;       // with ph_on: each query's pairs are counted once its list is final
+  int ph_on;
 };
 
 struct PlanArgs {
@@ -228,6 +243,7 @@ hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
 size_t shared_scan_tmp_bytes(int64_t n_clusters, int64_t pair_slots);
 hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s);
+PairHistArgs pair_hist_args(const SharedArgs &a);
 hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s);
 hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s);
@@ -325,6 +341,64 @@ __device__ __forceinline__ int lower_bound_u64(const uint64_t *a, int n, uint64_
     if (a[mid] < key) lo = mid + 1; else hi = mid;
   }
   return lo;
+}
+
+// One wave, query q with list cl[0..n): the leading clusters covering at
+// least seed_min rows stay with the query (cseed[q]); every later (cluster,
+// query) pair is counted in hist; rfull[q] gets the rows of the leading
+// clusters (of the whole list with eager_rows); for uint8 rows qnorm[q] gets
+// |q|^2 and the part of it over the scan's head.
+__device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const uint32_t *cl, int n) {
+  const int lane = lane_id();
+  // rows of the leading clusters, and of the whole list when eager_rows is
+  // set (otherwise the sizes of the later clusters are not needed here)
+  const bool all = h.eager_rows != 0;
+  uint64_t run = 0;
+  int cs = -1;
+  for (int i0 = 0; i0 < n; i0 += WAVE) {
+    const int i = i0 + lane;
+    const bool sizes = cs < 0 || all;
+    uint32_t c = 0xffffffffu;
+    uint64_t sz = 0;
+    if (i < n) {
+      c = cl[i];
+      if (sizes && c < h.n_clusters) sz = h.cl_off[(uint64_t)c + 1] - h.cl_off[c];
+    }
+    if (sizes) {
+      const uint64_t incl = wave_incl_scan_u64(sz);
+      int upto = WAVE - 1;
+      if (cs < 0) {
+        const uint64_t hit = ballot(i < n && run + incl >= h.seed_min);
+        if (hit) {
+          cs = i0 + __ffsll((unsigned long long)hit);  // first position past the seed
+          if (!all) upto = cs - 1 - i0;
+        }
+      }
+      run += bcast_u64(incl, upto);
+    }
+    if (cs >= 0 && i >= cs && c < h.n_clusters) atomicAdd(&h.hist[c], 1u);
+  }
+  if (lane == 0) {
+    h.cseed[q] = cs < 0 ? n : cs;
+    h.rfull[q] = run > 0xffffffffull ? 0u : (uint32_t)run;
+  }
+  // uint8 rows: |q|^2 and the part of it over the scan's head, one 16-byte
+  // chunk per lane (rows are at most 64 chunks); integer sums, so the order
+  // of the additions does not matter
+  if (h.is_u8) {
+    uint32_t p = 0;
+    if (16 * lane < h.row_bytes) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(h.queries +
+                                                       (uint64_t)q * h.row_bytes + 16 * lane);
+      p = __builtin_amdgcn_udot4(v.x, v.x, p, false);
+      p = __builtin_amdgcn_udot4(v.y, v.y, p, false);
+      p = __builtin_amdgcn_udot4(v.z, v.z, p, false);
+      p = __builtin_amdgcn_udot4(v.w, v.w, p, false);
+    }
+    const uint32_t full = wave_sum_u32(p);
+    const uint32_t head = wave_sum_u32(16 * lane < h.scan_head ? p : 0u);
+    if (lane == 0) h.qnorm[q] = make_uint2(full, head);
+  }
 }
 
 }  // namespace nr
