@@ -3,26 +3,30 @@
 // that a cluster listed by several queries of the batch is read from HBM once
 // for all of them.
 //
-//  hist    per query: the leading clusters of its list that cover at least
-//          seed_min rows stay with the query; every later (cluster, query)
-//          pair is counted per cluster;
-//  own     the per-query kernels refine each query's leading clusters plus
-//          the later clusters no other query lists (count 1).  Their top-k is
-//          exact over a subset of C(q), so its k-th entry (key, id) bounds the
-//          final k-th entry: a shared row can only enter the result if it
-//          ranks before it;
-//  prep    clusters with count >= 2 are shared: they are compacted into a
-//          list, their pairs grouped by cluster, and each is cut into work
-//          units of <= g queries x <= SHARED_ROWS rows;
+//  hist    per query (one wave, at the end of the route kernel once the
+//          query's list is final): the leading clusters of its list that
+//          cover at least seed_min rows stay with the query; every later
+//          (cluster, query) pair is counted per cluster; |q|^2 and its head
+//          part are kept for uint8 rows;
+//  seed    the per-query kernels refine each query's leading clusters.  Their
+//          top-k is exact over a subset of C(q), so its k-th entry bounds
+//          the final k-th entry: a later row can only enter the result if it
+//          ranks at or before it;
+//  prep    (on a second stream, beside the seed pass) one scan over the
+//          clusters places every cluster with pairs in the scan list and its
+//          pairs in pair_q; a scan over the list places each entry's work
+//          (rows x groups of <= g queries); the pairs are then scattered by
+//          cluster;
 //  scan    persistent waves take tiles of SHARED_TILE work from an atomic
-//          counter and walk the units of the tile in list order, staging the
-//          metadata of 64 list entries per load (one per lane).  A unit's g
-//          query slices sit in registers; each row is loaded once (8 lanes x
-//          16 bytes per 128-byte segment) and scored for all g queries; a row
-//          that ranks before its query's bound is appended to that query's
-//          survivor list;
-//  merge   own top-k + survivors -> top-k.  A query with more than
-//          SURVIVOR_CAP survivors is flagged and recomputed by the per-query
+//          counter and gather consecutive units of the tile into batches
+//          whose query rows sit in LDS.  Each row's head (its first
+//          scan_head bytes) is read once for all queries of its unit and
+//          drops the pairs whose head part alone exceeds the bound; the
+//          remaining rows are read whole and scored exactly, and a pair at
+//          or before its query's bound becomes a survivor (per-query slots,
+//          then a shared pool);
+//  merge   seed top-k + survivors -> top-k.  A query whose survivors found
+//          the pool full is flagged and recomputed by the per-query
 //          schedule.
 #include <cstring>
 
