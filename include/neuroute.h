@@ -226,8 +226,10 @@ nr_status nr_refine(const nr_index *index, const void *queries, int64_t nq, int3
  * nr_profile_read synchronises the recorded events and returns the summed
  * milliseconds per stage and the number of timed searches since the last
  * reset.  Stages, in launch order:
- *   encode, probe, route,
- *   plan    (per-query tiles; shared schedule: pair counts + own-pass tiles),
+ *   encode, probe,
+ *   route   (shared schedule: also the per-query pair counts, taken by the
+ *            route kernel once a query's list is final),
+ *   plan    (per-query tiles; shared schedule: seed-pass tiles),
  *   refine  (the per-query refinement kernel; shared schedule: own pass),
  *   merge   (per-query merge; shared schedule: own-pass merge),
  *   shared_prep, shared_scan, shared_merge (shared schedule only).  The
