@@ -514,10 +514,15 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
       // past the batch's slots or the row is replaced by zeros afterwards
       constexpr int QL = QMAX * QCH / WAVE;
       static_assert(QMAX * QCH % WAVE == 0, "whole loads of query chunks");
+      // the lane id made opaque here, so the few values derived from it below
+      // are recomputed per batch rather than kept live (and spilled) across
+      // the whole kernel
+      int lnb = lane;
+      __asm__ volatile("" : "+v"(lnb));
       uint4 qload[QL];
 #pragma unroll
       for (int t = 0; t < QL; ++t) {
-        const int c = t * WAVE + lane;
+        const int c = t * WAVE + lnb;
         const int sl = c / QCH;
         const int off = (c - sl * QCH) * 16;
         const uint32_t qsl = (uint32_t)__shfl((int)myq, sl);
@@ -528,7 +533,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
       const uint2 qn = IS_U8 ? a.qnorm[myq] : make_uint2(0, 0);
 #pragma unroll
       for (int t = 0; t < QL; ++t) {
-        const int c = t * WAVE + lane;
+        const int c = t * WAVE + lnb;
         const int sl = c / QCH;
         const int off = (c - sl * QCH) * 16;
         qs[c] = sl < nqs && off < rb ? qload[t] : make_uint4(0, 0, 0, 0);
@@ -644,24 +649,26 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
           nsv = 0;
         }
         uint4 hv[U];
-        bool ok[U];
-        int cus[U];
-        uint32_t vv[U];
+        // the unit of each load, 6 bits apiece (units < SCAN_UMAX = 64); the
+        // virtual row and its bound check are recomputed where needed
+        uint64_t cpack = 0;
 #pragma unroll
         for (int uu = 0; uu < U; ++uu) {
           const uint32_t v = v0 + uu * RPW + lane / HL;
-          ok[uu] = v < vtot;
-          vv[uu] = v;
-          if (ok[uu])
+          const bool ok = v < vtot;
+          if (ok)
             while (uv[cur + 1] <= v) ++cur;
-          cus[uu] = cur;
+          cpack |= (uint64_t)cur << (6 * uu);
           const uint64_t row = ub[cur] + (v - uv[cur]);
-          hv[uu] = ok[uu] ? load_stream(reinterpret_cast<const uint4 *>(a.scan_hb + row * a.scan_hs +
-                                                                        16 * hl))
-                          : make_uint4(0, 0, 0, 0);
+          hv[uu] = ok ? load_stream(reinterpret_cast<const uint4 *>(a.scan_hb + row * a.scan_hs +
+                                                                     16 * hl))
+                      : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int uu = 0; uu < U; ++uu) {
+          const uint32_t vu = v0 + uu * RPW + lane / HL;
+          const bool oku = vu < vtot;
+          const int cu = (int)((cpack >> (6 * uu)) & 63u);
           int32_t xx = 0;
           if (IS_U8) {
             uint32_t acc = 0;
@@ -671,12 +678,12 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
             acc = __builtin_amdgcn_udot4(hv[uu].w, hv[uu].w, acc, false);
             xx = (int32_t)acc;
           }
-          const uint32_t uqv = uq[cus[uu]];
+          const uint32_t uqv = uq[cu];
           const int slot0 = (int)(uqv & 0xffffu);
           const int gmu = (int)(uqv >> 16);
           uint32_t mask = 0;
           for (int j = 0; j < gmax; ++j) {
-            const bool valid = ok[uu] && j < gmu;
+            const bool valid = oku && j < gmu;
             if (!ballot(valid)) break;  // no row of this load has a j-th query
             const int slot = slot0 + (valid ? j : 0);
             const uint4 q4 = qs[slot * QCH + hl];
@@ -704,11 +711,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
           }
           const bool lead = hl == 0 && mask != 0;
           const uint64_t m = ballot(lead);
-          if (lead) {
-            const int cu = cus[uu];
-            sv[nsv + popc64(m & lanemask_lt())] =
-                ((uint32_t)cu << 20) | ((vv[uu] - uv[cu]) << 8) | mask;
-          }
+          if (lead)
+            sv[nsv + popc64(m & lanemask_lt())] = ((uint32_t)cu << 20) | ((vu - uv[cu]) << 8) | mask;
           nsv += popc64(m);
           listed += popc64(m);
         }
