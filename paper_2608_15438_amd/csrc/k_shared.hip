@@ -487,6 +487,11 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
       // ---- a batch of consecutive units of this tile; lane s fetches the
       // query of slot s as its unit joins, and nothing waits for those loads
       // until the batch is complete
+      // the lane id made opaque here, so the addresses derived from it in the
+      // batch setup are recomputed per batch rather than kept live (and
+      // spilled) across the whole kernel
+      int lnb = lane;
+      __asm__ volatile("" : "+v"(lnb));
       int nu = 0, nqs = 0, gmax = 0;
       uint32_t vtot = 0;
       uint32_t myq = 0;
@@ -500,7 +505,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
           uv[nu] = vtot;
           uq[nu] = (uint32_t)nqs | ((uint32_t)gm << 16);
         }
-        if (lane >= nqs && lane < nqs + gm) myq = a.pair_q[hp + gi * G + (lane - nqs)];
+        if (lnb >= nqs && lnb < nqs + gm) myq = a.pair_q[hp + gi * G + (lnb - nqs)];
         ++nu;
         nqs += gm;
         vtot += nrows;
@@ -514,11 +519,6 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
       // past the batch's slots or the row is replaced by zeros afterwards
       constexpr int QL = QMAX * QCH / WAVE;
       static_assert(QMAX * QCH % WAVE == 0, "whole loads of query chunks");
-      // the lane id made opaque here, so the few values derived from it below
-      // are recomputed per batch rather than kept live (and spilled) across
-      // the whole kernel
-      int lnb = lane;
-      __asm__ volatile("" : "+v"(lnb));
       uint4 qload[QL];
 #pragma unroll
       for (int t = 0; t < QL; ++t) {
@@ -538,18 +538,18 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
         const int off = (c - sl * QCH) * 16;
         qs[c] = sl < nqs && off < rb ? qload[t] : make_uint4(0, 0, 0, 0);
       }
-      if (lane < nqs) {
+      if (lnb < nqs) {
         const uint32_t bound =
             own_id < 0 ? 0xffffffffu : (a.is_u8 ? (uint32_t)own_d : __float_as_uint(own_d));
-        qi[lane] = myq;
-        tk[lane] = bound;
+        qi[lnb] = myq;
+        tk[lnb] = bound;
         if (IS_U8) {
-          qqs[lane] = (int32_t)qn.x;
-          th[lane] = bound == 0xffffffffu ? INT32_MAX : (int32_t)((int64_t)bound - (int64_t)qn.y);
+          qqs[lnb] = (int32_t)qn.x;
+          th[lnb] = bound == 0xffffffffu ? INT32_MAX : (int32_t)((int64_t)bound - (int64_t)qn.y);
         } else {
-          qqs[lane] = 0;
-          th[lane] = bound == 0xffffffffu ? (int32_t)__float_as_uint(INFINITY)
-                                          : (int32_t)__float_as_uint(__uint_as_float(bound) * 1.0001f);
+          qqs[lnb] = 0;
+          th[lnb] = bound == 0xffffffffu ? (int32_t)__float_as_uint(INFINITY)
+                                         : (int32_t)__float_as_uint(__uint_as_float(bound) * 1.0001f);
         }
       }
       __builtin_amdgcn_wave_barrier();
