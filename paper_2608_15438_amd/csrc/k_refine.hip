@@ -201,8 +201,12 @@ __device__ __forceinline__ void topk_insert(TopK &t, int k, uint32_t ck, int64_t
 }
 
 // ------------------------------------------------------------------ refine
+#ifndef NR_REFINE_WAVES1
+#define NR_REFINE_WAVES1 1      // waves per SIMD the registers are sized for (128-byte rows; 1: free)
+#endif
+
 template <int IS_U8, int NSEG, int U>
-__global__ void __launch_bounds__(256) k_refine(RefineArgs a) {
+__global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refine(RefineArgs a) {
   __shared__ uint32_t s_vs[4][STAGE_CLUSTERS + 1];
   __shared__ uint64_t s_ps[4][STAGE_CLUSTERS];
   const int lane = lane_id();
