@@ -73,13 +73,16 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   RouteLds &S = *reinterpret_cast<RouteLds *>(smem_raw);
   uint64_t *H = reinterpret_cast<uint64_t *>(smem_raw + sizeof(RouteLds));
-  uint32_t *st_c0 = reinterpret_cast<uint32_t *>(H + a.k_c);
+  uint32_t *st_c0 = reinterpret_cast<uint32_t *>(H + a.hcap);
   uint32_t *st_c1 = st_c0 + a.pst;
   int32_t *st_bin = reinterpret_cast<int32_t *>(st_c1 + a.pst);
   const int lane = lane_id();
   const int64_t q = blockIdx.x;
   if (q >= a.nq) return;
+  if (a.pass == 1 && !a.redo[q]) return;  // the second pass redoes only what the first gave up
   const int b = a.b, P = a.P, k_c = a.k_c;
+  const int hcap = a.hcap;  // heap slots in LDS (k_c, or fewer in a first pass)
+  bool abort_q = false;     // the heap would outgrow hcap: left to the second pass
   const float kx = lane < a.m_knots ? a.m_x[lane] : 0.0f;
   const float ky = lane < a.m_knots ? a.m_y[lane] : 0.0f;
   const float ks = lane < a.m_knots ? a.m_slope[lane] : 0.0f;
@@ -144,6 +147,12 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     // prune H to d <= theta (a prefix, as H is sorted)
     const uint64_t cut = ((uint64_t)__float_as_uint(theta) + 1ull) << 32;
     const int hv = wave_lower_bound_u64(H, h, cut);
+    if ((hv + nv < k_c ? hv + nv : k_c) > hcap) {
+      abort_q = true;
+      stop = true;
+      npend = 0;
+      return;
+    }
     S.bkey[lane] = key;
     __builtin_amdgcn_wave_barrier();
     int pos = WAVE + lane;
@@ -366,6 +375,10 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     }
   }
 
+  if (abort_q) {
+    if (lane == 0) a.redo[q] = 1;
+    return;
+  }
   for (int i = lane; i < h; i += WAVE) out[ndir + i] = (uint32_t)H[i];
   if (lane == 0) {
     a.nclus[q] = ndir + h;
@@ -410,14 +423,32 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
     if (blocks > 16384) blocks = 16384;
     hipLaunchKernelGGL(k_route_lookup, dim3((unsigned)blocks), dim3(256), 0, s, a);
   }
-  size_t lds = route_lds_bytes(a.k_c, a.pst);
-  if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void *)k_route,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(k_route, dim3((unsigned)a.nq), dim3(64), lds, s, a);
-  return hipGetLastError();
+  // A first pass keeps at most ROUTE_LIGHT_HEAP heap keys in LDS, so more
+  // waves fit on a CU; a query whose heap would grow past that gives up and
+  // is redone by a second pass with the full K_c slots.
+  auto launch = [&](int hcap, int pass) -> hipError_t {
+    RouteArgs b = a;
+    b.hcap = hcap;
+    b.pass = pass;
+    // stage every probe's range in LDS while the block stays within 48 KiB
+    const size_t fixed = route_lds_bytes(hcap, 0);
+    const size_t budget = 48 * 1024;
+    const size_t room = fixed < budget ? (budget - fixed) / (3 * sizeof(uint32_t)) : 0;
+    b.pst = (int)(room < (size_t)b.P ? room : (size_t)b.P);
+    const size_t lds = route_lds_bytes(hcap, b.pst);
+    if (lds > 64 * 1024) {
+      hipError_t e = hipFuncSetAttribute((const void *)k_route,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_route, dim3((unsigned)b.nq), dim3(64), lds, s, b);
+    return hipGetLastError();
+  };
+  if (a.k_c <= ROUTE_LIGHT_HEAP) return launch(a.k_c, 0);
+  hipError_t e = launch_fill_i32(a.redo, a.nq, 0, s);
+  if (e == hipSuccess) e = launch(ROUTE_LIGHT_HEAP, 0);
+  if (e == hipSuccess) e = launch(a.k_c, 1);
+  return e;
 }
 
 }  // namespace nr

@@ -56,6 +56,7 @@ struct Buffers {
   float *logits, *act0, *act1;
   uint32_t *codes;
   uint2 *lk;
+  int32_t *redo;
   float *costs;
   int32_t *bins, *counts;
   uint32_t *clus;
@@ -108,6 +109,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
   B.costs = c.take<float>((size_t)s.nq * s.P);
   B.bins = c.take<int32_t>((size_t)s.nq * s.P);
   B.lk = c.take<uint2>((size_t)s.nq * s.P);
+  B.redo = c.take<int32_t>((size_t)s.nq);
   B.counts = c.take<int32_t>((size_t)s.nq);
   B.clus = c.take<uint32_t>((size_t)s.nq * s.cap);
   B.nclus = c.take<int32_t>((size_t)s.nq);
@@ -383,14 +385,7 @@ hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
   a.counts = B.counts;
   a.bc_off = ix->d.bc_off;
   a.lk = B.lk;
-  // stage every probe's range in LDS while the block stays within 48 KiB
-  // (the heap of K_c keys comes first); larger lists read the rest from HBM
-  {
-    const size_t fixed = nr::route_lds_bytes((int)kc_eff(ix, p), 0);
-    const size_t budget = 48 * 1024;
-    const size_t room = fixed < budget ? (budget - fixed) / (3 * sizeof(uint32_t)) : 0;
-    a.pst = (int)(room < (size_t)P ? room : (size_t)P);
-  }
+  a.redo = B.redo;
   a.centroids = ix->d.centroids;
   a.k_c = (int)kc_eff(ix, p);
   a.b_batch = p->b_batch;

@@ -104,7 +104,9 @@ struct RouteArgs {
   const int32_t *counts;
   const uint32_t *bc_off;
   uint2 *lk;             // [nq x P] scratch: cluster range of each probe's bucket
-  int pst;               // probes per query whose ranges are staged in LDS
+  int pst;               // probes per query whose ranges are staged in LDS (set per pass)
+  int hcap, pass;        // heap slots in LDS and pass number (set by launch_route)
+  int32_t *redo;         // [nq] queries the first pass left to the second
   const float *centroids;
   int k_c, b_batch, b_min, t_low, u_heap, u_front;
   float alpha_front;
@@ -236,6 +238,7 @@ struct SharedArgs {
 
 hipError_t launch_encode_layer(const EncodeLayerArgs &a, hipStream_t s);
 hipError_t launch_probe(const ProbeArgs &a, hipStream_t s);
+constexpr int ROUTE_LIGHT_HEAP = 512;  // heap slots of the route's first pass
 size_t route_lds_bytes(int k_c, int pst);
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
