@@ -131,6 +131,8 @@ PairHistArgs pair_hist_args(const SharedArgs &a) {
   h.scan_head = a.scan_head;
   h.is_u8 = a.is_u8;
   h.eager_rows = a.eager_rows;
+  h.pair_rank = a.pair_rank;
+  h.cap = a.cap;
   return h;
 }
 
@@ -170,20 +172,18 @@ __global__ void k_shared_list(SharedArgs a) {
   }
 }
 
-// one wave per query: the query's pairs into their cluster's slots; the
-// pair counts, no longer needed, are counted back down to hand out the slots
+// one wave per query: each of the query's pairs into its cluster's slots, at
+// the rank its count returned
 __global__ void __launch_bounds__(256) k_pair_scatter(SharedArgs a) {
   const int lane = lane_id();
   const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (q >= a.nq) return;
   const int n = clamp_n(a.nclus[q], a.cap);
   const uint32_t *cl = a.clus + q * a.cap;
+  const uint32_t *rank = a.pair_rank + q * a.cap;
   for (int i = a.cseed[q] + lane; i < n; i += WAVE) {
     const uint32_t c = cl[i];
-    if (c < a.n_clusters) {
-      const uint32_t left = atomicSub(&a.hist[c], 1u);
-      a.pair_q[(uint32_t)a.hpos[c] + left - 1] = (uint32_t)q;
-    }
+    if (c < a.n_clusters) a.pair_q[(uint32_t)a.hpos[c] + rank[i]] = (uint32_t)q;
   }
 }
 

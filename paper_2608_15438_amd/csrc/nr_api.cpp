@@ -79,7 +79,7 @@ struct Buffers {
   unsigned long long *counter2;
   uint32_t *skey;
   int64_t *sid;
-  uint32_t *pair_q, *hist, *slist;
+  uint32_t *pair_q, *hist, *pair_rank, *slist;
   uint64_t *hpos;
   uint2 *qnorm;
   uint64_t *swork, *swork_off;
@@ -148,6 +148,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.pool2_key = c.take<uint32_t>(nr::SURVIVOR_POOL);
     B.pool2_id = c.take<int64_t>(nr::SURVIVOR_POOL);
     B.pair_q = c.take<uint32_t>((size_t)s.nq * s.cap);
+    B.pair_rank = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.qnorm = c.take<uint2>((size_t)s.nq);
     B.hist = c.take<uint32_t>(nc1);
     B.hpos = c.take<uint64_t>(nc1);
@@ -531,6 +532,7 @@ nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q
   a.own_rows = B.own_rows;
   a.hist = B.hist;
   a.hpos = B.hpos;
+  a.pair_rank = B.pair_rank;
   a.slist = B.slist;
   // the per-query rows of the whole list are diagnostics: taken here only
   // when the caller asked for per-query statistics

@@ -93,6 +93,8 @@ struct PairHistArgs {
   uint2 *qnorm;                 // [nq] uint8 rows: |q|^2 and its head part
   const unsigned char *queries;
   int row_bytes, scan_head, is_u8, eager_rows;
+  uint32_t *pair_rank;          // [nq x cap] each counted pair's rank among its cluster's pairs
+  int64_t cap;
 };
 
 struct RouteArgs {
@@ -205,7 +207,7 @@ struct SharedArgs {
   const float *own_dists;
   uint32_t *own_rows;         // [nq] copy of rtot kept for diagnostics
   uint32_t *hist;             // [n_clusters + 1] pairs per cluster past the leading clusters
-                              // (counted back to zero by the pair scatter)
+  uint32_t *pair_rank;        // [nq x cap] rank of each counted pair among its cluster's pairs
   uint64_t *hpos;             // [n_clusters + 1] exclusive scan over clusters: pairs before
                               // (low half, the cluster's start in pair_q) and clusters with
                               // pairs before (high half, its scan-list position)
@@ -348,7 +350,8 @@ __device__ __forceinline__ int lower_bound_u64(const uint64_t *a, int n, uint64_
 
 // One wave, query q with list cl[0..n): the leading clusters covering at
 // least seed_min rows stay with the query (cseed[q]); every later (cluster,
-// query) pair is counted in hist; rfull[q] gets the rows of the leading
+// query) pair is counted in hist (its rank among the cluster's pairs goes to
+// pair_rank); rfull[q] gets the rows of the leading
 // clusters (of the whole list with eager_rows); for uint8 rows qnorm[q] gets
 // |q|^2 and the part of it over the scan's head.
 __device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const uint32_t *cl, int n) {
@@ -379,7 +382,7 @@ __device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const ui
       }
       run += bcast_u64(incl, upto);
     }
-    if (cs >= 0 && i >= cs && c < h.n_clusters) atomicAdd(&h.hist[c], 1u);
+    if (cs >= 0 && i >= cs && c < h.n_clusters) h.pair_rank[q * h.cap + i] = atomicAdd(&h.hist[c], 1u);
   }
   if (lane == 0) {
     h.cseed[q] = cs < 0 ? n : cs;
