@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=4, help="workload 1..4 (4 = 1B x 128 uint8)")
+    ap.add_argument("--no-clustering", action="store_true",
+                    help="index without bucket-local clustering (every bucket one cluster)")
     ap.add_argument("--n", type=int, default=0, help="override the base size (smaller instance)")
     ap.add_argument("--probes", type=str, default="", help="comma list of probe budgets to sweep")
     ap.add_argument("--target-recall", type=float, default=0.90)
@@ -206,6 +208,9 @@ def main():
     w = CF.WORKLOADS[args.config]
     if args.n:
         w = CF.scaled(w, args.n)
+    if args.no_clustering:
+        import dataclasses
+        w = dataclasses.replace(w, cluster_rule="none", name=w.name + "-noclust")
     k = w.k
     t_all = time.time()
 

@@ -8,7 +8,8 @@ Follows the paper's index construction (Sec. 3.3) and binarisation (Sec. 3.2.3):
 3. bucket allocation: each row joins the bucket of its code;
 4. bucket-local clustering in latent space: K_B = ceil(|B| / t) clusters per
    bucket; small buckets are one cluster; larger ones run k-means++ on a
-   sample then a few Lloyd passes over the whole bucket;
+   sample then a few Lloyd passes over the whole bucket (rule "none": every
+   bucket is one cluster, the paper's ablation without clustering);
 5. the layout the search reads: rows permuted so each cluster is one
    contiguous span (sorted by code, local cluster, original id), a dense
    directory ``bc_off`` (code -> cluster range), ``cl_off`` (cluster -> row
@@ -330,6 +331,8 @@ def tau_sample_ids(seed: int, n: int, ns: int) -> np.ndarray:
 
 
 def _clusters_per_bucket(w: Workload, sizes: torch.Tensor) -> torch.Tensor:
+    if w.cluster_rule == "none":  # no bucket-local clustering: a bucket is one cluster
+        return torch.minimum(sizes, torch.ones_like(sizes))
     if w.cluster_rule == "fixed4":
         return torch.minimum(sizes, torch.full_like(sizes, 4))
     if w.cluster_rule == "per_bucket8":

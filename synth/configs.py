@@ -21,7 +21,7 @@ class Workload:
     n_queries: int
     # index construction
     tau_mode: str              # "zero" (sign) | "median"
-    cluster_rule: str          # "fixed4" | "per_bucket8" | "capacity"
+    cluster_rule: str          # "fixed4" | "per_bucket8" | "capacity" | "none" (one per bucket)
     capacity: int = 0          # t for cluster_rule == "capacity"
     # search defaults
     k: int = 10

@@ -17,6 +17,8 @@ CASES = {
     "tiny": (1, 0, 0, ()),
     "sift": (2, 60_000, 300, (("widths", (128, 256, 12)),)),
     "deep": (3, 40_000, 200, (("widths", (96, 256, 12)), ("capacity", 30))),
+    # the ablation without bucket-local clustering (every bucket one cluster)
+    "sift_noclust": (2, 60_000, 300, (("widths", (128, 256, 12)), ("cluster_rule", "none"))),
 }
 
 

@@ -10,7 +10,8 @@ from paper_2608_15438_amd import index_build as IB
 from tests.instances import instance, oracle_encoder
 
 CASES = [(1, 0, 0, {}), (2, 30_000, 10, {"widths": (128, 256, 10)}),
-         (3, 20_000, 10, {"widths": (96, 256, 9), "capacity": 40})]
+         (3, 20_000, 10, {"widths": (96, 256, 9), "capacity": 40}),
+         (2, 30_000, 10, {"widths": (128, 256, 10), "cluster_rule": "none"})]
 
 
 @pytest.mark.parametrize("cfg,n,nq,ov", CASES)
@@ -61,6 +62,20 @@ def test_cluster_count_rules(oracle_lib):
                       weights=np.diff(ix3.cl_off.astype(np.int64)), minlength=1 << w3.b)
     assert np.all(kb3 <= np.ceil(sz3 / 40))
     assert np.all(kb3[sz3 <= 40] == (sz3[sz3 <= 40] > 0))   # small buckets: one cluster
+
+
+def test_no_clustering_rule(oracle_lib):
+    # the ablation without bucket-local clustering: a bucket is one cluster,
+    # whose centroid is the mean logit of the whole bucket
+    w, ix, X, Q = instance(2, 30_000, 10, widths=(128, 256, 10), cluster_rule="none")
+    k_b = np.diff(ix.bc_off.astype(np.int64))
+    assert np.all(k_b <= 1)
+    lg = O.encode(oracle_encoder(ix), X)
+    codes = ((lg >= ix.tau) * (1 << np.arange(w.b))).sum(1)
+    sizes = np.bincount(codes, minlength=1 << w.b)
+    assert np.array_equal(k_b, (sizes > 0).astype(np.int64))
+    cl = ix.cl_off.astype(np.int64)
+    assert np.array_equal(np.diff(cl), sizes[sizes > 0])
 
 
 def test_build_is_deterministic(oracle_lib):
