@@ -209,6 +209,10 @@ template <int IS_U8, int NSEG, int U>
 __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refine(RefineArgs a) {
   __shared__ uint32_t s_vs[4][STAGE_CLUSTERS + 1];
   __shared__ uint64_t s_ps[4][STAGE_CLUSTERS];
+  // rows longer than 8 segments: the wave's copy of the query row (slot gl of
+  // segment s at s * 8 + gl), read a chunk at a time
+  constexpr int SC = 8;
+  __shared__ uint4 s_qrow[4][NSEG > SC ? NSEG * 8 : 1];
   const int lane = lane_id();
   const int w = threadIdx.x >> 6;
   const int g = lane >> 3;      // lane group: one row at a time
@@ -235,23 +239,33 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
     const int n_cl = clamp_count(a.nclus[q], a.cap);
     int c = a.tile_c0[t];
 
-    // this lane's slices of the query
-    uint4 qv[NSEG];
+    // this lane's slices of the query: in registers for rows of up to 8
+    // segments, from the wave's LDS copy for longer ones
+    uint4 qv[NSEG <= SC ? NSEG : 1];
+    uint4 *qrow = s_qrow[w];
     const unsigned char *qb = (const unsigned char *)a.queries + q * (int64_t)rb;
+    if constexpr (NSEG <= SC) {
 #pragma unroll
-    for (int s = 0; s < NSEG; ++s) {
-      const int off = 128 * s + 16 * gl;
-      qv[s] = off < rb ? *(const uint4 *)(qb + off) : make_uint4(0, 0, 0, 0);
+      for (int s = 0; s < NSEG; ++s) {
+        const int off = 128 * s + 16 * gl;
+        qv[s] = off < rb ? *(const uint4 *)(qb + off) : make_uint4(0, 0, 0, 0);
+      }
+    } else {
+      __builtin_amdgcn_wave_barrier();  // the previous tile is done with the copy
+      for (int i = lane; i < NSEG * 8; i += WAVE)
+        qrow[i] = 16 * i < rb ? *(const uint4 *)(qb + 16 * i) : make_uint4(0, 0, 0, 0);
+      __builtin_amdgcn_wave_barrier();
     }
     int32_t qq = 0;
     if (IS_U8) {
 #pragma unroll
       for (int s = 0; s < NSEG; ++s) {
+        const uint4 qs4 = NSEG <= SC ? qv[NSEG <= SC ? s : 0] : qrow[s * 8 + gl];
         uint32_t acc = (uint32_t)qq;
-        acc = __builtin_amdgcn_udot4(qv[s].x, qv[s].x, acc, false);
-        acc = __builtin_amdgcn_udot4(qv[s].y, qv[s].y, acc, false);
-        acc = __builtin_amdgcn_udot4(qv[s].z, qv[s].z, acc, false);
-        acc = __builtin_amdgcn_udot4(qv[s].w, qv[s].w, acc, false);
+        acc = __builtin_amdgcn_udot4(qs4.x, qs4.x, acc, false);
+        acc = __builtin_amdgcn_udot4(qs4.y, qs4.y, acc, false);
+        acc = __builtin_amdgcn_udot4(qs4.z, qs4.z, acc, false);
+        acc = __builtin_amdgcn_udot4(qs4.w, qs4.w, acc, false);
         qq = (int32_t)acc;
       }
       qq += __shfl_xor(qq, 1);
@@ -277,7 +291,6 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
       for (uint32_t vb = v; vb < vend; vb += 8 * U) {
         uint64_t phys[U];
         bool ok[U];
-        uint4 xv[U][NSEG];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           const uint32_t rv = vb + 8 * u + g;
@@ -288,6 +301,77 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
             phys[u] = ps[cur] + (rv - vs[cur]);
           }
         }
+        uint32_t key[U];
+        if constexpr (NSEG > SC) {
+          // long rows: chunks of SC segments, each accumulated in segment
+          // order, so the sums are those of the whole-row form
+          uint32_t xx[U], xq[U];
+          float fa[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            xx[u] = 0;
+            xq[u] = 0;
+            fa[u] = 0.0f;
+          }
+#pragma unroll 1
+          for (int s0 = 0; s0 < NSEG; s0 += SC) {
+            uint4 xc[U][SC];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+#pragma unroll
+              for (int s = 0; s < SC; ++s) {
+                const int off = 128 * (s0 + s) + 16 * gl;
+                xc[u][s] = (ok[u] && off < rb) ? load_payload(a.ra.seg(phys[u], off))
+                                               : make_uint4(0, 0, 0, 0);
+              }
+            }
+            uint4 qc[SC];
+#pragma unroll
+            for (int s = 0; s < SC; ++s) qc[s] = qrow[(s0 + s) * 8 + gl];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+#pragma unroll
+              for (int s = 0; s < SC; ++s) {
+                if (IS_U8) {
+                  xx[u] = __builtin_amdgcn_udot4(xc[u][s].x, xc[u][s].x, xx[u], false);
+                  xx[u] = __builtin_amdgcn_udot4(xc[u][s].y, xc[u][s].y, xx[u], false);
+                  xx[u] = __builtin_amdgcn_udot4(xc[u][s].z, xc[u][s].z, xx[u], false);
+                  xx[u] = __builtin_amdgcn_udot4(xc[u][s].w, xc[u][s].w, xx[u], false);
+                  xq[u] = __builtin_amdgcn_udot4(xc[u][s].x, qc[s].x, xq[u], false);
+                  xq[u] = __builtin_amdgcn_udot4(xc[u][s].y, qc[s].y, xq[u], false);
+                  xq[u] = __builtin_amdgcn_udot4(xc[u][s].z, qc[s].z, xq[u], false);
+                  xq[u] = __builtin_amdgcn_udot4(xc[u][s].w, qc[s].w, xq[u], false);
+                } else {
+                  const float t0 = __uint_as_float(xc[u][s].x) - __uint_as_float(qc[s].x);
+                  const float t1 = __uint_as_float(xc[u][s].y) - __uint_as_float(qc[s].y);
+                  const float t2 = __uint_as_float(xc[u][s].z) - __uint_as_float(qc[s].z);
+                  const float t3 = __uint_as_float(xc[u][s].w) - __uint_as_float(qc[s].w);
+                  fa[u] = fmaf(t0, t0, fa[u]);
+                  fa[u] = fmaf(t1, t1, fa[u]);
+                  fa[u] = fmaf(t2, t2, fa[u]);
+                  fa[u] = fmaf(t3, t3, fa[u]);
+                }
+              }
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            if (IS_U8) {
+              int32_t part = (int32_t)xx[u] - 2 * (int32_t)xq[u];
+              part += __shfl_xor(part, 1);
+              part += __shfl_xor(part, 2);
+              part += __shfl_xor(part, 4);
+              key[u] = (uint32_t)(part + qq);
+            } else {
+              float acc = fa[u];
+              acc += __shfl_xor(acc, 1);
+              acc += __shfl_xor(acc, 2);
+              acc += __shfl_xor(acc, 4);
+              key[u] = __float_as_uint(acc);
+            }
+          }
+        } else {
+        uint4 xv[U][NSEG];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
 #pragma unroll
@@ -297,7 +381,6 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
                                            : make_uint4(0, 0, 0, 0);
           }
         }
-        uint32_t key[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           if (IS_U8) {
@@ -336,6 +419,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
             acc += __shfl_xor(acc, 4);
             key[u] = __float_as_uint(acc);
           }
+        }
         }
         // candidates that may enter the top-k read their original id
 #pragma unroll
@@ -376,8 +460,8 @@ static hipError_t launch_refine_t(const RefineArgs &a, int nseg, int grid, hipSt
   NR_REFINE_CASE(3, 4)
   NR_REFINE_CASE(4, 2)
   NR_REFINE_CASE(8, 1)
-  NR_REFINE_CASE(16, 1)
-  NR_REFINE_CASE(48, 1)
+  NR_REFINE_CASE(16, 2)
+  NR_REFINE_CASE(48, 2)
 #undef NR_REFINE_CASE
   return hipErrorInvalidValue;
 }

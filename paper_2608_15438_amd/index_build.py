@@ -152,7 +152,7 @@ def cpu_row_source(w: Workload, which: str = "data") -> Callable[[np.ndarray], n
         return lambda ids: G.sift_rows(seed, centers, ids)
     if w.kind == "deep":
         centers = G.unit_centers(seed_c, w.n_centers, w.d)
-        return lambda ids: G.deep_rows(seed, centers, ids)
+        return lambda ids: G.deep_rows(seed, centers, ids, kappa=w.kappa, spectrum=w.spectrum)
     centers = G.gauss_centers(seed_c, w.n_centers, w.d)
     return lambda ids: G.gauss_rows(seed, centers, ids)
 

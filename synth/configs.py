@@ -1,4 +1,4 @@
-"""Workload table: sizes, generator kinds and seeds of the five evaluation cases.
+"""Workload table: sizes, generator kinds and seeds of the evaluation cases.
 
 Pure data.  Seeds follow one scheme: data = 1000+cfg, queries = 2000+cfg,
 calibration queries = 3000+cfg, encoder = 4000+cfg, sampling = 5000+cfg.
@@ -23,6 +23,8 @@ class Workload:
     tau_mode: str              # "zero" (sign) | "median"
     cluster_rule: str          # "fixed4" | "per_bucket8" | "capacity" | "none" (one per bucket)
     capacity: int = 0          # t for cluster_rule == "capacity"
+    kappa: float = 50.0        # "deep" rows: noise std (1+e)^-spectrum / sqrt(kappa) in
+    spectrum: float = 0.0      #   dimension e around unit centres, then normalised
     # search defaults
     k: int = 10
     l_sel: int = 16
@@ -73,7 +75,18 @@ SIFT1B = Workload(
     capacity=4000, l_sel=16, r_max=7, k_c=3000, probe_budgets=(256, 512, 640, 768, 896, 1024),
 )
 
-WORKLOADS = {w.cfg: w for w in (TINY, SIFT1M, DEEP100M, SIFT1B)}
+GLD10M = Workload(
+    name="gld-like-10M-f32-d1536-b16", cfg=5, kind="deep", n=10_000_000, d=1536, n_centers=10_000,
+    widths=(1536, 512, 16), n_queries=10_000, tau_mode="median",
+    cluster_rule="per_bucket8", kappa=10.0, spectrum=0.75, l_sel=13, r_max=5, k_c=4000,
+    probe_budgets=(64, 128, 256, 512, 1024),
+    notes="high-dimensional regime: 6 KB rows; noise std decaying as (1+e)^-3/4 (about 5.5 "
+          "effective noise dimensions, total power 0.64 x the centre's); the encoder keeps the "
+          "paper's first layer 1536->512 but not its deeper stack, whose untrained form loses "
+          "the neighbourhoods",
+)
+
+WORKLOADS = {w.cfg: w for w in (TINY, SIFT1M, DEEP100M, SIFT1B, GLD10M)}
 
 
 def scaled(w: Workload, n: int, n_queries: Optional[int] = None, **kw) -> Workload:

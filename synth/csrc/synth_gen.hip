@@ -80,7 +80,7 @@ __global__ void k_sift(uint32_t seed, const double *centers, int64_t n_centers, 
 }
 
 __global__ void k_deep(uint32_t seed, const double *centers, int64_t n_centers, int d,
-                       double inv_sqrt_kappa, const int64_t *ids, int64_t first, int64_t m,
+                       const double *scale, const int64_t *ids, int64_t first, int64_t m,
                        float *out) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= m) return;
@@ -90,14 +90,14 @@ __global__ void k_deep(uint32_t seed, const double *centers, int64_t n_centers, 
   {
     U16Stream st(row, seed);
     for (int e = 0; e < d; ++e) {
-      double y = c[e] + st.normal() * inv_sqrt_kappa;
+      double y = c[e] + st.normal() * scale[e];
       nrm2 = nrm2 + y * y;
     }
   }
   const double nrm = sqrt(nrm2);
   U16Stream st(row, seed);
   for (int e = 0; e < d; ++e) {
-    double y = c[e] + st.normal() * inv_sqrt_kappa;
+    double y = c[e] + st.normal() * scale[e];
     out[i * d + e] = (float)(y / nrm);
   }
 }
@@ -116,20 +116,23 @@ __global__ void k_gauss(uint32_t seed, const double *centers, int64_t n_centers,
 
 extern "C" {
 
-// kind: 0 = SIFT-like uint8, 1 = Deep-like fp32 unit rows, 2 = Gaussian fp32.
+// kind: 0 = SIFT-like uint8, 1 = unit fp32 rows (Deep-like, GLD-like), 2 = Gaussian fp32.
 // Rows are ids[i] (DEVICE int64) when ids is not NULL, else first + i.
-// centers: DEVICE fp64 [n_centers x d]; out: DEVICE [m x d].  Returns a hipError_t.
+// centers: DEVICE fp64 [n_centers x d]; out: DEVICE [m x d].  param is the
+// noise std of kinds 0 and 2; scale (DEVICE fp64 [d]) the per-dimension noise
+// std of kind 1.  Returns a hipError_t.
 int synth_rows(int kind, uint32_t seed, const double *centers, int64_t n_centers, int d,
-               double param, const int64_t *ids, int64_t first, int64_t m, void *out,
-               hipStream_t stream) {
+               double param, const double *scale, const int64_t *ids, int64_t first, int64_t m,
+               void *out, hipStream_t stream) {
   if (m <= 0) return 0;
   if (d % 4 != 0 && kind == 0) return (int)hipErrorInvalidValue;
+  if (kind == 1 && !scale) return (int)hipErrorInvalidValue;
   dim3 block(256), grid((unsigned)((m + 255) / 256));
   if (kind == 0)
     hipLaunchKernelGGL(k_sift, grid, block, 0, stream, seed, centers, n_centers, d, param, ids,
                        first, m, (uint8_t *)out);
   else if (kind == 1)
-    hipLaunchKernelGGL(k_deep, grid, block, 0, stream, seed, centers, n_centers, d, param, ids,
+    hipLaunchKernelGGL(k_deep, grid, block, 0, stream, seed, centers, n_centers, d, scale, ids,
                        first, m, (float *)out);
   else
     hipLaunchKernelGGL(k_gauss, grid, block, 0, stream, seed, centers, n_centers, d, param, ids,

@@ -13,6 +13,9 @@ Workload shapes (the paper's evaluation data, Sec. 4.1 and Table 1):
   plus sigma=12 noise, rounded half-to-even and clipped to [0,255];
 * Deep-like: fp32 unit-norm rows, d=96, a mixture of unit centres plus
   N(0, I/kappa) noise with kappa=50, then L2-normalised;
+* GLD-like (the high-dimensional regime of Sec. 4.1): the same construction
+  at d=1536, with a noise std that decays as (1+e)^-3/4 over the dimensions
+  so that the rows have a low intrinsic dimension, as image embeddings do;
 * Gaussian mixture: fp32 rows, centres ~ N(0, 4I), unit noise (tiny case).
 
 Nothing here computes any part of the search method.
@@ -49,7 +52,7 @@ def _u32_words(seed, rows, n_words, tag):
     return out[:, :n_words]
 
 
-def irwin_hall_normals(seed, rows, d, tag=TAG_NOISE, chunk=4096):
+def irwin_hall_normals(seed, rows, d, tag=TAG_NOISE, chunk=0):
     """Approximately standard-normal fp64 values [len(rows), d].
 
     Element e of a row sums the twelve u16 draws with indices 12e..12e+11 of
@@ -58,6 +61,8 @@ def irwin_hall_normals(seed, rows, d, tag=TAG_NOISE, chunk=4096):
     """
     rows = np.asarray(rows, dtype=np.int64)
     n16 = 12 * d
+    # about 64K Philox calls per block keeps the working arrays cache-sized
+    chunk = chunk or max(1, 65536 // ((n16 // 2 + 3) // 4))
     out = np.empty((len(rows), d), dtype=np.float64)
     for s0 in range(0, len(rows), chunk):
         words = _u32_words(seed, rows[s0:s0 + chunk], (n16 + 1) // 2, tag)
@@ -115,14 +120,22 @@ def sift_rows(seed, centers, rows, sigma=12.0):
     return np.clip(np.rint(x), 0, 255).astype(np.uint8)
 
 
-def deep_rows(seed, centers, rows, kappa=50.0):
-    """fp32 unit rows normalize(centre + z / sqrt(kappa))."""
+def noise_scale(d, kappa=50.0, spectrum=0.0):
+    """Per-dimension noise std of unit rows: (1 + e)^-spectrum / sqrt(kappa),
+    fp64 [d] (a constant 1 / sqrt(kappa) for spectrum 0).  Both generators
+    take this table as an input."""
+    e = np.arange(d, dtype=np.float64)
+    return (1.0 / np.sqrt(kappa)) * (1.0 + e) ** (-spectrum) if spectrum else \
+        np.full(d, 1.0 / np.sqrt(kappa))
+
+
+def deep_rows(seed, centers, rows, kappa=50.0, spectrum=0.0):
+    """fp32 unit rows normalize(centre + scale * z), scale = noise_scale()."""
     rows = np.asarray(rows, dtype=np.int64)
     d = centers.shape[1]
     comp = component_of(seed, rows, centers.shape[0])
     z = irwin_hall_normals(seed, rows, d)
-    c = 1.0 / np.sqrt(kappa)
-    y = centers[comp] + z * c
+    y = centers[comp] + z * noise_scale(d, kappa, spectrum)[None, :]
     nrm2 = np.zeros(len(rows), dtype=np.float64)
     for e in range(d):                      # fixed ascending order
         nrm2 = nrm2 + y[:, e] * y[:, e]

@@ -34,7 +34,8 @@ def lib():
             raise RuntimeError(f"{SO} missing: run synth.gpu.build()")
         L = C.CDLL(SO)
         L.synth_rows.argtypes = [C.c_int, C.c_uint32, C.c_void_p, C.c_int64, C.c_int, C.c_double,
-                                 C.c_void_p, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p]
+                                 C.c_void_p, C.c_void_p, C.c_int64, C.c_int64, C.c_void_p,
+                                 C.c_void_p]
         L.synth_rows.restype = C.c_int
         _lib = L
     return _lib
@@ -54,18 +55,22 @@ class GpuRows:
             self.param = 12.0
         elif w.kind == "deep":
             c = G.unit_centers(seed_c, w.n_centers, w.d)
-            self.param = 1.0 / np.sqrt(50.0)
+            self.param = 0.0
         else:
             c = G.gauss_centers(seed_c, w.n_centers, w.d)
             self.param = 1.0
         self.device = torch.device(device)
         self.centers = torch.from_numpy(np.ascontiguousarray(c, np.float64)).to(self.device)
+        self.scale = None
+        if w.kind == "deep":
+            self.scale = torch.from_numpy(G.noise_scale(w.d, w.kappa, w.spectrum)).to(self.device)
         self.dtype = torch.uint8 if w.kind == "sift" else torch.float32
 
     def _run(self, ids_t, first, m, out):
         st = torch.cuda.current_stream(self.device).cuda_stream
         rc = lib().synth_rows(self.KIND[self.w.kind], self.seed, self.centers.data_ptr(),
                               self.centers.shape[0], self.w.d, self.param,
+                              None if self.scale is None else self.scale.data_ptr(),
                               None if ids_t is None else ids_t.data_ptr(), first, m,
                               out.data_ptr(), C.c_void_p(st))
         if rc != 0:

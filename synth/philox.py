@@ -31,27 +31,18 @@ def philox4x32_10(c0, c1, c2, c3, k0, k1):
     All arguments are broadcastable uint32 arrays (or scalars).  Returns the
     four uint32 output words as a tuple of arrays.
     """
-    c0 = np.asarray(c0, dtype=np.uint32)
-    c1 = np.asarray(c1, dtype=np.uint32)
-    c2 = np.asarray(c2, dtype=np.uint32)
-    c3 = np.asarray(c3, dtype=np.uint32)
-    c0, c1, c2, c3 = np.broadcast_arrays(c0, c1, c2, c3)
-    c0 = c0.astype(np.uint32)
-    c1 = c1.astype(np.uint32)
-    c2 = c2.astype(np.uint32)
-    c3 = c3.astype(np.uint32)
-    k0 = np.uint32(k0)
-    k1 = np.uint32(k1)
-    with np.errstate(over="ignore"):
-        for rnd in range(10):
-            p0 = M0 * c0.astype(np.uint64)
-            p1 = M1 * c2.astype(np.uint64)
-            hi0 = (p0 >> _SH32).astype(np.uint32)
-            lo0 = (p0 & _MASK32).astype(np.uint32)
-            hi1 = (p1 >> _SH32).astype(np.uint32)
-            lo1 = (p1 & _MASK32).astype(np.uint32)
-            c0, c1, c2, c3 = hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0
-            if rnd != 9:
-                k0 = np.uint32(k0 + W0)
-                k1 = np.uint32(k1 + W1)
+    c0, c1, c2, c3 = np.broadcast_arrays(*(np.asarray(c, dtype=np.uint32) for c in (c0, c1, c2, c3)))
+    # words held in uint64 (values below 2^32), so the 32x32 -> 64 products
+    # need no conversions
+    c0, c1, c2, c3 = (c.astype(np.uint64) for c in (c0, c1, c2, c3))
+    k0 = int(k0) & 0xFFFFFFFF
+    k1 = int(k1) & 0xFFFFFFFF
+    for rnd in range(10):
+        p0 = M0 * c0
+        p1 = M1 * c2
+        c0, c1, c2, c3 = ((p1 >> _SH32) ^ c1) ^ np.uint64(k0), p1 & _MASK32, \
+            ((p0 >> _SH32) ^ c3) ^ np.uint64(k1), p0 & _MASK32
+        k0 = (k0 + int(W0)) & 0xFFFFFFFF
+        k1 = (k1 + int(W1)) & 0xFFFFFFFF
+    c0, c1, c2, c3 = (c.astype(np.uint32) for c in (c0, c1, c2, c3))
     return c0, c1, c2, c3

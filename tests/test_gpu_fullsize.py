@@ -1,6 +1,6 @@
 """Parity at the benchmark's full sizes and launch configuration: the whole
-10,000-query batch goes through nr_search on the 1B x 128 uint8 and the
-100M x 96 fp32 indexes (built on the GPU from the seeded generators); a
+10,000-query batch goes through nr_search on the 1B x 128 uint8, the
+100M x 96 fp32 and the 10M x 1536 fp32 indexes (built on the GPU from the seeded generators); a
 seeded sample of queries is recomputed one by one by the oracle, with the
 rows of their candidate clusters staged in host memory."""
 import gc
@@ -28,7 +28,8 @@ GATE = dict(m_x=[0.0, 1.0], m_y=[0.5, 2.0])
                                                 (4, 640, NR.NR_REFINE_PER_QUERY, "copy"),
                                                 (4, 520, NR.NR_REFINE_AUTO, "split"),
                                                 (3, 256, NR.NR_REFINE_AUTO, "copy"),
-                                                (3, 256, NR.NR_REFINE_AUTO, "rows")])
+                                                (3, 256, NR.NR_REFINE_AUTO, "rows"),
+                                                (5, 64, NR.NR_REFINE_AUTO, "copy")])
 def test_full_size_sampled_queries(cfg, P, mode, layout):
     if not torch.cuda.is_available():
         pytest.skip("no HIP device")

@@ -19,6 +19,8 @@ CASES = {
     "deep": (3, 40_000, 200, (("widths", (96, 256, 12)), ("capacity", 30))),
     # the ablation without bucket-local clustering (every bucket one cluster)
     "sift_noclust": (2, 60_000, 300, (("widths", (128, 256, 12)), ("cluster_rule", "none"))),
+    # 1536-d fp32 rows (6 KB) through a five-layer encoder
+    "gld": (5, 20_000, 100, (("widths", (1536, 512, 256, 128, 64, 10)),)),
 }
 
 
@@ -171,6 +173,35 @@ def test_refine_given_clusters(dev, name, k, layout):
                                  torch.from_numpy(n).to(dev))
     oi, od, _ = O.refine(c["ix"].rows, c["ix"].row_ids, c["ix"].cl_off, c["Q"], lists, k)
     _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
+
+
+# every refine kernel shape by row length: rows past 8 x 128 bytes keep the
+# query in LDS and accumulate 8 segments at a time; lengths that are not a
+# multiple of 128 bytes (they are multiples of 16) leave a ragged last segment
+@pytest.mark.parametrize("cfg,d", [(3, 300), (3, 384), (3, 700), (3, 1536),
+                                   (2, 1104), (2, 2048), (2, 4096)])
+@pytest.mark.parametrize("layout", ["gix", "gix_split"])
+def test_refine_row_lengths(dev, cfg, d, layout):
+    ov = dict(d=d, widths=(d, 64, 8), n_centers=30, cluster_rule="capacity", capacity=30)
+    w, ix, X, Q = instance(cfg, 3000, 40, **ov)
+    gix = NR.Index.from_built(ix if layout == "gix" else split_index(ix, dev), dev)
+    rng = np.random.default_rng(7 + d)
+    nc = len(ix.cl_off) - 1
+    cap = min(nc, 48)
+    lists = [np.sort(rng.choice(nc, size=int(rng.integers(0, cap + 1)), replace=False))
+             for _ in range(len(Q))]
+    cl = np.zeros((len(Q), cap), np.uint32)
+    n = np.zeros(len(Q), np.int32)
+    for q, L in enumerate(lists):
+        cl[q, :len(L)] = L
+        n[q] = len(L)
+    for k in (1, 10, 64):
+        gi, gd = gix.nr_refine(torch.from_numpy(Q).to(dev), k,
+                               torch.from_numpy(cl.view(np.int32)).to(dev),
+                               torch.from_numpy(n).to(dev))
+        oi, od, _ = O.refine(ix.rows, ix.row_ids, ix.cl_off, Q,
+                             [L.astype(np.uint32) for L in lists], k)
+        _assert_topk(dict(w=w, X=X, Q=Q), gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
 
 
 # ------------------------------------------------------------------ whole path
@@ -332,6 +363,10 @@ def test_shared_schedule_work_counters(dev, name, layout):
     p = default_params(c, **MODES["shared_seed64"][1])
     gi, gd = c[layout].nr_search(c["Qd"], 10, 256, p, logits=c["lgd"])
     w = c[layout].nr_last_work()
+    if c["w"].row_bytes > 1024:
+        # rows past 8 x 128 bytes always take the per-query schedule
+        assert w["shared_pairs"] == 0 and w["rows"] == w["own_rows"] > 0
+        return
     assert w["shared_pairs"] > 0 and w["survivors"] > 0 and w["full_rows"] > 0
     assert w["rows"] == w["own_rows"] + w["shared_pair_rows"]
     assert w["rows_read"] == w["own_rows"] + w["shared_rows"] + w["fallback_rows"]

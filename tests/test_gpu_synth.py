@@ -17,7 +17,7 @@ def dev():
     return torch.device("cuda")
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
 def test_gpu_rows_match_numpy(dev, cfg):
     w = CF.WORKLOADS[cfg]
     ids = np.concatenate([np.arange(300), np.array([w.n - 1, 123457 % w.n, 7])])
