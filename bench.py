@@ -312,16 +312,18 @@ def main():
     per_query = {name: round(float(qs[i]), 2) for name, i in NR.QS.items()}
     log("per-query means", per_query, "work", work)
     # the two refinement kernels.  Algorithmic bytes: k_refine reads whole rows;
-    # k_scan reads the head of every scanned row, then the rows it reads whole
-    # (the tail, or with whole rows after the heads the whole row) -- one
-    # launch of each per search: the batch fits one chunk
+    # k_scan reads the head of every scanned row, then what it reads of the
+    # rows its heads left open (whole rows, or the 1 KB slabs of long rows up
+    # to the last one some query needed; without whole rows after the heads,
+    # minus the head already read) -- one launch of each per search: the
+    # batch fits one chunk
     nt = max(n_timed, 1)
     kernels = {}
     hb = work["head_bytes"]
+    scan_body = work["body_bytes"] - (0 if ix.head_copy else work["full_rows"] * hb)
     for kname, stage, nrows, ab in (
             ("k_refine", "refine", work["own_rows"], work["own_rows"] * w.row_bytes),
-            ("k_scan", "shared_scan", work["shared_rows"],
-             work["shared_rows"] * hb + work["full_rows"] * (w.row_bytes - (0 if ix.head_copy else hb)))):
+            ("k_scan", "shared_scan", work["shared_rows"], work["shared_rows"] * hb + scan_body)):
         ms = stage_ms[stage] / nt
         if ms <= 0 or nrows <= 0:
             continue
@@ -336,7 +338,7 @@ def main():
     st5 = sum(stage_ms[x] for x in ("plan", "refine", "merge", "shared_prep", "shared_scan",
                                     "shared_merge")) / nt
     b5 = ((work["own_rows"] + work["fallback_rows"]) * w.row_bytes + work["shared_rows"] * hb
-          + work["full_rows"] * (w.row_bytes - (0 if ix.head_copy else hb)))
+          + scan_body)
     cand_bytes = rows * w.row_bytes
     refine_stage = {"ms": round(st5, 4), "bytes_read": int(b5), "candidate_bytes": int(cand_bytes),
                     "candidate_gbs": round(cand_bytes / (st5 * 1e-3) / 1e9, 1),

@@ -157,7 +157,9 @@ typedef struct {
  * the bounds of all queries listing its cluster; only rows whose head leaves
  * some query open are read whole, and those at or before the bound are merged
  * into the query's result.  AUTO picks SHARED for batches of at least 512
- * queries.  Rows longer than 1024 bytes always use PER_QUERY. */
+ * queries.  Distances of rows longer than 1024 bytes are summed per 1 KB slab
+ * (each slab reduced over its lanes, the slabs added in order) under both
+ * schedules, so the two still agree bit for bit. */
 enum { NR_REFINE_AUTO = 0, NR_REFINE_PER_QUERY = 1, NR_REFINE_SHARED = 2 };
 
 /* Per-query counters written by nr_search_ex when `qstats` is not NULL. */
@@ -253,8 +255,12 @@ nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches
  *   NR_WORK_FLAGGED        queries recomputed after their survivors overflowed
  *   NR_WORK_FALLBACK_ROWS  rows read by that recomputation
  *   NR_WORK_SHARED_PAIR_ROWS rows scored by the scan, summed over its pairs
- *   NR_WORK_FULL_ROWS      rows the scan read whole (their head left a query open)
+ *   NR_WORK_FULL_ROWS      rows the scan read past their head (it left a query open)
  *   NR_WORK_HEAD_BYTES     bytes of a row the scan reads for every row (its head)
+ *   NR_WORK_BODY_BYTES     bytes the scan read from those rows: whole rows; for
+ *                          fp32 rows longer than 1024 bytes the first 1 KB slab,
+ *                          then per (row, query) pair still at or before its bound
+ *                          the further slabs until its running sum passes it
  * ROWS_READ = OWN_ROWS + SHARED_ROWS + FALLBACK_ROWS and
  * ROWS = OWN_ROWS + SHARED_PAIR_ROWS. */
 enum {
@@ -270,7 +276,8 @@ enum {
   NR_WORK_SHARED_PAIR_ROWS = 9,
   NR_WORK_FULL_ROWS = 10,
   NR_WORK_HEAD_BYTES = 11,
-  NR_WORK = 12
+  NR_WORK_BODY_BYTES = 12,
+  NR_WORK = 13
 };
 nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *work, int32_t n_work);
 

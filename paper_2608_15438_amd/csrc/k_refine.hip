@@ -303,18 +303,22 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
         }
         uint32_t key[U];
         if constexpr (NSEG > SC) {
-          // long rows: chunks of SC segments, each accumulated in segment
-          // order, so the sums are those of the whole-row form
+          // long rows: slabs of SC segments (1 KB).  Each slab is accumulated
+          // in segment order per lane, reduced over the row's 8 lanes, and
+          // added to the row's running sum in slab order: the arithmetic the
+          // batch-shared scan uses for rows this long
           uint32_t xx[U], xq[U];
-          float fa[U];
+          float fs[U];
 #pragma unroll
           for (int u = 0; u < U; ++u) {
             xx[u] = 0;
             xq[u] = 0;
-            fa[u] = 0.0f;
+            fs[u] = 0.0f;
           }
+          const int nsl = (rb + 128 * SC - 1) / (128 * SC);
 #pragma unroll 1
-          for (int s0 = 0; s0 < NSEG; s0 += SC) {
+          for (int sl = 0; sl < nsl; ++sl) {
+            const int s0 = sl * SC;
             uint4 xc[U][SC];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -330,6 +334,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
             for (int s = 0; s < SC; ++s) qc[s] = qrow[(s0 + s) * 8 + gl];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
+              float fa = 0.0f;
 #pragma unroll
               for (int s = 0; s < SC; ++s) {
                 if (IS_U8) {
@@ -346,28 +351,31 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
                   const float t1 = __uint_as_float(xc[u][s].y) - __uint_as_float(qc[s].y);
                   const float t2 = __uint_as_float(xc[u][s].z) - __uint_as_float(qc[s].z);
                   const float t3 = __uint_as_float(xc[u][s].w) - __uint_as_float(qc[s].w);
-                  fa[u] = fmaf(t0, t0, fa[u]);
-                  fa[u] = fmaf(t1, t1, fa[u]);
-                  fa[u] = fmaf(t2, t2, fa[u]);
-                  fa[u] = fmaf(t3, t3, fa[u]);
+                  fa = fmaf(t0, t0, fa);
+                  fa = fmaf(t1, t1, fa);
+                  fa = fmaf(t2, t2, fa);
+                  fa = fmaf(t3, t3, fa);
                 }
+              }
+              if (!IS_U8) {
+                fa += __shfl_xor(fa, 1);
+                fa += __shfl_xor(fa, 2);
+                fa += __shfl_xor(fa, 4);
+                fs[u] = sl == 0 ? fa : fs[u] + fa;
               }
             }
           }
 #pragma unroll
           for (int u = 0; u < U; ++u) {
             if (IS_U8) {
+              // integer sums: the slab order does not matter
               int32_t part = (int32_t)xx[u] - 2 * (int32_t)xq[u];
               part += __shfl_xor(part, 1);
               part += __shfl_xor(part, 2);
               part += __shfl_xor(part, 4);
               key[u] = (uint32_t)(part + qq);
             } else {
-              float acc = fa[u];
-              acc += __shfl_xor(acc, 1);
-              acc += __shfl_xor(acc, 2);
-              acc += __shfl_xor(acc, 4);
-              key[u] = __float_as_uint(acc);
+              key[u] = __float_as_uint(fs[u]);
             }
           }
         } else {

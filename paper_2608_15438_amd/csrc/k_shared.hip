@@ -208,8 +208,9 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   const int64_t nc1 = a.n_clusters + 1;
   hipError_t e = launch_fill_i32(a.scnt, a.nq, 0, s);
   if (e == hipSuccess) e = launch_fill_i32(a.flag, a.nq, 0, s);
-  if (e == hipSuccess) e = launch_fill_i32((int32_t *)(a.wstats + 3), 2, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t *)(a.wstats + 3), 4, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.pool_cnt, 2, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.open_cnt, 2, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
   if (e != hipSuccess) return e;
   size_t tmp = a.scan_tmp_bytes;
@@ -298,6 +299,11 @@ __device__ __forceinline__ void add_survivor(const SharedArgs &a, uint32_t q, ui
 //            load the whole row and compute the exact distance for the listed
 //            queries in the same arithmetic and order as k_refine; rows at or
 //            before the query's bound become survivors.
+// Rows longer than 8 x 128 bytes hold only one 1 KB slab of each query row in
+// LDS at a time: phase B runs slab by slab over the listed rows, keeps every
+// (row, query) pair's running sum in LDS, and tests the survivors after the
+// last slab (slab partials are reduced over the 8 lanes and added in slab
+// order, as k_refine does for such rows).
 constexpr int SCAN_UMAX = 64;    // units per batch
 
 template <int HL>
@@ -348,15 +354,19 @@ __device__ __forceinline__ uint32_t pair_key(const uint4 *xv, const uint4 *qv, i
 }
 
 template <int IS_U8, int NSEG, int HL, int U>
-__global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(SharedArgs a) {
+__global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 2 : 1))
+    k_scan(SharedArgs a) {
+  constexpr bool LONG = NSEG > 8;            // query rows staged a 1 KB slab at a time
   constexpr int RPW = WAVE / HL;             // virtual rows per phase-A load
   constexpr int STEP = RPW * U;              // virtual rows per phase-A pass
   constexpr int SCAP = STEP + NR_SCAN_SLACK;  // listed rows before phase B runs
   constexpr int G = SHARED_G;
-  constexpr int QCH = NSEG * 8;              // 16-byte chunks of a (padded) query row
+  constexpr int QCH = LONG ? 64 : NSEG * 8;  // 16-byte chunks of a (padded) query row or slab
   constexpr int QMAX = NSEG <= 1 ? NR_SCAN_QMAX1 : (NSEG <= 2 ? 16 : 8);  // query slots per batch
-  constexpr int UB = NSEG <= 1 ? NR_SCAN_UB1 : (NSEG <= 4 ? 2 : 1);      // phase-B rows per lane group
+  constexpr int UB = NSEG <= 1 ? NR_SCAN_UB1 : (NSEG <= 4 || LONG ? 2 : 1);  // phase-B rows per lane group
   static_assert(QMAX <= WAVE, "one query slot per lane");
+  static_assert(!LONG || QMAX == G, "a long-row slab holds one unit's queries per slot");
+  constexpr int NSB = LONG ? 1 : NSEG;       // segments held per row by the short-row phase B
   __shared__ uint64_t s_ub[4][SCAN_UMAX];        // unit: first payload row
   __shared__ uint32_t s_uv[4][SCAN_UMAX + 1];    // unit: first virtual row
   __shared__ uint32_t s_uq[4][SCAN_UMAX];        // unit: first query slot | queries << 16
@@ -366,6 +376,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
   __shared__ uint32_t s_qi[4][QMAX];             // query id
   __shared__ int32_t s_qq[4][QMAX];              // |q|^2 (uint8)
   __shared__ uint32_t s_sv[4][SCAP];             // listed rows: unit << 20 | row << 8 | mask
+  __shared__ uint32_t s_run[4][LONG ? SCAP * G : 1];  // long rows: running sum per (listed row, query)
+  __shared__ int32_t s_runx[4][LONG && IS_U8 ? SCAP : 1];  // long uint8 rows: running |x|^2
   const int lane = lane_id();
   const int w = threadIdx.x >> 6;
   const int grp = lane >> 3;  // phase B: 8 lanes per row
@@ -380,13 +392,15 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
   uint32_t *qi = s_qi[w];
   int32_t *qqs = s_qq[w];
   uint32_t *sv = s_sv[w];
+  uint32_t *run = s_run[w];
+  int32_t *runx = s_runx[w];
   const int64_t NS = (int64_t)(a.hpos[a.n_clusters] >> 32);
   const uint64_t W = a.swork_off[NS];
   const uint64_t ntiles = (W + SHARED_TILE - 1) / SHARED_TILE;
   const int rb = a.row_bytes;
   const int k = a.k;
   const unsigned char *queries = (const unsigned char *)a.queries;
-  unsigned long long full_rows = 0;
+  unsigned long long full_rows = 0, body_bytes = 0;
   uint32_t nbatch = 0, tested_batches = 0;  // direct batches: see below
   uint64_t tested_rows = 0, open_rows = 0;
   if (ntiles == 0) return;
@@ -555,18 +569,18 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
       __builtin_amdgcn_wave_barrier();
 
       // ---- phase B: whole rows of the listed (row, queries), UB rows per lane group
-      auto phase_b = [&](int nsv) {
+      auto phase_b_short = [&](int nsv) {
         for (int e0 = 0; e0 < nsv; e0 += 8 * UB) {
           uint32_t ent[UB];
           uint64_t row[UB];
-          uint4 xv[UB][NSEG];
+          uint4 xv[UB][NSB];
 #pragma unroll
           for (int b = 0; b < UB; ++b) {
             const int e = e0 + 8 * b + grp;
             ent[b] = e < nsv ? sv[e] : 0u;
             row[b] = ub[ent[b] >> 20] + ((ent[b] >> 8) & 0xfffu);
 #pragma unroll
-            for (int s = 0; s < NSEG; ++s) {
+            for (int s = 0; s < NSB; ++s) {
               const int off = 128 * s + 16 * gl;
               xv[b][s] = ((ent[b] & 0xffu) && off < rb) ? load_stream(a.ra.seg(row[b], off))
                                                        : make_uint4(0, 0, 0, 0);
@@ -580,7 +594,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
             if (IS_U8) {
               uint32_t acc = 0;
 #pragma unroll
-              for (int s = 0; s < NSEG; ++s) {
+              for (int s = 0; s < NSB; ++s) {
                 acc = __builtin_amdgcn_udot4(xv[b][s].x, xv[b][s].x, acc, false);
                 acc = __builtin_amdgcn_udot4(xv[b][s].y, xv[b][s].y, acc, false);
                 acc = __builtin_amdgcn_udot4(xv[b][s].z, xv[b][s].z, acc, false);
@@ -593,10 +607,10 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
               const bool bit = ((mask >> j) & 1u) != 0;
               if (!ballot(bit)) continue;
               const int slot = slot0 + (bit ? j : 0);
-              uint4 qv[NSEG];
+              uint4 qv[NSB];
 #pragma unroll
-              for (int s = 0; s < NSEG; ++s) qv[s] = qs[slot * QCH + 8 * s + gl];
-              const uint32_t key = pair_key<IS_U8, NSEG>(xv[b], qv, xx, qqs[slot]);
+              for (int s = 0; s < NSB; ++s) qv[s] = qs[slot * QCH + 8 * s + gl];
+              const uint32_t key = pair_key<IS_U8, NSB>(xv[b], qv, xx, qqs[slot]);
               // at or before the bound: a survivor (ties included; the merge orders them)
               if (bit && gl == 0 && key <= tk[slot]) {
                 add_survivor(a, qi[slot], key, a.row_ids[row[b]]);
@@ -605,6 +619,168 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
           }
         }
         full_rows += (unsigned long long)nsv;
+        body_bytes += (unsigned long long)nsv * (uint32_t)rb;
+      };
+
+      // ---- phase B for long rows, slab by slab.  Lane c of a slab load holds
+      // 16-byte chunk c of slot t's slab (slot t's query id is qi[t])
+      auto stage_slab = [&](int s0) {
+        __builtin_amdgcn_wave_barrier();  // every read of the previous slab is done
+        uint4 sl[QMAX];
+#pragma unroll
+        for (int t = 0; t < QMAX; ++t) {
+          const int off = 128 * s0 + 16 * lane;
+          sl[t] = t < nqs && off < rb
+                      ? *(const uint4 *)(queries + (uint64_t)qi[t] * rb + off)
+                      : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int t = 0; t < QMAX; ++t) qs[t * QCH + lane] = sl[t];
+        __builtin_amdgcn_wave_barrier();
+      };
+      auto phase_b_long = [&](int nsv) {
+        const int nsl = (rb + 1023) / 1024;
+        // uint8 rows are finished here, slab by slab; for fp32 rows only the
+        // first slab is, and the pairs it leaves at or before their bound go
+        // to the open list (their running sums are bounds: see below)
+        const int nslk = IS_U8 ? nsl : 1;
+        full_rows += (unsigned long long)nsv;
+        for (int sl = 0; sl < nslk && nsv > 0; ++sl) {
+          const int s0 = 8 * sl;
+          if (sl > 0) stage_slab(s0);
+          body_bytes += (unsigned long long)nsv * (uint32_t)(rb - 1024 * sl < 1024 ? rb - 1024 * sl : 1024);
+          for (int e0 = 0; e0 < nsv; e0 += 8 * UB) {
+            uint32_t ent[UB];
+            uint64_t row[UB];
+            uint4 xv[UB][8];
+#pragma unroll
+            for (int b = 0; b < UB; ++b) {
+              const int e = e0 + 8 * b + grp;
+              ent[b] = e < nsv ? sv[e] : 0u;
+              row[b] = ub[ent[b] >> 20] + ((ent[b] >> 8) & 0xfffu);
+#pragma unroll
+              for (int s = 0; s < 8; ++s) {
+                const int off = 128 * (s0 + s) + 16 * gl;
+                xv[b][s] = ((ent[b] & 0xffu) && off < rb) ? load_stream(a.ra.seg(row[b], off))
+                                                         : make_uint4(0, 0, 0, 0);
+              }
+            }
+#pragma unroll
+            for (int b = 0; b < UB; ++b) {
+              const uint32_t mask = ent[b] & 0xffu;
+              if (!ballot(mask != 0)) continue;
+              const int e = e0 + 8 * b + grp;
+              if (IS_U8) {
+                uint32_t acc = 0;
+#pragma unroll
+                for (int s = 0; s < 8; ++s) {
+                  acc = __builtin_amdgcn_udot4(xv[b][s].x, xv[b][s].x, acc, false);
+                  acc = __builtin_amdgcn_udot4(xv[b][s].y, xv[b][s].y, acc, false);
+                  acc = __builtin_amdgcn_udot4(xv[b][s].z, xv[b][s].z, acc, false);
+                  acc = __builtin_amdgcn_udot4(xv[b][s].w, xv[b][s].w, acc, false);
+                }
+                const int32_t p = group8_sum((int32_t)acc);
+                if (mask && gl == 0) runx[e] = sl == 0 ? p : runx[e] + p;
+              }
+              const int slot0 = (int)(uq[ent[b] >> 20] & 0xffffu);
+              uint32_t live = 0;  // the listed queries still at or before their bound
+              for (int j = 0; j < gmax; ++j) {
+                const bool bit = ((mask >> j) & 1u) != 0;
+                if (!ballot(bit)) continue;
+                const int slot = slot0 + (bit ? j : 0);
+                uint4 qv[8];
+#pragma unroll
+                for (int s = 0; s < 8; ++s) qv[s] = qs[slot * QCH + 8 * s + gl];
+                uint32_t pbits;
+                if (IS_U8) {
+                  uint32_t xq = 0;
+#pragma unroll
+                  for (int s = 0; s < 8; ++s) {
+                    xq = __builtin_amdgcn_udot4(xv[b][s].x, qv[s].x, xq, false);
+                    xq = __builtin_amdgcn_udot4(xv[b][s].y, qv[s].y, xq, false);
+                    xq = __builtin_amdgcn_udot4(xv[b][s].z, qv[s].z, xq, false);
+                    xq = __builtin_amdgcn_udot4(xv[b][s].w, qv[s].w, xq, false);
+                  }
+                  const int32_t p = group8_sum((int32_t)xq);
+                  pbits = (uint32_t)(sl == 0 ? p : (int32_t)run[bit ? e * G + j : 0] + p);
+                  live |= (bit ? 1u : 0u) << j;  // uint8 partial sums are not bounds
+                } else {
+                  float acc = 0.0f;
+#pragma unroll
+                  for (int s = 0; s < 8; ++s) {
+                    const float t0 = __uint_as_float(xv[b][s].x) - __uint_as_float(qv[s].x);
+                    const float t1 = __uint_as_float(xv[b][s].y) - __uint_as_float(qv[s].y);
+                    const float t2 = __uint_as_float(xv[b][s].z) - __uint_as_float(qv[s].z);
+                    const float t3 = __uint_as_float(xv[b][s].w) - __uint_as_float(qv[s].w);
+                    acc = fmaf(t0, t0, acc);
+                    acc = fmaf(t1, t1, acc);
+                    acc = fmaf(t2, t2, acc);
+                    acc = fmaf(t3, t3, acc);
+                  }
+                  // the first slab's sum.  Later slabs only add non-negative
+                  // terms, rounded to nearest, so the running sum never
+                  // decreases: a pair past its bound now stays past it
+                  pbits = __float_as_uint(group8_sum(acc));
+                  live |= (bit && pbits <= tk[slot] ? 1u : 0u) << j;
+                }
+                if (bit && gl == 0) run[e * G + j] = pbits;
+              }
+              if (mask && gl == 0 && live != mask) sv[e] = (ent[b] & ~0xffu) | live;
+            }
+          }
+          __builtin_amdgcn_wave_barrier();
+        }
+        if (IS_U8) {
+          // the finished pairs: at or before the bound, a survivor
+          for (int e = lane; e < nsv; e += WAVE) {
+            const uint32_t ent = sv[e];
+            const uint32_t mask = ent & 0xffu;
+            const int slot0 = (int)(uq[ent >> 20] & 0xffffu);
+            const uint64_t row = ub[ent >> 20] + ((ent >> 8) & 0xfffu);
+            for (int j = 0; j < G; ++j) {
+              if (!((mask >> j) & 1u)) continue;
+              const int slot = slot0 + j;
+              const uint32_t key = (uint32_t)(runx[e] - 2 * (int32_t)run[e * G + j] + qqs[slot]);
+              if (key <= tk[slot]) add_survivor(a, qi[slot], key, a.row_ids[row]);
+            }
+          }
+          if (nsl > 1 && nsv > 0) stage_slab(0);  // slab 0 back for the heads of the next rows
+        } else {
+          // the open pairs, appended with one atomic per 64 listed rows; a
+          // pair that finds the list full flags its query for recomputation
+          for (int c0 = 0; c0 < nsv; c0 += WAVE) {
+            const int e = c0 + lane;
+            const uint32_t ent = e < nsv ? sv[e] : 0u;
+            const uint32_t mask = ent & 0xffu;
+            const uint32_t cnt = wave_sum_u32((uint32_t)__popc(mask));
+            if (cnt == 0) continue;
+            unsigned long long base = 0;
+            if (lane == 0) base = atomicAdd(a.open_cnt, (unsigned long long)cnt);
+            base = bcast_u64(base, 0);
+            uint32_t before = 0;  // open pairs of the lower lanes
+#pragma unroll
+            for (int j = 0; j < G; ++j) before += (uint32_t)popc64(ballot((mask >> j) & 1u) & lanemask_lt());
+            const int slot0 = (int)(uq[ent >> 20] & 0xffffu);
+            const uint64_t row = ub[ent >> 20] + ((ent >> 8) & 0xfffu);
+            uint32_t o = 0;
+            for (int j = 0; j < G; ++j) {
+              if (!((mask >> j) & 1u)) continue;
+              const unsigned long long p = base + before + o++;
+              const int slot = slot0 + j;
+              if (p < OPEN_PAIRS) {
+                a.open_q[p] = qi[slot];
+                a.open_key[p] = run[e * G + j];
+                a.open_row[p] = row;
+              } else {
+                a.flag[qi[slot]] = 1;
+              }
+            }
+          }
+        }
+      };
+
+      auto phase_b = [&](int nsv) {
+        if constexpr (LONG) phase_b_long(nsv); else phase_b_short(nsv);
       };
 
       // ---- direct batches: when the heads this wave has tested so far (at
@@ -725,6 +901,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : 1) k_scan(Sh
     }
   }
   if (lane == 0 && full_rows) atomicAdd((unsigned long long *)&a.wstats[3], full_rows);
+  if (lane == 0 && body_bytes) atomicAdd((unsigned long long *)&a.wstats[4], body_bytes);
 }
 
 template <int IS_U8, int NSEG>
@@ -746,6 +923,7 @@ static hipError_t launch_scan_t(const SharedArgs &a, int nseg, int hl, int grid,
   if (nseg <= 3) return launch_scan_h<IS_U8, 3>(a, hl, grid, s);
   if (nseg <= 4) return launch_scan_h<IS_U8, 4>(a, hl, grid, s);
   if (nseg <= 8) return launch_scan_h<IS_U8, 8>(a, hl, grid, s);
+  if (nseg <= 48) return launch_scan_h<IS_U8, 48>(a, hl, grid, s);
   return hipErrorInvalidValue;
 }
 
@@ -758,6 +936,66 @@ hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStr
   const int grid = n_cu * NR_SHARED_BLOCKS_PER_CU;
   return dtype == NR_U8 ? launch_scan_t<1>(a, nseg, hl, grid, s)
                         : launch_scan_t<0>(a, nseg, hl, grid, s);
+}
+
+// ------------------------------------------------------------------ open pairs
+// The pairs of fp32 rows past 1 KB that the scan's first slab left at or
+// before their bound: 8 lanes per pair add the remaining 1 KB slabs in order
+// to the stored running sum (each slab accumulated per lane in segment order
+// and reduced over the 8 lanes, as everywhere else for such rows), stop once
+// the sum is past the bound, and keep the pair as a survivor otherwise.
+__global__ void __launch_bounds__(256) k_scan_open(SharedArgs a) {
+  const int lane = lane_id();
+  const int gl = lane & 7;
+  const uint64_t n0 = *a.open_cnt;
+  const uint64_t n = n0 < OPEN_PAIRS ? n0 : OPEN_PAIRS;
+  const int rb = a.row_bytes;
+  const int k = a.k;
+  const int nsl = (rb + 1023) / 1024;
+  const unsigned char *queries = (const unsigned char *)a.queries;
+  unsigned long long body = 0;
+  const uint64_t stride = (uint64_t)gridDim.x * (blockDim.x >> 3);
+  for (uint64_t p = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3; p < n; p += stride) {
+    const uint32_t q = a.open_q[p];
+    const uint64_t row = a.open_row[p];
+    float run = __uint_as_float(a.open_key[p]);
+    const int64_t own_id = a.own_ids[(int64_t)q * k + k - 1];
+    const uint32_t bound = own_id < 0 ? 0xffffffffu : __float_as_uint(a.own_dists[(int64_t)q * k + k - 1]);
+    const unsigned char *qb = queries + (uint64_t)q * rb;
+    bool open = true;
+    for (int sl = 1; sl < nsl && open; ++sl) {
+      uint4 xv[8], qv[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int off = 1024 * sl + 128 * s + 16 * gl;
+        xv[s] = off < rb ? load_stream(a.ra.seg(row, off)) : make_uint4(0, 0, 0, 0);
+        qv[s] = off < rb ? *(const uint4 *)(qb + off) : make_uint4(0, 0, 0, 0);
+      }
+      float acc = 0.0f;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const float t0 = __uint_as_float(xv[s].x) - __uint_as_float(qv[s].x);
+        const float t1 = __uint_as_float(xv[s].y) - __uint_as_float(qv[s].y);
+        const float t2 = __uint_as_float(xv[s].z) - __uint_as_float(qv[s].z);
+        const float t3 = __uint_as_float(xv[s].w) - __uint_as_float(qv[s].w);
+        acc = fmaf(t0, t0, acc);
+        acc = fmaf(t1, t1, acc);
+        acc = fmaf(t2, t2, acc);
+        acc = fmaf(t3, t3, acc);
+      }
+      run = run + group8_sum(acc);
+      body += (unsigned long long)(rb - 1024 * sl < 1024 ? rb - 1024 * sl : 1024);
+      open = __float_as_uint(run) <= bound;
+    }
+    if (open && gl == 0) add_survivor(a, q, __float_as_uint(run), a.row_ids[row]);
+  }
+  if (gl == 0 && body) atomicAdd((unsigned long long *)&a.wstats[4], body);
+}
+
+hipError_t launch_scan_open(const SharedArgs &a, int dtype, int n_cu, hipStream_t s) {
+  if (a.nq <= 0 || dtype == NR_U8 || a.row_bytes <= 1024) return hipSuccess;
+  hipLaunchKernelGGL(k_scan_open, dim3(n_cu * 8), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ merge

@@ -75,6 +75,9 @@ struct Buffers {
   int32_t *scnt, *flag;
   unsigned long long *pool_cnt;
   uint32_t *pool_q, *pool_key, *poff, *pcur, *pool2_key;
+  unsigned long long *open_cnt;
+  uint32_t *open_q, *open_key;
+  uint64_t *open_row;
   int64_t *pool_id, *pool2_id;
   unsigned long long *counter2;
   uint32_t *skey;
@@ -125,7 +128,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
   B.pid = c.take<int64_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
   B.shared = s.shared;
   B.rfull = c.take<uint32_t>((size_t)s.nq);
-  B.wstats = c.take<int64_t>(4);
+  B.wstats = c.take<int64_t>(5);
   if (s.shared) {
     const size_t nc1 = (size_t)s.n_clusters + 1;
     B.own_ids = c.take<int64_t>((size_t)s.nq * s.k);
@@ -147,6 +150,10 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.pcur = c.take<uint32_t>((size_t)s.nq);
     B.pool2_key = c.take<uint32_t>(nr::SURVIVOR_POOL);
     B.pool2_id = c.take<int64_t>(nr::SURVIVOR_POOL);
+    B.open_cnt = c.take<unsigned long long>(1);
+    B.open_q = c.take<uint32_t>(nr::OPEN_PAIRS);
+    B.open_key = c.take<uint32_t>(nr::OPEN_PAIRS);
+    B.open_row = c.take<uint64_t>(nr::OPEN_PAIRS);
     B.pair_q = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.pair_rank = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.qnorm = c.take<uint2>((size_t)s.nq);
@@ -553,6 +560,10 @@ nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q
   a.pcur = B.pcur;
   a.pool2_key = B.pool2_key;
   a.pool2_id = B.pool2_id;
+  a.open_cnt = B.open_cnt;
+  a.open_q = B.open_q;
+  a.open_key = B.open_key;
+  a.open_row = B.open_row;
   a.counter = B.counter2;
   a.wstats = B.wstats;
   a.scan_tmp = B.scan_tmp;
@@ -584,6 +595,7 @@ hipError_t run_refine_shared(const nr_index *ix, const nr::SharedArgs &a, const 
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[3], s);  // the part of the prep the seed pass did not hide
   e = nr::launch_shared_refine(a, ix->d.dtype, ix->n_cu, s);
+  if (e == hipSuccess) e = nr::launch_scan_open(a, ix->d.dtype, ix->n_cu, s);
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[4], s);
   e = nr::launch_shared_merge(a, s);
@@ -991,7 +1003,7 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
   v[NR_WORK_TILES] = t;
   v[NR_WORK_OWN_ROWS] = v[NR_WORK_ROWS];
   if (B.shared) {
-    int64_t ws[4] = {0, 0, 0, 0};
+    int64_t ws[5] = {0, 0, 0, 0, 0};
     uint32_t pairs = 0;
     HIP_OK(hipMemcpy(ws, B.wstats, sizeof(ws), hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(&pairs, B.hpos + ix->d.n_clusters, 4, hipMemcpyDeviceToHost));
@@ -1014,6 +1026,7 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
     v[NR_WORK_SHARED_PAIRS] = pairs;
     v[NR_WORK_SHARED_PAIR_ROWS] = ws[2];
     v[NR_WORK_FULL_ROWS] = ws[3];
+    v[NR_WORK_BODY_BYTES] = ws[4];
     v[NR_WORK_HEAD_BYTES] = scan_head(ix);
   }
   v[NR_WORK_ROWS_READ] = v[NR_WORK_OWN_ROWS] + v[NR_WORK_SHARED_ROWS] + v[NR_WORK_FALLBACK_ROWS];

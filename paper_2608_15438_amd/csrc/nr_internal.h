@@ -36,8 +36,12 @@ constexpr int SURVIVOR_CAP = NR_SURVIVOR_CAP;  // survivors a query keeps in its
 #define NR_SURVIVOR_POOL (1u << 22)
 #endif
 constexpr uint32_t SURVIVOR_POOL = NR_SURVIVOR_POOL;  // survivors past SURVIVOR_CAP, all queries
+#ifndef NR_OPEN_PAIRS
+#define NR_OPEN_PAIRS (1u << 22)
+#endif
+constexpr uint32_t OPEN_PAIRS = NR_OPEN_PAIRS;  // fp32 rows past 1 KB: pairs open after slab 0
 constexpr int SHARED_G = 8;               // queries scored per shared work unit (at most)
-constexpr int SHARED_MAX_NSEG = 8;        // rows of at most 8 x 128 bytes use the shared scan
+constexpr int SHARED_MAX_NSEG = 48;       // rows of at most 48 x 128 bytes use the shared scan
 constexpr uint32_t SHARED_ROWS = 2048;    // rows per shared work unit (at most)
 constexpr int MAX_KC = 16384;             // top-K_c heap held in LDS
 
@@ -228,8 +232,12 @@ struct SharedArgs {
   uint32_t *pcur;             // [nq] scatter cursors
   uint32_t *pool2_key;        // [SURVIVOR_POOL] pooled survivors grouped by query
   int64_t *pool2_id;
+  unsigned long long *open_cnt;  // fp32 rows past 1 KB: (query, row) pairs still at or
+  uint32_t *open_q, *open_key;   // before the bound after the first 1 KB slab, their
+  uint64_t *open_row;            // running sum and payload row [OPEN_PAIRS]
   unsigned long long *counter;  // work-unit counter
-  int64_t *wstats;            // [4] scanned rows, seed tiles, scanned pair rows, rows read whole
+  int64_t *wstats;            // [5] scanned rows, seed tiles, scanned pair rows, rows read
+                              // past their heads, bytes read by phase B
   void *scan_tmp;
   size_t scan_tmp_bytes;
   int64_t *out_ids;
@@ -251,6 +259,8 @@ hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s);
 PairHistArgs pair_hist_args(const SharedArgs &a);
 hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s);
 hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStream_t s);
+// the open pairs' remaining slabs (fp32 rows past 1 KB; a no-op otherwise)
+hipError_t launch_scan_open(const SharedArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s);
 hipError_t launch_unique_rows(const uint64_t *hpos, const uint64_t *cl_off, int64_t n_clusters,
                               int64_t *out, hipStream_t s);
@@ -388,21 +398,25 @@ __device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const ui
     h.cseed[q] = cs < 0 ? n : cs;
     h.rfull[q] = run > 0xffffffffull ? 0u : (uint32_t)run;
   }
-  // uint8 rows: |q|^2 and the part of it over the scan's head, one 16-byte
-  // chunk per lane (rows are at most 64 chunks); integer sums, so the order
-  // of the additions does not matter
+  // uint8 rows: |q|^2 and the part of it over the scan's head (at most 128
+  // bytes, so within lanes 0..7's first chunks), lane c taking the 16-byte
+  // chunks c, c + 64, ...; integer sums, so the order of the additions does
+  // not matter
   if (h.is_u8) {
-    uint32_t p = 0;
-    if (16 * lane < h.row_bytes) {
+    uint32_t p = 0, ph = 0;
+    for (int c = lane; 16 * c < h.row_bytes; c += WAVE) {
       const uint4 v = *reinterpret_cast<const uint4 *>(h.queries +
-                                                       (uint64_t)q * h.row_bytes + 16 * lane);
-      p = __builtin_amdgcn_udot4(v.x, v.x, p, false);
-      p = __builtin_amdgcn_udot4(v.y, v.y, p, false);
-      p = __builtin_amdgcn_udot4(v.z, v.z, p, false);
-      p = __builtin_amdgcn_udot4(v.w, v.w, p, false);
+                                                       (uint64_t)q * h.row_bytes + 16 * c);
+      uint32_t t = 0;
+      t = __builtin_amdgcn_udot4(v.x, v.x, t, false);
+      t = __builtin_amdgcn_udot4(v.y, v.y, t, false);
+      t = __builtin_amdgcn_udot4(v.z, v.z, t, false);
+      t = __builtin_amdgcn_udot4(v.w, v.w, t, false);
+      p += t;
+      if (16 * c < h.scan_head) ph += t;
     }
     const uint32_t full = wave_sum_u32(p);
-    const uint32_t head = wave_sum_u32(16 * lane < h.scan_head ? p : 0u);
+    const uint32_t head = wave_sum_u32(ph);
     if (lane == 0) h.qnorm[q] = make_uint2(full, head);
   }
 }

@@ -32,7 +32,7 @@ QS = dict(probes=0, clusters=1, direct=2, scored=3, stopped=4, rows=5, tiles=6, 
 STAGES = ("encode", "probe", "route", "plan", "refine", "merge", "shared_prep", "shared_scan",
           "shared_merge")
 WORK = ("tiles", "rows", "rows_read", "own_rows", "shared_rows", "shared_pairs", "survivors",
-        "flagged", "fallback_rows", "shared_pair_rows", "full_rows", "head_bytes")
+        "flagged", "fallback_rows", "shared_pair_rows", "full_rows", "head_bytes", "body_bytes")
 
 # every symbol include/neuroute.h declares
 EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_encode",

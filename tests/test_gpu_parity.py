@@ -176,7 +176,8 @@ def test_refine_given_clusters(dev, name, k, layout):
 
 
 # every refine kernel shape by row length: rows past 8 x 128 bytes keep the
-# query in LDS and accumulate 8 segments at a time; lengths that are not a
+# query in LDS and accumulate 8 segments at a time (in the scan, one 1 KB slab
+# of the batch's queries at a time); lengths that are not a
 # multiple of 128 bytes (they are multiples of 16) leave a ragged last segment
 @pytest.mark.parametrize("cfg,d", [(3, 300), (3, 384), (3, 700), (3, 1536),
                                    (2, 1104), (2, 2048), (2, 4096)])
@@ -202,6 +203,16 @@ def test_refine_row_lengths(dev, cfg, d, layout):
         oi, od, _ = O.refine(ix.rows, ix.row_ids, ix.cl_off, Q,
                              [L.astype(np.uint32) for L in lists], k)
         _assert_topk(dict(w=w, X=X, Q=Q), gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
+    # the whole search: the batch-shared schedule (seed pass of 64 rows, the
+    # rest through the scan) returns exactly the per-query schedule's lists
+    Qd = torch.from_numpy(Q).to(dev)
+    base = dict(l_sel=8, r_max=4, k_c=64, m_x=[0.0, 4.0], m_y=[1.0, 3.0])
+    for P in (16, 128):
+        pi, pd = gix.nr_search(Qd, 10, P, NR.Params(refine_mode=NR.NR_REFINE_PER_QUERY, **base))
+        si, sd = gix.nr_search(Qd, 10, P, NR.Params(refine_mode=NR.NR_REFINE_SHARED,
+                                                    shared_seed_rows=64, **base))
+        assert gix.nr_last_work()["shared_pairs"] > 0
+        assert torch.equal(pi, si) and torch.equal(pd, sd)
 
 
 # ------------------------------------------------------------------ whole path
@@ -363,15 +374,18 @@ def test_shared_schedule_work_counters(dev, name, layout):
     p = default_params(c, **MODES["shared_seed64"][1])
     gi, gd = c[layout].nr_search(c["Qd"], 10, 256, p, logits=c["lgd"])
     w = c[layout].nr_last_work()
-    if c["w"].row_bytes > 1024:
-        # rows past 8 x 128 bytes always take the per-query schedule
-        assert w["shared_pairs"] == 0 and w["rows"] == w["own_rows"] > 0
-        return
     assert w["shared_pairs"] > 0 and w["survivors"] > 0 and w["full_rows"] > 0
     assert w["rows"] == w["own_rows"] + w["shared_pair_rows"]
     assert w["rows_read"] == w["own_rows"] + w["shared_rows"] + w["fallback_rows"]
     assert w["shared_rows"] <= w["shared_pair_rows"] and w["flagged"] == 0
     assert w["full_rows"] <= w["shared_pair_rows"]
+    rb = c["w"].row_bytes
+    if rb <= 1024:
+        assert w["body_bytes"] == w["full_rows"] * rb
+    else:  # the first 1 KB slab of every row read past its head, then per
+        # (row, query) pair the slabs it needed
+        assert (w["full_rows"] * 1024 <= w["body_bytes"]
+                <= w["full_rows"] * 1024 + w["shared_pair_rows"] * (rb - 1024))
     assert w["head_bytes"] == 16 * (1 if c["w"].dtype == "u8" else 4)
     pi, pd = c[layout].nr_search(c["Qd"], 10, 256, default_params(c, **MODES["per_query"][1]),
                                  logits=c["lgd"])
