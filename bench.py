@@ -54,6 +54,8 @@ def parse():
     ap.add_argument("--oracle-threads", type=int, default=0)
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--margin-quantile", type=float, default=0.95)
+    ap.add_argument("--seed-rows", type=int, default=0,
+                    help="shared schedule: rows of each query's own (seed) pass; 0 = the library's")
     ap.add_argument("--quick", action="store_true",
                     help="no recall ground truth and no oracle (for counter passes)")
     ap.add_argument("--copy-calib", action="store_true",
@@ -245,7 +247,7 @@ def main():
     del row_of_id
     m_x, m_y = CAL.fit_margin(xs, ys, args.margin_quantile)
     params = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c,
-                       m_x=m_x.tolist(), m_y=m_y.tolist())
+                       m_x=m_x.tolist(), m_y=m_y.tolist(), shared_seed_rows=args.seed_rows)
     if args.grid:
         grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch)
         return
@@ -321,9 +323,13 @@ def main():
     kernels = {}
     hb = work["head_bytes"]
     scan_body = work["body_bytes"] - (0 if ix.head_copy else work["full_rows"] * hb)
+    # the open-pair pass (fp32 rows past 1 KB): the row bytes of the slabs it
+    # read; it reads the same amount of query bytes, mostly from cache
     for kname, stage, nrows, ab in (
             ("k_refine", "refine", work["own_rows"], work["own_rows"] * w.row_bytes),
-            ("k_scan", "shared_scan", work["shared_rows"], work["shared_rows"] * hb + scan_body)):
+            ("k_scan", "shared_scan", work["shared_rows"], work["shared_rows"] * hb + scan_body),
+            ("k_scan_open", "shared_open", work["open_bytes"] // max(1, w.row_bytes - 1024),
+             work["open_bytes"])):
         ms = stage_ms[stage] / nt
         if ms <= 0 or nrows <= 0:
             continue
@@ -336,9 +342,9 @@ def main():
     traffic = measured_traffic(dom, w.name)
     # the whole refinement stage (step 5): every launch from the plan to the merge
     st5 = sum(stage_ms[x] for x in ("plan", "refine", "merge", "shared_prep", "shared_scan",
-                                    "shared_merge")) / nt
+                                    "shared_open", "shared_merge")) / nt
     b5 = ((work["own_rows"] + work["fallback_rows"]) * w.row_bytes + work["shared_rows"] * hb
-          + scan_body)
+          + scan_body + work["open_bytes"])
     cand_bytes = rows * w.row_bytes
     refine_stage = {"ms": round(st5, 4), "bytes_read": int(b5), "candidate_bytes": int(cand_bytes),
                     "candidate_gbs": round(cand_bytes / (st5 * 1e-3) / 1e9, 1),
@@ -403,7 +409,7 @@ def grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch):
         else list(w.probe_budgets)
     gates = [float(x) for x in args.grid_gates.split(",")]
     batches = [int(x) for x in args.grid_batches.split(",")]
-    step5 = ("plan", "refine", "merge", "shared_prep", "shared_scan", "shared_merge")
+    step5 = ("plan", "refine", "merge", "shared_prep", "shared_scan", "shared_open", "shared_merge")
 
     def run_all(Qr, B, P, params, qstats=False):
         outs = []

@@ -142,7 +142,8 @@ typedef struct {
   int32_t lowq_or;
   int32_t refine_mode;   /* NR_REFINE_AUTO / _PER_QUERY / _SHARED (same results) */
   int32_t shared_seed_rows; /* shared schedule: rows of each list's leading clusters
-                               kept for the query's own pass (>= k); 0: 4096 */
+                               kept for the query's own pass (>= k); 0: 4096, or
+                               1024 for rows longer than 1024 bytes */
   int32_t m_knots;
   float m_x[NR_MAX_KNOTS];
   float m_y[NR_MAX_KNOTS];
@@ -234,11 +235,14 @@ nr_status nr_refine(const nr_index *index, const void *queries, int64_t nq, int3
  *   plan    (per-query tiles; shared schedule: seed-pass tiles),
  *   refine  (the per-query refinement kernel; shared schedule: own pass),
  *   merge   (per-query merge; shared schedule: own-pass merge),
- *   shared_prep, shared_scan, shared_merge (shared schedule only).  The
- *   scan's preparation runs on a second stream of the library's, beside the
- *   seed pass, so shared_prep counts only the part the seed pass did not hide;
- *   shared_merge includes the per-query redo of queries that lost survivors. */
-#define NR_STAGES 9
+ *   shared_prep, shared_scan, shared_open, shared_merge (shared schedule
+ *   only; shared_open is the pass over fp32 rows longer than 1024 bytes that
+ *   finishes the (row, query) pairs the scan's first 1 KB slab left open).
+ *   The scan's preparation runs on a second stream of the library's, beside
+ *   the seed pass, so shared_prep counts only the part the seed pass did not
+ *   hide; shared_merge includes the per-query redo of queries that lost
+ *   survivors. */
+#define NR_STAGES 10
 nr_status nr_profile_enable(nr_index *index, int32_t on);
 nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches, int32_t reset);
 
@@ -257,10 +261,11 @@ nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches
  *   NR_WORK_SHARED_PAIR_ROWS rows scored by the scan, summed over its pairs
  *   NR_WORK_FULL_ROWS      rows the scan read past their head (it left a query open)
  *   NR_WORK_HEAD_BYTES     bytes of a row the scan reads for every row (its head)
- *   NR_WORK_BODY_BYTES     bytes the scan read from those rows: whole rows; for
- *                          fp32 rows longer than 1024 bytes the first 1 KB slab,
- *                          then per (row, query) pair still at or before its bound
- *                          the further slabs until its running sum passes it
+ *   NR_WORK_BODY_BYTES     bytes the scan read from those rows: whole rows (for
+ *                          fp32 rows longer than 1024 bytes, their first 1 KB slab)
+ *   NR_WORK_OPEN_BYTES     row bytes the open-pair pass read: per (row, query) pair
+ *                          the first slab left at or before its bound, the further
+ *                          1 KB slabs until its running sum passes the bound
  * ROWS_READ = OWN_ROWS + SHARED_ROWS + FALLBACK_ROWS and
  * ROWS = OWN_ROWS + SHARED_PAIR_ROWS. */
 enum {
@@ -277,7 +282,8 @@ enum {
   NR_WORK_FULL_ROWS = 10,
   NR_WORK_HEAD_BYTES = 11,
   NR_WORK_BODY_BYTES = 12,
-  NR_WORK = 13
+  NR_WORK_OPEN_BYTES = 13,
+  NR_WORK = 14
 };
 nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *work, int32_t n_work);
 

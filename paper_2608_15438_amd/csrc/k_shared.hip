@@ -208,7 +208,7 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   const int64_t nc1 = a.n_clusters + 1;
   hipError_t e = launch_fill_i32(a.scnt, a.nq, 0, s);
   if (e == hipSuccess) e = launch_fill_i32(a.flag, a.nq, 0, s);
-  if (e == hipSuccess) e = launch_fill_i32((int32_t *)(a.wstats + 3), 4, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t *)(a.wstats + 3), 6, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.pool_cnt, 2, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.open_cnt, 2, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
@@ -989,7 +989,7 @@ __global__ void __launch_bounds__(256) k_scan_open(SharedArgs a) {
     }
     if (open && gl == 0) add_survivor(a, q, __float_as_uint(run), a.row_ids[row]);
   }
-  if (gl == 0 && body) atomicAdd((unsigned long long *)&a.wstats[4], body);
+  if (gl == 0 && body) atomicAdd((unsigned long long *)&a.wstats[5], body);
 }
 
 hipError_t launch_scan_open(const SharedArgs &a, int dtype, int n_cu, hipStream_t s) {

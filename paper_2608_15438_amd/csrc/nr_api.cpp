@@ -128,7 +128,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
   B.pid = c.take<int64_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
   B.shared = s.shared;
   B.rfull = c.take<uint32_t>((size_t)s.nq);
-  B.wstats = c.take<int64_t>(5);
+  B.wstats = c.take<int64_t>(6);
   if (s.shared) {
     const size_t nc1 = (size_t)s.n_clusters + 1;
     B.own_ids = c.take<int64_t>((size_t)s.nq * s.k);
@@ -520,7 +520,8 @@ nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q
   a.scan_head = scan_head(ix);
   a.scan_hb = (const unsigned char *)ix->d.rows;  // the head plane, or the rows themselves
   a.scan_hs = ix->d.head_bytes > 0 ? (uint64_t)ix->d.head_bytes : (uint64_t)a.row_bytes;
-  const uint32_t seed = p->shared_seed_rows > 0 ? (uint32_t)p->shared_seed_rows : nr::SEED_ROWS;
+  const uint32_t seed = p->shared_seed_rows > 0 ? (uint32_t)p->shared_seed_rows
+                        : (a.row_bytes > 1024 ? nr::SEED_ROWS_LONG : nr::SEED_ROWS);
   a.seed_min = seed > (uint32_t)k ? seed : (uint32_t)k;
   a.n_clusters = ix->d.n_clusters;
   a.ra = row_addr(ix);
@@ -595,15 +596,17 @@ hipError_t run_refine_shared(const nr_index *ix, const nr::SharedArgs &a, const 
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[3], s);  // the part of the prep the seed pass did not hide
   e = nr::launch_shared_refine(a, ix->d.dtype, ix->n_cu, s);
-  if (e == hipSuccess) e = nr::launch_scan_open(a, ix->d.dtype, ix->n_cu, s);
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[4], s);
+  if (e == hipSuccess) e = nr::launch_scan_open(a, ix->d.dtype, ix->n_cu, s);
+  if (e != hipSuccess) return e;
+  if (ev) (void)hipEventRecord(ev[5], s);
   e = nr::launch_shared_merge(a, s);
   if (e != hipSuccess) return e;
   RefineOpts fb;
   fb.qmask = B.flag;
   e = run_refine(ix, q, nq, k, clus, nclus, cap, B, out_ids, out_dists, qstats, s, nullptr, fb);
-  if (e == hipSuccess && ev) (void)hipEventRecord(ev[5], s);
+  if (e == hipSuccess && ev) (void)hipEventRecord(ev[6], s);
   return e;
 }
 
@@ -1003,7 +1006,7 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
   v[NR_WORK_TILES] = t;
   v[NR_WORK_OWN_ROWS] = v[NR_WORK_ROWS];
   if (B.shared) {
-    int64_t ws[5] = {0, 0, 0, 0, 0};
+    int64_t ws[6] = {0, 0, 0, 0, 0, 0};
     uint32_t pairs = 0;
     HIP_OK(hipMemcpy(ws, B.wstats, sizeof(ws), hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(&pairs, B.hpos + ix->d.n_clusters, 4, hipMemcpyDeviceToHost));
@@ -1027,6 +1030,7 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
     v[NR_WORK_SHARED_PAIR_ROWS] = ws[2];
     v[NR_WORK_FULL_ROWS] = ws[3];
     v[NR_WORK_BODY_BYTES] = ws[4];
+    v[NR_WORK_OPEN_BYTES] = ws[5];
     v[NR_WORK_HEAD_BYTES] = scan_head(ix);
   }
   v[NR_WORK_ROWS_READ] = v[NR_WORK_OWN_ROWS] + v[NR_WORK_SHARED_ROWS] + v[NR_WORK_FALLBACK_ROWS];

@@ -28,6 +28,8 @@ constexpr uint32_t OWN_TILE_MIN_ROWS = NR_OWN_TILE_MIN_ROWS;  // smallest tile o
 #define NR_SEED_ROWS 4096
 #endif
 constexpr uint32_t SEED_ROWS = NR_SEED_ROWS;      // rows of a query's first clusters refined on their own
+constexpr uint32_t SEED_ROWS_LONG = 1024;          // the same for rows past 1 KB, which the scan
+                                                   // mostly settles after their first 1 KB
 #ifndef NR_SURVIVOR_CAP
 #define NR_SURVIVOR_CAP 2048
 #endif
@@ -236,8 +238,9 @@ struct SharedArgs {
   uint32_t *open_q, *open_key;   // before the bound after the first 1 KB slab, their
   uint64_t *open_row;            // running sum and payload row [OPEN_PAIRS]
   unsigned long long *counter;  // work-unit counter
-  int64_t *wstats;            // [5] scanned rows, seed tiles, scanned pair rows, rows read
-                              // past their heads, bytes read by phase B
+  int64_t *wstats;            // [6] scanned rows, seed tiles, scanned pair rows, rows read
+                              // past their heads, bytes the scan read from them, row
+                              // bytes of the open-pair pass
   void *scan_tmp;
   size_t scan_tmp_bytes;
   int64_t *out_ids;

@@ -27,12 +27,13 @@ NR_MAX_K = 64
 NR_MAX_PROBES = 1024
 NR_QSTATS = 8
 NR_REFINE_AUTO, NR_REFINE_PER_QUERY, NR_REFINE_SHARED = 0, 1, 2
-NR_STAGES = 9
+NR_STAGES = 10
 QS = dict(probes=0, clusters=1, direct=2, scored=3, stopped=4, rows=5, tiles=6, batches=7)
 STAGES = ("encode", "probe", "route", "plan", "refine", "merge", "shared_prep", "shared_scan",
-          "shared_merge")
+          "shared_open", "shared_merge")
 WORK = ("tiles", "rows", "rows_read", "own_rows", "shared_rows", "shared_pairs", "survivors",
-        "flagged", "fallback_rows", "shared_pair_rows", "full_rows", "head_bytes", "body_bytes")
+        "flagged", "fallback_rows", "shared_pair_rows", "full_rows", "head_bytes", "body_bytes",
+        "open_bytes")
 
 # every symbol include/neuroute.h declares
 EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_encode",

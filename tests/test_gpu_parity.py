@@ -382,10 +382,12 @@ def test_shared_schedule_work_counters(dev, name, layout):
     rb = c["w"].row_bytes
     if rb <= 1024:
         assert w["body_bytes"] == w["full_rows"] * rb
-    else:  # the first 1 KB slab of every row read past its head, then per
-        # (row, query) pair the slabs it needed
-        assert (w["full_rows"] * 1024 <= w["body_bytes"]
-                <= w["full_rows"] * 1024 + w["shared_pair_rows"] * (rb - 1024))
+    else:  # the first 1 KB slab of every row read past its head; then, per
+        # (row, query) pair it left open, the further slabs that pair needed
+        assert w["body_bytes"] == w["full_rows"] * 1024
+        assert w["open_bytes"] <= w["shared_pair_rows"] * (rb - 1024)
+    if c["w"].dtype == "u8" or rb <= 1024:
+        assert w["open_bytes"] == 0
     assert w["head_bytes"] == 16 * (1 if c["w"].dtype == "u8" else 4)
     pi, pd = c[layout].nr_search(c["Qd"], 10, 256, default_params(c, **MODES["per_query"][1]),
                                  logits=c["lgd"])
