@@ -15,9 +15,9 @@
 //
 // H is a sorted array of u64 keys (d bits << 32 | cluster) in LDS.  A batch
 // is sorted across the wave (bitonic), then merged by ranks: batch element i
-// lands at i + |{h < key_i}|, a heap element moves up by |{batch < h}|; the
-// moving tail is rewritten from the top down so no element is overwritten
-// before it is read.  A first pass looks up every probe's bucket in the
+// lands at slot i + |{h < key_i}|, and the other slots of the moving tail take
+// the heap keys in order; the tail is rewritten from the top down, 64 slots at
+// a time, so no key is overwritten before it is read.  A first pass looks up every probe's bucket in the
 // directory (one thread per probe); the per-query pass stages the ranges of
 // its first pst probes in LDS with one round of loads and walks them 64 at a
 // time.
@@ -32,6 +32,7 @@ struct RouteLds {
   uint32_t pend[WAVE];            // pending batch (cluster ids)
   uint64_t bkey[WAVE];            // sorted batch keys
   float wd[WAVE];                 // distances of the window's first multi-bucket clusters
+  int32_t mk[WAVE];               // merge: batch element (+1) landing in each slot of a chunk
 };
 
 // M(x): piecewise linear through the knots, constant outside them.  Knot j
@@ -80,6 +81,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   const int64_t q = blockIdx.x;
   if (q >= a.nq) return;
   if (a.pass == 1 && !a.redo[q]) return;  // the second pass redoes only what the first gave up
+  S.mk[lane] = 0;
   const int b = a.b, P = a.P, k_c = a.k_c;
   const int hcap = a.hcap;  // heap slots in LDS (k_c, or fewer in a first pass)
   bool abort_q = false;     // the heap would outgrow hcap: left to the second pass
@@ -157,26 +159,32 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     __builtin_amdgcn_wave_barrier();
     int pos = WAVE + lane;
     if (lane < nv) pos = lane + lower_bound_u64(H, hv, key);
-    // move the tail of H that batch keys overtake
+    // merge from the top down, 64 destination slots at a time: the batch's
+    // slots are marked in LDS, and every other slot d takes heap key
+    // d - (batch slots below d); reads of a chunk come before its writes,
+    // and every source lies at or below its slot
     if (nv > 0) {
-      const int j0 = wave_lower_bound_u64(H, hv, S.bkey[0]);
-      int top = hv;
-      while (top > j0) {
-        int lo = top - WAVE > j0 ? top - WAVE : j0;
-        int j = lo + lane;
-        uint64_t hk = 0;
-        int np = -1;
-        if (j < top) {
-          hk = H[j];
-          np = j + lower_bound_u64(S.bkey, nv, hk);
+      const int d_lo = (int)bcast_u32((uint32_t)pos, 0);  // the first batch key's slot
+      const int d_hi = hv + nv < k_c ? hv + nv : k_c;
+      for (int c1 = d_hi; c1 > d_lo;) {
+        const int c0 = c1 - WAVE > d_lo ? c1 - WAVE : d_lo;
+        if (lane < nv && pos >= c0 && pos < c1) S.mk[pos - c0] = lane + 1;
+        const int below = popc64(ballot(lane < nv && pos < c0));
+        __builtin_amdgcn_wave_barrier();
+        const int d = c0 + lane;
+        const bool act = d < c1;
+        const int m = act ? S.mk[lane] : 0;
+        const uint64_t mm = ballot(m > 0);
+        uint64_t v = 0;
+        if (act) v = m > 0 ? S.bkey[m - 1] : H[d - below - popc64(mm & lanemask_lt())];
+        __builtin_amdgcn_wave_barrier();
+        if (act) {
+          H[d] = v;
+          S.mk[lane] = 0;
         }
         __builtin_amdgcn_wave_barrier();
-        if (j < top && np < k_c) H[np] = hk;
-        __builtin_amdgcn_wave_barrier();
-        top = lo;
+        c1 = c0;
       }
-      if (lane < nv && pos < k_c) H[pos] = key;
-      __builtin_amdgcn_wave_barrier();
     }
     h = hv + nv < k_c ? hv + nv : k_c;
     const bool kept = lane < nv && pos < k_c;
