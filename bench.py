@@ -54,6 +54,8 @@ def parse():
     ap.add_argument("--oracle-threads", type=int, default=0)
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--margin-quantile", type=float, default=0.95)
+    ap.add_argument("--refine-mode", choices=("auto", "per_query", "shared"), default="auto",
+                    help="refinement schedule (the same results either way)")
     ap.add_argument("--seed-rows", type=int, default=0,
                     help="shared schedule: rows of each query's own (seed) pass; 0 = the library's")
     ap.add_argument("--quick", action="store_true",
@@ -247,7 +249,9 @@ def main():
     del row_of_id
     m_x, m_y = CAL.fit_margin(xs, ys, args.margin_quantile)
     params = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c,
-                       m_x=m_x.tolist(), m_y=m_y.tolist(), shared_seed_rows=args.seed_rows)
+                       m_x=m_x.tolist(), m_y=m_y.tolist(), shared_seed_rows=args.seed_rows,
+                       refine_mode={"auto": NR.NR_REFINE_AUTO, "per_query": NR.NR_REFINE_PER_QUERY,
+                                    "shared": NR.NR_REFINE_SHARED}[args.refine_mode])
     if args.grid:
         grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch)
         return

@@ -316,9 +316,22 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
             fs[u] = 0.0f;
           }
           const int nsl = (rb + 128 * SC - 1) / (128 * SC);
+          // fp32: the running sum only grows (non-negative terms rounded to
+          // nearest), so a row whose sum is already past the list's k-th key
+          // cannot enter it and reads no further slabs
+          const uint32_t bound = tk.kth_key;
 #pragma unroll 1
           for (int sl = 0; sl < nsl; ++sl) {
             const int s0 = sl * SC;
+            if (!IS_U8 && sl > 0) {
+              bool any = false;
+#pragma unroll
+              for (int u = 0; u < U; ++u) {
+                ok[u] = ok[u] && __float_as_uint(fs[u]) <= bound;
+                any |= ok[u];
+              }
+              if (!ballot(any)) break;
+            }
             uint4 xc[U][SC];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
