@@ -569,7 +569,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
       __builtin_amdgcn_wave_barrier();
 
       // ---- phase B: whole rows of the listed (row, queries), UB rows per lane group
-      auto phase_b_short = [&](int nsv) {
+      auto phase_b_short = [&](int nsv) __attribute__((always_inline)) {
         for (int e0 = 0; e0 < nsv; e0 += 8 * UB) {
           uint32_t ent[UB];
           uint64_t row[UB];
@@ -624,7 +624,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
 
       // ---- phase B for long rows, slab by slab.  Lane c of a slab load holds
       // 16-byte chunk c of slot t's slab (slot t's query id is qi[t])
-      auto stage_slab = [&](int s0) {
+      auto stage_slab = [&](int s0) __attribute__((always_inline)) {
         __builtin_amdgcn_wave_barrier();  // every read of the previous slab is done
         uint4 sl[QMAX];
 #pragma unroll
@@ -638,7 +638,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
         for (int t = 0; t < QMAX; ++t) qs[t * QCH + lane] = sl[t];
         __builtin_amdgcn_wave_barrier();
       };
-      auto phase_b_long = [&](int nsv) {
+      auto phase_b_long = [&](int nsv) __attribute__((always_inline)) {
         const int nsl = (rb + 1023) / 1024;
         // uint8 rows are finished here, slab by slab; for fp32 rows only the
         // first slab is, and the pairs it leaves at or before their bound go
@@ -779,7 +779,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
         }
       };
 
-      auto phase_b = [&](int nsv) {
+      auto phase_b = [&](int nsv) __attribute__((always_inline)) {
         if constexpr (LONG) phase_b_long(nsv); else phase_b_short(nsv);
       };
 
