@@ -80,11 +80,11 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   const int lane = lane_id();
   const int64_t q = blockIdx.x;
   if (q >= a.nq) return;
-  if (a.pass == 1 && !a.redo[q]) return;  // the second pass redoes only what the first gave up
+  if (a.pass > 0 && a.redo[q] != a.pass) return;  // a later pass redoes only what the last gave up
   S.mk[lane] = 0;
   const int b = a.b, P = a.P, k_c = a.k_c;
   const int hcap = a.hcap;  // heap slots in LDS (k_c, or fewer in a first pass)
-  bool abort_q = false;     // the heap would outgrow hcap: left to the second pass
+  bool abort_q = false;     // the heap would outgrow hcap: left to the next pass
   const float kx = lane < a.m_knots ? a.m_x[lane] : 0.0f;
   const float ky = lane < a.m_knots ? a.m_y[lane] : 0.0f;
   const float ks = lane < a.m_knots ? a.m_slope[lane] : 0.0f;
@@ -384,7 +384,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   }
 
   if (abort_q) {
-    if (lane == 0) a.redo[q] = 1;
+    if (lane == 0) a.redo[q] = a.pass + 1;
     return;
   }
   for (int i = lane; i < h; i += WAVE) out[ndir + i] = (uint32_t)H[i];
@@ -433,7 +433,8 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
   }
   // A first pass keeps at most ROUTE_LIGHT_HEAP heap keys in LDS, so more
   // waves fit on a CU; a query whose heap would grow past that gives up and
-  // is redone by a second pass with the full K_c slots.
+  // is redone by the next pass, with ROUTE_MID_HEAP slots and then (for
+  // larger K_c) the full K_c; every pass runs Algorithm 2 from the start.
   auto launch = [&](int hcap, int pass) -> hipError_t {
     RouteArgs b = a;
     b.hcap = hcap;
@@ -453,9 +454,12 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
     return hipGetLastError();
   };
   if (a.k_c <= ROUTE_LIGHT_HEAP) return launch(a.k_c, 0);
+  int tiers[3], nt = 0;
+  tiers[nt++] = ROUTE_LIGHT_HEAP;
+  if (a.k_c > ROUTE_MID_HEAP) tiers[nt++] = ROUTE_MID_HEAP;
+  tiers[nt++] = a.k_c;
   hipError_t e = launch_fill_i32(a.redo, a.nq, 0, s);
-  if (e == hipSuccess) e = launch(ROUTE_LIGHT_HEAP, 0);
-  if (e == hipSuccess) e = launch(a.k_c, 1);
+  for (int p = 0; p < nt && e == hipSuccess; ++p) e = launch(tiers[p], p);
   return e;
 }
 

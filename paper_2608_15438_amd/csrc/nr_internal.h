@@ -252,6 +252,7 @@ struct SharedArgs {
 hipError_t launch_encode_layer(const EncodeLayerArgs &a, hipStream_t s);
 hipError_t launch_probe(const ProbeArgs &a, hipStream_t s);
 constexpr int ROUTE_LIGHT_HEAP = 512;  // heap slots of the route's first pass
+constexpr int ROUTE_MID_HEAP = 2048;   // and of its second when K_c is larger still
 size_t route_lds_bytes(int k_c, int pst);
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
