@@ -13,17 +13,22 @@
 //   stop once |H| = K_c, b_proc >= B_min and t_low >= T_low.
 // C(q) = C_dir (visiting order) followed by H in (d, cluster) order.
 //
-// H is a sorted array of u64 keys (d bits << 32 | cluster) in LDS.  A batch
-// is sorted across the wave (bitonic), then merged by ranks: batch element i
-// lands at slot i + |{h < key_i}|, and the other slots of the moving tail take
-// the heap keys in order; the tail is rewritten from the top down, 64 slots at
-// a time, so no key is overwritten before it is read.  A first pass looks up every probe's bucket in the
+// H is a sorted array of u64 keys (d bits << 32 | cluster) in LDS, fronted by
+// a sorted 64-key staging buffer.  A batch is sorted across the wave
+// (bitonic), then merged by ranks: batch element i lands at slot
+// i + |{h < key_i}|, and the other slots of the moving tail take the old keys
+// in order; the tail is rewritten from the top down, 64 slots at a time, so no
+// key is overwritten before it is read.  A batch that cannot push H past K_c
+// merges into the buffer, which moves into H when it fills, before a batch
+// that needs the K_c-smallest cut, and at the end.  A first pass looks up every probe's bucket in the
 // directory (one thread per probe); the per-query pass stages the ranges of
 // its first pst probes in LDS with one round of loads and walks them 64 at a
 // time.
 #include "nr_internal.h"
 
 namespace nr {
+
+constexpr int ROUTE_DIRECT_HEAP = 256;  // below this many keys H takes batches directly
 
 struct RouteLds {
   uint32_t wc0[WAVE], wc1[WAVE];  // probe window: cluster ranges
@@ -70,11 +75,15 @@ __device__ __forceinline__ int wave_lower_bound_u64(const uint64_t *a, int n, ui
   return lo;
 }
 
+// BUF: the staging buffer in front of H (passes whose heap may grow past the
+// light first pass's size; small heaps merge straight into H)
+template <bool BUF>
 __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   RouteLds &S = *reinterpret_cast<RouteLds *>(smem_raw);
   uint64_t *H = reinterpret_cast<uint64_t *>(smem_raw + sizeof(RouteLds));
-  uint32_t *st_c0 = reinterpret_cast<uint32_t *>(H + a.hcap);
+  uint64_t *HB = H + a.hcap;  // the heap's staging buffer (sorted; BUF only)
+  uint32_t *st_c0 = reinterpret_cast<uint32_t *>(HB + (BUF ? WAVE : 0));
   uint32_t *st_c1 = st_c0 + a.pst;
   int32_t *st_bin = reinterpret_cast<int32_t *>(st_c1 + a.pst);
   const int lane = lane_id();
@@ -94,6 +103,11 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   uint32_t *out = a.clus + q * a.cap;
 
   int h = 0, ndir = 0, npend = 0;
+  // H = H[0, hh) (sorted, in LDS) united with the staging buffer HB[0, hbn)
+  // (sorted): batches that cannot make H overflow K_c merge into the small
+  // buffer, which is merged into H only when it fills, at a truncation, and at
+  // the end, so H itself moves rarely
+  int hh = 0, hbn = 0;
   float d_min = INFINITY;
   int b_proc = 0, t_low = 0, n_scored = 0, n_batches = 0;
   bool stop = false;
@@ -124,6 +138,53 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   };
   int npre = 0;  // S.wd holds the distances of window clusters [0, npre)
 
+  // merge the nk keys held sorted in lanes 0..nk-1 into the sorted A[0, an),
+  // keeping the first acap slots; returns each lane's key's slot.  From the
+  // top down, 64 destination slots at a time: the keys' slots are marked in
+  // LDS, and every other slot d takes A[d - (keys below d)]; reads of a chunk
+  // come before its writes, and every source lies at or below its slot
+  auto merge_keys = [&](uint64_t *A, int an, int acap, uint64_t key, int nk)
+      __attribute__((always_inline)) {
+    S.bkey[lane] = key;
+    __builtin_amdgcn_wave_barrier();
+    int pos = WAVE + lane;
+    if (lane < nk) pos = lane + lower_bound_u64(A, an, key);
+    if (nk > 0) {
+      const int d_lo = (int)bcast_u32((uint32_t)pos, 0);  // the first key's slot
+      const int d_hi = an + nk < acap ? an + nk : acap;
+      for (int c1 = d_hi; c1 > d_lo;) {
+        const int c0 = c1 - WAVE > d_lo ? c1 - WAVE : d_lo;
+        if (lane < nk && pos >= c0 && pos < c1) S.mk[pos - c0] = lane + 1;
+        const int below = popc64(ballot(lane < nk && pos < c0));
+        __builtin_amdgcn_wave_barrier();
+        const int d = c0 + lane;
+        const bool act = d < c1;
+        const int m = act ? S.mk[lane] : 0;
+        const uint64_t mm = ballot(m > 0);
+        uint64_t v = 0;
+        if (act) v = m > 0 ? S.bkey[m - 1] : A[d - below - popc64(mm & lanemask_lt())];
+        __builtin_amdgcn_wave_barrier();
+        if (act) {
+          A[d] = v;
+          S.mk[lane] = 0;
+        }
+        __builtin_amdgcn_wave_barrier();
+        c1 = c0;
+      }
+    }
+    return pos;
+  };
+  // the buffer's first nb keys into H[0, nh) (their union fits K_c)
+  auto flush = [&](int nh, int nb) __attribute__((always_inline)) {
+    hh = nh;
+    if (nb > 0) {
+      const uint64_t bk = lane < nb ? HB[lane] : ~0ull;
+      merge_keys(H, hh, k_c, bk, nb);
+      hh += nb;
+    }
+    hbn = 0;
+  };
+
   // score the pending batch and fold it into H; with pre >= 0 the batch is
   // window clusters pre, pre + 1, ... whose distances may already be in S.wd
   auto run_batch = [&](int pre) {
@@ -146,47 +207,38 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     uint64_t key = valid ? (((uint64_t)__float_as_uint(d) << 32) | cid) : ~0ull;
     key = wave_sort_u64(key, nb);
     const int nv = popc64(ballot(valid));
-    // prune H to d <= theta (a prefix, as H is sorted)
+    // prune H and the buffer to d <= theta (prefixes, as both are sorted)
     const uint64_t cut = ((uint64_t)__float_as_uint(theta) + 1ull) << 32;
-    const int hv = wave_lower_bound_u64(H, h, cut);
+    const int hvh = wave_lower_bound_u64(H, hh, cut);
+    const int hvb = BUF ? wave_lower_bound_u64(HB, hbn, cut) : 0;
+    const int hv = hvh + hvb;
     if ((hv + nv < k_c ? hv + nv : k_c) > hcap) {
       abort_q = true;
       stop = true;
       npend = 0;
       return;
     }
-    S.bkey[lane] = key;
-    __builtin_amdgcn_wave_barrier();
     int pos = WAVE + lane;
-    if (lane < nv) pos = lane + lower_bound_u64(H, hv, key);
-    // merge from the top down, 64 destination slots at a time: the batch's
-    // slots are marked in LDS, and every other slot d takes heap key
-    // d - (batch slots below d); reads of a chunk come before its writes,
-    // and every source lies at or below its slot
-    if (nv > 0) {
-      const int d_lo = (int)bcast_u32((uint32_t)pos, 0);  // the first batch key's slot
-      const int d_hi = hv + nv < k_c ? hv + nv : k_c;
-      for (int c1 = d_hi; c1 > d_lo;) {
-        const int c0 = c1 - WAVE > d_lo ? c1 - WAVE : d_lo;
-        if (lane < nv && pos >= c0 && pos < c1) S.mk[pos - c0] = lane + 1;
-        const int below = popc64(ballot(lane < nv && pos < c0));
-        __builtin_amdgcn_wave_barrier();
-        const int d = c0 + lane;
-        const bool act = d < c1;
-        const int m = act ? S.mk[lane] : 0;
-        const uint64_t mm = ballot(m > 0);
-        uint64_t v = 0;
-        if (act) v = m > 0 ? S.bkey[m - 1] : H[d - below - popc64(mm & lanemask_lt())];
-        __builtin_amdgcn_wave_barrier();
-        if (act) {
-          H[d] = v;
-          S.mk[lane] = 0;
-        }
-        __builtin_amdgcn_wave_barrier();
-        c1 = c0;
+    if (hv + nv > k_c) {
+      // the K_c smallest must be chosen: the buffer goes into H first
+      flush(hvh, hvb);
+      pos = merge_keys(H, hh, k_c, key, nv);
+      hh = hh + nv < k_c ? hh + nv : k_c;
+    } else {
+      // every valid key is kept: straight into a small H, else into the
+      // buffer (emptied into H when full)
+      hh = hvh;
+      hbn = hvb;
+      if (!BUF || (hbn == 0 && hh < ROUTE_DIRECT_HEAP)) {
+        pos = merge_keys(H, hh, k_c, key, nv);
+        hh += nv;
+      } else {
+        if (hbn + nv > WAVE) flush(hh, hbn);
+        if (nv > 0) pos = merge_keys(HB, hbn, WAVE, key, nv);
+        hbn += nv;
       }
     }
-    h = hv + nv < k_c ? hv + nv : k_c;
+    h = hh + hbn;
     const bool kept = lane < nv && pos < k_c;
     const float dk = __uint_as_float((uint32_t)(key >> 32));
     const int u_heap = popc64(ballot(kept));
@@ -387,6 +439,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     if (lane == 0) a.redo[q] = a.pass + 1;
     return;
   }
+  flush(hh, hbn);
   for (int i = lane; i < h; i += WAVE) out[ndir + i] = (uint32_t)H[i];
   if (lane == 0) {
     a.nclus[q] = ndir + h;
@@ -421,7 +474,9 @@ __global__ void k_route_lookup(RouteArgs a) {
 }
 
 size_t route_lds_bytes(int k_c, int pst) {
-  return sizeof(RouteLds) + sizeof(uint64_t) * (size_t)k_c + 3 * sizeof(uint32_t) * (size_t)pst;
+  // the staging buffer only for heaps past the light first pass's size
+  const size_t buf = k_c > ROUTE_LIGHT_HEAP ? WAVE : 0;
+  return sizeof(RouteLds) + sizeof(uint64_t) * ((size_t)k_c + buf) + 3 * sizeof(uint32_t) * (size_t)pst;
 }
 
 hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
@@ -445,12 +500,16 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
     const size_t room = fixed < budget ? (budget - fixed) / (3 * sizeof(uint32_t)) : 0;
     b.pst = (int)(room < (size_t)b.P ? room : (size_t)b.P);
     const size_t lds = route_lds_bytes(hcap, b.pst);
+    const void *fn = hcap > ROUTE_LIGHT_HEAP ? (const void *)k_route<true>
+                                             : (const void *)k_route<false>;
     if (lds > 64 * 1024) {
-      hipError_t e = hipFuncSetAttribute((const void *)k_route,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(k_route, dim3((unsigned)b.nq), dim3(64), lds, s, b);
+    if (hcap > ROUTE_LIGHT_HEAP)
+      hipLaunchKernelGGL(k_route<true>, dim3((unsigned)b.nq), dim3(64), lds, s, b);
+    else
+      hipLaunchKernelGGL(k_route<false>, dim3((unsigned)b.nq), dim3(64), lds, s, b);
     return hipGetLastError();
   };
   if (a.k_c <= ROUTE_LIGHT_HEAP) return launch(a.k_c, 0);
