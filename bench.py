@@ -317,7 +317,9 @@ def main():
     qs = qs.double().mean(0).cpu().numpy()
     per_query = {name: round(float(qs[i]), 2) for name, i in NR.QS.items()}
     log("per-query means", per_query, "work", work)
-    # the two refinement kernels.  Algorithmic bytes: k_refine reads whole rows;
+    # the refinement kernels.  Algorithmic bytes: k_refine reads whole rows (of
+    # fp32 rows past 1 KB, the slabs it reached before the row's sum passed the
+    # list's k-th key: refine_bytes);
     # k_scan reads the head of every scanned row, then what it reads of the
     # rows its heads left open (whole rows, or the 1 KB slabs of long rows up
     # to the last one some query needed; without whole rows after the heads,
@@ -330,7 +332,7 @@ def main():
     # the open-pair pass (fp32 rows past 1 KB): the row bytes of the slabs it
     # read; it reads the same amount of query bytes, mostly from cache
     for kname, stage, nrows, ab in (
-            ("k_refine", "refine", work["own_rows"], work["own_rows"] * w.row_bytes),
+            ("k_refine", "refine", work["own_rows"], work["refine_bytes"]),
             ("k_scan", "shared_scan", work["shared_rows"], work["shared_rows"] * hb + scan_body),
             ("k_scan_open", "shared_open", work["open_bytes"] // max(1, w.row_bytes - 1024),
              work["open_bytes"])):
@@ -347,8 +349,7 @@ def main():
     # the whole refinement stage (step 5): every launch from the plan to the merge
     st5 = sum(stage_ms[x] for x in ("plan", "refine", "merge", "shared_prep", "shared_scan",
                                     "shared_open", "shared_merge")) / nt
-    b5 = ((work["own_rows"] + work["fallback_rows"]) * w.row_bytes + work["shared_rows"] * hb
-          + scan_body + work["open_bytes"])
+    b5 = work["refine_bytes"] + work["shared_rows"] * hb + scan_body + work["open_bytes"]
     cand_bytes = rows * w.row_bytes
     refine_stage = {"ms": round(st5, 4), "bytes_read": int(b5), "candidate_bytes": int(cand_bytes),
                     "candidate_gbs": round(cand_bytes / (st5 * 1e-3) / 1e9, 1),

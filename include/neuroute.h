@@ -266,6 +266,9 @@ nr_status nr_profile_read(nr_index *index, double *stage_ms, int64_t *n_searches
  *   NR_WORK_OPEN_BYTES     row bytes the open-pair pass read: per (row, query) pair
  *                          the first slab left at or before its bound, the further
  *                          1 KB slabs until its running sum passes the bound
+ *   NR_WORK_REFINE_BYTES   row bytes the per-query kernel read: whole rows; for fp32
+ *                          rows longer than 1024 bytes the 1 KB slabs it read before
+ *                          the row's running sum passed the tile list's k-th key
  * ROWS_READ = OWN_ROWS + SHARED_ROWS + FALLBACK_ROWS and
  * ROWS = OWN_ROWS + SHARED_PAIR_ROWS. */
 enum {
@@ -283,7 +286,8 @@ enum {
   NR_WORK_HEAD_BYTES = 11,
   NR_WORK_BODY_BYTES = 12,
   NR_WORK_OPEN_BYTES = 13,
-  NR_WORK = 14
+  NR_WORK_REFINE_BYTES = 14,
+  NR_WORK = 15
 };
 nr_status nr_last_work(nr_index *index, hipStream_t stream, int64_t *work, int32_t n_work);
 

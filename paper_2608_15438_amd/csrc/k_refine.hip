@@ -223,6 +223,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
   const int rb = a.row_bytes;
   const int k = a.k;
   if (total == 0) return;  // nothing to do: skip the counter (an empty redo launch)
+  unsigned long long nbytes = 0;  // row bytes this lane group read (its lane 0)
 
   for (;;) {
     int t = 0;
@@ -332,6 +333,9 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
               }
               if (!ballot(any)) break;
             }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+              if (ok[u] && gl == 0) nbytes += (uint32_t)(rb - 128 * s0 < 128 * SC ? rb - 128 * s0 : 128 * SC);
             uint4 xc[U][SC];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -392,6 +396,9 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
             }
           }
         } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (ok[u] && gl == 0) nbytes += (uint32_t)rb;
         uint4 xv[U][NSEG];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -467,6 +474,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
       a.pid[(int64_t)t * k + lane] = lane < tk.cnt ? tk.id : -1;
     }
   }
+  if (a.rbytes && gl == 0 && nbytes) atomicAdd(a.rbytes, nbytes);
 }
 
 template <int IS_U8>

@@ -128,7 +128,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
   B.pid = c.take<int64_t>((size_t)s.nq * nr::MAX_TILES_PER_QUERY * s.k);
   B.shared = s.shared;
   B.rfull = c.take<uint32_t>((size_t)s.nq);
-  B.wstats = c.take<int64_t>(6);
+  B.wstats = c.take<int64_t>(7);
   if (s.shared) {
     const size_t nc1 = (size_t)s.n_clusters + 1;
     B.own_ids = c.take<int64_t>((size_t)s.nq * s.k);
@@ -457,7 +457,10 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
     pa.nclus_out = B.nclus_own;
     pa.tile_min = nr::OWN_TILE_MIN_ROWS;
   }
-  hipError_t e = nr::launch_plan(pa, s);
+  // the search's refine bytes count from its first refinement launch on (the
+  // redo of queries whose survivors overflowed adds to them)
+  hipError_t e = o.qmask ? hipSuccess : nr::launch_fill_i32((int32_t *)(B.wstats + 6), 2, 0, s);
+  if (e == hipSuccess) e = nr::launch_plan(pa, s);
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[0], s);
   nr::RefineArgs ra{};
@@ -482,6 +485,7 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   ra.counter = B.counter;
   ra.pkey = B.pkey;
   ra.pid = B.pid;
+  ra.rbytes = (unsigned long long *)(B.wstats + 6);
   e = nr::launch_refine(ra, ix->d.dtype, ix->n_cu, s);
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[1], s);
@@ -1003,10 +1007,11 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
   std::vector<uint32_t> full(nq);
   HIP_OK(hipMemcpy(full.data(), B.rfull, 4 * nq, hipMemcpyDeviceToHost));
   for (uint32_t x : full) v[NR_WORK_ROWS] += x;
+  HIP_OK(hipMemcpy(&v[NR_WORK_REFINE_BYTES], B.wstats + 6, 8, hipMemcpyDeviceToHost));
   v[NR_WORK_TILES] = t;
   v[NR_WORK_OWN_ROWS] = v[NR_WORK_ROWS];
   if (B.shared) {
-    int64_t ws[6] = {0, 0, 0, 0, 0, 0};
+    int64_t ws[6] = {0, 0, 0, 0, 0, 0};  // the first six counters
     uint32_t pairs = 0;
     HIP_OK(hipMemcpy(ws, B.wstats, sizeof(ws), hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(&pairs, B.hpos + ix->d.n_clusters, 4, hipMemcpyDeviceToHost));

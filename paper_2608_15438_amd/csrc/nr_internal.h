@@ -172,6 +172,7 @@ struct RefineArgs {
   int32_t *counter;
   uint32_t *pkey;        // [nq x MAX_TILES_PER_QUERY x k]
   int64_t *pid;
+  unsigned long long *rbytes;  // row bytes the kernel read (added to)
 };
 
 struct MergeArgs {
@@ -238,9 +239,9 @@ struct SharedArgs {
   uint32_t *open_q, *open_key;   // before the bound after the first 1 KB slab, their
   uint64_t *open_row;            // running sum and payload row [OPEN_PAIRS]
   unsigned long long *counter;  // work-unit counter
-  int64_t *wstats;            // [6] scanned rows, seed tiles, scanned pair rows, rows read
+  int64_t *wstats;            // [7] scanned rows, seed tiles, scanned pair rows, rows read
                               // past their heads, bytes the scan read from them, row
-                              // bytes of the open-pair pass
+                              // bytes of the open-pair pass, row bytes of k_refine
   void *scan_tmp;
   size_t scan_tmp_bytes;
   int64_t *out_ids;

@@ -33,7 +33,7 @@ STAGES = ("encode", "probe", "route", "plan", "refine", "merge", "shared_prep", 
           "shared_open", "shared_merge")
 WORK = ("tiles", "rows", "rows_read", "own_rows", "shared_rows", "shared_pairs", "survivors",
         "flagged", "fallback_rows", "shared_pair_rows", "full_rows", "head_bytes", "body_bytes",
-        "open_bytes")
+        "open_bytes", "refine_bytes")
 
 # every symbol include/neuroute.h declares
 EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_encode",

@@ -388,6 +388,9 @@ def test_shared_schedule_work_counters(dev, name, layout):
         assert w["open_bytes"] <= w["shared_pair_rows"] * (rb - 1024)
     if c["w"].dtype == "u8" or rb <= 1024:
         assert w["open_bytes"] == 0
+        assert w["refine_bytes"] == (w["own_rows"] + w["fallback_rows"]) * rb
+    else:
+        assert 0 < w["refine_bytes"] <= (w["own_rows"] + w["fallback_rows"]) * rb
     assert w["head_bytes"] == 16 * (1 if c["w"].dtype == "u8" else 4)
     pi, pd = c[layout].nr_search(c["Qd"], 10, 256, default_params(c, **MODES["per_query"][1]),
                                  logits=c["lgd"])
