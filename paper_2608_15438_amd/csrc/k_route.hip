@@ -514,9 +514,10 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
   };
   if (a.k_c <= ROUTE_LIGHT_HEAP) return launch(a.k_c, 0);
   int tiers[3], nt = 0;
-  tiers[nt++] = ROUTE_LIGHT_HEAP;
+  if (!a.skip_light) tiers[nt++] = ROUTE_LIGHT_HEAP;
   if (a.k_c > ROUTE_MID_HEAP) tiers[nt++] = ROUTE_MID_HEAP;
   tiers[nt++] = a.k_c;
+  if (nt == 1) return launch(a.k_c, 0);
   hipError_t e = launch_fill_i32(a.redo, a.nq, 0, s);
   for (int p = 0; p < nt && e == hipSuccess; ++p) e = launch(tiers[p], p);
   return e;

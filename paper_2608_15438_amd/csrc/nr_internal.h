@@ -114,6 +114,7 @@ struct RouteArgs {
   uint2 *lk;             // [nq x P] scratch: cluster range of each probe's bucket
   int pst;               // probes per query whose ranges are staged in LDS (set per pass)
   int hcap, pass;        // heap slots in LDS and pass number (set by launch_route)
+  int skip_light;        // start at the middle heap (the light pass would overflow)
   int32_t *redo;         // [nq] queries the first pass left to the second
   const float *centroids;
   int k_c, b_batch, b_min, t_low, u_heap, u_front;
