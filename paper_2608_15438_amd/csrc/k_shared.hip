@@ -363,7 +363,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
   constexpr int G = SHARED_G;
   constexpr int QCH = LONG ? 64 : NSEG * 8;  // 16-byte chunks of a (padded) query row or slab
   constexpr int QMAX = NSEG <= 1 ? NR_SCAN_QMAX1 : (NSEG <= 2 ? 16 : 8);  // query slots per batch
-  constexpr int UB = NSEG <= 1 ? NR_SCAN_UB1 : (NSEG <= 4 || LONG ? 2 : 1);  // phase-B rows per lane group
+  constexpr int UB = NSEG <= 1 ? NR_SCAN_UB1 : (NSEG <= 4 || (LONG && IS_U8) ? 2 : 1);  // phase-B rows per lane group
   static_assert(QMAX <= WAVE, "one query slot per lane");
   static_assert(!LONG || QMAX == G, "a long-row slab holds one unit's queries per slot");
   constexpr int NSB = LONG ? 1 : NSEG;       // segments held per row by the short-row phase B
@@ -376,7 +376,10 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
   __shared__ uint32_t s_qi[4][QMAX];             // query id
   __shared__ int32_t s_qq[4][QMAX];              // |q|^2 (uint8)
   __shared__ uint32_t s_sv[4][SCAP];             // listed rows: unit << 20 | row << 8 | mask
-  __shared__ uint32_t s_run[4][LONG ? SCAP * G : 1];  // long rows: running sum per (listed row, query)
+  __shared__ uint32_t s_run[4][LONG && IS_U8 ? SCAP * G : 1];  // long uint8 rows: running x.q per (listed row, query)
+  constexpr int OPENL = 128;                     // long fp32 rows: open pairs held before they go out
+  __shared__ uint32_t s_ol[4][LONG && !IS_U8 ? OPENL : 1];  // listed row << 8 | query slot
+  __shared__ uint32_t s_ok[4][LONG && !IS_U8 ? OPENL : 1];  // its first slab's sum
   __shared__ int32_t s_runx[4][LONG && IS_U8 ? SCAP : 1];  // long uint8 rows: running |x|^2
   const int lane = lane_id();
   const int w = threadIdx.x >> 6;
@@ -394,6 +397,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
   uint32_t *sv = s_sv[w];
   uint32_t *run = s_run[w];
   int32_t *runx = s_runx[w];
+  uint32_t *ol = s_ol[w];
+  uint32_t *olk = s_ok[w];
   const int64_t NS = (int64_t)(a.hpos[a.n_clusters] >> 32);
   const uint64_t W = a.swork_off[NS];
   const uint64_t ntiles = (W + SHARED_TILE - 1) / SHARED_TILE;
@@ -645,6 +650,32 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
         // to the open list (their running sums are bounds: see below)
         const int nslk = IS_U8 ? nsl : 1;
         full_rows += (unsigned long long)nsv;
+        // fp32: the open pairs, collected in LDS and sent out with one atomic
+        // per OPENL of them; a pair that finds the open list full flags its
+        // query for recomputation
+        int nopen = 0;
+        auto flush_open = [&]() __attribute__((always_inline)) {
+          __builtin_amdgcn_wave_barrier();
+          unsigned long long base = 0;
+          if (lane == 0) base = atomicAdd(a.open_cnt, (unsigned long long)nopen);
+          base = bcast_u64(base, 0);
+          for (int i = lane; i < nopen; i += WAVE) {
+            const uint32_t v = ol[i];
+            const int slot = (int)(v & 0xffu);
+            const uint32_t ent = sv[v >> 8];
+            const uint64_t row = ub[ent >> 20] + ((ent >> 8) & 0xfffu);
+            const unsigned long long p = base + (unsigned long long)i;
+            if (p < OPEN_PAIRS) {
+              a.open_q[p] = qi[slot];
+              a.open_key[p] = olk[i];
+              a.open_row[p] = row;
+            } else {
+              a.flag[qi[slot]] = 1;
+            }
+          }
+          nopen = 0;
+          __builtin_amdgcn_wave_barrier();
+        };
         for (int sl = 0; sl < nslk && nsv > 0; ++sl) {
           const int s0 = 8 * sl;
           if (sl > 0) stage_slab(s0);
@@ -683,7 +714,6 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
                 if (mask && gl == 0) runx[e] = sl == 0 ? p : runx[e] + p;
               }
               const int slot0 = (int)(uq[ent[b] >> 20] & 0xffffu);
-              uint32_t live = 0;  // the listed queries still at or before their bound
               for (int j = 0; j < gmax; ++j) {
                 const bool bit = ((mask >> j) & 1u) != 0;
                 if (!ballot(bit)) continue;
@@ -703,7 +733,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
                   }
                   const int32_t p = group8_sum((int32_t)xq);
                   pbits = (uint32_t)(sl == 0 ? p : (int32_t)run[bit ? e * G + j : 0] + p);
-                  live |= (bit ? 1u : 0u) << j;  // uint8 partial sums are not bounds
+                  if (bit && gl == 0) run[e * G + j] = pbits;
                 } else {
                   float acc = 0.0f;
 #pragma unroll
@@ -721,11 +751,20 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
                   // terms, rounded to nearest, so the running sum never
                   // decreases: a pair past its bound now stays past it
                   pbits = __float_as_uint(group8_sum(acc));
-                  live |= (bit && pbits <= tk[slot] ? 1u : 0u) << j;
+                  const bool op = bit && gl == 0 && pbits <= tk[slot];
+                  const uint64_t om = ballot(op);
+                  if (om) {
+                    const int c = popc64(om);
+                    if (nopen + c > OPENL) flush_open();
+                    if (op) {
+                      const int i = nopen + popc64(om & lanemask_lt());
+                      ol[i] = ((uint32_t)e << 8) | (uint32_t)slot;
+                      olk[i] = pbits;
+                    }
+                    nopen += c;
+                  }
                 }
-                if (bit && gl == 0) run[e * G + j] = pbits;
               }
-              if (mask && gl == 0 && live != mask) sv[e] = (ent[b] & ~0xffu) | live;
             }
           }
           __builtin_amdgcn_wave_barrier();
@@ -745,37 +784,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
             }
           }
           if (nsl > 1 && nsv > 0) stage_slab(0);  // slab 0 back for the heads of the next rows
-        } else {
-          // the open pairs, appended with one atomic per 64 listed rows; a
-          // pair that finds the list full flags its query for recomputation
-          for (int c0 = 0; c0 < nsv; c0 += WAVE) {
-            const int e = c0 + lane;
-            const uint32_t ent = e < nsv ? sv[e] : 0u;
-            const uint32_t mask = ent & 0xffu;
-            const uint32_t cnt = wave_sum_u32((uint32_t)__popc(mask));
-            if (cnt == 0) continue;
-            unsigned long long base = 0;
-            if (lane == 0) base = atomicAdd(a.open_cnt, (unsigned long long)cnt);
-            base = bcast_u64(base, 0);
-            uint32_t before = 0;  // open pairs of the lower lanes
-#pragma unroll
-            for (int j = 0; j < G; ++j) before += (uint32_t)popc64(ballot((mask >> j) & 1u) & lanemask_lt());
-            const int slot0 = (int)(uq[ent >> 20] & 0xffffu);
-            const uint64_t row = ub[ent >> 20] + ((ent >> 8) & 0xfffu);
-            uint32_t o = 0;
-            for (int j = 0; j < G; ++j) {
-              if (!((mask >> j) & 1u)) continue;
-              const unsigned long long p = base + before + o++;
-              const int slot = slot0 + j;
-              if (p < OPEN_PAIRS) {
-                a.open_q[p] = qi[slot];
-                a.open_key[p] = run[e * G + j];
-                a.open_row[p] = row;
-              } else {
-                a.flag[qi[slot]] = 1;
-              }
-            }
-          }
+        } else if (nopen > 0) {
+          flush_open();
         }
       };
 
