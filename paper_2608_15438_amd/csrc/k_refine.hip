@@ -12,7 +12,10 @@
 //                 exact in int32;   fp32: fmaf((x-q), (x-q), acc);
 //         the 8 partial sums are combined with xor shuffles; a sorted top-k
 //         of (distance, original id) lives in lanes 0..k-1 and a candidate
-//         reads its original id only when it can enter it;
+//         reads its original id only when it can enter it.  Rows past 1 KB
+//         are summed per 1 KB slab (reduced over the 8 lanes, added in slab
+//         order) against the query row in LDS, and an fp32 row stops being
+//         read once its sum passes the list's k-th key;
 //  merge  (one wave per query)  the tiles' partial top-k lists are merged.
 #include "nr_internal.h"
 

@@ -24,7 +24,9 @@
 //          drops the pairs whose head part alone exceeds the bound; the
 //          remaining rows are read whole and scored exactly, and a pair at
 //          or before its query's bound becomes a survivor (per-query slots,
-//          then a shared pool);
+//          then a shared pool).  fp32 rows past 1 KB are scored on their
+//          first 1 KB slab only; the pairs it leaves open are finished by
+//          the open-pair pass, slab by slab;
 //  merge   seed top-k + survivors -> top-k.  A query whose survivors found
 //          the pool full is flagged and recomputed by the per-query
 //          schedule.
@@ -300,10 +302,12 @@ __device__ __forceinline__ void add_survivor(const SharedArgs &a, uint32_t q, ui
 //            queries in the same arithmetic and order as k_refine; rows at or
 //            before the query's bound become survivors.
 // Rows longer than 8 x 128 bytes hold only one 1 KB slab of each query row in
-// LDS at a time: phase B runs slab by slab over the listed rows, keeps every
-// (row, query) pair's running sum in LDS, and tests the survivors after the
-// last slab (slab partials are reduced over the 8 lanes and added in slab
-// order, as k_refine does for such rows).
+// LDS at a time (slab partials are reduced over the 8 lanes and added in slab
+// order, as k_refine does for such rows).  uint8 rows: phase B runs slab by
+// slab over the listed rows, keeps every (row, query) pair's running sums in
+// LDS, and tests the survivors after the last slab.  fp32 rows: phase B runs
+// the first slab only; a pair whose sum is still at or before its bound goes
+// to the open list, which k_scan_open finishes.
 constexpr int SCAN_UMAX = 64;    // units per batch
 
 template <int HL>
