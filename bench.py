@@ -253,7 +253,7 @@ def main():
                        refine_mode={"auto": NR.NR_REFINE_AUTO, "per_query": NR.NR_REFINE_PER_QUERY,
                                     "shared": NR.NR_REFINE_SHARED}[args.refine_mode])
     if args.grid:
-        grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch)
+        grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch, ix.head_copy)
         return
 
     # ---- probe-budget sweep: recall and QPS per point
@@ -403,7 +403,7 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch):
+def grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch, head_copy):
     """Probe budget x gate (margin quantile of M) x early stop x batch size.
     Batch 1 runs the first 1,000 queries one call each; larger batches run the
     whole query set in consecutive calls of that size.  Per point: QPS of an
@@ -451,9 +451,14 @@ def grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch):
                     qs = torch.cat([o[2] for o in run_all(Qr, B, P, params, qstats=True)])
                     qm = qs.double().mean(0).cpu().numpy()
                     rows = float(qs[:, NR.QS["rows"]].double().sum())
-                    # rows read: the shared schedule (one call) reports them; the
-                    # per-query schedule reads every candidate row
-                    read = work["rows_read"] if B >= nq and work["shared_pairs"] else rows
+                    # rows and bytes read: the shared schedule (one call) reports
+                    # them; the per-query schedule reads every candidate row
+                    shared = B >= nq and work["shared_pairs"]
+                    read = work["rows_read"] if shared else rows
+                    hb = work["head_bytes"]
+                    nbytes = (work["refine_bytes"] + work["shared_rows"] * hb + work["body_bytes"]
+                              - (0 if head_copy else work["full_rows"] * hb) + work["open_bytes"]
+                              ) if shared else rows * w.row_bytes
                     t5 = sum(st[x] for x in step5)
                     pt = {"workload": w.name, "probe_budget": P, "gate": f"q{int(round(gq * 100))}",
                           "early_stop": es, "batch": B, "queries": nq,
@@ -465,7 +470,7 @@ def grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch):
                           "centroids_scored_per_query": round(float(qm[NR.QS["scored"]]), 2),
                           "centroid_batches_per_query": round(float(qm[NR.QS["batches"]]), 2),
                           "stopped_frac": round(float(qm[NR.QS["stopped"]]), 3),
-                          "refine_gbs": round(read * w.row_bytes / (t5 * 1e-3) / 1e9, 1) if t5 else None,
+                          "refine_gbs": round(nbytes / (t5 * 1e-3) / 1e9, 1) if t5 else None,
                           "stage_ms_per_call": {x: round(v / max(ncalls, 1), 4) for x, v in st.items()},
                           "calls": ncalls}
                     print(json.dumps(pt), flush=True)
