@@ -136,7 +136,33 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     }
     return acc;
   };
-  int npre = 0;  // S.wd holds the distances of window clusters [0, npre)
+  int p = 0;                 // next probe of the sequence
+  int wb = 0;                // window: probes [wb, wb + WAVE), slot = lane
+  bool have_window = false;
+  // S.wd holds the distances of the window's multi-bucket clusters numbered
+  // [pbase, pbase + npre) (numbers in window slot order; wtotal in all)
+  int npre = 0, pbase = 0;
+  uint32_t wtotal = 0;
+  auto precompute = [&](int from) __attribute__((always_inline)) {
+    const int lim = cnt - wb < WAVE ? cnt - wb : WAVE;
+    const int n = (int)wtotal - from < WAVE ? (int)wtotal - from : WAVE;
+    float dw = 0.0f;
+    if (lane < n) {
+      const uint32_t num = (uint32_t)(from + lane);
+      // the slot owning number num: the last slot whose prefix is <= num
+      int lo = 0, hi = lim - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (S.wpre[mid] <= num) lo = mid; else hi = mid - 1;
+      }
+      dw = centroid_dist(S.wc0[lo] + (num - S.wpre[lo]));
+    }
+    __builtin_amdgcn_wave_barrier();
+    S.wd[lane] = dw;
+    __builtin_amdgcn_wave_barrier();
+    pbase = from;
+    npre = n;
+  };
 
   // merge the nk keys held sorted in lanes 0..nk-1 into the sorted A[0, an),
   // keeping the first acap slots; returns each lane's key's slot.  From the
@@ -193,9 +219,12 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     n_scored += nb;
     float d = INFINITY;
     uint32_t cid = 0;
+    // a window batch whose distances are not all in S.wd first scores the
+    // next 64 of the window's clusters at once
+    if (pre >= 0 && (pre < pbase || pre + nb > pbase + npre)) precompute(pre);
     if (lane < nb) {
       cid = S.pend[lane];
-      d = pre >= 0 && pre + lane < npre ? S.wd[pre + lane] : centroid_dist(cid);
+      d = pre >= 0 ? S.wd[pre - pbase + lane] : centroid_dist(cid);
     }
     float dm = wave_min_f32(d);
     d_min = dm < d_min ? dm : d_min;
@@ -250,9 +279,6 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     if (full_and_quiet()) stop = true;
   };
 
-  int p = 0;                 // next probe of the sequence
-  int wb = 0;                // window: probes [wb, wb + WAVE), slot = lane
-  bool have_window = false;
   // the window after the current one is fetched ahead: it usually starts
   // where the current one ends
   // the query's first nst probe ranges are staged in LDS at once; windows
@@ -316,24 +342,11 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
         const uint32_t wsz = lane < limw ? S.wc1[lane] - S.wc0[lane] : 0u;
         const uint32_t msz = wsz >= 2 ? wsz : 0u;
         const uint32_t incl = wave_incl_scan_u32(msz);
-        const uint32_t total = (uint32_t)__shfl((int)incl, WAVE - 1);
+        wtotal = (uint32_t)__shfl((int)incl, WAVE - 1);
         S.wpre[lane] = incl - msz;
         __builtin_amdgcn_wave_barrier();
-        npre = total < (uint32_t)WAVE ? (int)total : WAVE;
-        if (npre > 0) {
-          float dw = 0.0f;
-          if (lane < npre) {
-            // the slot owning number lane: the last slot whose prefix is <= lane
-            int lo = 0, hi = limw - 1;
-            while (lo < hi) {
-              const int mid = (lo + hi + 1) >> 1;
-              if (S.wpre[mid] <= (uint32_t)lane) lo = mid; else hi = mid - 1;
-            }
-            dw = centroid_dist(S.wc0[lo] + ((uint32_t)lane - S.wpre[lo]));
-          }
-          S.wd[lane] = dw;
-          __builtin_amdgcn_wave_barrier();
-        }
+        npre = 0;
+        if (wtotal > 0) precompute(0);
       }
       const int off = p - wb;
       const int lim = cnt - wb < WAVE ? cnt - wb : WAVE;
