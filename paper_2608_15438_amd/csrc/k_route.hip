@@ -58,6 +58,25 @@ __device__ __forceinline__ float margin_dev(int m, float kx, float ky, float ks,
   return v;
 }
 
+// the keys of lanes 0..n-1 in ascending order (lanes from n on keep theirs):
+// each lane counts the keys ranked before its own (by value, then lane) from
+// scalar broadcasts and places its key at that rank through tmp[0, n) in LDS;
+// for small n this is far shorter than a shuffle network
+__device__ __forceinline__ uint64_t rank_sort_u64(uint64_t key, int n, uint64_t *tmp) {
+  const int l = lane_id();
+  const int klo = (int)(uint32_t)key, khi = (int)(uint32_t)(key >> 32);
+  int r = 0;
+  for (int j = 0; j < n; ++j) {
+    const uint64_t kj = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(khi, j) << 32) |
+                        (uint32_t)__builtin_amdgcn_readlane(klo, j);
+    r += (kj < key || (kj == key && j < l)) ? 1 : 0;
+  }
+  __builtin_amdgcn_wave_barrier();
+  if (l < n) tmp[r] = key;
+  __builtin_amdgcn_wave_barrier();
+  return l < n ? tmp[l] : key;
+}
+
 // entries of sorted a[0..n) below key, the same key in every lane: each round
 // samples 64 evenly spaced entries and keeps the gap the key falls in
 __device__ __forceinline__ int wave_lower_bound_u64(const uint64_t *a, int n, uint64_t key) {
@@ -234,7 +253,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     const float theta_f = d_min + am;
     const bool valid = lane < nb && d <= theta;
     uint64_t key = valid ? (((uint64_t)__float_as_uint(d) << 32) | cid) : ~0ull;
-    key = wave_sort_u64(key, nb);
+    key = nb <= 32 ? rank_sort_u64(key, nb, S.bkey) : wave_sort_u64(key, nb);
     const int nv = popc64(ballot(valid));
     // prune H and the buffer to d <= theta (prefixes, as both are sorted)
     const uint64_t cut = ((uint64_t)__float_as_uint(theta) + 1ull) << 32;
