@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--oracle-threads", type=int, default=0)
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--margin-quantile", type=float, default=0.95)
+    ap.add_argument("--calib", choices=("gt", "bootstrap"), default="gt",
+                    help="calibration targets: brute-force top-k, or the search's own "
+                         "top-k at the largest budget with gate and early stop off")
     ap.add_argument("--refine-mode", choices=("auto", "per_query", "shared"), default="auto",
                     help="refinement schedule (the same results either way)")
     ap.add_argument("--seed-rows", type=int, default=0,
@@ -244,8 +247,27 @@ def main():
     fwd = IB._TorchEncoder(ix.encoder, dev)
     row_of_id = torch.empty_like(ix.row_ids)
     row_of_id[ix.row_ids] = torch.arange(w.n, device=dev)
-    xs, ys = CAL.margin_points(fwd(Qc), torch.from_numpy(gtc).to(dev), row_of_id, ix.cl_off,
-                               ix.bc_off, ix.centroids)
+    targets = torch.from_numpy(gtc).to(dev)
+    if args.calib == "bootstrap":
+        # the paper's supervision: the search itself in a higher-recall
+        # setting (the largest budget, gate and early stop off)
+        loose = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c, gate_on=False,
+                          early_stop_on=False)
+        targets = CAL.bootstrap_targets(gix, Qc, k, NR.NR_MAX_PROBES, loose)
+        agree = float((targets.cpu() == torch.from_numpy(gtc)).double().mean())
+        log(f"bootstrapped calibration targets: {agree:.3f} of them equal the brute-force ones")
+    lgc = fwd(Qc)
+    xs, ys = CAL.margin_points(lgc, targets, row_of_id, ix.cl_off, ix.bc_off, ix.centroids)
+    # the bucket-score cutoff the same targets give (reported; the search runs
+    # with S_max = +inf)
+    sc = CAL.bucket_scores(lgc, torch.as_tensor(np.asarray(ix.tau), device=dev),
+                           CAL.target_codes(targets, row_of_id, ix.cl_off, ix.bc_off),
+                           min(w.l_sel, w.b), w.r_max)
+    s95, pcov, qcov = CAL.fit_s_max(sc, 0.95)
+    calib = {"targets": "bootstrap" if args.calib == "bootstrap" else "brute-force",
+             "queries": nc, "s_max_95": round(s95, 4), "pair_coverage": round(pcov, 4),
+             "query_coverage": round(qcov, 4)}
+    log("calibration", calib)
     del row_of_id
     m_x, m_y = CAL.fit_margin(xs, ys, args.margin_quantile)
     params = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c,
@@ -396,6 +418,7 @@ def main():
         "kernels": kernels,
         "refine_stage": refine_stage,
         "cpu_baseline": cpu,
+        "calibration": calib,
         "sweep": sweep,
         "hbm_stream_read_gbs": round(stream_gbs, 1),
         "setup_s": {"index_build": round(t_build, 1), "total": round(time.time() - t_all, 1)},
