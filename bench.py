@@ -54,6 +54,10 @@ def parse():
     ap.add_argument("--oracle-threads", type=int, default=0)
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--margin-quantile", type=float, default=0.95)
+    ap.add_argument("--train-steps", type=int, default=0,
+                    help="train the encoder with L_sim for this many Adam steps first (0: seeded)")
+    ap.add_argument("--train-batch", type=int, default=4096)
+    ap.add_argument("--train-lr", type=float, default=2e-4)
     ap.add_argument("--calib", choices=("gt", "bootstrap"), default="gt",
                     help="calibration targets: brute-force top-k, or the search's own "
                          "top-k at the largest budget with gate and early stop off")
@@ -226,7 +230,17 @@ def main():
     data = GpuRows(w, "data", dev)
     t0 = time.time()
     hb = args.head_bytes if args.head_bytes >= 0 else 16 * (1 if w.dtype == "u8" else 4)
-    ix = IB.build_index(w, data, device=dev, chunk=1 << 20, keep_codes=False,
+    enc = None
+    if args.train_steps:
+        # L_sim training of the seeded encoder on batches of the base rows
+        from paper_2608_15438_amd import train as TR
+        t1 = time.time()
+        enc = TR.train_encoder(IB.seeded_encoder(w), data, w.n, args.train_steps,
+                               batch=args.train_batch, lr=args.train_lr, gamma=0.6,
+                               seed=w.seed("sample"), device=dev, log=lambda s: log("  ", s))
+        torch.cuda.synchronize()
+        log(f"encoder trained in {time.time() - t1:.1f}s")
+    ix = IB.build_index(w, data, device=dev, chunk=1 << 20, keep_codes=False, encoder=enc,
                         payload_fn=lambda perm: data(perm), log=lambda s: log("  index:", s),
                         head_bytes=hb, head_copy=not args.head_split)
     torch.cuda.synchronize()
@@ -399,6 +413,8 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "d": w.d, "b": w.b, "queries": w.n_queries,
+                   "encoder": (f"L_sim-trained, {args.train_steps} steps of {args.train_batch}"
+                               if args.train_steps else "seeded"),
                    "layout": (f"head{ix.head_bytes}+" + ("rows" if ix.head_copy else "tail"))
                    if ix.head_bytes else "row-major",
                    "k": k, "probe_budget": P, "l_sel": params.l_sel, "r_max": params.r_max,

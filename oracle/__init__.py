@@ -302,3 +302,27 @@ def recall_at_k(result_ids: np.ndarray, gt_ids: np.ndarray, k: int) -> float:
             continue
         total += len(R & G) / min(k, len(G))
     return total / len(result_ids)
+
+
+def lsim(x: np.ndarray, lat: np.ndarray, gamma: float, tau_emb: float) -> float:
+    """The selective similarity loss L_sim of one batch (Sec. 3.2.2, Eq.
+    similarityconfig with the mask of Eq. 8), written out in fp64 loops over
+    the pairs: rho = sqrt(L_dim / E_dim); a pair i != j counts when its input
+    distance is at most tau_emb or its latent distance at most
+    gamma * rho * tau_emb; the loss is the mean over counted pairs of
+    (latent distance - gamma * rho * input distance)^2."""
+    x = np.asarray(x, dtype=np.float64)
+    lat = np.asarray(lat, dtype=np.float64)
+    B, E = x.shape
+    rho = np.sqrt(lat.shape[1] / E)
+    num, den = 0.0, 0
+    for i in range(B):
+        se = np.sqrt(((x - x[i]) ** 2).sum(1))
+        sl = np.sqrt(((lat - lat[i]) ** 2).sum(1))
+        for j in range(B):
+            if j == i:
+                continue
+            if se[j] <= tau_emb or sl[j] <= gamma * rho * tau_emb:
+                num += (sl[j] - gamma * rho * se[j]) ** 2
+                den += 1
+    return num / den if den else 0.0

@@ -1,0 +1,72 @@
+"""L_sim (Sec. 3.2.2): the oracle's loops pinned on hand-worked cases, the
+training module's GEMM form checked against them, its gradient against
+finite differences, and a few Adam steps lowering the loss."""
+import math
+
+import numpy as np
+import torch
+
+import oracle as O
+from paper_2608_15438_amd import train as TR
+
+
+def test_oracle_lsim_hand_case():
+    # three points on a line in 2-d, latents in 1-d: rho = sqrt(1/2)
+    x = np.array([[0.0, 0.0], [1.0, 0.0], [3.0, 0.0]])
+    lat = np.array([[0.0], [2.0], [2.5]])
+    g, tau = 1.0, 1.5
+    rho = math.sqrt(0.5)
+    # input distances 1, 3, 2; latent distances 2, 2.5, 0.5; gate on latents
+    # gamma * rho * tau = 1.0607: pairs (0,1) by input (1 <= 1.5), (1,2) by
+    # latent (0.5), (0,2) by neither; each counted twice (i, j) and (j, i)
+    exp = ((2 - rho * 1) ** 2 + (0.5 - rho * 2) ** 2) / 2
+    assert abs(O.lsim(x, lat, g, tau) - exp) < 1e-12
+    # no pair under either threshold (gamma * rho * 0.1 < 0.5): zero
+    assert O.lsim(x, lat, g, 0.1) == 0.0
+
+
+def test_oracle_lsim_exact_map_is_zero():
+    # latents that scale input distances by gamma * rho give zero loss
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((12, 4))
+    g = 0.6
+    rho = math.sqrt(2 / 4)
+    # a map that preserves distances up to gamma*rho in 2-d: project onto a
+    # 2-d subspace of points that lie in it
+    x[:, 2:] = 0.0
+    lat = x[:, :2] * g * rho
+    assert O.lsim(x, lat, g, 10.0) < 1e-24
+
+
+def test_gemm_form_matches_oracle():
+    rng = np.random.default_rng(2)
+    for B, E, L in ((20, 8, 3), (33, 16, 5)):
+        x = rng.standard_normal((B, E))
+        lat = rng.standard_normal((B, L))
+        for tau in (0.5, 2.0, 4.0):
+            got, _, _ = TR.lsim_loss(torch.from_numpy(x), torch.from_numpy(lat), 0.6, tau)
+            exp = O.lsim(x, lat, 0.6, tau)
+            assert abs(float(got) - exp) <= 1e-9 * max(1.0, exp), (B, tau)
+
+
+def test_gradient_matches_finite_differences():
+    rng = np.random.default_rng(3)
+    x = torch.from_numpy(rng.standard_normal((10, 6)))
+    lat = torch.from_numpy(rng.standard_normal((10, 3))).requires_grad_(True)
+    # the mask is piecewise constant; away from its edges the loss is smooth
+    f = lambda l: TR.lsim_loss(x, l, 0.6, 2.5)[0]
+    assert torch.autograd.gradcheck(f, (lat,), eps=1e-6, atol=1e-6)
+
+
+def test_training_lowers_the_loss():
+    from synth import configs as CF
+    from paper_2608_15438_amd import index_build as IB
+    w = CF.scaled(CF.SIFT1M, 4000, 10, widths=(128, 64, 8))
+    X = torch.from_numpy(IB.cpu_row_source(w)(np.arange(w.n)).astype(np.float32))
+    enc = IB.seeded_encoder(w)
+    rows = lambda ids: X[ids.cpu()]
+    xb = X[:512] * enc.input_scale
+    before = TR.lsim_loss(xb, TR._Mlp(enc, "cpu")(X[:512]), 0.6, None)[0].item()
+    enc2 = TR.train_encoder(enc, rows, w.n, steps=30, batch=512, lr=2e-3, device="cpu")
+    after = TR.lsim_loss(xb, TR._Mlp(enc2, "cpu")(X[:512]), 0.6, None)[0].item()
+    assert after < before
