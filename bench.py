@@ -54,8 +54,9 @@ def parse():
     ap.add_argument("--oracle-threads", type=int, default=0)
     ap.add_argument("--no-oracle", action="store_true")
     ap.add_argument("--margin-quantile", type=float, default=0.95)
-    ap.add_argument("--train-steps", type=int, default=0,
-                    help="train the encoder with L_sim for this many Adam steps first (0: seeded)")
+    ap.add_argument("--train-steps", type=int, default=2000,
+                    help="train the seeded encoder with L_sim for this many Adam steps before "
+                         "the index is built (0: keep the seeded encoder)")
     ap.add_argument("--train-batch", type=int, default=4096)
     ap.add_argument("--train-lr", type=float, default=2e-4)
     ap.add_argument("--calib", choices=("gt", "bootstrap"), default="gt",
