@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--no-clustering", action="store_true",
                     help="index without bucket-local clustering (every bucket one cluster)")
     ap.add_argument("--n", type=int, default=0, help="override the base size (smaller instance)")
+    ap.add_argument("--k-c", type=int, default=0,
+                    help="override the centroid heap size K_c (the workload name gets a -kc suffix)")
     ap.add_argument("--probes", type=str, default="", help="comma list of probe budgets to sweep")
     ap.add_argument("--target-recall", type=float, default=0.90)
     ap.add_argument("--refine-steps", type=int, default=4,
@@ -223,6 +225,9 @@ def main():
     if args.no_clustering:
         import dataclasses
         w = dataclasses.replace(w, cluster_rule="none", name=w.name + "-noclust")
+    if args.k_c and args.k_c != w.k_c:
+        import dataclasses
+        w = dataclasses.replace(w, k_c=args.k_c, name=f"{w.name}-kc{args.k_c}")
     k = w.k
     t_all = time.time()
 
