@@ -131,6 +131,54 @@ def test_candidate_clusters_bit_exact(dev, name, pset, P):
         assert np.array_equal(clus[q, :n[q]], L), q
 
 
+
+def _worked_cases():
+    import os
+    rows = []
+    path = os.path.join(os.path.dirname(__file__), "golden", "alg2_worked_example.txt")
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            f = [c.strip() for c in line.split("|")]
+            rows.append(dict(name=f[0], k_c=int(f[1]), t_low=int(f[2]), es=int(f[3]),
+                             lowq_or=int(f[4]), exp=[int(x) for x in f[5].split()]))
+    return rows
+
+
+@pytest.mark.parametrize("case", _worked_cases(), ids=lambda c: c["name"])
+def test_route_worked_example(dev, case):
+    """The hand-worked Alg. 2 cases on the GPU.  Three code bits with
+    deviations 1, 2, 4 make the probe sequence codes 0..6 in order, one bin
+    each; every centroid differs from the query's logits in dimension 0 only,
+    by mu, so d_cent = mu^2 exactly, as in the one-dimensional example."""
+    mu = np.array([1, 2, 3, 100, 0.5, 4, 5, 6, 100, 7, 8, 100], np.float32)
+    lg = np.array([[-1.0, -2.0, -4.0]], np.float32)
+    cent = np.stack([lg[0, 0] - mu, np.full(12, lg[0, 1]), np.full(12, lg[0, 2])], 1)
+    cent = np.ascontiguousarray(cent, np.float32)
+    n, d = 12, 16
+    bc_off = np.array([0, 3, 4, 6, 8, 9, 11, 12, 12], np.int32)
+    gix = NR.Index(n=n, d=d, dtype=NR.NR_U8, b=3, weights=[np.zeros((3, d), np.float32)],
+                   biases=[np.zeros(3, np.float32)], input_scale=1.0, tau=np.zeros(3, np.float32),
+                   rows=torch.zeros((n, d), dtype=torch.uint8, device=dev),
+                   row_ids=torch.arange(n, dtype=torch.int64, device=dev),
+                   bc_off=torch.from_numpy(bc_off).to(dev),
+                   cl_off=torch.arange(n + 1, dtype=torch.int64, device=dev),
+                   centroids=torch.from_numpy(cent).to(dev))
+    # M(x) = 10 everywhere: two knots with a flat segment
+    p = NR.Params(l_sel=3, r_max=3, k_c=case["k_c"], b_batch=2, b_min=1, t_low=case["t_low"],
+                  u_heap=1, u_front=1, alpha_front=0.5, gate_on=True,
+                  early_stop_on=bool(case["es"]), lowq_or=bool(case["lowq_or"]),
+                  m_x=[0.0, 1.0], m_y=[10.0, 10.0])
+    gc, _, gb, gn = [t.cpu().numpy() for t in gix.nr_probe(torch.from_numpy(lg).to(dev), 7, p)]
+    assert gn[0] == 7 and gc[0].view(np.uint32).tolist() == list(range(7))
+    assert gb[0].tolist() == list(range(7))
+    clus, cnt = gix.nr_route(torch.from_numpy(lg).to(dev), 7, p)
+    got = clus.cpu().numpy()[0, :int(cnt[0])].tolist()
+    assert got == case["exp"]
+    oc, _, ob, on = O.probes(lg, np.zeros(3, np.float32), 3, 3, 7, p.s_max, p.n_bins)
+    assert O.route(lg, oc, ob, on, bc_off.astype(np.uint32), cent, oracle_params(p))[0].tolist() \
+        == case["exp"]
+    gix.close()
+
 # ------------------------------------------------------------------ step 5
 def _assert_topk(c, gi, gd, oi, od):
     if c["w"].dtype == "u8":
