@@ -115,6 +115,47 @@ def test_probe_full_budget_covers_all_codes(dev):
         assert sorted(gc[q].tolist()) == list(range(256))
 
 
+
+def _alg1_cases():
+    import os
+    rows = []
+    path = os.path.join(os.path.dirname(__file__), "golden", "alg1_worked_examples.txt")
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            f = [c.strip() for c in line.split("|")]
+            rows.append(dict(name=f[0], b=int(f[1]), tau=np.array(f[2].split(), np.float32),
+                             logits=np.array(f[3].split(), np.float32), l_sel=int(f[4]),
+                             r_max=int(f[5]), s_max=float(f[6]), n_bins=int(f[7]), P=int(f[8]),
+                             codes=[int(x) for x in f[9].split()],
+                             costs=[float(x) for x in f[10].split()],
+                             bins=[int(x) for x in f[11].split()]))
+    return rows
+
+
+@pytest.mark.parametrize("ex", _alg1_cases(), ids=lambda e: e["name"])
+def test_probe_worked_examples(dev, ex):
+    """The hand-worked Alg. 1 sequences (ties, a logit exactly at tau, finite
+    S_max with bins) on the GPU, through a one-row index with that tau."""
+    b, d = ex["b"], 16
+    bc_off = np.ones((1 << b) + 1, np.int32)
+    bc_off[0] = 0
+    gix = NR.Index(n=1, d=d, dtype=NR.NR_U8, b=b, weights=[np.zeros((b, d), np.float32)],
+                   biases=[np.zeros(b, np.float32)], input_scale=1.0, tau=ex["tau"],
+                   rows=torch.zeros((1, d), dtype=torch.uint8, device=dev),
+                   row_ids=torch.zeros(1, dtype=torch.int64, device=dev),
+                   bc_off=torch.from_numpy(bc_off).to(dev),
+                   cl_off=torch.tensor([0, 1], dtype=torch.int64, device=dev),
+                   centroids=torch.zeros((1, b), dtype=torch.float32, device=dev))
+    p = NR.Params(l_sel=ex["l_sel"], r_max=ex["r_max"], s_max=ex["s_max"], n_bins=ex["n_bins"])
+    lg = torch.from_numpy(ex["logits"][None].copy()).to(dev)
+    gc, gs, gb, gn = [t.cpu().numpy() for t in gix.nr_probe(lg, ex["P"], p)]
+    n = int(gn[0])
+    assert n == len(ex["codes"])
+    assert gc[0, :n].view(np.uint32).tolist() == ex["codes"]
+    assert gs[0, :n].tolist() == ex["costs"]
+    assert gb[0, :n].tolist() == ex["bins"]
+    gix.close()
+
 # ------------------------------------------------------------------ steps 3-4
 @pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("pset", list(PARAM_SETS))
