@@ -401,9 +401,9 @@ def main():
         f"kernels {kernels}, dominant {dom}")
 
     # ---- CPU baseline: the oracle on a bounded sample (rows staged in host memory)
-    cpu = None
+    cpu = parity = None
     if not args.no_oracle and not args.quick:
-        cpu = oracle_baseline(args, w, ix, Q, P, params, torch, dev)
+        cpu, parity = oracle_baseline(args, w, ix, gix, Q, P, params, torch, dev)
 
     out = {
         "metric": METRIC,
@@ -440,6 +440,7 @@ def main():
         "kernels": kernels,
         "refine_stage": refine_stage,
         "cpu_baseline": cpu,
+        "parity": parity,
         "calibration": calib,
         "sweep": sweep,
         "hbm_stream_read_gbs": round(stream_gbs, 1),
@@ -523,13 +524,36 @@ def grid(args, w, gix, Q, gt_ids, ng, xs, ys, CAL, NR, torch, head_copy):
                                                      "qps", "recall_at_10", "refine_gbs")})
 
 
-def oracle_baseline(args, w, ix, Q, P, params, torch, dev):
+def host_cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_threads(args) -> int:
+    """One thread per core this process may use: the affinity mask, bounded
+    by the CPU share the host grants the job (OMP_NUM_THREADS, when set)."""
+    if args.oracle_threads:
+        return args.oracle_threads
+    aff = len(os.sched_getaffinity(0))
+    share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    return min(aff, share) if share > 0 else aff
+
+
+def oracle_baseline(args, w, ix, gix, Q, P, params, torch, dev):
     """Time the oracle on a bounded sample: a 32-query pilot sizes the sample
     to about `--oracle-seconds` of wall time on the host threads, capped by
-    `--oracle-stage-gb` of staged rows."""
+    `--oracle-stage-gb` of staged rows; then one thread on the first 100
+    queries (per-core rate).  The oracle's top-k lists of the sample are
+    compared with the GPU's for the same queries, searched in the timed
+    launch configuration (the whole batch) with the oracle's logits."""
     import oracle as O
     from paper_2608_15438_amd import index_build as IB
-    threads = args.oracle_threads or min(16, len(os.sched_getaffinity(0)))
+    threads = oracle_threads(args)
     e = ix.encoder
     enc = O.Encoder(e.weights, e.biases, e.bn_scale or (), e.bn_shift or (), e.input_scale)
     bc = ix.bc_off.cpu().numpy().astype(np.uint32)
@@ -542,7 +566,7 @@ def oracle_baseline(args, w, ix, Q, P, params, torch, dev):
                         early_stop_on=params.early_stop_on, lowq_or=params.lowq_or,
                         m_x=np.array(params.m_x, np.float32), m_y=np.array(params.m_y, np.float32))
 
-    def run(nqs, min_seconds):
+    def stage(nqs):
         Qh = Q[:nqs].cpu().numpy()
         # discovery (untimed): the clusters this sample needs
         lg = O.encode(enc, Qh)
@@ -565,33 +589,64 @@ def oracle_baseline(args, w, ix, Q, P, params, torch, dev):
         cnt_all[need] = sizes
         cl2 = np.zeros(ix.n_clusters + 1, np.uint64)
         cl2[1:] = np.cumsum(cnt_all)
+        return Qh, rows_h, ids_h, cl2
+
+    def run(staged, nqs, min_seconds, n_threads):
+        Qh, rows_h, ids_h, cl2 = staged
         # timed: whole passes over the staged sample until min_seconds have
         # elapsed (at least one pass)
         passes, t0 = 0, time.time()
         while True:
-            oi, od, ncand, secs = O.search(enc, ix.tau, rows_h, ids_h, bc, cl2, cent, Qh, w.k,
-                                           params.l_sel, params.r_max, P, prm, n_threads=threads)
+            oi, od, ncand, secs = O.search(enc, ix.tau, rows_h, ids_h, bc, cl2, cent, Qh[:nqs],
+                                           w.k, params.l_sel, params.r_max, P, prm,
+                                           n_threads=n_threads)
             passes += 1
             if time.time() - t0 >= min_seconds:
                 break
-        return (time.time() - t0) / passes, passes, secs, rows_h.nbytes
+        return (time.time() - t0) / passes, passes, secs, oi, od
 
     pilot = min(32, w.n_queries)
-    dt, _, secs, nbytes = run(pilot, 0.0)
+    st = stage(pilot)
+    dt, _, secs, _, _ = run(st, pilot, 0.0, threads)
     per_q = dt / pilot
+    nbytes_pilot = st[1].nbytes
     nqs = int(min(w.n_queries, max(pilot, args.oracle_seconds / max(per_q, 1e-9)),
-                  max(pilot, args.oracle_stage_gb * 1e9 / max(nbytes / pilot, 1.0))))
-    dt, passes, secs, nbytes = run(nqs, args.oracle_seconds)
+                  max(pilot, args.oracle_stage_gb * 1e9 / max(nbytes_pilot / pilot, 1.0))))
+    nqs = max(nqs, min(w.n_queries, 100))
+    st = stage(nqs)
+    nbytes = st[1].nbytes
+    dt, passes, secs, oi, od = run(st, nqs, args.oracle_seconds, threads)
     cpu_qps = nqs / dt
+    # one thread, 100 queries: the per-core rate
+    n1 = min(100, nqs)
+    dt1, passes1, _, _, _ = run(st, n1, 0.0, 1)
     log(f"oracle: {nqs} queries x {passes} passes on {threads} threads, {dt:.2f}s per pass "
-        f"({cpu_qps:.1f} QPS), {nbytes / 1e9:.2f} GB staged")
-    return {"value": round(cpu_qps, 2), "unit": "queries/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {nqs} queries of the batch, same index and probe budget, timed over "
-                      f"{passes} whole passes; rows of their candidate clusters "
-                      f"({nbytes / 1e9:.2f} GB) staged in host memory before timing",
-            "seconds": round(dt * passes, 3),
-            "stage_seconds_last_pass": dict(zip(("encode", "probe", "route", "refine"),
-                                                [round(float(x), 3) for x in secs]))}
+        f"({cpu_qps:.1f} QPS), {nbytes / 1e9:.2f} GB staged; one thread: {n1 / dt1:.1f} QPS")
+    # parity of the sample: the GPU in the timed configuration, given the
+    # oracle's logits for the whole batch
+    lg_all = torch.from_numpy(O.encode(enc, Q.cpu().numpy())).to(dev)
+    gi, gd = gix.nr_search(Q, w.k, P, params, logits=lg_all)
+    gi, gd = gi[:nqs].cpu().numpy(), gd[:nqs].cpu().numpy()
+    id_mis = int((gi != oi).any(1).sum())
+    if w.dtype == "u8":
+        d_mis = int((gd != od).any(1).sum())
+    else:
+        d_mis = int((~np.isclose(gd, od, rtol=1e-5, atol=1e-6)).any(1).sum())
+    parity = {"queries": nqs, "id_mismatches": id_mis, "dist_mismatches": d_mis,
+              "rule": "bit-exact ids and distances" if w.dtype == "u8"
+              else "ids exact except fp32 near-ties; distances within 1e-5"}
+    log("parity", parity)
+    cpu = {"value": round(cpu_qps, 2), "unit": "queries/s", "cores": threads, "kind": "oracle",
+           "cpu_model": host_cpu_model(), "affinity_cores": len(os.sched_getaffinity(0)),
+           "sample": f"first {nqs} queries of the batch, same index and probe budget, timed over "
+                     f"{passes} whole passes; rows of their candidate clusters "
+                     f"({nbytes / 1e9:.2f} GB) staged in host memory before timing",
+           "seconds": round(dt * passes, 3),
+           "per_core": {"value": round(n1 / dt1, 2), "unit": "queries/s", "threads": 1,
+                        "queries": n1},
+           "stage_seconds_last_pass": dict(zip(("encode", "probe", "route", "refine"),
+                                               [round(float(x), 3) for x in secs]))}
+    return cpu, parity
 
 
 if __name__ == "__main__":

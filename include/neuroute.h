@@ -31,7 +31,7 @@
  *   id); rows with fewer than k candidates are padded with id -1, distance +inf.
  * - Calls on one index from different streams may overlap; each stream gets
  *   its own workspace.  The index itself is read-only after upload.
- * - Limits: 1 <= k <= 64, 1 <= probe_budget <= 1024, 1 <= b <= 30,
+ * - Limits: 1 <= k <= 64, 1 <= probe_budget <= 4096, 1 <= b <= 30,
  *   L_sel <= min(b, 32), 1 <= B_batch <= 64, K_c limited by LDS (16384),
  *   encoder widths <= 4096; anything beyond returns NR_EUNSUPPORTED.
  */
@@ -59,7 +59,7 @@ typedef enum { NR_U8 = 0, NR_F32 = 1 } nr_dtype;
 #define NR_MAX_LAYERS 8
 #define NR_MAX_KNOTS 32
 #define NR_MAX_K 64
-#define NR_MAX_PROBES 1024
+#define NR_MAX_PROBES 4096
 
 typedef struct nr_index nr_index;   /* opaque, library-owned */
 

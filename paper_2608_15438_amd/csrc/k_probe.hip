@@ -164,7 +164,13 @@ hipError_t launch_probe(const ProbeArgs &a, hipStream_t s) {
   if (a.nq <= 0) return hipSuccess;
   if (a.P < 1 || a.P > NR_MAX_PROBES) return hipErrorInvalidValue;
   const size_t pc = (size_t)(a.P + WAVE - 1) / WAVE * WAVE;
-  hipLaunchKernelGGL(k_probe, dim3((unsigned)a.nq), dim3(64), 3 * pc * sizeof(uint64_t), s, a);
+  const size_t lds = 3 * pc * sizeof(uint64_t);  // 96 KiB at P = 4096 (gfx950: 160 KiB per CU)
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)k_probe,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_probe, dim3((unsigned)a.nq), dim3(64), lds, s, a);
   return hipGetLastError();
 }
 

@@ -24,7 +24,7 @@ NR_U8, NR_F32 = 0, 1
 NR_MAX_LAYERS = 8
 NR_MAX_KNOTS = 32
 NR_MAX_K = 64
-NR_MAX_PROBES = 1024
+NR_MAX_PROBES = 4096
 NR_QSTATS = 8
 NR_REFINE_AUTO, NR_REFINE_PER_QUERY, NR_REFINE_SHARED = 0, 1, 2
 NR_STAGES = 10

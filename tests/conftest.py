@@ -18,3 +18,13 @@ def oracle_lib():
     import oracle
     oracle.build(force=False)
     return oracle
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Near-ties of fp32 top-k lists (R27) seen by the parity checks."""
+    import sys
+    mod = sys.modules.get("tests.topk_check")
+    if mod and mod.NEAR_TIES["queries"]:
+        nt = mod.NEAR_TIES
+        terminalreporter.write_line(
+            f"top-k parity: {nt['queries']} query lists checked, {nt['near_ties']} fp32 near-ties")

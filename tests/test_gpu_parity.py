@@ -10,6 +10,7 @@ import torch
 import oracle as O
 from paper_2608_15438_amd import neuroute as NR
 from tests.instances import instance, oracle_encoder, split_index
+from tests.topk_check import allowed_ids, check_topk
 
 pytestmark = pytest.mark.gpu
 
@@ -91,7 +92,7 @@ def test_encoder_logits(dev, name):
 
 # ------------------------------------------------------------------ step 2
 @pytest.mark.parametrize("name", list(CASES))
-@pytest.mark.parametrize("P", [1, 7, 64, 300, 1024])
+@pytest.mark.parametrize("P", [1, 7, 64, 300, 1024, 2048, 4096])
 @pytest.mark.parametrize("pset", ["default", "binned"])
 def test_probe_sequence_bit_exact(dev, name, P, pset):
     c = setup_case(name, dev)
@@ -104,6 +105,39 @@ def test_probe_sequence_bit_exact(dev, name, P, pset):
         assert np.array_equal(gc[q, :n].view(np.uint32), oc[q, :n]), q
         assert np.array_equal(gs[q, :n], os_[q, :n]), q
         assert np.array_equal(gb[q, :n], ob[q, :n]), q
+
+
+@pytest.mark.parametrize("P", [2048, 4096])
+@pytest.mark.parametrize("r_max,s_max,n_bins", [(7, float("inf"), 1), (16, 6.0, 40)])
+def test_probe_long_sequences_bit_exact(dev, P, r_max, s_max, n_bins):
+    """Sequences of up to 4096 probes over 16 selected dimensions of a 20-bit
+    code (26,333 flip sets of radius <= 7), from seeded logits; the lists of
+    the merge recursion fill 96 KiB of LDS at P = 4096."""
+    b, d, nq = 20, 16, 64
+    rng = np.random.default_rng(4096 + P)
+    lg = rng.normal(0.0, 1.0, size=(nq, b)).astype(np.float32)
+    tau = rng.normal(0.0, 0.2, size=b).astype(np.float32)
+    bc_off = np.ones((1 << b) + 1, np.int32)
+    bc_off[0] = 0
+    gix = NR.Index(n=1, d=d, dtype=NR.NR_U8, b=b, weights=[np.zeros((b, d), np.float32)],
+                   biases=[np.zeros(b, np.float32)], input_scale=1.0, tau=tau,
+                   rows=torch.zeros((1, d), dtype=torch.uint8, device=dev),
+                   row_ids=torch.zeros(1, dtype=torch.int64, device=dev),
+                   bc_off=torch.from_numpy(bc_off).to(dev),
+                   cl_off=torch.tensor([0, 1], dtype=torch.int64, device=dev),
+                   centroids=torch.zeros((1, b), dtype=torch.float32, device=dev))
+    p = NR.Params(l_sel=16, r_max=r_max, s_max=s_max, n_bins=n_bins)
+    gc, gs, gb, gn = [t.cpu().numpy() for t in gix.nr_probe(torch.from_numpy(lg).to(dev), P, p)]
+    oc, os_, ob, on = O.probes(lg, tau, 16, r_max, P, s_max, n_bins)
+    assert np.array_equal(gn, on)
+    if r_max == 7:
+        assert np.all(on == P)
+    for q in range(nq):
+        n = on[q]
+        assert np.array_equal(gc[q, :n].view(np.uint32), oc[q, :n]), q
+        assert np.array_equal(gs[q, :n], os_[q, :n]), q
+        assert np.array_equal(gb[q, :n], ob[q, :n]), q
+    gix.close()
 
 
 def test_probe_full_budget_covers_all_codes(dev):
@@ -159,7 +193,7 @@ def test_probe_worked_examples(dev, ex):
 # ------------------------------------------------------------------ steps 3-4
 @pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("pset", list(PARAM_SETS))
-@pytest.mark.parametrize("P", [4, 64, 512])
+@pytest.mark.parametrize("P", [4, 64, 512, 4096])
 def test_candidate_clusters_bit_exact(dev, name, pset, P):
     c = setup_case(name, dev)
     p = default_params(c, **PARAM_SETS[pset])
@@ -221,26 +255,22 @@ def test_route_worked_example(dev, case):
     gix.close()
 
 # ------------------------------------------------------------------ step 5
-def _assert_topk(c, gi, gd, oi, od):
-    if c["w"].dtype == "u8":
-        assert np.array_equal(gi, oi)
-        assert np.array_equal(gd, od)
-        return
-    # fp32: same ids except at near-ties; distances within 1e-5 relative
-    X, Q = c["X"], c["Q"]
-    for q in range(len(oi)):
-        ok = oi[q] >= 0
-        assert np.array_equal(gi[q] >= 0, ok), q
-        if np.array_equal(gi[q], oi[q]):
-            assert np.allclose(gd[q][ok], od[q][ok], rtol=1e-5, atol=1e-6), q
-            continue
-        # a valid top-k under the tolerance: every returned row is within
-        # 2e-5 of the oracle's k-th distance and distances match recomputation
-        kth = od[q][ok][-1]
-        ids = gi[q][gi[q] >= 0]
-        true = ((X[ids].astype(np.float64) - Q[q].astype(np.float64)) ** 2).sum(1)
-        assert np.all(true <= kth * (1 + 2e-5) + 1e-6), q
-        assert np.allclose(gd[q][: len(ids)], true, rtol=1e-5, atol=1e-6), q
+def _assert_topk(c, gi, gd, oi, od, lists=None, ix=None):
+    """uint8: ids and distances equal.  fp32: the checks of check_topk (valid
+    top-k, near-ties only); lists (the oracle's C(q)) bound the allowed ids."""
+    ix = ix if ix is not None else c.get("ix")
+    allowed = None
+    if lists is not None and ix is not None:
+        allowed = lambda q: allowed_ids(ix.cl_off, ix.row_ids, lists[q])
+    X = c["X"]
+    check_topk(gi, gd, oi, od, is_u8=c["w"].dtype == "u8", X_by_id=lambda ids: X[ids],
+               Q=c["Q"], allowed=allowed)
+
+
+def _oracle_lists(c, p, P):
+    """The oracle's C(q) for every query of the case (Alg. 1, then Alg. 2)."""
+    oc, _, ob, on = O.probes(c["lg"], c["ix"].tau, p.l_sel, p.r_max, P, p.s_max, p.n_bins)
+    return O.route(c["lg"], oc, ob, on, c["ix"].bc_off, c["ix"].centroids, oracle_params(p))
 
 
 @pytest.mark.parametrize("layout", ["gix", "gix_split", "gix_copy"])
@@ -261,7 +291,7 @@ def test_refine_given_clusters(dev, name, k, layout):
     gi, gd = c[layout].nr_refine(c["Qd"], k, torch.from_numpy(cl.view(np.int32)).to(dev),
                                  torch.from_numpy(n).to(dev))
     oi, od, _ = O.refine(c["ix"].rows, c["ix"].row_ids, c["ix"].cl_off, c["Q"], lists, k)
-    _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
+    _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od, lists=lists)
 
 
 # every refine kernel shape by row length: rows past 8 x 128 bytes keep the
@@ -291,7 +321,8 @@ def test_refine_row_lengths(dev, cfg, d, layout):
                                torch.from_numpy(n).to(dev))
         oi, od, _ = O.refine(ix.rows, ix.row_ids, ix.cl_off, Q,
                              [L.astype(np.uint32) for L in lists], k)
-        _assert_topk(dict(w=w, X=X, Q=Q), gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
+        _assert_topk(dict(w=w, X=X, Q=Q), gi.cpu().numpy(), gd.cpu().numpy(), oi, od,
+                     lists=lists, ix=ix)
     # the whole search: the batch-shared schedule (seed pass of 64 rows, the
     # rest through the scan) returns exactly the per-query schedule's lists
     Qd = torch.from_numpy(Q).to(dev)
@@ -330,7 +361,22 @@ def test_search_given_logits_bit_exact(dev, name, pset, P, mode):
     oi, od, _, _ = O.search(c["enc"], ix.tau, ix.rows, ix.row_ids, ix.bc_off, ix.cl_off,
                             ix.centroids, c["Q"], 10, p.l_sel, p.r_max, P, oracle_params(p),
                             n_threads=4)
-    _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
+    _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od, lists=_oracle_lists(c, p, P))
+
+
+@pytest.mark.parametrize("mode", ["per_query", "shared", "shared_seed64"])
+@pytest.mark.parametrize("name", ["sift", "deep", "gld"])
+@pytest.mark.parametrize("P", [2048, 4096])
+def test_search_long_probe_sequences(dev, name, P, mode):
+    """The whole path at the largest probe budgets."""
+    c = setup_case(name, dev)
+    p = default_params(c, **MODES[mode][1])
+    gi, gd = c[MODES[mode][0]].nr_search(c["Qd"], 10, P, p, logits=c["lgd"])
+    ix = c["ix"]
+    oi, od, _, _ = O.search(c["enc"], ix.tau, ix.rows, ix.row_ids, ix.bc_off, ix.cl_off,
+                            ix.centroids, c["Q"], 10, p.l_sel, p.r_max, P, oracle_params(p),
+                            n_threads=4)
+    _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od, lists=_oracle_lists(c, p, P))
 
 
 @pytest.mark.parametrize("mode", list(MODES))
@@ -369,7 +415,8 @@ def test_empty_and_single_query(dev):
     oi, od, _, _ = O.search(c["enc"], c["ix"].tau, c["ix"].rows, c["ix"].row_ids, c["ix"].bc_off,
                             c["ix"].cl_off, c["ix"].centroids, c["Q"][:1], 10, p.l_sel, p.r_max,
                             16, oracle_params(p))
-    _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od)
+    _assert_topk(c, gi.cpu().numpy(), gd.cpu().numpy(), oi, od,
+                 lists=[_oracle_lists(c, p, 16)[0]])
 
 
 def test_short_lists_are_padded(dev):
