@@ -64,6 +64,11 @@ def parse():
     ap.add_argument("--calib", choices=("gt", "bootstrap"), default="gt",
                     help="calibration targets: brute-force top-k, or the search's own "
                          "top-k at the largest budget with gate and early stop off")
+    ap.add_argument("--s-max-coverage", type=float, default=0.0,
+                    help="apply the bucket-score cutoff S_max fitted at this pair coverage "
+                         "(0: S_max = +inf, the enumeration bounded by the probe budget alone)")
+    ap.add_argument("--n-bins", type=int, default=32,
+                    help="score bins of Algorithm 1 when S_max is applied")
     ap.add_argument("--refine-mode", choices=("auto", "per_query", "shared"), default="auto",
                     help="refinement schedule (the same results either way)")
     ap.add_argument("--seed-rows", type=int, default=0,
@@ -264,9 +269,6 @@ def main():
                              ix.row_ids, torch.cat([Q[:ng], Qc]), k)
     gt_ids, gtc = gt_all[:ng], gt_all[ng:]
     log(f"ground truth for {ng}+{nc} queries in {time.time() - t0:.1f}s")
-    fwd = IB._TorchEncoder(ix.encoder, dev)
-    row_of_id = torch.empty_like(ix.row_ids)
-    row_of_id[ix.row_ids] = torch.arange(w.n, device=dev)
     targets = torch.from_numpy(gtc).to(dev)
     if args.calib == "bootstrap":
         # the paper's supervision: the search itself in a higher-recall
@@ -276,22 +278,23 @@ def main():
         targets = CAL.bootstrap_targets(gix, Qc, k, NR.NR_MAX_PROBES, loose)
         agree = float((targets.cpu() == torch.from_numpy(gtc)).double().mean())
         log(f"bootstrapped calibration targets: {agree:.3f} of them equal the brute-force ones")
-    lgc = fwd(Qc)
-    xs, ys = CAL.margin_points(lgc, targets, row_of_id, ix.cl_off, ix.bc_off, ix.centroids)
-    # the bucket-score cutoff the same targets give (reported; the search runs
-    # with S_max = +inf)
-    sc = CAL.bucket_scores(lgc, torch.as_tensor(np.asarray(ix.tau), device=dev),
-                           CAL.target_codes(targets, row_of_id, ix.cl_off, ix.bc_off),
-                           min(w.l_sel, w.b), w.r_max)
+    # bucket scores of the targets and margin points: the library's calibration kernel
+    sc, xs, ys = CAL.gpu_calibration(gix, gix.nr_encode(Qc), targets, min(w.l_sel, w.b), w.r_max)
     s95, pcov, qcov = CAL.fit_s_max(sc, 0.95)
     calib = {"targets": "bootstrap" if args.calib == "bootstrap" else "brute-force",
              "queries": nc, "s_max_95": round(s95, 4), "pair_coverage": round(pcov, 4),
              "query_coverage": round(qcov, 4)}
+    s_max, n_bins = float("inf"), 1
+    if args.s_max_coverage > 0:
+        s_max, pc, qc = CAL.fit_s_max(sc, args.s_max_coverage)
+        n_bins = args.n_bins
+        calib.update({"applied_s_max": round(s_max, 5), "applied_coverage": args.s_max_coverage,
+                      "applied_pair_coverage": round(pc, 4), "n_bins": n_bins})
     log("calibration", calib)
-    del row_of_id
     m_x, m_y = CAL.fit_margin(xs, ys, args.margin_quantile)
-    params = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c,
-                       m_x=m_x.tolist(), m_y=m_y.tolist(), shared_seed_rows=args.seed_rows,
+    params = NR.Params(l_sel=min(w.l_sel, w.b), r_max=w.r_max, k_c=w.k_c, s_max=s_max,
+                       n_bins=n_bins, m_x=m_x.tolist(), m_y=m_y.tolist(),
+                       shared_seed_rows=args.seed_rows,
                        refine_mode={"auto": NR.NR_REFINE_AUTO, "per_query": NR.NR_REFINE_PER_QUERY,
                                     "shared": NR.NR_REFINE_SHARED}[args.refine_mode])
     if args.grid:

@@ -225,6 +225,49 @@ nr_status nr_refine(const nr_index *index, const void *queries, int64_t nq, int3
                     const uint32_t *clusters, const int32_t *n_clusters, int64_t cap,
                     int64_t *out_ids, float *out_dists, hipStream_t stream);
 
+/* Calibration inputs (Sec. 3.4 "Calibration": "Bucket-score cutoff" and
+ * "Centroid gating margin"), for calibration queries with known top-K target
+ * rows (from a higher-recall run of the search, or exact k-NN):
+ *   logits      DEVICE fp32 [nq x b] of the calibration queries;
+ *   target_ids  DEVICE int64 [nq x K], original row ids (< 0: no target), K <= 64;
+ *   scores      DEVICE fp32 [nq x K] out: the score Algorithm 1 gives each
+ *               target's bucket under (l_sel, r_max) -- bit for bit the cost
+ *               of that bucket in the probe sequence -- or +inf when the
+ *               enumeration cannot reach it;
+ *   margin_xy   DEVICE fp32 [nq x 2] out: x = the smallest squared latent
+ *               distance from the query to any centroid of a bucket holding a
+ *               target, y = the distance of the farthest target's cluster
+ *               minus x (x = +inf, y = 0 when the query has no target).
+ * The first call on an index builds its inverse permutation (4 bytes per row,
+ * freed with the index).  Fitting S_max and M(x) from these arrays is the
+ * caller's (quantiles of a few thousand numbers). */
+nr_status nr_calibrate(const nr_index *index, const float *logits, int64_t nq,
+                       const int64_t *target_ids, int32_t K, int32_t l_sel, int32_t r_max,
+                       float *scores, float *margin_xy, hipStream_t stream);
+
+/* Encoder training with the selective similarity loss L_sim (Sec. 3.2.2,
+ * the loss of Eq. "similarityconfig" with the mask of Eq. 8), for one
+ * mini-batch of B <= 65536 rows.
+ * nr_pair_sqdist: out DEVICE fp32 [B x B] = squared Euclidean distances of the
+ *   rows of x (DEVICE fp32 [B x D], the inputs as the encoder sees them),
+ *   diagonal 0, computed as |x_i|^2 + |x_j|^2 - 2 x_i.x_j on the fp32 matrix
+ *   cores after centring the batch on its mean; ws: DEVICE fp32 scratch of
+ *   nr_pair_sqdist_ws(B, D) floats.
+ * nr_lsim_grad: given those distances (S_emb = their square roots) and the
+ *   latents lat (DEVICE fp32 [B x L], L <= 32), with m_ij = [i != j and
+ *   (S_emb(i,j) <= tau_emb or S_lat(i,j) <= gamma_rho * tau_emb)] and
+ *   d_ij = S_lat(i,j) - gamma_rho * S_emb(i,j) (gamma_rho = gamma * sqrt(L/E)):
+ *   num_cnt (DEVICE fp64 [2], overwritten) = (sum m d^2, sum m), so that
+ *   L_sim = num / cnt; grad_lat (DEVICE fp32 [B x L]) = cnt * dL_sim/dlat
+ *   with the mask held fixed, i.e. sum_j 2 (m_ij d_ij + m_ji d_ji)
+ *   (l_i - l_j) / S_lat(i,j). */
+size_t nr_pair_sqdist_ws(int64_t B, int32_t D);
+nr_status nr_pair_sqdist(const float *x, int64_t B, int32_t D, float *ws, float *out,
+                         hipStream_t stream);
+nr_status nr_lsim_grad(const float *d2_emb, const float *lat, int64_t B, int32_t L,
+                       float gamma_rho, float tau_emb, double *num_cnt, float *grad_lat,
+                       hipStream_t stream);
+
 /* Stage timing with HIP events on the launch stream (off by default).
  * nr_profile_read synchronises the recorded events and returns the summed
  * milliseconds per stage and the number of timed searches since the last

@@ -1,5 +1,8 @@
 """Calibration of the centroid-stage gate margin M(x) (Sec. 3.4, "Centroid
-gating margin"), untimed and shared by both search paths.
+gating margin") and of the bucket-score cutoff S_max ("Bucket-score
+cutoff"), untimed and shared by both search paths.  The per-query inputs
+come from the library's calibration kernel (gpu_calibration); the PyTorch
+versions below define the same quantities and serve the CPU checks.
 
 For each calibration query with known top-K targets: x = the best centroid
 distance among all centroids of the buckets that hold its targets, y = the
@@ -113,6 +116,16 @@ def bucket_scores(logits: torch.Tensor, tau: torch.Tensor, codes: torch.Tensor, 
         s = s + torch.where(flipped[:, :, r], d_rank[:, r:r + 1].expand_as(s), torch.zeros_like(s))
     bad = outside | (n_flip > r_max) | (codes < 0)
     return torch.where(bad, torch.full_like(s, float("inf")), s)
+
+
+def gpu_calibration(gix, logits: torch.Tensor, targets: torch.Tensor, l_sel: int, r_max: int):
+    """Bucket scores [nq, K] and margin points (xs, ys) of the calibration
+    queries from the library's calibration kernel (nr_calibrate): the
+    enumeration's own score of each target bucket, and x / y in the search's
+    own squared latent distance.  Queries without targets are dropped."""
+    scores, xy = gix.nr_calibrate(logits.float().contiguous(), targets.contiguous(), l_sel, r_max)
+    ok = torch.isfinite(xy[:, 0])
+    return scores, xy[ok, 0].double().cpu().numpy(), xy[ok, 1].double().cpu().numpy()
 
 
 def fit_s_max(scores: torch.Tensor, coverage: float = 0.95):

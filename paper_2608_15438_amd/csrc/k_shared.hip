@@ -12,11 +12,10 @@
 //          top-k is exact over a subset of C(q), so its k-th entry bounds
 //          the final k-th entry: a later row can only enter the result if it
 //          ranks at or before it;
-//  prep    (on a second stream, beside the seed pass) one scan over the
-//          clusters places every cluster with pairs in the scan list and its
-//          pairs in pair_q; a scan over the list places each entry's work
-//          (rows x groups of <= g queries); the pairs are then scattered by
-//          cluster;
+//  prep    (on a second stream, beside the seed pass) the clusters with
+//          pairs, found through a bitmap the counting set, form the scan
+//          list in cluster order with their pair and work ranges (rows x
+//          groups of <= g queries); the pairs are then scattered by cluster;
 //  scan    persistent waves take tiles of SHARED_TILE work from an atomic
 //          counter and gather consecutive units of the tile into batches
 //          whose query rows sit in LDS.  Each row's head (its first
@@ -31,8 +30,6 @@
 //          the pool full is flagged and recomputed by the per-query
 //          schedule.
 #include <cstring>
-
-#include <rocprim/rocprim.hpp>
 
 #include "nr_internal.h"
 
@@ -111,17 +108,22 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
 
 
 // ------------------------------------------------------------------ hist
-
-// ------------------------------------------------------------------ hist
 // The pair counts are taken at the end of the route kernel, per query, once
-// its list is final (pair_hist_wave); the counts start from zero.
-hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s) {
-  return launch_fill_i32((int32_t *)a.hist, a.n_clusters + 1, 0, s);
+// its list is final (pair_hist_wave): hist[c] counts cluster c's pairs and
+// the first pair of a cluster sets bit c of `touched`.  Both start a search
+// at zero: the prep clears what it read, so only a fresh workspace needs the
+// full clear below.
+hipError_t launch_shared_hist(const SharedArgs &a, bool fresh, hipStream_t s) {
+  if (!fresh) return hipSuccess;
+  hipError_t e = launch_fill_i32((int32_t *)a.hist, a.n_clusters + 1, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.touched, list_words(a.n_clusters), 0, s);
+  return e;
 }
 
 PairHistArgs pair_hist_args(const SharedArgs &a) {
   PairHistArgs h;
   h.hist = a.hist;
+  h.touched = a.touched;
   h.cl_off = a.cl_off;
   h.n_clusters = a.n_clusters;
   h.seed_min = a.seed_min;
@@ -139,38 +141,155 @@ PairHistArgs pair_hist_args(const SharedArgs &a) {
 }
 
 // ------------------------------------------------------------------ prep
-// One scan over the clusters gives both where each cluster's pairs start in
-// pair_q (low half) and its position in the scan list (high half): a
-// cluster with h pairs adds h to the first and 1 to the second when h > 0.
-struct HistPack {
-  const uint32_t *hist;
-  __device__ uint64_t operator()(uint32_t h) const {
-    return (uint64_t)h | ((uint64_t)(h > 0 ? 1u : 0u) << 32);
-  }
+// The scan list holds the clusters with pairs in cluster order, each with
+// its pair range in pair_q and its range in the scan's work space (rows x
+// groups of <= g queries).  It is built from the `touched` bitmap, so the
+// prep costs one pass over n_clusters / 32 words plus work per listed
+// cluster, not per index cluster:
+//   count  thread t of block b owns LIST_WPT bitmap words; it sums entries,
+//          pairs and work over its set bits (block sums too);
+//   scan   one block turns the block sums into exclusive offsets and the
+//          totals (list length, pairs, work);
+//   emit   each thread scans its block's thread sums, walks its bits again
+//          and writes its entries, each cluster's pair start (for the
+//          scatter), and clears hist and its bitmap words for the next
+//          search;
+//   scatter one wave per query puts each pair at its cluster's start plus
+//          the rank its counting atomic returned.
+
+struct ListSums {
+  uint32_t n, h;
+  uint64_t w;
 };
 
-// the work of scan-list entry i, 0 past the list
-struct ListWork {
-  const uint64_t *swork;
-  const uint64_t *total;  // hpos[n_clusters]: list length in the high half
-  __device__ uint64_t operator()(int64_t i) const {
-    return i < (int64_t)(*total >> 32) ? swork[i] : 0ull;
+__device__ __forceinline__ ListSums list_thread_sums(const SharedArgs &a, int64_t w0,
+                                                     int64_t nwords) {
+  ListSums r{0u, 0u, 0ull};
+  for (int j = 0; j < LIST_WPT; ++j) {
+    const int64_t wi = w0 + j;
+    if (wi >= nwords) break;
+    uint32_t bits = a.touched[wi];
+    while (bits) {
+      const uint64_t c = (uint64_t)wi * 32 + (uint64_t)(__ffs(bits) - 1);
+      bits &= bits - 1;
+      const uint32_t hc = a.hist[c];
+      const uint64_t sz = a.cl_off[c + 1] - a.cl_off[c];
+      r.n += 1;
+      r.h += hc;
+      r.w += (uint64_t)((hc + a.g - 1) / a.g) * sz;
+    }
   }
-};
+  return r;
+}
 
-typedef rocprim::transform_iterator<const uint32_t *, HistPack, uint64_t> HistPackInput;
-typedef rocprim::transform_iterator<rocprim::counting_iterator<int64_t>, ListWork, uint64_t>
-    ListWorkInput;
+// block-wide exclusive scan of (n, h, w) over LIST_THREADS threads; returns
+// the thread's exclusive prefix and writes the block total to *tot
+__device__ __forceinline__ ListSums list_block_scan(ListSums v, ListSums *tot) {
+  __shared__ uint32_t sn[LIST_THREADS / WAVE], sh[LIST_THREADS / WAVE];
+  __shared__ uint64_t sw[LIST_THREADS / WAVE];
+  const int lane = lane_id(), wv = threadIdx.x / WAVE;
+  const uint32_t in = wave_incl_scan_u32(v.n), ih = wave_incl_scan_u32(v.h);
+  const uint64_t iw = wave_incl_scan_u64(v.w);
+  if (lane == WAVE - 1) {
+    sn[wv] = in;
+    sh[wv] = ih;
+    sw[wv] = iw;
+  }
+  __syncthreads();
+  uint32_t bn = 0, bh = 0;
+  uint64_t bw = 0;
+  ListSums t{0u, 0u, 0ull};
+  for (int i = 0; i < LIST_THREADS / WAVE; ++i) {
+    if (i == wv) {
+      bn = t.n;
+      bh = t.h;
+      bw = t.w;
+    }
+    t.n += sn[i];
+    t.h += sh[i];
+    t.w += sw[i];
+  }
+  *tot = t;
+  return ListSums{bn + in - v.n, bh + ih - v.h, bw + iw - v.w};
+}
 
-// one thread per cluster with pairs: its list entry and the entry's work
-__global__ void k_shared_list(SharedArgs a) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < a.n_clusters; c += stride) {
-    const uint32_t h = a.hist[c];
-    if (h == 0) continue;
-    const uint32_t i = (uint32_t)(a.hpos[c] >> 32);
-    a.slist[i] = (uint32_t)c;
-    a.swork[i] = (uint64_t)((h + a.g - 1) / a.g) * (a.cl_off[c + 1] - a.cl_off[c]);
+__global__ void __launch_bounds__(LIST_THREADS) k_list_count(SharedArgs a) {
+  const int64_t nwords = list_words(a.n_clusters);
+  const int64_t t = (int64_t)blockIdx.x * LIST_THREADS + threadIdx.x;
+  const ListSums v = list_thread_sums(a, t * LIST_WPT, nwords);
+  a.thr_n[t] = v.n;
+  a.thr_h[t] = v.h;
+  a.thr_w[t] = v.w;
+  ListSums tot;
+  (void)list_block_scan(v, &tot);
+  if (threadIdx.x == 0) {
+    a.blk_n[blockIdx.x] = tot.n;
+    a.blk_h[blockIdx.x] = tot.h;
+    a.blk_w[blockIdx.x] = tot.w;
+  }
+}
+
+// one block: exclusive offsets of the blocks' sums, in place, and the totals
+__global__ void __launch_bounds__(LIST_THREADS) k_list_scan(SharedArgs a, int64_t nblk) {
+  const int64_t per = (nblk + LIST_THREADS - 1) / LIST_THREADS;
+  const int64_t b0 = (int64_t)threadIdx.x * per;
+  const int64_t b1 = b0 + per < nblk ? b0 + per : nblk;
+  ListSums v{0u, 0u, 0ull};
+  for (int64_t b = b0; b < b1; ++b) {
+    v.n += a.blk_n[b];
+    v.h += a.blk_h[b];
+    v.w += a.blk_w[b];
+  }
+  ListSums tot;
+  ListSums run = list_block_scan(v, &tot);
+  for (int64_t b = b0; b < b1; ++b) {
+    const ListSums x{a.blk_n[b], a.blk_h[b], a.blk_w[b]};
+    a.blk_n[b] = run.n;
+    a.blk_h[b] = run.h;
+    a.blk_w[b] = run.w;
+    run.n += x.n;
+    run.h += x.h;
+    run.w += x.w;
+  }
+  if (threadIdx.x == 0) {
+    a.lmeta[0] = tot.n;       // list length
+    a.lmeta[1] = tot.h;       // pairs
+    a.lmeta[2] = tot.w;       // work
+    a.swork_off[tot.n] = tot.w;
+  }
+}
+
+__global__ void __launch_bounds__(LIST_THREADS) k_list_emit(SharedArgs a) {
+  const int64_t nwords = list_words(a.n_clusters);
+  const int64_t t = (int64_t)blockIdx.x * LIST_THREADS + threadIdx.x;
+  const ListSums v{a.thr_n[t], a.thr_h[t], a.thr_w[t]};
+  ListSums tot;
+  const ListSums ex = list_block_scan(v, &tot);
+  uint32_t i = a.blk_n[blockIdx.x] + ex.n;
+  uint32_t hp = a.blk_h[blockIdx.x] + ex.h;
+  uint64_t wo = a.blk_w[blockIdx.x] + ex.w;
+  const int64_t w0 = t * LIST_WPT;
+  for (int j = 0; j < LIST_WPT; ++j) {
+    const int64_t wi = w0 + j;
+    if (wi >= nwords) break;
+    uint32_t bits = a.touched[wi];
+    if (!bits) continue;
+    a.touched[wi] = 0u;
+    while (bits) {
+      const uint64_t c = (uint64_t)wi * 32 + (uint64_t)(__ffs(bits) - 1);
+      bits &= bits - 1;
+      const uint32_t hc = a.hist[c];
+      const uint64_t sz = a.cl_off[c + 1] - a.cl_off[c];
+      a.hist[c] = 0u;
+      a.slist[i] = (uint32_t)c;
+      a.lpair[i] = hp;
+      a.lpm[i] = hc;
+      a.swork_off[i] = wo;
+      a.hpos[c] = hp;
+      i += 1;
+      hp += hc;
+      wo += (uint64_t)((hc + a.g - 1) / a.g) * sz;
+    }
   }
 }
 
@@ -185,29 +304,14 @@ __global__ void __launch_bounds__(256) k_pair_scatter(SharedArgs a) {
   const uint32_t *rank = a.pair_rank + q * a.cap;
   for (int i = a.cseed[q] + lane; i < n; i += WAVE) {
     const uint32_t c = cl[i];
-    if (c < a.n_clusters) a.pair_q[(uint32_t)a.hpos[c] + rank[i]] = (uint32_t)q;
+    if (c < a.n_clusters) {
+      const uint64_t pos = (uint64_t)a.hpos[c] + rank[i];
+      if (pos < (uint64_t)a.nq * (uint64_t)a.cap) a.pair_q[pos] = (uint32_t)q;
+    }
   }
 }
 
-// entries of the work scan: the list is at most one entry per cluster and
-// per pair slot
-static size_t work_scan_size(int64_t n_clusters, int64_t pair_slots) {
-  return (size_t)(pair_slots < n_clusters ? pair_slots : n_clusters) + 1;
-}
-
-size_t shared_scan_tmp_bytes(int64_t n_clusters, int64_t pair_slots) {
-  size_t b1 = 0, b2 = 0;
-  const HistPackInput hin((const uint32_t *)nullptr, HistPack{nullptr});
-  (void)rocprim::exclusive_scan(nullptr, b1, hin, (uint64_t *)nullptr, (uint64_t)0,
-                                (size_t)n_clusters + 1, rocprim::plus<uint64_t>());
-  const ListWorkInput win(rocprim::counting_iterator<int64_t>(0), ListWork{nullptr, nullptr});
-  (void)rocprim::exclusive_scan(nullptr, b2, win, (uint64_t *)nullptr, (uint64_t)0,
-                                work_scan_size(n_clusters, pair_slots), rocprim::plus<uint64_t>());
-  return b1 > b2 ? b1 : b2;
-}
-
 hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
-  const int64_t nc1 = a.n_clusters + 1;
   hipError_t e = launch_fill_i32(a.scnt, a.nq, 0, s);
   if (e == hipSuccess) e = launch_fill_i32(a.flag, a.nq, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)(a.wstats + 3), 6, 0, s);
@@ -215,21 +319,10 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.open_cnt, 2, 0, s);
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
   if (e != hipSuccess) return e;
-  size_t tmp = a.scan_tmp_bytes;
-  const HistPackInput hin(a.hist, HistPack{a.hist});
-  e = rocprim::exclusive_scan(a.scan_tmp, tmp, hin, a.hpos, (uint64_t)0, (size_t)nc1,
-                              rocprim::plus<uint64_t>(), s);
-  if (e != hipSuccess) return e;
-  int64_t blocks = (nc1 + 255) / 256;
-  if (blocks > 16384) blocks = 16384;
-  hipLaunchKernelGGL(k_shared_list, dim3((unsigned)blocks), dim3(256), 0, s, a);
-  tmp = a.scan_tmp_bytes;
-  const ListWorkInput win(rocprim::counting_iterator<int64_t>(0),
-                          ListWork{a.swork, a.hpos + a.n_clusters});
-  e = rocprim::exclusive_scan(a.scan_tmp, tmp, win, a.swork_off, (uint64_t)0,
-                              work_scan_size(a.n_clusters, a.nq * a.cap),
-                              rocprim::plus<uint64_t>(), s);
-  if (e != hipSuccess) return e;
+  const int64_t nblk = list_blocks(a.n_clusters);
+  hipLaunchKernelGGL(k_list_count, dim3((unsigned)nblk), dim3(LIST_THREADS), 0, s, a);
+  hipLaunchKernelGGL(k_list_scan, dim3(1), dim3(LIST_THREADS), 0, s, a, nblk);
+  hipLaunchKernelGGL(k_list_emit, dim3((unsigned)nblk), dim3(LIST_THREADS), 0, s, a);
   if (a.nq > 0)
     hipLaunchKernelGGL(k_pair_scatter, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
@@ -403,8 +496,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
   int32_t *runx = s_runx[w];
   uint32_t *ol = s_ol[w];
   uint32_t *olk = s_ok[w];
-  const int64_t NS = (int64_t)(a.hpos[a.n_clusters] >> 32);
-  const uint64_t W = a.swork_off[NS];
+  const int64_t NS = (int64_t)a.lmeta[0];
+  const uint64_t W = a.lmeta[2];
   const uint64_t ntiles = (W + SHARED_TILE - 1) / SHARED_TILE;
   const int rb = a.row_bytes;
   const int k = a.k;
@@ -451,8 +544,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
         l_wo = a.swork_off[ii];
         l_base = a.cl_off[c];
         l_sz = a.cl_off[(uint64_t)c + 1] - l_base;
-        l_hp = (uint32_t)a.hpos[c];
-        l_m = (uint32_t)a.hpos[(uint64_t)c + 1] - l_hp;
+        l_hp = a.lpair[ii];
+        l_m = a.lpm[ii];
       }
     };
     stage();
@@ -1186,17 +1279,18 @@ hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s) {
 
 // ------------------------------------------------------------------ diagnostics
 // rows of the shared clusters (each read once by the scan) -> out[0] and
-// rows scored by the scan summed over pairs -> out[2]
-__global__ void k_unique_rows(const uint64_t *hpos, const uint64_t *cl_off, int64_t n_clusters,
-                              int64_t *out) {
+// rows scored by the scan summed over pairs -> out[2], over the scan list
+__global__ void k_unique_rows(const uint32_t *slist, const uint32_t *lpm, const uint64_t *lmeta,
+                              const uint64_t *cl_off, int64_t *out) {
   __shared__ unsigned long long part[2][256];
   unsigned long long acc = 0, accp = 0;
+  const int64_t ns = (int64_t)lmeta[0];
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_clusters; c += stride) {
-    const uint32_t m = (uint32_t)hpos[c + 1] - (uint32_t)hpos[c];
-    const uint64_t sz = cl_off[c + 1] - cl_off[c];
-    if (m > 0) acc += sz;
-    accp += (uint64_t)m * sz;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < ns; i += stride) {
+    const uint32_t c = slist[i];
+    const uint64_t sz = cl_off[(uint64_t)c + 1] - cl_off[c];
+    acc += sz;
+    accp += (uint64_t)lpm[i] * sz;
   }
   part[0][threadIdx.x] = acc;
   part[1][threadIdx.x] = accp;
@@ -1214,9 +1308,9 @@ __global__ void k_unique_rows(const uint64_t *hpos, const uint64_t *cl_off, int6
   }
 }
 
-hipError_t launch_unique_rows(const uint64_t *hpos, const uint64_t *cl_off, int64_t n_clusters,
-                              int64_t *out, hipStream_t s) {
-  hipLaunchKernelGGL(k_unique_rows, dim3(1024), dim3(256), 0, s, hpos, cl_off, n_clusters, out);
+hipError_t launch_unique_rows(const uint32_t *slist, const uint32_t *lpm, const uint64_t *lmeta,
+                              const uint64_t *cl_off, int64_t *out, hipStream_t s) {
+  hipLaunchKernelGGL(k_unique_rows, dim3(1024), dim3(256), 0, s, slist, lpm, lmeta, cl_off, out);
   return hipGetLastError();
 }
 

@@ -82,13 +82,12 @@ struct Buffers {
   unsigned long long *counter2;
   uint32_t *skey;
   int64_t *sid;
-  uint32_t *pair_q, *hist, *pair_rank, *slist;
-  uint64_t *hpos;
+  uint32_t *pair_q, *hist, *pair_rank, *slist, *touched, *hpos, *lpair, *lpm;
+  uint32_t *thr_n, *thr_h, *blk_n, *blk_h;
+  uint64_t *thr_w, *blk_w, *lmeta;
   uint2 *qnorm;
-  uint64_t *swork, *swork_off;
+  uint64_t *swork_off;
   int64_t *wstats;
-  void *scan_tmp;
-  size_t scan_tmp_bytes;
   bool shared;
   hipStream_t aux;   // from the workspace
   hipEvent_t fork, join;
@@ -158,12 +157,20 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.pair_rank = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.qnorm = c.take<uint2>((size_t)s.nq);
     B.hist = c.take<uint32_t>(nc1);
-    B.hpos = c.take<uint64_t>(nc1);
+    B.touched = c.take<uint32_t>((size_t)nr::list_words(s.n_clusters));
+    B.hpos = c.take<uint32_t>(nc1);
     B.slist = c.take<uint32_t>(nc1);
-    B.swork = c.take<uint64_t>(nc1);
+    B.lpair = c.take<uint32_t>(nc1);
+    B.lpm = c.take<uint32_t>(nc1);
     B.swork_off = c.take<uint64_t>(nc1);
-    B.scan_tmp_bytes = nr::shared_scan_tmp_bytes(s.n_clusters, s.nq * s.cap);
-    B.scan_tmp = c.take<char>(B.scan_tmp_bytes);
+    B.lmeta = c.take<uint64_t>(4);
+    const size_t nblk = (size_t)nr::list_blocks(s.n_clusters);
+    B.thr_n = c.take<uint32_t>(nblk * nr::LIST_THREADS);
+    B.thr_h = c.take<uint32_t>(nblk * nr::LIST_THREADS);
+    B.thr_w = c.take<uint64_t>(nblk * nr::LIST_THREADS);
+    B.blk_n = c.take<uint32_t>(nblk);
+    B.blk_h = c.take<uint32_t>(nblk);
+    B.blk_w = c.take<uint64_t>(nblk);
   }
   *bytes = align_up(c.off, 256);
   return B;
@@ -179,6 +186,10 @@ struct Workspace {
   Buffers last{};
   int64_t last_nq = 0;
   int64_t last_cap = 0;
+  // the shared schedule's pair counts and cluster bitmap are all zero at
+  // this address of hist (each search's prep clears what it used); any other
+  // carving of the workspace may overwrite them, so it resets this
+  const uint32_t *clean_hist = nullptr;
 };
 
 struct EventSet {
@@ -187,12 +198,14 @@ struct EventSet {
 
 }  // namespace
 
+
 struct nr_index {
   nr_index_desc d;               // scalars and borrowed device pointers
   std::vector<int32_t> widths;
   float *params = nullptr;       // device copy of all layers
   std::vector<const float *> W, bias, bn_scale, bn_shift;
   float *tau = nullptr;
+  uint32_t *row_of_id = nullptr;  // inverse permutation, made by the first calibration
   int maxw = 0;
   int n_cu = 0;
   std::mutex mu;
@@ -232,6 +245,7 @@ nr_status workspace_for(nr_index *ix, hipStream_t stream, const Shape &s, Buffer
       return fail(NR_ENOMEM, "workspace allocation of %zu bytes failed", grow);
     }
     w->bytes = grow;
+    w->clean_hist = nullptr;
   }
   if (s.shared && !w->aux) {
     HIP_OK(hipStreamCreateWithFlags(&w->aux, hipStreamNonBlocking));
@@ -240,6 +254,7 @@ nr_status workspace_for(nr_index *ix, hipStream_t stream, const Shape &s, Buffer
   }
   size_t dummy;
   *out = carve(w->base, s, &dummy);
+  if (!s.shared || out->hist != w->clean_hist) w->clean_hist = nullptr;
   out->aux = w->aux;
   out->fork = w->fork;
   out->join = w->join;
@@ -547,13 +562,22 @@ nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q
   a.own_dists = B.own_dists;
   a.own_rows = B.own_rows;
   a.hist = B.hist;
+  a.touched = B.touched;
   a.hpos = B.hpos;
   a.pair_rank = B.pair_rank;
   a.slist = B.slist;
+  a.lpair = B.lpair;
+  a.lpm = B.lpm;
+  a.lmeta = B.lmeta;
+  a.thr_n = B.thr_n;
+  a.thr_h = B.thr_h;
+  a.thr_w = B.thr_w;
+  a.blk_n = B.blk_n;
+  a.blk_h = B.blk_h;
+  a.blk_w = B.blk_w;
   // the per-query rows of the whole list are diagnostics: taken here only
   // when the caller asked for per-query statistics
   a.eager_rows = qstats != nullptr;
-  a.swork = B.swork;
   a.swork_off = B.swork_off;
   a.pair_q = B.pair_q;
   a.qnorm = B.qnorm;
@@ -575,8 +599,6 @@ nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q
   a.open_row = B.open_row;
   a.counter = B.counter2;
   a.wstats = B.wstats;
-  a.scan_tmp = B.scan_tmp;
-  a.scan_tmp_bytes = B.scan_tmp_bytes;
   a.out_ids = out_ids;
   a.out_dists = out_dists;
   a.qstats = qstats;
@@ -792,6 +814,7 @@ nr_status nr_index_free(nr_index *ix) {
     for (auto &ev : es.ev) (void)hipEventDestroy(ev);
   if (ix->params) (void)hipFree(ix->params);
   if (ix->tau) (void)hipFree(ix->tau);
+  if (ix->row_of_id) (void)hipFree(ix->row_of_id);
   delete ix;
   return NR_OK;
 }
@@ -925,7 +948,10 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
       sa = shared_args(ix, p, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
                        out_dists + q0 * k, qs);
       ph = nr::pair_hist_args(sa);
-      HIP_OK(nr::launch_shared_hist(sa, stream));  // zero the pair counts
+      // pair counts and bitmap start at zero: cleared in full only for a new
+      // workspace (or after a search that stopped early), else by the last prep
+      HIP_OK(nr::launch_shared_hist(sa, w->clean_hist != B.hist, stream));
+      w->clean_hist = nullptr;
     }
     HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, qs, stream,
                      B.shared ? &ph : nullptr));
@@ -933,6 +959,7 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
     if (B.shared) {
       HIP_OK(run_refine_shared(ix, sa, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
                                out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr));
+      w->clean_hist = B.hist;
     } else {
       HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
                         out_dists + q0 * k, qs, stream, prof ? &es.ev[4] : nullptr));
@@ -953,6 +980,79 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
 nr_status nr_search(const nr_index *ix, const void *queries, int64_t nq, int32_t k, int32_t P,
                     const nr_params *p, int64_t *out_ids, float *out_dists, hipStream_t stream) {
   return nr_search_ex(ix, queries, nullptr, nq, k, P, p, out_ids, out_dists, nullptr, stream);
+}
+
+nr_status nr_calibrate(const nr_index *cix, const float *logits, int64_t nq,
+                       const int64_t *target_ids, int32_t K, int32_t l_sel, int32_t r_max,
+                       float *scores, float *margin_xy, hipStream_t stream) {
+  nr_index *ix = const_cast<nr_index *>(cix);
+  if (nr_status s = check_index(ix)) return s;
+  if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
+  if (K < 1 || K > NR_MAX_K) return fail(NR_EUNSUPPORTED, "K must be in [1, %d]", NR_MAX_K);
+  if (l_sel < 0 || l_sel > ix->d.b || l_sel > 32)
+    return fail(NR_EINVAL, "l_sel %d outside [0, min(b=%d, 32)]", l_sel, ix->d.b);
+  if (r_max < 0) return fail(NR_EINVAL, "r_max must be >= 0");
+  if (nq == 0) return NR_OK;
+  if (!logits || !target_ids || !scores || !margin_xy) return fail(NR_EINVAL, "NULL buffer");
+  {
+    std::lock_guard<std::mutex> g(ix->mu);
+    if (!ix->row_of_id) {
+      if (hipMalloc(&ix->row_of_id, sizeof(uint32_t) * (size_t)ix->d.n) != hipSuccess) {
+        (void)hipGetLastError();
+        ix->row_of_id = nullptr;
+        return fail(NR_ENOMEM, "inverse permutation (%lld rows) could not be allocated",
+                    (long long)ix->d.n);
+      }
+      HIP_OK(nr::launch_inverse_perm(ix->d.row_ids, ix->d.n, ix->row_of_id, stream));
+    }
+  }
+  nr::CalibArgs a{};
+  a.logits = logits;
+  a.tau = ix->tau;
+  a.nq = nq;
+  a.n = ix->d.n;
+  a.b = ix->d.b;
+  a.l_sel = l_sel;
+  a.r_max = r_max;
+  a.K = K;
+  a.targets = target_ids;
+  a.row_of_id = ix->row_of_id;
+  a.cl_off = ix->d.cl_off;
+  a.n_clusters = ix->d.n_clusters;
+  a.n_codes = (int64_t)1 << ix->d.b;
+  a.bc_off = ix->d.bc_off;
+  a.centroids = ix->d.centroids;
+  a.scores = scores;
+  a.xy = margin_xy;
+  HIP_OK(nr::launch_calib(a, stream));
+  return NR_OK;
+}
+
+size_t nr_pair_sqdist_ws(int64_t B, int32_t D) {
+  return B > 0 && D > 0 ? nr::pair_sqdist_ws_floats(B, D) : 0;
+}
+
+nr_status nr_pair_sqdist(const float *x, int64_t B, int32_t D, float *ws, float *out,
+                         hipStream_t stream) {
+  if (B < 0 || D < 1) return fail(NR_EINVAL, "B must be >= 0 and D >= 1");
+  if (B > 65536) return fail(NR_EUNSUPPORTED, "B %lld > 65536", (long long)B);
+  if (B == 0) return NR_OK;
+  if (!x || !ws || !out) return fail(NR_EINVAL, "NULL buffer");
+  HIP_OK(nr::launch_pair_sqdist(x, B, D, ws, out, stream));
+  return NR_OK;
+}
+
+nr_status nr_lsim_grad(const float *d2_emb, const float *lat, int64_t B, int32_t L,
+                       float gamma_rho, float tau_emb, double *num_cnt, float *grad_lat,
+                       hipStream_t stream) {
+  if (B < 0 || L < 1) return fail(NR_EINVAL, "B must be >= 0 and L >= 1");
+  if (L > 32) return fail(NR_EUNSUPPORTED, "L %d > 32", L);
+  if (B > 65536) return fail(NR_EUNSUPPORTED, "B %lld > 65536", (long long)B);
+  if (!std::isfinite(gamma_rho) || !std::isfinite(tau_emb))
+    return fail(NR_EINVAL, "gamma_rho and tau_emb must be finite");
+  if (!d2_emb || !lat || !num_cnt || !grad_lat) return fail(NR_EINVAL, "NULL buffer");
+  HIP_OK(nr::launch_lsim_grad(d2_emb, lat, B, L, gamma_rho, tau_emb, num_cnt, grad_lat, stream));
+  return NR_OK;
 }
 
 nr_status nr_profile_enable(nr_index *ix, int32_t on) {
@@ -1000,7 +1100,7 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
   if (B.shared) {
     HIP_OK(nr::launch_fill_i32((int32_t *)B.wstats, 2, 0, stream));      // wstats[0]
     HIP_OK(nr::launch_fill_i32((int32_t *)(B.wstats + 2), 2, 0, stream));  // wstats[2]
-    HIP_OK(nr::launch_unique_rows(B.hpos, ix->d.cl_off, ix->d.n_clusters, B.wstats, stream));
+    HIP_OK(nr::launch_unique_rows(B.slist, B.lpm, B.lmeta, ix->d.cl_off, B.wstats, stream));
     HIP_OK(nr::launch_list_rows(B.clus, B.nclus, w->last_cap, (int64_t)nq, ix->d.cl_off,
                                 ix->d.n_clusters, B.rfull, stream));
   }
@@ -1016,9 +1116,9 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
   v[NR_WORK_OWN_ROWS] = v[NR_WORK_ROWS];
   if (B.shared) {
     int64_t ws[6] = {0, 0, 0, 0, 0, 0};  // the first six counters
-    uint32_t pairs = 0;
+    uint64_t pairs = 0;
     HIP_OK(hipMemcpy(ws, B.wstats, sizeof(ws), hipMemcpyDeviceToHost));
-    HIP_OK(hipMemcpy(&pairs, B.hpos + ix->d.n_clusters, 4, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(&pairs, B.lmeta + 1, 8, hipMemcpyDeviceToHost));
     std::vector<uint32_t> own(nq);
     std::vector<int32_t> flag(nq), scnt(nq);
     HIP_OK(hipMemcpy(own.data(), B.own_rows, 4 * nq, hipMemcpyDeviceToHost));
@@ -1035,7 +1135,7 @@ nr_status nr_last_work(nr_index *ix, hipStream_t stream, int64_t *work, int32_t 
       }
     }
     v[NR_WORK_SHARED_ROWS] = ws[0];
-    v[NR_WORK_SHARED_PAIRS] = pairs;
+    v[NR_WORK_SHARED_PAIRS] = (int64_t)pairs;
     v[NR_WORK_SHARED_PAIR_ROWS] = ws[2];
     v[NR_WORK_FULL_ROWS] = ws[3];
     v[NR_WORK_BODY_BYTES] = ws[4];

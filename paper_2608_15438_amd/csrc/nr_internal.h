@@ -46,6 +46,15 @@ constexpr int SHARED_G = 8;               // queries scored per shared work unit
 constexpr int SHARED_MAX_NSEG = 48;       // rows of at most 48 x 128 bytes use the shared scan
 constexpr uint32_t SHARED_ROWS = 2048;    // rows per shared work unit (at most)
 constexpr int MAX_KC = 16384;             // top-K_c heap held in LDS
+// the shared schedule's scan-list build: LIST_WPT bitmap words per thread
+constexpr int LIST_WPT = 8;
+constexpr int LIST_THREADS = 256;
+__host__ __device__ inline int64_t list_words(int64_t n_clusters) { return (n_clusters + 31) / 32; }
+__host__ __device__ inline int64_t list_blocks(int64_t n_clusters) {
+  const int64_t per = (int64_t)LIST_WPT * LIST_THREADS;
+  const int64_t b = (list_words(n_clusters) + per - 1) / per;
+  return b > 0 ? b : 1;
+}
 
 // ---------------------------------------------------------------- kernels
 // Addressing of the permuted payload: bytes [0, h) of row r at hb + r * hs,
@@ -88,9 +97,26 @@ struct ProbeArgs {
   int32_t *counts;       // [nq]
 };
 
+// calibration (k_calib.hip): bucket scores of the targets and margin points
+struct CalibArgs {
+  const float *logits;          // [nq x b]
+  const float *tau;             // [b]
+  int64_t nq, n;
+  int b, l_sel, r_max, K;
+  const int64_t *targets;       // [nq x K] original ids, < 0: none
+  const uint32_t *row_of_id;    // [n] permuted row of each original id
+  const uint64_t *cl_off;       // [n_clusters + 1]
+  int64_t n_clusters, n_codes;  // n_codes = 2^b
+  const uint32_t *bc_off;       // [n_codes + 1]
+  const float *centroids;       // [n_clusters x b]
+  float *scores;                // [nq x K]
+  float *xy;                    // [nq x 2]
+};
+
 // per-query pair counting of the shared schedule (see pair_hist_wave)
 struct PairHistArgs {
   uint32_t *hist;               // [n_clusters + 1] pairs per cluster past the leading clusters
+  uint32_t *touched;            // [ceil(n_clusters / 32)] bit c: cluster c has pairs
   const uint64_t *cl_off;
   int64_t n_clusters;
   uint32_t seed_min;            // rows the leading clusters cover at least
@@ -215,13 +241,18 @@ struct SharedArgs {
   const float *own_dists;
   uint32_t *own_rows;         // [nq] copy of rtot kept for diagnostics
   uint32_t *hist;             // [n_clusters + 1] pairs per cluster past the leading clusters
+  uint32_t *touched;          // [list_words] bit c: cluster c has pairs
   uint32_t *pair_rank;        // [nq x cap] rank of each counted pair among its cluster's pairs
-  uint64_t *hpos;             // [n_clusters + 1] exclusive scan over clusters: pairs before
-                              // (low half, the cluster's start in pair_q) and clusters with
-                              // pairs before (high half, its scan-list position)
-  uint32_t *slist;            // [n_clusters] scanned clusters (those with pairs) in cluster order
-  uint64_t *swork;            // [list] rows x query groups of slist[i]
-  uint64_t *swork_off;        // [list + 1] exclusive scan of swork
+  uint32_t *hpos;             // [n_clusters] start of cluster c's pairs in pair_q (clusters
+                              // with pairs only)
+  uint32_t *slist;            // [n_clusters] the scan list: clusters with pairs, in order
+  uint32_t *lpair, *lpm;      // [list] start in pair_q and number of pairs of entry i
+  uint64_t *swork_off;        // [list + 1] start of entry i in the work space
+  uint64_t *lmeta;            // [4] list length, pairs, work
+  uint32_t *thr_n, *thr_h;    // [list_blocks x LIST_THREADS] per-thread sums of the prep
+  uint64_t *thr_w;
+  uint32_t *blk_n, *blk_h;    // [list_blocks] per-block sums, then their offsets
+  uint64_t *blk_w;
   int eager_rows;             // 1: rfull gets the rows of the whole list (else the leading ones)
   uint32_t *pair_q;           // [pairs] query of each scanned pair, grouped by cluster
   uint2 *qnorm;               // [nq] uint8 rows: (|q|^2, |q head|^2 over scan_head bytes)
@@ -243,8 +274,6 @@ struct SharedArgs {
   int64_t *wstats;            // [7] scanned rows, seed tiles, scanned pair rows, rows read
                               // past their heads, bytes the scan read from them, row
                               // bytes of the open-pair pass, row bytes of k_refine
-  void *scan_tmp;
-  size_t scan_tmp_bytes;
   int64_t *out_ids;
   float *out_dists;
   int32_t *qstats;
@@ -260,20 +289,30 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
-size_t shared_scan_tmp_bytes(int64_t n_clusters, int64_t pair_slots);
-hipError_t launch_shared_hist(const SharedArgs &a, hipStream_t s);
+// fresh: the workspace is new, so clear the pair counts and the bitmap
+hipError_t launch_shared_hist(const SharedArgs &a, bool fresh, hipStream_t s);
 PairHistArgs pair_hist_args(const SharedArgs &a);
 hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s);
 hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStream_t s);
 // the open pairs' remaining slabs (fp32 rows past 1 KB; a no-op otherwise)
 hipError_t launch_scan_open(const SharedArgs &a, int dtype, int n_cu, hipStream_t s);
 hipError_t launch_shared_merge(const SharedArgs &a, hipStream_t s);
-hipError_t launch_unique_rows(const uint64_t *hpos, const uint64_t *cl_off, int64_t n_clusters,
-                              int64_t *out, hipStream_t s);
+hipError_t launch_unique_rows(const uint32_t *slist, const uint32_t *lpm, const uint64_t *lmeta,
+                              const uint64_t *cl_off, int64_t *out, hipStream_t s);
 hipError_t launch_list_rows(const uint32_t *clus, const int32_t *nclus, int64_t cap, int64_t nq,
                             const uint64_t *cl_off, int64_t n_clusters, uint32_t *rows,
                             hipStream_t s);
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+
+hipError_t launch_inverse_perm(const int64_t *row_ids, int64_t n, uint32_t *row_of_id,
+                               hipStream_t s);
+hipError_t launch_calib(const CalibArgs &a, hipStream_t s);
+// L_sim training (k_lsim.hip)
+size_t pair_sqdist_ws_floats(int64_t B, int D);
+hipError_t launch_pair_sqdist(const float *x, int64_t B, int D, float *ws, float *out,
+                              hipStream_t s);
+hipError_t launch_lsim_grad(const float *d2, const float *lat, int64_t B, int L, float gr,
+                            float tau, double *num_cnt, float *grad, hipStream_t s);
 
 hipError_t launch_stream_read(const void *buf, int64_t bytes, uint32_t *sink, int n_cu,
                               hipStream_t s);
@@ -367,7 +406,8 @@ __device__ __forceinline__ int lower_bound_u64(const uint64_t *a, int n, uint64_
 // One wave, query q with list cl[0..n): the leading clusters covering at
 // least seed_min rows stay with the query (cseed[q]); every later (cluster,
 // query) pair is counted in hist (its rank among the cluster's pairs goes to
-// pair_rank); rfull[q] gets the rows of the leading
+// pair_rank; the first pair of a cluster sets its bit in touched); rfull[q]
+// gets the rows of the leading
 // clusters (of the whole list with eager_rows); for uint8 rows qnorm[q] gets
 // |q|^2 and the part of it over the scan's head.
 __device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const uint32_t *cl, int n) {
@@ -398,7 +438,11 @@ __device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const ui
       }
       run += bcast_u64(incl, upto);
     }
-    if (cs >= 0 && i >= cs && c < h.n_clusters) h.pair_rank[q * h.cap + i] = atomicAdd(&h.hist[c], 1u);
+    if (cs >= 0 && i >= cs && c < h.n_clusters) {
+      const uint32_t r = atomicAdd(&h.hist[c], 1u);
+      h.pair_rank[q * h.cap + i] = r;
+      if (r == 0) atomicOr(&h.touched[c >> 5], 1u << (c & 31));  // the cluster's first pair
+    }
   }
   if (lane == 0) {
     h.cseed[q] = cs < 0 ? n : cs;

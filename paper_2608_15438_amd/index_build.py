@@ -210,6 +210,16 @@ def _segment_ids(sizes: torch.Tensor) -> torch.Tensor:
     return torch.repeat_interleave(torch.arange(len(sizes), device=sizes.device), sizes)
 
 
+def sqdist_rows(A: torch.Tensor, Bm: torch.Tensor) -> torch.Tensor:
+    """fp64 squared distances of matching rows, the dimensions added in
+    order (a fixed order: the HIP builder adds them the same way)."""
+    acc = torch.zeros(A.shape[0], dtype=torch.float64, device=A.device)
+    for j in range(A.shape[1]):
+        t = A[:, j] - Bm[:, j]
+        acc = acc + t * t
+    return acc
+
+
 def _pair_argmin(X, seg_of_pt, cent, cent_start, K, chunk=1 << 22):
     """For each point p: argmin_j ||X[p] - cent[cent_start[g] + j]||^2 over its
     group's K[g] centroids (lowest j on ties)."""
@@ -229,7 +239,7 @@ def _pair_argmin(X, seg_of_pt, cent, cent_start, K, chunk=1 << 22):
         first = torch.cumsum(kp, 0) - kp
         j = torch.arange(len(pid), device=X.device) - torch.repeat_interleave(first, kp)
         cid = cent_start[seg_of_pt[pid]] + j
-        d = ((X[pid] - cent[cid]) ** 2).sum(dim=1)
+        d = sqdist_rows(X[pid], cent[cid])
         # segment argmin: min distance then lowest j
         best = torch.full((end - start,), float("inf"), dtype=d.dtype, device=X.device)
         best.scatter_reduce_(0, pid - start, d, reduce="amin", include_self=True)
@@ -253,24 +263,45 @@ def mix32(x: torch.Tensor, seed: int) -> torch.Tensor:
     return (h >> 16) ^ h
 
 
+# D^2 weights of the k-means++ draws are integers: floor(D^2 * 2^WEIGHT_BITS),
+# capped at 2^WEIGHT_CAP_BITS, so that their sums are exact and a group's
+# total (at most SAMPLE_CAP members) stays below 2^53
+WEIGHT_BITS = 20
+WEIGHT_CAP_BITS = 30
+SAMPLE_CAP = 1 << 21
+
+
+def d2_weights(D2: torch.Tensor) -> torch.Tensor:
+    w = torch.floor(D2 * float(1 << WEIGHT_BITS))
+    return torch.clamp(w, max=float(1 << WEIGHT_CAP_BITS)).to(torch.int64)
+
+
 def bucket_kmeans(X: torch.Tensor, sizes: torch.Tensor, K: torch.Tensor, seed: int,
-                  group_keys: torch.Tensor):
+                  group_keys: torch.Tensor, ids: torch.Tensor):
     """k-means++ on a sample then N_LLOYD Lloyd passes, independently per group.
 
-    X: fp64 points sorted by group (contiguous); sizes[g], K[g] >= 2.
+    X: fp64 points sorted by (group, original id), ids their original ids;
+    sizes[g], K[g] >= 2.  The sample of a group is its first
+    min(|g|, 64 K[g]) members ordered by (mix32(id, seed), id); k-means++
+    starts from the first of them and draws each further centre with
+    probability proportional to its integer D^2 weight, using the group's
+    pre-drawn uniform U (cumulative weights in sample order, the first member
+    whose running sum exceeds floor(U * total)).  Every sum here is either
+    exact (integers) or taken in a fixed order, so the HIP builder, which
+    follows the same steps, gets the same clusters.
     Returns (labels per point in [0, K[g]), centroids fp64 [sum K, dim],
     kept mask per centroid: clusters left empty after the last pass are dropped).
     """
     dev = X.device
-    ng = len(sizes)
     seg = _segment_ids(sizes)
     starts = torch.cumsum(sizes, 0) - sizes
     cstart = torch.cumsum(K, 0) - K
     dim = X.shape[1]
     # seeded shuffle inside each group: the sample is the first S_g members
-    h = mix32(torch.arange(X.shape[0], device=dev, dtype=torch.int64), seed)
+    h = mix32(ids.to(torch.int64), seed)
     order = torch.sort(seg * (1 << 32) + h, stable=True).indices
-    S = torch.minimum(sizes, K * SAMPLE_PER_CLUSTER)
+    S = torch.minimum(torch.minimum(sizes, K * SAMPLE_PER_CLUSTER),
+                      torch.full_like(sizes, SAMPLE_CAP))
     pos_in_group = torch.arange(X.shape[0], device=dev) - starts[seg]
     in_sample = pos_in_group < S[seg]
     samp = order[in_sample]                    # point indices, grouped, shuffled
@@ -283,15 +314,16 @@ def bucket_kmeans(X: torch.Tensor, sizes: torch.Tensor, K: torch.Tensor, seed: i
                         dtype=torch.float64, device=dev)
     cent = torch.zeros((int(K.sum()), dim), dtype=torch.float64, device=dev)
     cent[cstart] = Xs[sstart]                  # first centre: first sampled member
-    D2 = ((Xs - cent[cstart][sseg]) ** 2).sum(dim=1)
+    D2 = sqdist_rows(Xs, cent[cstart][sseg])
     for r in range(1, kmax):
         act_g = K > r
         act_p = act_g[sseg]
-        w2 = torch.where(act_p, D2, torch.zeros_like(D2))
+        w2 = torch.where(act_p, d2_weights(D2), torch.zeros_like(D2, dtype=torch.int64))
         cs = torch.cumsum(w2, 0)
-        tot_before = torch.where(sstart > 0, cs[(sstart - 1).clamp_min(0)], torch.zeros_like(sstart, dtype=cs.dtype))
+        tot_before = torch.where(sstart > 0, cs[(sstart - 1).clamp_min(0)],
+                                 torch.zeros_like(sstart, dtype=cs.dtype))
         tot = cs[sstart + S - 1] - tot_before
-        target = tot_before + U[:, r] * tot
+        target = tot_before + torch.floor(U[:, r] * tot.to(torch.float64)).to(torch.int64)
         pick = torch.searchsorted(cs, target, right=True)
         pick = torch.minimum(torch.maximum(pick, sstart), sstart + S - 1)
         # all-zero weights (duplicate points): take the first sampled member
@@ -299,7 +331,7 @@ def bucket_kmeans(X: torch.Tensor, sizes: torch.Tensor, K: torch.Tensor, seed: i
         g_act = torch.nonzero(act_g).squeeze(1)
         cent[cstart[g_act] + r] = Xs[pick[g_act]]
         newc = cent[cstart[sseg] + torch.clamp(K[sseg] - 1, max=r)]
-        D2 = torch.where(act_p, torch.minimum(D2, ((Xs - newc) ** 2).sum(dim=1)), D2)
+        D2 = torch.where(act_p, torch.minimum(D2, sqdist_rows(Xs, newc)), D2)
     labels = None
     for _ in range(N_LLOYD):
         labels = _pair_argmin(X, seg, cent, cstart, K)
@@ -350,14 +382,17 @@ def _clusters_per_bucket(w: Workload, sizes: torch.Tensor) -> torch.Tensor:
 def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 20,
                 encoder: Optional[Encoder] = None, keep_codes: bool = True,
                 payload_fn: Optional[Callable] = None, log=None,
-                head_bytes: int = 0, head_copy: bool = False) -> Index:
+                head_bytes: int = 0, head_copy: bool = False,
+                logits_fn: Optional[Callable] = None) -> Index:
     """Build the index of workload ``w`` from ``rows_fn(ids) -> rows``.
 
     ``rows_fn`` returns numpy or torch rows for an int64 id array.  With
     ``payload_fn(perm) -> rows`` the permuted payload is produced directly
     (e.g. regenerated on the GPU) instead of gathered from ``rows_fn``.
     With ``head_bytes`` > 0 the payload starts with a head plane, followed by
-    the tails or (``head_copy``) by the whole rows.
+    the tails or (``head_copy``) by the whole rows.  ``logits_fn(ids)``, when
+    given, supplies the fp32 logits of rows (e.g. the search library's
+    encoder) in place of this module's fp64 forward pass.
     """
     dev = torch.device(device)
     enc = encoder or seeded_encoder(w)
@@ -371,6 +406,11 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
             r = torch.from_numpy(r)
         return r.to(dev)
 
+    def logits_of(ids):
+        if logits_fn is not None:
+            return torch.as_tensor(logits_fn(ids)).to(dev).to(torch.float32)
+        return fwd(rows_t(ids))
+
     say = log or (lambda *a: None)
     # (2) thresholds
     if w.tau_mode == "zero":
@@ -380,7 +420,7 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
         perm = tau_sample_ids(w.seed("sample"), n, ns)
         ls = []
         for s0 in range(0, len(perm), chunk):
-            ls.append(fwd(rows_t(perm[s0:s0 + chunk])))
+            ls.append(logits_of(perm[s0:s0 + chunk]))
         L = torch.cat(ls)
         tau = torch.sort(L, dim=0).values[(L.shape[0] - 1) // 2].contiguous()
     say("tau done")
@@ -390,7 +430,7 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
     sums = torch.zeros((nb, b), dtype=torch.float64, device=dev)
     for s0 in range(0, n, chunk):
         ids = np.arange(s0, min(n, s0 + chunk))
-        lg = fwd(rows_t(ids))
+        lg = logits_of(ids)
         c = _codes(lg, tau)
         codes[s0:s0 + len(ids)] = c
         sums.index_add_(0, c, lg.double())
@@ -416,10 +456,10 @@ def build_index(w: Workload, rows_fn: Callable, device="cpu", chunk: int = 1 << 
         mem_np = member.cpu().numpy()
         for s0 in range(0, len(mem_np), chunk):
             ids = mem_np[s0:s0 + chunk]
-            Xm[s0:s0 + len(ids)] = fwd(rows_t(ids)).double()
+            Xm[s0:s0 + len(ids)] = logits_of(ids).double()
         gsizes = sizes[multi]
         gK = KB[multi]
-        lab, cent, kept = bucket_kmeans(Xm, gsizes, gK, w.seed("sample"), multi)
+        lab, cent, kept = bucket_kmeans(Xm, gsizes, gK, w.seed("sample"), multi, member)
         # renumber kept clusters densely inside each bucket
         cstart = torch.cumsum(gK, 0) - gK
         gseg = _segment_ids(gK)

@@ -36,7 +36,8 @@ WORK = ("tiles", "rows", "rows_read", "own_rows", "shared_rows", "shared_pairs",
         "open_bytes", "refine_bytes")
 
 # every symbol include/neuroute.h declares
-EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_encode",
+EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex",
+           "nr_encode", "nr_calibrate", "nr_pair_sqdist_ws", "nr_pair_sqdist", "nr_lsim_grad",
            "nr_probe", "nr_route", "nr_route_capacity", "nr_refine", "nr_profile_enable",
            "nr_profile_read", "nr_last_work", "nr_stream_read", "nr_status_string",
            "nr_last_error")
@@ -94,6 +95,11 @@ def lib():
         L.nr_search_ex.argtypes = [P, P, P, C.c_int64, C.c_int32, C.c_int32, C.POINTER(nr_params),
                                    P, P, P, P]
         L.nr_encode.argtypes = [P, P, C.c_int64, P, P]
+        L.nr_pair_sqdist_ws.argtypes = [C.c_int64, C.c_int32]
+        L.nr_pair_sqdist_ws.restype = C.c_size_t
+        L.nr_pair_sqdist.argtypes = [P, C.c_int64, C.c_int32, P, P, P]
+        L.nr_lsim_grad.argtypes = [P, P, C.c_int64, C.c_int32, C.c_float, C.c_float, P, P, P]
+        L.nr_calibrate.argtypes = [P, P, C.c_int64, P, C.c_int32, C.c_int32, C.c_int32, P, P, P]
         L.nr_probe.argtypes = [P, P, C.c_int64, C.c_int32, C.POINTER(nr_params), P, P, P, P, P]
         L.nr_route.argtypes = [P, P, C.c_int64, C.c_int32, C.POINTER(nr_params), P, P, C.c_int64, P]
         L.nr_route_capacity.argtypes = [P, C.c_int32, C.POINTER(nr_params)]
@@ -106,6 +112,7 @@ def lib():
         for name in EXPORTS:
             getattr(L, name).restype = getattr(L, name).restype or C.c_int
         L.nr_route_capacity.restype = C.c_int64
+        L.nr_pair_sqdist_ws.restype = C.c_size_t
         L.nr_status_string.restype = C.c_char_p
         L.nr_last_error.restype = C.c_char_p
         _lib = L
@@ -153,6 +160,31 @@ def nr_stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None):
     _dev(buf, "buf")
     _check(lib().nr_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
                                 _stream(stream)), "nr_stream_read")
+
+
+def nr_pair_sqdist(x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """Squared distances [B, B] of the rows of x (fp32 [B, D], device)."""
+    _dev(x, "x")
+    B, D = x.shape
+    ws = torch.empty(int(lib().nr_pair_sqdist_ws(B, D)), dtype=torch.float32, device=x.device)
+    if out is None:
+        out = torch.empty((B, B), dtype=torch.float32, device=x.device)
+    _check(lib().nr_pair_sqdist(_ptr(x), B, D, _ptr(ws), _ptr(out), _stream(stream)),
+           "nr_pair_sqdist")
+    return out
+
+
+def nr_lsim_grad(d2_emb: torch.Tensor, lat: torch.Tensor, gamma_rho: float, tau_emb: float,
+                 stream=None):
+    """(num_cnt fp64 [2], grad_lat fp32 [B, L]) of L_sim for one batch."""
+    _dev(d2_emb, "d2_emb")
+    _dev(lat, "lat")
+    B, L = lat.shape
+    num_cnt = torch.empty(2, dtype=torch.float64, device=lat.device)
+    grad = torch.empty((B, L), dtype=torch.float32, device=lat.device)
+    _check(lib().nr_lsim_grad(_ptr(d2_emb), _ptr(lat), B, L, float(gamma_rho), float(tau_emb),
+                              _ptr(num_cnt), _ptr(grad), _stream(stream)), "nr_lsim_grad")
+    return num_cnt, grad
 
 
 # --------------------------------------------------------------------------
@@ -312,6 +344,18 @@ class Index:
         _check(lib().nr_encode(self.handle, _ptr(queries), queries.shape[0], _ptr(out),
                                _stream(stream)), "nr_encode")
         return out
+
+    def nr_calibrate(self, logits, target_ids, l_sel, r_max, stream=None):
+        """Bucket scores [nq, K] of the targets and margin points [nq, 2]."""
+        _dev(logits, "logits")
+        _dev(target_ids, "target_ids")
+        nq, K = target_ids.shape
+        scores = torch.empty((nq, K), dtype=torch.float32, device=logits.device)
+        xy = torch.empty((nq, 2), dtype=torch.float32, device=logits.device)
+        _check(lib().nr_calibrate(self.handle, _ptr(logits), nq, _ptr(target_ids), K, l_sel,
+                                  r_max, _ptr(scores), _ptr(xy), _stream(stream)),
+               "nr_calibrate")
+        return scores, xy
 
     def nr_probe(self, logits, probe_budget, params: Params, stream=None):
         _dev(logits, "logits")

@@ -1,6 +1,9 @@
 """Encoder training with the selective similarity loss L_sim (Sec. 3.2.2,
-Eq. similarityconfig and the mask of Eq. 8), untimed and on the GPU through
-PyTorch (its pairwise-distance products run as library GEMMs).
+Eq. similarityconfig and the mask of Eq. 8), untimed.  On the GPU the
+pairwise input distances run on the library's fp32 matrix-core kernel
+(nr_pair_sqdist) and the loss, mask and latent gradient in one fused pass
+over the pairs (nr_lsim_grad); the encoder's own layers are torch Linear
+modules.  lsim_loss below is the same loss in PyTorch (CPU checks).
 
 For a mini-batch of B rows x (scaled as the encoder sees them) and their
 latents l, with rho = sqrt(L_dim / E_dim):
@@ -53,6 +56,40 @@ def lsim_loss(x: torch.Tensor, lat: torch.Tensor, gamma: float, tau_emb: Optiona
     return loss, tau_emb, float(n) / (B * (B - 1))
 
 
+class _LsimGpu(torch.autograd.Function):
+    """L_sim of one batch from the fused kernel's (numerator, count) and
+    latent gradient; backward hands that gradient on (the mask held fixed)."""
+
+    @staticmethod
+    def forward(ctx, lat, num_cnt, grad):
+        cnt = num_cnt[1].clamp_min(1.0)
+        ctx.save_for_backward(grad, cnt)
+        return (num_cnt[0] / cnt).to(lat.dtype)
+
+    @staticmethod
+    def backward(ctx, g):
+        grad, cnt = ctx.saved_tensors
+        return (grad * (g / cnt)).to(grad.dtype), None, None
+
+
+def lsim_loss_gpu(x: torch.Tensor, lat: torch.Tensor, gamma: float,
+                  tau_emb: Optional[float] = None, quantile: float = 0.005):
+    """(L_sim, tau_emb used, mask fraction) of one batch on the library's
+    kernels; tau_emb defaults to the quantile of the off-diagonal input
+    distances (taken on their squares, the same order)."""
+    from . import neuroute as NR
+    B, E = x.shape
+    L = lat.shape[1]
+    gr = gamma * math.sqrt(L / E)
+    d2 = NR.nr_pair_sqdist(x.float().contiguous())
+    if tau_emb is None:
+        off = ~torch.eye(B, dtype=torch.bool, device=x.device)
+        tau_emb = math.sqrt(float(torch.quantile(d2[off][: 1 << 24], quantile)))
+    num_cnt, grad = NR.nr_lsim_grad(d2, lat.detach().float().contiguous(), gr, tau_emb)
+    loss = _LsimGpu.apply(lat, num_cnt, grad)
+    return loss, tau_emb, float(num_cnt[1]) / (B * (B - 1))
+
+
 class _Mlp(torch.nn.Module):
     """The encoder as trainable fp32 layers (ReLU between layers, the input
     scaled as at query time)."""
@@ -96,10 +133,12 @@ def train_encoder(enc: Encoder, rows_fn: Callable, n: int, steps: int, batch: in
         x = torch.as_tensor(rows_fn(ids.to(dev))).to(dev).float()
         xs = x * enc.input_scale
         lat = net(x)
-        loss, tau, frac = lsim_loss(xs, lat, gamma, tau_emb, quantile)
+        fn = lsim_loss_gpu if dev.type == "cuda" else lsim_loss
+        loss, tau, frac = fn(xs, lat, gamma, tau_emb, quantile)
         opt.zero_grad(set_to_none=True)
         loss.backward()
         opt.step()
         if log and (it % max(1, steps // 10) == 0 or it == steps - 1):
-            log(f"train step {it}: L_sim {float(loss):.5f}, tau_emb {tau:.4f}, mask {frac:.4%}")
+            log(f"train step {it}: L_sim {float(loss.detach()):.5f}, tau_emb {tau:.4f}, "
+                f"mask {frac:.4%}")
     return net.encoder(enc)

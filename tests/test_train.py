@@ -70,3 +70,76 @@ def test_training_lowers_the_loss():
     enc2 = TR.train_encoder(enc, rows, w.n, steps=30, batch=512, lr=2e-3, device="cpu")
     after = TR.lsim_loss(xb, TR._Mlp(enc2, "cpu")(X[:512]), 0.6, None)[0].item()
     assert after < before
+
+
+# ---------------------------------------------------------------- GPU kernels
+import pytest
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    return torch.device("cuda")
+
+
+def _batch(B, E, L, seed):
+    rng = np.random.default_rng(seed)
+    centres = rng.uniform(0, 160, size=(8, E))
+    x = np.clip(np.rint(centres[rng.integers(0, 8, B)] + 12 * rng.standard_normal((B, E))),
+                0, 255) / 255.0
+    lat = rng.standard_normal((B, L)) * 0.5
+    return x.astype(np.float32), lat.astype(np.float32)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("B,E", [(1, 16), (100, 128), (257, 96), (300, 1536)])
+def test_gpu_pair_sqdist(B, E):
+    """The matrix-core distances against fp64 differences: within 1e-5 of
+    the squared norm scale of the centred batch (the expansion's rounding)."""
+    dev = _gpu()
+    from paper_2608_15438_amd import neuroute as NR
+    x, _ = _batch(B, E, 4, B + E)
+    d2 = NR.nr_pair_sqdist(torch.from_numpy(x).to(dev)).cpu().numpy().astype(np.float64)
+    xd = x.astype(np.float64)
+    ref = ((xd[:, None, :] - xd[None, :, :]) ** 2).sum(2)
+    scale = ((xd - xd.mean(0)) ** 2).sum(1).max()
+    assert np.all(np.diag(d2) == 0)
+    assert np.abs(d2 - ref).max() <= 1e-5 * max(scale, 1e-12)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("B,E,L", [(64, 128, 16), (200, 128, 24), (333, 96, 20)])
+def test_gpu_lsim_against_oracle(B, E, L):
+    """Loss of the fused kernel against the oracle's fp64 loops within 1e-4
+    (relative), at a tau_emb that no pair lies within 1e-3 of; its latent
+    gradient against PyTorch autograd of the GEMM-form loss in fp64."""
+    dev = _gpu()
+    x, lat = _batch(B, E, L, 7 * B)
+    g = 0.6
+    rho = math.sqrt(L / E)
+    xd = x.astype(np.float64)
+    se = np.sqrt(((xd[:, None, :] - xd[None, :, :]) ** 2).sum(2))
+    ld = lat.astype(np.float64)
+    sl = np.sqrt(((ld[:, None, :] - ld[None, :, :]) ** 2).sum(2))
+    off = ~np.eye(B, dtype=bool)
+    tau = float(np.quantile(se[off], 0.02))
+    # move tau into a gap of both thresholds' distance sets
+    for _ in range(200):
+        near = (np.abs(se[off] - tau) <= 1e-3 * tau).any() or \
+               (np.abs(sl[off] - g * rho * tau) <= 1e-3 * g * rho * tau).any()
+        if not near:
+            break
+        tau *= 1.0007
+    assert not near
+    exp = O.lsim(xd, ld, g, tau)
+    xt = torch.from_numpy(x).to(dev)
+    lt = torch.from_numpy(lat).to(dev).requires_grad_(True)
+    loss, _, frac = TR.lsim_loss_gpu(xt, lt, g, tau)
+    assert abs(float(loss) - exp) <= 1e-4 * abs(exp)
+    loss.backward()
+    lt64 = torch.from_numpy(ld).requires_grad_(True)
+    ref, _, _ = TR.lsim_loss(torch.from_numpy(xd), lt64, g, tau)
+    ref.backward()
+    gref = lt64.grad.numpy()
+    got = lt.grad.cpu().numpy().astype(np.float64)
+    assert np.abs(got - gref).max() <= 1e-4 * np.abs(gref).max()
