@@ -198,6 +198,25 @@ nr_status nr_search_ex(const nr_index *index, const void *queries, const float *
                        int64_t nq, int32_t k, int32_t probe_budget, const nr_params *params,
                        int64_t *out_ids, float *out_dists, int32_t *qstats, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the search
+ * of nr_search_ex (logits optional, no per-query counters) without any
+ * allocation.  Its working buffers live in one fixed device array of
+ * NR_NOALLOC_SCRATCH_BYTES per GPU, which the library maps when it first
+ * uploads an index on that GPU and which stays held until the process ends.
+ * The batch runs in chunks of as many queries as that array holds (about
+ * 1,500 at P = 304, K_c = 3000, k = 10); refinement always uses the
+ * per-query schedule, whatever params->refine_mode says (every schedule
+ * returns the same lists).  All calls on one GPU share the array and it keeps
+ * the last call's contents: calls that overlap in time on one GPU (other
+ * streams or threads) race, so the caller must serialise them.  Returns
+ * NR_EUNSUPPORTED when one query's buffers would not fit in the array.  Not
+ * covered by nr_last_work or the stage timers. */
+#define NR_NOALLOC_SCRATCH_BYTES (64u << 20)
+nr_status nr_search_noalloc(const nr_index *index, const void *queries, const float *logits,
+                            int64_t nq, int32_t k, int32_t probe_budget, const nr_params *params,
+                            int64_t *out_ids, float *out_dists, hipStream_t stream);
+
 /* Step 1 only: logits DEVICE fp32 [nq x b]. */
 nr_status nr_encode(const nr_index *index, const void *queries, int64_t nq, float *logits,
                     hipStream_t stream);

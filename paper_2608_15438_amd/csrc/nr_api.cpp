@@ -198,6 +198,37 @@ struct EventSet {
 
 }  // namespace
 
+// Working memory of nr_search_noalloc: one fixed array per GPU, part of the
+// library's code object, held until the process ends.  Host code never uses
+// the name itself (on the host it is only a stand-in for the symbol): the
+// device address comes from hipGetSymbolAddress, per device.
+static __device__ __align__(256) unsigned char scratch[NR_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+char *g_scratch[MAX_DEVICES] = {};
+
+// The address of `scratch` on the current device `dev`, looked up once per
+// device (the library's index upload does it first).
+nr_status scratch_address(int dev, char **out) {
+  if (dev < 0 || dev >= MAX_DEVICES)
+    return fail(NR_EUNSUPPORTED, "device ordinal %d outside [0, %d)", dev, MAX_DEVICES);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(NR_EDEVICE, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev,
+                  hipGetErrorString(e));
+    g_scratch[dev] = static_cast<char *>(p);
+  }
+  *out = g_scratch[dev];
+  return NR_OK;
+}
+
+}  // namespace
 
 struct nr_index {
   nr_index_desc d;               // scalars and borrowed device pointers
@@ -770,6 +801,10 @@ nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&ix->n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return cleanup(fail(NR_EDEVICE, "device query failed"));
+  {  // the no-alloc entry point's array on this device
+    char *sp = nullptr;
+    if (nr_status st = scratch_address(dev, &sp)) return cleanup(st);
+  }
   // validate the borrowed CSR arrays and the permutation
   uint32_t *bitmap = nullptr;
   int32_t *flags = nullptr;
@@ -974,6 +1009,58 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
   w->last = B;
   w->last_nq = nq - (nq - 1) / sh.nq * sh.nq;
   w->last_cap = cap;
+  return NR_OK;
+}
+
+nr_status nr_search_noalloc(const nr_index *cix, const void *queries, const float *logits,
+                            int64_t nq, int32_t k, int32_t P, const nr_params *p,
+                            int64_t *out_ids, float *out_dists, hipStream_t stream) {
+  const nr_index *ix = cix;
+  if (nr_status s = check_index(ix)) return s;
+  if (nr_status s = check_params(ix, P, p)) return s;
+  if (k < 1) return fail(NR_EINVAL, "k must be >= 1");
+  if (k > NR_MAX_K) return fail(NR_EUNSUPPORTED, "k %d > %d", k, NR_MAX_K);
+  if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
+  if (nq == 0) return NR_OK;
+  if (!queries || !out_ids || !out_dists) return fail(NR_EINVAL, "NULL buffer");
+  int dev = 0;
+  HIP_OK(hipGetDevice(&dev));
+  char *base = nullptr;
+  if (nr_status s = scratch_address(dev, &base)) return s;
+  const int64_t cap = nr_route_capacity(ix, P, p);
+  // the largest chunk of queries whose buffers fit in the array (the carved
+  // size grows by a fixed amount per query, up to 256-byte alignment per buffer)
+  auto need = [&](int64_t nqc) {
+    Shape sh = shape_of(ix, nqc, P, k, cap);
+    sh.nq = nqc;
+    size_t bytes = 0;
+    carve(nullptr, sh, &bytes);
+    return bytes;
+  };
+  const size_t limit = NR_NOALLOC_SCRATCH_BYTES;
+  if (need(1) > limit)
+    return fail(NR_EUNSUPPORTED, "one query needs %zu bytes of working memory, more than the "
+                                 "%zu-byte no-alloc array", need(1), limit);
+  const size_t per = need(2) - need(1);
+  int64_t chunk = per ? (int64_t)((limit - need(1)) / per) + 1 : nr::QUERY_CHUNK;
+  if (chunk > nr::QUERY_CHUNK) chunk = nr::QUERY_CHUNK;
+  if (chunk > nq) chunk = nq;
+  while (chunk > 1 && need(chunk) > limit) --chunk;
+  Shape sh = shape_of(ix, chunk, P, k, cap);
+  sh.nq = chunk;
+  size_t used = 0;
+  Buffers B = carve(base, sh, &used);
+  const size_t qrow = ix->d.d * elem_size(ix);
+  for (int64_t q0 = 0; q0 < nq; q0 += chunk) {
+    const int64_t n = nq - q0 < chunk ? nq - q0 : chunk;
+    const void *qp = (const char *)queries + q0 * qrow;
+    const float *lg = logits ? logits + q0 * ix->d.b : B.logits;
+    if (!logits) HIP_OK(run_encode(ix, qp, n, B.logits, B, stream));
+    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream));
+    HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, nullptr, stream));
+    HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
+                      out_dists + q0 * k, nullptr, stream, nullptr));
+  }
   return NR_OK;
 }
 

@@ -27,6 +27,7 @@ NR_MAX_K = 64
 NR_MAX_PROBES = 4096
 NR_QSTATS = 8
 NR_REFINE_AUTO, NR_REFINE_PER_QUERY, NR_REFINE_SHARED = 0, 1, 2
+NR_NOALLOC_SCRATCH_BYTES = 64 << 20
 NR_STAGES = 10
 QS = dict(probes=0, clusters=1, direct=2, scored=3, stopped=4, rows=5, tiles=6, batches=7)
 STAGES = ("encode", "probe", "route", "plan", "refine", "merge", "shared_prep", "shared_scan",
@@ -36,7 +37,7 @@ WORK = ("tiles", "rows", "rows_read", "own_rows", "shared_rows", "shared_pairs",
         "open_bytes", "refine_bytes")
 
 # every symbol include/neuroute.h declares
-EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex",
+EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_search_noalloc",
            "nr_encode", "nr_calibrate", "nr_pair_sqdist_ws", "nr_pair_sqdist", "nr_lsim_grad",
            "nr_probe", "nr_route", "nr_route_capacity", "nr_refine", "nr_profile_enable",
            "nr_profile_read", "nr_last_work", "nr_stream_read", "nr_status_string",
@@ -94,6 +95,8 @@ def lib():
         L.nr_search.argtypes = [P, P, C.c_int64, C.c_int32, C.c_int32, C.POINTER(nr_params), P, P, P]
         L.nr_search_ex.argtypes = [P, P, P, C.c_int64, C.c_int32, C.c_int32, C.POINTER(nr_params),
                                    P, P, P, P]
+        L.nr_search_noalloc.argtypes = [P, P, P, C.c_int64, C.c_int32, C.c_int32,
+                                        C.POINTER(nr_params), P, P, P]
         L.nr_encode.argtypes = [P, P, C.c_int64, P, P]
         L.nr_pair_sqdist_ws.argtypes = [C.c_int64, C.c_int32]
         L.nr_pair_sqdist_ws.restype = C.c_size_t
@@ -337,6 +340,24 @@ class Index:
                                       C.byref(p), _ptr(ids), _ptr(dists), _ptr(qs), _stream(stream)),
                    "nr_search_ex")
         return (ids, dists, qs) if qstats else (ids, dists)
+
+    def nr_search_noalloc(self, queries, k, probe_budget, params: Params, out_ids, out_dists,
+                          logits=None, stream=None):
+        """The search that allocates nothing: the caller passes the outputs
+        (DEVICE int64 / fp32 [nq, k])."""
+        _dev(queries, "queries")
+        _dev(out_ids, "out_ids")
+        _dev(out_dists, "out_dists")
+        nq = queries.shape[0]
+        if tuple(out_ids.shape) != (nq, k) or tuple(out_dists.shape) != (nq, k):
+            raise ValueError("out_ids and out_dists must be [nq, k]")
+        if logits is not None:
+            _dev(logits, "logits")
+        p = params.c()
+        _check(lib().nr_search_noalloc(self.handle, _ptr(queries), _ptr(logits), nq, k,
+                                       probe_budget, C.byref(p), _ptr(out_ids), _ptr(out_dists),
+                                       _stream(stream)), "nr_search_noalloc")
+        return out_ids, out_dists
 
     def nr_encode(self, queries, stream=None):
         _dev(queries, "queries")
