@@ -120,8 +120,11 @@ typedef struct {
  * the k_c best under the gate d <= d_min + M(d_min) (gate_on), and stops
  * (early_stop_on) once the heap is full, at least b_min bins were visited and
  * t_low consecutive batches were low quality: fewer than u_heap entries kept
- * AND (OR when lowq_or) fewer than u_front of them within
- * d_min + alpha_front * M(d_min).  M is piecewise linear through m_knots
+ * OR (lowq_or = 1) / AND (lowq_or = 0) fewer than u_front of them within
+ * d_min + alpha_front * M(d_min).  With u_heap = u_front = 1 the OR reading
+ * means "no entry reached the front" (alpha_front decides) and the AND
+ * reading "no entry was kept" (alpha_front plays no part); the Python
+ * binding defaults to the OR reading.  M is piecewise linear through m_knots
  * knots (m_x strictly increasing, m_y non-decreasing), constant outside them,
  * and 0 when m_knots == 0; distances are squared L2 in latent space.
  */
@@ -179,7 +182,10 @@ enum {
 /* Upload an index: validates the description and the device CSR arrays
  * (monotone offsets, bounds, row_ids a permutation), copies the encoder and
  * tau to the device and borrows the DEVICE arrays.  Synchronises `stream`.
- * On success *out owns the library's copies until nr_index_free. */
+ * On success *out owns the library's copies until nr_index_free.  With n = 0
+ * and every DEVICE array NULL the index holds only the encoder and tau:
+ * nr_encode works on it (to encode a base for index construction), the
+ * search entry points return NR_EINVAL. */
 nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t stream);
 
 /* Release an index and its workspaces (synchronises the device). */
@@ -286,6 +292,70 @@ nr_status nr_pair_sqdist(const float *x, int64_t B, int32_t D, float *ws, float 
 nr_status nr_lsim_grad(const float *d2_emb, const float *lat, int64_t B, int32_t L,
                        float gamma_rho, float tau_emb, double *num_cnt, float *grad_lat,
                        hipStream_t stream);
+
+/* ---- Index construction on the GPU (Sec. 3.3 "Bucket allocation" and
+ * "In-bucket clustering"; thresholds, Sec. 3.2.3).  Untimed, run once.
+ * The latents of the base rows come from nr_encode on an encoder-only index
+ * (nr_index_upload with n = 0 and every DEVICE array NULL).  All arrays are
+ * DEVICE memory unless marked HOST; calls synchronise `stream` where they
+ * return HOST values.  The k-means of multi-cluster buckets: the sample is
+ * the first min(|B|, sample_per_cluster * K_B) members ordered by
+ * (mix32(id, seed), id); k-means++ from its first member, each further centre
+ * drawn by the bucket's uniform U[r] with probability proportional to
+ * floor(D^2 * 2^20) (capped at 2^30); then `lloyd` Lloyd passes over the
+ * bucket; distances and sums in fp64 in a fixed order; clusters left empty are
+ * dropped.  Rows of a cluster are stored in original-id order. */
+enum { NR_CLUSTER_NONE = 0, NR_CLUSTER_CAPACITY = 1, NR_CLUSTER_FIXED = 2,
+       NR_CLUSTER_PER_BUCKET = 3 };
+
+/* tau [b] = per latent dimension the lower median ((ns - 1) / 2-th smallest)
+ * of logits [ns x b]. */
+nr_status nr_build_tau(const float *logits, int64_t ns, int32_t b, float *tau, hipStream_t stream);
+
+/* codes [m] = Eq. 10 codes of logits [m x b] under tau [b]; sizes [2^b] is
+ * incremented per code (zero it before the first of several calls). */
+nr_status nr_build_codes(const float *logits, int64_t m, int32_t b, const float *tau,
+                         uint32_t *codes, uint32_t *sizes, hipStream_t stream);
+
+/* Clusters per bucket K_B from the bucket sizes [2^b] of n rows: rule
+ * NR_CLUSTER_CAPACITY ceil(size / param), NR_CLUSTER_FIXED min(size, param),
+ * NR_CLUSTER_PER_BUCKET capacity t = max(1, round-half-even(mean non-empty
+ * size / param)), NR_CLUSTER_NONE min(size, 1).  kb [2^b] out; mlist [2^b]
+ * out: the codes with K_B >= 2, ascending, in its first n_multi entries. */
+typedef struct {
+  int64_t max_clusters;   /* sum of K_B */
+  int64_t n_multi;        /* buckets with K_B >= 2 */
+  int32_t kmax;           /* largest K_B */
+  uint32_t t;             /* capacity used (rules CAPACITY and PER_BUCKET) */
+} nr_build_plan_info;
+nr_status nr_build_plan(const uint32_t *sizes, int64_t n, int32_t b, int32_t rule, uint32_t param,
+                        uint32_t *kb, uint32_t *mlist, nr_build_plan_info *info /* HOST */,
+                        hipStream_t stream);
+
+typedef struct {
+  int64_t n;
+  int32_t b;
+  const float *logits;      /* [n x b] latents by original id */
+  const uint32_t *codes;    /* [n] */
+  const uint32_t *sizes;    /* [2^b] */
+  const uint32_t *kb;       /* [2^b] from nr_build_plan */
+  const uint32_t *mlist;    /* [n_multi] from nr_build_plan */
+  int64_t max_clusters, n_multi;
+  int32_t kmax;
+  const double *uniforms;   /* [n_multi x kmax] the k-means++ draws, fp64 in (0, 1) */
+  uint32_t seed;
+  int32_t lloyd;            /* >= 1 */
+  int32_t sample_per_cluster;
+} nr_build_desc;
+
+/* The index arrays: row_ids [n] (rows in (code, cluster, id) order),
+ * bc_off [2^b + 1], cl_off [max_clusters + 1], centroids [max_clusters x b]
+ * (fp32 means of the members' latents); *n_clusters (HOST) the clusters kept:
+ * the first n_clusters + 1 / n_clusters entries of cl_off / centroids are the
+ * index's.  Working memory is allocated and freed inside the call. */
+nr_status nr_build_index(const nr_build_desc *desc, int64_t *row_ids, uint32_t *bc_off,
+                         uint64_t *cl_off, float *centroids, int64_t *n_clusters,
+                         hipStream_t stream);
 
 /* Stage timing with HIP events on the launch stream (off by default).
  * nr_profile_read synchronises the recorded events and returns the summed

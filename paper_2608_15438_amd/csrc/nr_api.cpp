@@ -237,6 +237,7 @@ struct nr_index {
   std::vector<const float *> W, bias, bn_scale, bn_shift;
   float *tau = nullptr;
   uint32_t *row_of_id = nullptr;  // inverse permutation, made by the first calibration
+  bool enc_only = false;          // encoder and tau only (index construction)
   int maxw = 0;
   int n_cu = 0;
   std::mutex mu;
@@ -684,6 +685,31 @@ nr_status check_index(const nr_index *ix) {
   return NR_OK;
 }
 
+// device buffers of one call, freed when it ends
+struct DevScratch {
+  std::vector<void *> ptrs;
+  ~DevScratch() {
+    for (void *p : ptrs) (void)hipFree(p);
+  }
+  template <class T>
+  T *get(size_t count) {
+    void *p = nullptr;
+    if (hipMalloc(&p, sizeof(T) * (count > 0 ? count : 1)) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    ptrs.push_back(p);
+    return static_cast<T *>(p);
+  }
+};
+
+// entry points that read the payload or the directory
+nr_status check_search_index(const nr_index *ix) {
+  if (!ix) return fail(NR_EINVAL, "index is NULL");
+  if (ix->enc_only) return fail(NR_EINVAL, "the index holds only an encoder (n = 0)");
+  return NR_OK;
+}
+
 nr_status make_events(nr_index *ix, EventSet *es) {
   for (int i = 0; i <= NR_STAGES; ++i) HIP_OK(hipEventCreate(&es->ev[i]));
   return NR_OK;
@@ -721,7 +747,10 @@ nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t
   if (!desc || !out) return fail(NR_EINVAL, "desc and out must not be NULL");
   *out = nullptr;
   const nr_index_desc &d = *desc;
-  if (d.n < 1) return fail(NR_EINVAL, "n must be >= 1");
+  // encoder and tau only: no payload, nothing borrowed
+  const bool enc_only = d.n == 0 && !d.rows && !d.row_ids && !d.bc_off && !d.cl_off &&
+                        !d.centroids;
+  if (d.n < 1 && !enc_only) return fail(NR_EINVAL, "n must be >= 1");
   if (d.n >= (int64_t)1 << 32) return fail(NR_EUNSUPPORTED, "n must be < 2^32");
   if (d.d < 1) return fail(NR_EINVAL, "d must be >= 1");
   if (d.dtype != NR_U8 && d.dtype != NR_F32) return fail(NR_EINVAL, "dtype must be NR_U8 or NR_F32");
@@ -740,7 +769,7 @@ nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t
   for (int l = 0; l < d.n_layers; ++l)
     if (!d.weights[l]) return fail(NR_EINVAL, "weights[%d] is NULL", l);
   if (!std::isfinite(d.input_scale)) return fail(NR_EINVAL, "input_scale must be finite");
-  if (!d.rows || !d.row_ids || !d.bc_off || !d.cl_off || !d.centroids)
+  if (!enc_only && (!d.rows || !d.row_ids || !d.bc_off || !d.cl_off || !d.centroids))
     return fail(NR_EINVAL, "rows, row_ids, bc_off, cl_off and centroids are required");
   if ((uintptr_t)d.rows % 16 != 0) return fail(NR_EINVAL, "rows must be 16-byte aligned");
   if (d.head_bytes != 0 &&
@@ -749,7 +778,7 @@ nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t
     return fail(NR_EINVAL, "head_bytes must be 0, 16, 32, 64 or 128, at most the row size "
                            "(row size - 16 without head_copy)");
   if (d.head_copy != 0 && d.head_copy != 1) return fail(NR_EINVAL, "head_copy must be 0 or 1");
-  if (d.n_clusters < 1 || d.n_clusters >= ((int64_t)1 << 32))
+  if (!enc_only && (d.n_clusters < 1 || d.n_clusters >= ((int64_t)1 << 32)))
     return fail(NR_EINVAL, "n_clusters must be in [1, 2^32)");
 
   nr_index *ix = new (std::nothrow) nr_index();
@@ -804,6 +833,11 @@ nr_status nr_index_upload(const nr_index_desc *desc, nr_index **out, hipStream_t
   {  // the no-alloc entry point's array on this device
     char *sp = nullptr;
     if (nr_status st = scratch_address(dev, &sp)) return cleanup(st);
+  }
+  if (enc_only) {
+    ix->enc_only = true;
+    *out = ix;
+    return NR_OK;
   }
   // validate the borrowed CSR arrays and the permutation
   uint32_t *bitmap = nullptr;
@@ -881,7 +915,7 @@ nr_status nr_encode(const nr_index *cix, const void *queries, int64_t nq, float 
 nr_status nr_probe(const nr_index *cix, const float *logits, int64_t nq, int32_t P,
                    const nr_params *p, uint32_t *codes, float *costs, int32_t *bins,
                    int32_t *counts, hipStream_t stream) {
-  if (nr_status s = check_index(cix)) return s;
+  if (nr_status s = check_search_index(cix)) return s;
   if (nr_status s = check_params(cix, P, p)) return s;
   if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
   if (nq == 0) return NR_OK;
@@ -894,7 +928,7 @@ nr_status nr_route(const nr_index *cix, const float *logits, int64_t nq, int32_t
                    const nr_params *p, uint32_t *clusters, int32_t *n_clusters, int64_t cap,
                    hipStream_t stream) {
   nr_index *ix = const_cast<nr_index *>(cix);
-  if (nr_status s = check_index(ix)) return s;
+  if (nr_status s = check_search_index(ix)) return s;
   if (nr_status s = check_params(ix, P, p)) return s;
   if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
   if (nq == 0) return NR_OK;
@@ -920,7 +954,7 @@ nr_status nr_refine(const nr_index *cix, const void *queries, int64_t nq, int32_
                     const uint32_t *clusters, const int32_t *n_clusters, int64_t cap,
                     int64_t *out_ids, float *out_dists, hipStream_t stream) {
   nr_index *ix = const_cast<nr_index *>(cix);
-  if (nr_status s = check_index(ix)) return s;
+  if (nr_status s = check_search_index(ix)) return s;
   if (k < 1) return fail(NR_EINVAL, "k must be >= 1");
   if (k > NR_MAX_K) return fail(NR_EUNSUPPORTED, "k %d > %d", k, NR_MAX_K);
   if (nq < 0 || cap < 1) return fail(NR_EINVAL, "nq must be >= 0 and cap >= 1");
@@ -947,7 +981,7 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
                        int64_t nq, int32_t k, int32_t P, const nr_params *p, int64_t *out_ids,
                        float *out_dists, int32_t *qstats, hipStream_t stream) {
   nr_index *ix = const_cast<nr_index *>(cix);
-  if (nr_status s = check_index(ix)) return s;
+  if (nr_status s = check_search_index(ix)) return s;
   if (nr_status s = check_params(ix, P, p)) return s;
   if (k < 1) return fail(NR_EINVAL, "k must be >= 1");
   if (k > NR_MAX_K) return fail(NR_EUNSUPPORTED, "k %d > %d", k, NR_MAX_K);
@@ -1016,7 +1050,7 @@ nr_status nr_search_noalloc(const nr_index *cix, const void *queries, const floa
                             int64_t nq, int32_t k, int32_t P, const nr_params *p,
                             int64_t *out_ids, float *out_dists, hipStream_t stream) {
   const nr_index *ix = cix;
-  if (nr_status s = check_index(ix)) return s;
+  if (nr_status s = check_search_index(ix)) return s;
   if (nr_status s = check_params(ix, P, p)) return s;
   if (k < 1) return fail(NR_EINVAL, "k must be >= 1");
   if (k > NR_MAX_K) return fail(NR_EUNSUPPORTED, "k %d > %d", k, NR_MAX_K);
@@ -1073,7 +1107,7 @@ nr_status nr_calibrate(const nr_index *cix, const float *logits, int64_t nq,
                        const int64_t *target_ids, int32_t K, int32_t l_sel, int32_t r_max,
                        float *scores, float *margin_xy, hipStream_t stream) {
   nr_index *ix = const_cast<nr_index *>(cix);
-  if (nr_status s = check_index(ix)) return s;
+  if (nr_status s = check_search_index(ix)) return s;
   if (nq < 0) return fail(NR_EINVAL, "nq must be >= 0");
   if (K < 1 || K > NR_MAX_K) return fail(NR_EUNSUPPORTED, "K must be in [1, %d]", NR_MAX_K);
   if (l_sel < 0 || l_sel > ix->d.b || l_sel > 32)
@@ -1139,6 +1173,136 @@ nr_status nr_lsim_grad(const float *d2_emb, const float *lat, int64_t B, int32_t
     return fail(NR_EINVAL, "gamma_rho and tau_emb must be finite");
   if (!d2_emb || !lat || !num_cnt || !grad_lat) return fail(NR_EINVAL, "NULL buffer");
   HIP_OK(nr::launch_lsim_grad(d2_emb, lat, B, L, gamma_rho, tau_emb, num_cnt, grad_lat, stream));
+  return NR_OK;
+}
+
+nr_status nr_build_tau(const float *logits, int64_t ns, int32_t b, float *tau, hipStream_t stream) {
+  if (ns < 1 || b < 1 || b > 30) return fail(NR_EINVAL, "ns must be >= 1 and b in [1, 30]");
+  if (!logits || !tau) return fail(NR_EINVAL, "NULL buffer");
+  HIP_OK(nr::launch_build_tau(logits, ns, b, tau, stream));
+  return NR_OK;
+}
+
+nr_status nr_build_codes(const float *logits, int64_t m, int32_t b, const float *tau,
+                         uint32_t *codes, uint32_t *sizes, hipStream_t stream) {
+  if (m < 0 || b < 1 || b > 30) return fail(NR_EINVAL, "m must be >= 0 and b in [1, 30]");
+  if (m == 0) return NR_OK;
+  if (!logits || !tau || !codes || !sizes) return fail(NR_EINVAL, "NULL buffer");
+  HIP_OK(nr::launch_build_codes(logits, m, b, tau, codes, sizes, stream));
+  return NR_OK;
+}
+
+nr_status nr_build_plan(const uint32_t *sizes, int64_t n, int32_t b, int32_t rule, uint32_t param,
+                        uint32_t *kb, uint32_t *mlist, nr_build_plan_info *info,
+                        hipStream_t stream) {
+  if (n < 1 || n >= ((int64_t)1 << 32)) return fail(NR_EINVAL, "n must be in [1, 2^32)");
+  if (b < 1 || b > 30) return fail(NR_EINVAL, "b must be in [1, 30]");
+  if (!sizes || !kb || !mlist || !info) return fail(NR_EINVAL, "NULL buffer");
+  if (rule < NR_CLUSTER_NONE || rule > NR_CLUSTER_PER_BUCKET)
+    return fail(NR_EINVAL, "unknown cluster rule %d", rule);
+  if (rule != NR_CLUSTER_NONE && param < 1) return fail(NR_EINVAL, "param must be >= 1");
+  const int64_t nb = (int64_t)1 << b;
+  DevScratch ds;
+  uint32_t *multi = ds.get<uint32_t>(nb + 1), *mpos = ds.get<uint32_t>(nb + 1);
+  unsigned long long *cnt = ds.get<unsigned long long>(4);
+  uint64_t *blk = ds.get<uint64_t>(nr::build_scan_blocks(nb));
+  if (!multi || !mpos || !cnt || !blk) return fail(NR_ENOMEM, "plan scratch allocation failed");
+  HIP_OK(nr::launch_fill_i32((int32_t *)cnt, 8, 0, stream));
+  uint32_t t = param;
+  int r = rule;
+  if (rule == NR_CLUSTER_PER_BUCKET) {
+    HIP_OK(nr::launch_build_nonempty(sizes, nb, cnt + 3, stream));
+    unsigned long long ne = 0;
+    HIP_OK(hipMemcpyAsync(&ne, cnt + 3, 8, hipMemcpyDeviceToHost, stream));
+    HIP_OK(hipStreamSynchronize(stream));
+    const double mean = ne ? (double)n / (double)ne : 0.0;
+    const double tt = std::nearbyint(mean / (double)param);  // half to even
+    t = tt < 1.0 ? 1u : (uint32_t)tt;
+    r = NR_CLUSTER_CAPACITY;
+  }
+  nr::BuildArgs a{};
+  a.b = b;
+  a.sizes = sizes;
+  a.rule = r;
+  a.t = t;
+  a.kb = kb;
+  a.multi = multi;
+  a.mpos = mpos;
+  a.mlist = mlist;
+  a.stats = cnt;
+  a.blk = blk;
+  HIP_OK(nr::run_build_plan(a, stream));
+  unsigned long long st[3] = {0, 0, 0};
+  HIP_OK(hipMemcpyAsync(st, cnt, sizeof(st), hipMemcpyDeviceToHost, stream));
+  HIP_OK(hipStreamSynchronize(stream));
+  info->max_clusters = (int64_t)st[0];
+  info->n_multi = (int64_t)st[1];
+  info->kmax = (int32_t)st[2];
+  info->t = t;
+  return NR_OK;
+}
+
+nr_status nr_build_index(const nr_build_desc *d, int64_t *row_ids, uint32_t *bc_off,
+                         uint64_t *cl_off, float *centroids, int64_t *n_clusters,
+                         hipStream_t stream) {
+  if (!d || !row_ids || !bc_off || !cl_off || !centroids || !n_clusters)
+    return fail(NR_EINVAL, "NULL argument");
+  if (d->n < 1 || d->n >= ((int64_t)1 << 32)) return fail(NR_EINVAL, "n must be in [1, 2^32)");
+  if (d->b < 1 || d->b > 30) return fail(NR_EINVAL, "b must be in [1, 30]");
+  if (!d->logits || !d->codes || !d->sizes || !d->kb || (d->n_multi > 0 && (!d->mlist ||
+      !d->uniforms)))
+    return fail(NR_EINVAL, "NULL input array");
+  if (d->lloyd < 1) return fail(NR_EINVAL, "lloyd must be >= 1");
+  if (d->sample_per_cluster < 1) return fail(NR_EINVAL, "sample_per_cluster must be >= 1");
+  if (d->max_clusters < 1 || d->max_clusters >= ((int64_t)1 << 32))
+    return fail(NR_EINVAL, "max_clusters must be in [1, 2^32)");
+  if (d->n_multi > 0 && d->kmax < 2) return fail(NR_EINVAL, "kmax must be >= 2");
+  const int64_t nb = (int64_t)1 << d->b, n = d->n, mc = d->max_clusters;
+  DevScratch ds;
+  nr::BuildArgs a{};
+  a.n = n;
+  a.b = d->b;
+  a.lg = d->logits;
+  a.codes = d->codes;
+  a.sizes = d->sizes;
+  a.kb = const_cast<uint32_t *>(d->kb);
+  a.mlist = const_cast<uint32_t *>(d->mlist);
+  a.n_multi = d->n_multi;
+  a.U = d->uniforms;
+  a.kmax = d->kmax;
+  a.seed = d->seed;
+  a.lloyd = d->lloyd;
+  a.spc = d->sample_per_cluster;
+  const int64_t most = std::max(std::max(nb, n), mc) + 1;
+  a.blk = ds.get<uint64_t>(nr::build_scan_blocks(most));
+  a.kbpre = ds.get<uint64_t>(nb + 1);
+  a.boff = ds.get<uint64_t>(nb + 1);
+  a.cursor = ds.get<uint32_t>(nb);
+  a.nkept = ds.get<uint32_t>(nb);
+  a.ncl = ds.get<uint32_t>(nb);
+  a.ids = ds.get<uint32_t>(n);
+  a.ids_tmp = ds.get<uint32_t>(n);
+  a.label = ds.get<uint32_t>(n);
+  a.skey = ds.get<uint64_t>(n);
+  a.skey_tmp = ds.get<uint64_t>(n);
+  a.d2 = ds.get<double>(n);
+  a.cent = ds.get<double>((size_t)mc * d->b);
+  a.ccnt = ds.get<uint32_t>(mc);
+  a.csize = ds.get<uint64_t>(mc);
+  if (!a.blk || !a.kbpre || !a.boff || !a.cursor || !a.nkept || !a.ncl || !a.ids || !a.ids_tmp ||
+      !a.label || !a.skey || !a.skey_tmp || !a.d2 || !a.cent || !a.ccnt || !a.csize)
+    return fail(NR_ENOMEM, "build scratch allocation failed");
+  a.bc_off = bc_off;
+  a.row_ids = row_ids;
+  a.centroids = centroids;
+  HIP_OK(nr::run_build_index(a, stream));
+  uint32_t ncl = 0;
+  HIP_OK(hipMemcpyAsync(&ncl, bc_off + nb, 4, hipMemcpyDeviceToHost, stream));
+  HIP_OK(hipStreamSynchronize(stream));
+  if ((int64_t)ncl > mc) return fail(NR_ECORRUPT, "more clusters than planned");
+  HIP_OK(nr::launch_build_cl_off(a.csize, (int64_t)ncl, cl_off, a.blk, stream));
+  HIP_OK(hipStreamSynchronize(stream));
+  *n_clusters = ncl;
   return NR_OK;
 }
 

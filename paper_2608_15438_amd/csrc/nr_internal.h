@@ -47,7 +47,7 @@ constexpr int SHARED_MAX_NSEG = 48;       // rows of at most 48 x 128 bytes use 
 constexpr uint32_t SHARED_ROWS = 2048;    // rows per shared work unit (at most)
 constexpr int MAX_KC = 16384;             // top-K_c heap held in LDS
 // the shared schedule's scan-list build: LIST_WPT bitmap words per thread
-constexpr int LIST_WPT = 8;
+constexpr int LIST_WPT = 1;
 constexpr int LIST_THREADS = 256;
 __host__ __device__ inline int64_t list_words(int64_t n_clusters) { return (n_clusters + 31) / 32; }
 __host__ __device__ inline int64_t list_blocks(int64_t n_clusters) {
@@ -307,6 +307,46 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_inverse_perm(const int64_t *row_ids, int64_t n, uint32_t *row_of_id,
                                hipStream_t s);
 hipError_t launch_calib(const CalibArgs &a, hipStream_t s);
+// index construction (k_build.hip)
+struct BuildArgs {
+  int64_t n;
+  int b;
+  const float *lg;            // [n x b] latents by original id
+  const uint32_t *codes;      // [n]
+  const uint32_t *sizes;      // [2^b]
+  int rule;
+  uint32_t t;
+  uint32_t *kb, *multi, *mpos, *mlist;   // [2^b] (+1 for the scans)
+  unsigned long long *stats;  // [3] sum kb, multi buckets, max kb
+  uint64_t *blk;              // scan scratch [build_scan_blocks(max items)]
+  uint64_t *kbpre, *boff;     // [2^b + 1]
+  uint32_t *cursor, *nkept, *ncl;        // [2^b] (+1)
+  uint32_t *ids, *ids_tmp, *label;       // [n]
+  uint64_t *skey, *skey_tmp;  // [n]
+  double *d2;                 // [n]
+  int64_t n_multi;
+  const double *U;            // [n_multi x kmax]
+  int kmax;
+  uint32_t seed;
+  int lloyd, spc;
+  double *cent;               // [max_clusters x b]
+  uint32_t *ccnt;             // [max_clusters]
+  uint32_t *bc_off;           // [2^b + 1] out
+  int64_t *row_ids;           // [n] out
+  uint64_t *csize;            // [max_clusters]
+  float *centroids;           // [max_clusters x b] out
+};
+size_t build_scan_blocks(int64_t n);
+hipError_t launch_build_tau(const float *lg, int64_t ns, int b, float *tau, hipStream_t s);
+hipError_t launch_build_codes(const float *lg, int64_t m, int b, const float *tau, uint32_t *codes,
+                              uint32_t *sizes, hipStream_t s);
+hipError_t launch_build_nonempty(const uint32_t *sizes, int64_t nb, unsigned long long *out,
+                                 hipStream_t s);
+hipError_t run_build_plan(const BuildArgs &a, hipStream_t s);
+hipError_t run_build_index(const BuildArgs &a, hipStream_t s);
+hipError_t launch_build_cl_off(const uint64_t *csize, int64_t n_clusters, uint64_t *cl_off,
+                               uint64_t *blk, hipStream_t s);
+
 // L_sim training (k_lsim.hip)
 size_t pair_sqdist_ws_floats(int64_t B, int D);
 hipError_t launch_pair_sqdist(const float *x, int64_t B, int D, float *ws, float *out,

@@ -39,6 +39,7 @@ WORK = ("tiles", "rows", "rows_read", "own_rows", "shared_rows", "shared_pairs",
 # every symbol include/neuroute.h declares
 EXPORTS = ("nr_index_upload", "nr_index_free", "nr_search", "nr_search_ex", "nr_search_noalloc",
            "nr_encode", "nr_calibrate", "nr_pair_sqdist_ws", "nr_pair_sqdist", "nr_lsim_grad",
+           "nr_build_tau", "nr_build_codes", "nr_build_plan", "nr_build_index",
            "nr_probe", "nr_route", "nr_route_capacity", "nr_refine", "nr_profile_enable",
            "nr_profile_read", "nr_last_work", "nr_stream_read", "nr_status_string",
            "nr_last_error")
@@ -61,6 +62,22 @@ class nr_index_desc(C.Structure):
                 ("rows", C.c_void_p), ("row_ids", C.c_void_p), ("bc_off", C.c_void_p),
                 ("cl_off", C.c_void_p), ("centroids", C.c_void_p), ("n_clusters", C.c_int64),
                 ("head_bytes", C.c_int32), ("head_copy", C.c_int32)]
+
+
+class nr_build_plan_info(C.Structure):
+    _fields_ = [("max_clusters", C.c_int64), ("n_multi", C.c_int64), ("kmax", C.c_int32),
+                ("t", C.c_uint32)]
+
+
+class nr_build_desc(C.Structure):
+    _fields_ = [("n", C.c_int64), ("b", C.c_int32), ("logits", C.c_void_p), ("codes", C.c_void_p),
+                ("sizes", C.c_void_p), ("kb", C.c_void_p), ("mlist", C.c_void_p),
+                ("max_clusters", C.c_int64), ("n_multi", C.c_int64), ("kmax", C.c_int32),
+                ("uniforms", C.c_void_p), ("seed", C.c_uint32), ("lloyd", C.c_int32),
+                ("sample_per_cluster", C.c_int32)]
+
+
+NR_CLUSTER_NONE, NR_CLUSTER_CAPACITY, NR_CLUSTER_FIXED, NR_CLUSTER_PER_BUCKET = 0, 1, 2, 3
 
 
 class nr_params(C.Structure):
@@ -102,6 +119,12 @@ def lib():
         L.nr_pair_sqdist_ws.restype = C.c_size_t
         L.nr_pair_sqdist.argtypes = [P, C.c_int64, C.c_int32, P, P, P]
         L.nr_lsim_grad.argtypes = [P, P, C.c_int64, C.c_int32, C.c_float, C.c_float, P, P, P]
+        L.nr_build_tau.argtypes = [P, C.c_int64, C.c_int32, P, P]
+        L.nr_build_codes.argtypes = [P, C.c_int64, C.c_int32, P, P, P, P]
+        L.nr_build_plan.argtypes = [P, C.c_int64, C.c_int32, C.c_int32, C.c_uint32, P, P,
+                                    C.POINTER(nr_build_plan_info), P]
+        L.nr_build_index.argtypes = [C.POINTER(nr_build_desc), P, P, P, P,
+                                     C.POINTER(C.c_int64), P]
         L.nr_calibrate.argtypes = [P, P, C.c_int64, P, C.c_int32, C.c_int32, C.c_int32, P, P, P]
         L.nr_probe.argtypes = [P, P, C.c_int64, C.c_int32, C.POINTER(nr_params), P, P, P, P, P]
         L.nr_route.argtypes = [P, P, C.c_int64, C.c_int32, C.POINTER(nr_params), P, P, C.c_int64, P]
@@ -190,6 +213,39 @@ def nr_lsim_grad(d2_emb: torch.Tensor, lat: torch.Tensor, gamma_rho: float, tau_
     return num_cnt, grad
 
 
+def nr_build_tau(logits: torch.Tensor, stream=None):
+    _dev(logits, "logits")
+    ns, b = logits.shape
+    tau = torch.empty(b, dtype=torch.float32, device=logits.device)
+    _check(lib().nr_build_tau(_ptr(logits), ns, b, _ptr(tau), _stream(stream)), "nr_build_tau")
+    return tau
+
+
+def nr_build_codes(logits: torch.Tensor, tau: torch.Tensor, codes: torch.Tensor,
+                   sizes: torch.Tensor, stream=None):
+    _dev(logits, "logits")
+    m, b = logits.shape
+    _check(lib().nr_build_codes(_ptr(logits), m, b, _ptr(tau), _ptr(codes), _ptr(sizes),
+                                _stream(stream)), "nr_build_codes")
+
+
+def nr_build_plan(sizes: torch.Tensor, n: int, b: int, rule: int, param: int, stream=None):
+    """(kb, mlist, info) of the cluster rule."""
+    kb = torch.empty(1 << b, dtype=torch.int32, device=sizes.device)
+    mlist = torch.empty(1 << b, dtype=torch.int32, device=sizes.device)
+    info = nr_build_plan_info()
+    _check(lib().nr_build_plan(_ptr(sizes), n, b, rule, param, _ptr(kb), _ptr(mlist),
+                               C.byref(info), _stream(stream)), "nr_build_plan")
+    return kb, mlist, info
+
+
+def nr_build_index(desc: nr_build_desc, row_ids, bc_off, cl_off, centroids, stream=None):
+    nc = C.c_int64()
+    _check(lib().nr_build_index(C.byref(desc), _ptr(row_ids), _ptr(bc_off), _ptr(cl_off),
+                                _ptr(centroids), C.byref(nc), _stream(stream)), "nr_build_index")
+    return nc.value
+
+
 # --------------------------------------------------------------------------
 # search parameters
 # --------------------------------------------------------------------------
@@ -209,7 +265,7 @@ class Params:
     alpha_front: float = 0.6
     gate_on: bool = True
     early_stop_on: bool = True
-    lowq_or: bool = False
+    lowq_or: bool = True
     refine_mode: int = NR_REFINE_AUTO
     shared_seed_rows: int = 0
     m_x: Sequence[float] = field(default_factory=list)
@@ -261,8 +317,10 @@ class Index:
                     dst[l] = a.ctypes.data_as(C.POINTER(C.c_float))
         tau = np.ascontiguousarray(tau, np.float32)
         self._keep += [widths, tau, wp, bp, sp, hp]
-        self.dev = [_dev(rows, "rows"), _dev(row_ids, "row_ids"), _dev(bc_off, "bc_off"),
-                    _dev(cl_off, "cl_off"), _dev(centroids, "centroids")]
+        enc_only = rows is None
+        self.dev = [] if enc_only else [_dev(rows, "rows"), _dev(row_ids, "row_ids"),
+                                        _dev(bc_off, "bc_off"), _dev(cl_off, "cl_off"),
+                                        _dev(centroids, "centroids")]
         desc = nr_index_desc()
         desc.n, desc.d, desc.dtype, desc.b, desc.n_layers = n, d, dtype, b, L
         desc.widths = widths.ctypes.data_as(C.POINTER(C.c_int32))
@@ -272,16 +330,29 @@ class Index:
         desc.bn_shift = hp
         desc.input_scale = input_scale
         desc.tau = tau.ctypes.data_as(C.POINTER(C.c_float))
-        desc.rows, desc.row_ids, desc.bc_off, desc.cl_off, desc.centroids = [
-            t.data_ptr() for t in self.dev]
-        desc.n_clusters = centroids.shape[0]
+        if not enc_only:
+            desc.rows, desc.row_ids, desc.bc_off, desc.cl_off, desc.centroids = [
+                t.data_ptr() for t in self.dev]
+        desc.n_clusters = 0 if enc_only else centroids.shape[0]
         desc.head_bytes = int(head_bytes)
         desc.head_copy = int(head_copy)
         self.n, self.d, self.dtype, self.b = n, d, dtype, b
-        self.n_clusters = int(centroids.shape[0])
+        self.n_clusters = 0 if enc_only else int(centroids.shape[0])
         h = C.c_void_p()
         _check(lib().nr_index_upload(C.byref(desc), C.byref(h), _stream(stream)), "nr_index_upload")
         self.handle = h
+
+    @classmethod
+    def encoder_only(cls, enc, dtype, tau=None, stream=None):
+        """An index holding only the encoder (and tau): for nr_encode, e.g.
+        to encode a base before its index exists."""
+        b = enc.weights[-1].shape[0]
+        d = enc.weights[0].shape[1]
+        t = np.zeros(b, np.float32) if tau is None else tau
+        return cls(n=0, d=d, dtype=dtype, b=b, weights=enc.weights, biases=enc.biases,
+                   bn_scale=enc.bn_scale, bn_shift=enc.bn_shift, input_scale=enc.input_scale,
+                   tau=t, rows=None, row_ids=None, bc_off=None, cl_off=None, centroids=None,
+                   stream=stream)
 
     @classmethod
     def from_built(cls, ix, device="cuda", stream=None):

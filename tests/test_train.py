@@ -122,15 +122,13 @@ def test_gpu_lsim_against_oracle(B, E, L):
     ld = lat.astype(np.float64)
     sl = np.sqrt(((ld[:, None, :] - ld[None, :, :]) ** 2).sum(2))
     off = ~np.eye(B, dtype=bool)
-    tau = float(np.quantile(se[off], 0.02))
-    # move tau into a gap of both thresholds' distance sets
-    for _ in range(200):
-        near = (np.abs(se[off] - tau) <= 1e-3 * tau).any() or \
-               (np.abs(sl[off] - g * rho * tau) <= 1e-3 * g * rho * tau).any()
-        if not near:
-            break
-        tau *= 1.0007
-    assert not near
+    # tau in the widest gap, around the 2 % quantile, of the values either
+    # threshold compares with: input distances and latent distances / (gamma rho)
+    vals = np.sort(np.concatenate([se[off], sl[off] / (g * rho)]))
+    lo, hi = np.searchsorted(vals, np.quantile(se[off], [0.015, 0.025]))
+    k = lo + int(np.argmax(vals[lo + 1:hi + 1] - vals[lo:hi]))
+    tau = float(0.5 * (vals[k] + vals[k + 1]))
+    assert vals[k + 1] - vals[k] >= 2e-5 * tau
     exp = O.lsim(xd, ld, g, tau)
     xt = torch.from_numpy(x).to(dev)
     lt = torch.from_numpy(lat).to(dev).requires_grad_(True)
