@@ -376,16 +376,24 @@ def main():
     scan_body = work["body_bytes"] - (0 if ix.head_copy else work["full_rows"] * hb)
     # the open-pair pass (fp32 rows past 1 KB): the row bytes of the slabs it
     # read; it reads the same amount of query bytes, mostly from cache
-    for kname, stage, nrows, ab in (
-            ("k_refine", "refine", work["own_rows"], work["refine_bytes"]),
-            ("k_scan", "shared_scan", work["shared_rows"], work["shared_rows"] * hb + scan_body),
+    # candidate bytes (every (query, row) pair the kernel settles, at the whole
+    # row's size: what a per-query refinement of the same pairs reads)
+    for kname, stage, nrows, ab, cand in (
+            ("k_refine", "refine", work["own_rows"], work["refine_bytes"],
+             work["own_rows"] * w.row_bytes),
+            ("k_scan", "shared_scan", work["shared_rows"], work["shared_rows"] * hb + scan_body,
+             work["shared_pair_rows"] * w.row_bytes),
             ("k_scan_open", "shared_open", work["open_bytes"] // max(1, w.row_bytes - 1024),
-             work["open_bytes"])):
+             work["open_bytes"], 0)):
         ms = stage_ms[stage] / nt
         if ms <= 0 or nrows <= 0:
             continue
         kernels[kname] = {"avg_launch_ms": round(ms, 4), "alg_bytes_per_launch": int(ab),
-                          "rows_per_launch": int(nrows), "achieved_gbs": round(ab / (ms * 1e-3) / 1e9, 1)}
+                          "rows_per_launch": int(nrows),
+                          "achieved_gbs": round(ab / (ms * 1e-3) / 1e9, 1),
+                          "candidate_bytes_per_launch": int(cand),
+                          "candidate_gbs": round(cand / (ms * 1e-3) / 1e9, 1),
+                          "candidate_frac": round(cand / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     dom = max(kernels, key=lambda n: kernels[n]["avg_launch_ms"])
     refine_ms = kernels[dom]["avg_launch_ms"]
     alg_bytes = kernels[dom]["alg_bytes_per_launch"]
@@ -428,6 +436,8 @@ def main():
                    if ix.head_bytes else "row-major",
                    "k": k, "probe_budget": P, "l_sel": params.l_sel, "r_max": params.r_max,
                    "k_c": params.k_c, "gate": f"q{int(round(args.margin_quantile * 100))}",
+                   "low_quality": "or" if params.lowq_or else "and",
+                   "s_max": params.s_max if np.isfinite(params.s_max) else "inf",
                    "early_stop": True, "parallelism": "single-gpu"},
         "recall_at_10": round(recall, 5),
         "recall_queries": ng,
@@ -439,7 +449,11 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "alg_bytes_per_launch": int(alg_bytes),
-                     "avg_launch_ms": round(refine_ms, 4)},
+                     "avg_launch_ms": round(refine_ms, 4),
+                     "bytes": "gathered: the bytes the kernel reads (heads of the rows it scans, "
+                              "rows it reads whole)",
+                     "candidate_frac": kernels[dom]["candidate_frac"],
+                     "stage_frac": refine_stage["frac_of_peak"]},
         "kernels": kernels,
         "refine_stage": refine_stage,
         "cpu_baseline": cpu,

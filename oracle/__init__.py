@@ -179,7 +179,7 @@ class RouteParams:
     alpha_front: float = 0.6
     gate_on: bool = True
     early_stop_on: bool = True
-    lowq_or: bool = False
+    lowq_or: bool = True
     m_x: np.ndarray = field(default_factory=lambda: np.zeros(0, np.float32))
     m_y: np.ndarray = field(default_factory=lambda: np.zeros(0, np.float32))
 

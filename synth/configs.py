@@ -81,7 +81,7 @@ GLD10M = Workload(
     cluster_rule="per_bucket8", kappa=10.0, spectrum=0.75, l_sel=13, r_max=5, k_c=4000,
     probe_budgets=(16, 32, 64, 128, 256, 512, 1024),
     notes="high-dimensional regime: 6 KB rows; noise std decaying as (1+e)^-3/4 (about 5.5 "
-          "effective noise dimensions, total power 0.64 x the centre's); the encoder keeps the "
+          "effective noise dimensions, total power 0.26 x the centre's); the encoder keeps the "
           "paper's first layer 1536->512 but not its deeper stack, whose untrained form loses "
           "the neighbourhoods",
 )

@@ -70,6 +70,10 @@ PARAM_SETS = {
     "no_gate_no_stop": dict(gate_on=False, early_stop_on=False),
     "small_heap_fast_stop": dict(k_c=5, b_batch=3, b_min=1, t_low=1),
     "or_reading": dict(k_c=8, b_batch=7, b_min=1, t_low=2, lowq_or=True),
+    "and_reading": dict(k_c=8, b_batch=7, b_min=1, t_low=2, lowq_or=False),
+    # the front threshold decides under the OR reading: a wide and a narrow front
+    "front_wide": dict(k_c=8, b_batch=5, b_min=1, t_low=1, alpha_front=0.95),
+    "front_narrow": dict(k_c=8, b_batch=5, b_min=1, t_low=1, alpha_front=0.05),
     "binned": dict(s_max=1.5, n_bins=6),
     "one_per_batch": dict(b_batch=1, k_c=16),
     # margins through several knots: the segment search and both clamps
@@ -215,7 +219,8 @@ def _worked_cases():
         if line.strip() and not line.startswith("#"):
             f = [c.strip() for c in line.split("|")]
             rows.append(dict(name=f[0], k_c=int(f[1]), t_low=int(f[2]), es=int(f[3]),
-                             lowq_or=int(f[4]), exp=[int(x) for x in f[5].split()]))
+                             lowq_or=int(f[4]), exp=[int(x) for x in f[5].split()],
+                             alpha=float(f[7])))
     return rows
 
 
@@ -240,7 +245,7 @@ def test_route_worked_example(dev, case):
                    centroids=torch.from_numpy(cent).to(dev))
     # M(x) = 10 everywhere: two knots with a flat segment
     p = NR.Params(l_sel=3, r_max=3, k_c=case["k_c"], b_batch=2, b_min=1, t_low=case["t_low"],
-                  u_heap=1, u_front=1, alpha_front=0.5, gate_on=True,
+                  u_heap=1, u_front=1, alpha_front=case["alpha"], gate_on=True,
                   early_stop_on=bool(case["es"]), lowq_or=bool(case["lowq_or"]),
                   m_x=[0.0, 1.0], m_y=[10.0, 10.0])
     gc, _, gb, gn = [t.cpu().numpy() for t in gix.nr_probe(torch.from_numpy(lg).to(dev), 7, p)]

@@ -39,7 +39,7 @@ def _golden():
             f = [c.strip() for c in line.split("|")]
             rows.append(dict(name=f[0], k_c=int(f[1]), t_low=int(f[2]), es=int(f[3]),
                              lowq_or=int(f[4]), exp=[int(x) for x in f[5].split()],
-                             stopped=int(f[6])))
+                             stopped=int(f[6]), alpha=float(f[7])))
     return rows
 
 
@@ -47,7 +47,8 @@ def _golden():
 def test_worked_example(oracle_lib, case):
     bc_off, mu, codes, bins = _micro()
     prm = O.RouteParams(k_c=case["k_c"], b_batch=2, b_min=1, t_low=case["t_low"], u_heap=1,
-                        u_front=1, alpha_front=0.5, gate_on=True, early_stop_on=bool(case["es"]),
+                        u_front=1, alpha_front=case["alpha"], gate_on=True,
+                        early_stop_on=bool(case["es"]),
                         lowq_or=bool(case["lowq_or"]), m_x=np.array([0.0]), m_y=np.array([10.0]))
     lists, st = O.route(np.zeros((1, 1), np.float32), codes, bins, np.array([7], np.int32),
                         bc_off, mu, prm, with_stats=True)
