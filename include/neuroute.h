@@ -275,17 +275,17 @@ nr_status nr_calibrate(const nr_index *index, const float *logits, int64_t nq,
  * mini-batch of B <= 65536 rows.
  * nr_pair_sqdist: out DEVICE fp32 [B x B] = squared Euclidean distances of the
  *   rows of x (DEVICE fp32 [B x D], the inputs as the encoder sees them),
- *   diagonal 0, computed as |x_i|^2 + |x_j|^2 - 2 x_i.x_j on the fp32 matrix
- *   cores after centring the batch on its mean; ws: DEVICE fp32 scratch of
- *   nr_pair_sqdist_ws(B, D) floats.
+ *   diagonal 0, symmetric bit for bit, computed as |x_i|^2 + |x_j|^2 -
+ *   2 x_i.x_j on the fp32 matrix cores after centring the batch on its mean;
+ *   ws: DEVICE fp32 scratch of nr_pair_sqdist_ws(B, D) floats.
  * nr_lsim_grad: given those distances (S_emb = their square roots) and the
  *   latents lat (DEVICE fp32 [B x L], L <= 32), with m_ij = [i != j and
  *   (S_emb(i,j) <= tau_emb or S_lat(i,j) <= gamma_rho * tau_emb)] and
  *   d_ij = S_lat(i,j) - gamma_rho * S_emb(i,j) (gamma_rho = gamma * sqrt(L/E)):
  *   num_cnt (DEVICE fp64 [2], overwritten) = (sum m d^2, sum m), so that
  *   L_sim = num / cnt; grad_lat (DEVICE fp32 [B x L]) = cnt * dL_sim/dlat
- *   with the mask held fixed, i.e. sum_j 2 (m_ij d_ij + m_ji d_ji)
- *   (l_i - l_j) / S_lat(i,j). */
+ *   with the mask held fixed, i.e. sum_j 4 m_ij d_ij (l_i - l_j) / S_lat(i,j)
+ *   (d2_emb must be symmetric, as nr_pair_sqdist writes it). */
 size_t nr_pair_sqdist_ws(int64_t B, int32_t D);
 nr_status nr_pair_sqdist(const float *x, int64_t B, int32_t D, float *ws, float *out,
                          hipStream_t stream);

@@ -16,12 +16,11 @@
 // k_lsim_grad: one pass over the pairs that yields the loss's numerator and
 // mask count and the gradient with respect to the latents.  The mask is a
 // constant of the step (as in the paper's formulation, the thresholds select
-// pairs), so for row i
-//   dL/dl_i = (1 / sum m) sum_j 2 (m_ij d_ij + m_ji d_ji) (l_i - l_j) / S_lat(i, j),
-// d_ij = S_lat(i, j) - gamma rho S_emb(i, j), where S_emb(i, j) is read from
-// the (i, j) entry and S_emb(j, i) from the (j, i) entry of the distance
-// matrix; the kernel writes the sum without the 1 / sum m factor.  Latent
-// distances are taken directly from the coordinate differences (L <= 32).
+// pairs) and the distances are symmetric, so for row i
+//   dL/dl_i = (1 / sum m) sum_j 4 m_ij d_ij (l_i - l_j) / S_lat(i, j),
+// d_ij = S_lat(i, j) - gamma rho S_emb(i, j); the kernel writes the sum
+// without the 1 / sum m factor.  Latent distances are taken directly from the
+// coordinate differences (L <= 32).
 #include "nr_internal.h"
 
 namespace nr {
@@ -72,6 +71,9 @@ __global__ void __launch_bounds__(256) k_pair_sqdist(const float *x, int64_t B, 
   __shared__ float Bs[LS_K][LS_M + 4];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
+  // tiles on and above the diagonal; each writes its mirror too, so the
+  // matrix is symmetric bit for bit
+  if (blockIdx.y < blockIdx.x) return;
   const int64_t i0 = (int64_t)blockIdx.x * LS_M, j0 = (int64_t)blockIdx.y * LS_M;
   const int wm = (wave & 1) * 32, wn = (wave >> 1) * 32;
   v4f_l acc[2][2];
@@ -115,7 +117,9 @@ __global__ void __launch_bounds__(256) k_pair_sqdist(const float *x, int64_t B, 
         if (ri >= B) continue;
         float v = (norm[ri] + nj) - 2.0f * acc[i][j][r];
         v = v > 0.f ? v : 0.f;
-        out[ri * B + cj] = ri == cj ? 0.f : v;
+        if (ri == cj) v = 0.f;
+        out[ri * B + cj] = v;
+        out[cj * B + ri] = v;
       }
     }
 }
@@ -161,17 +165,15 @@ __global__ void __launch_bounds__(256) k_lsim_grad(const float *d2, const float 
         }
       }
       const float sl = sqrtf(sl2);
-      const float se_ij = sqrtf(d2[i * B + j]);
-      const float se_ji = sqrtf(d2[j * B + i]);
-      const bool lat_in = sl <= lat_thr;
-      const bool m_ij = se_ij <= tau || lat_in;
-      const bool m_ji = se_ji <= tau || lat_in;
-      const float d_ij = sl - gr * se_ij, d_ji = sl - gr * se_ji;
-      if (m_ij) {
-        num += (double)d_ij * (double)d_ij;
-        cnt += 1.0;
-      }
-      const float coef = 2.0f * ((m_ij ? d_ij : 0.f) + (m_ji ? d_ji : 0.f));
+      // the (j, i) entry: consecutive rows i read consecutive words
+      const float se = sqrtf(d2[j * B + i]);
+      const bool m = se <= tau || sl <= lat_thr;
+      if (!m) continue;
+      const float dd = sl - gr * se;
+      num += (double)dd * (double)dd;
+      cnt += 1.0;
+      // the pairs (i, j) and (j, i) contribute alike
+      const float coef = 4.0f * dd;
       if (coef != 0.f && sl > 0.f) {
         const float s = coef / sl;
 #pragma unroll

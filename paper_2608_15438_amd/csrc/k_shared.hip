@@ -13,9 +13,9 @@
 //          the final k-th entry: a later row can only enter the result if it
 //          ranks at or before it;
 //  prep    (on a second stream, beside the seed pass) the clusters with
-//          pairs, found through a bitmap the counting set, form the scan
-//          list in cluster order with their pair and work ranges (rows x
-//          groups of <= g queries); the pairs are then scattered by cluster;
+//          pairs, marked in a bitmap, form the scan list in cluster order with
+//          their pair and work ranges (rows x groups of <= g queries); the
+//          pairs are then scattered by cluster;
 //  scan    persistent waves take tiles of SHARED_TILE work from an atomic
 //          counter and gather consecutive units of the tile into batches
 //          whose query rows sit in LDS.  Each row's head (its first
@@ -109,10 +109,10 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
 
 // ------------------------------------------------------------------ hist
 // The pair counts are taken at the end of the route kernel, per query, once
-// its list is final (pair_hist_wave): hist[c] counts cluster c's pairs and
-// the first pair of a cluster sets bit c of `touched`.  Both start a search
-// at zero: the prep clears what it read, so only a fresh workspace needs the
-// full clear below.
+// its list is final (pair_hist_wave): hist[c] counts cluster c's pairs.  The
+// prep marks every cluster with pairs in the bitmap `touched` (k_touch).
+// Both start a search at zero: the prep clears what it read, so only a fresh
+// workspace needs the full clear below.
 hipError_t launch_shared_hist(const SharedArgs &a, bool fresh, hipStream_t s) {
   if (!fresh) return hipSuccess;
   hipError_t e = launch_fill_i32((int32_t *)a.hist, a.n_clusters + 1, 0, s);
@@ -123,7 +123,6 @@ hipError_t launch_shared_hist(const SharedArgs &a, bool fresh, hipStream_t s) {
 PairHistArgs pair_hist_args(const SharedArgs &a) {
   PairHistArgs h;
   h.hist = a.hist;
-  h.touched = a.touched;
   h.cl_off = a.cl_off;
   h.n_clusters = a.n_clusters;
   h.seed_min = a.seed_min;
@@ -293,6 +292,20 @@ __global__ void __launch_bounds__(LIST_THREADS) k_list_emit(SharedArgs a) {
   }
 }
 
+// one wave per query: the bit of every cluster the query's pairs list (the
+// atomics return nothing, so no lane waits on them)
+__global__ void __launch_bounds__(256) k_touch(SharedArgs a) {
+  const int lane = lane_id();
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (q >= a.nq) return;
+  const int n = clamp_n(a.nclus[q], a.cap);
+  const uint32_t *cl = a.clus + q * a.cap;
+  for (int i = a.cseed[q] + lane; i < n; i += WAVE) {
+    const uint32_t c = cl[i];
+    if (c < a.n_clusters) atomicOr(&a.touched[c >> 5], 1u << (c & 31));
+  }
+}
+
 // one wave per query: each of the query's pairs into its cluster's slots, at
 // the rank its count returned
 __global__ void __launch_bounds__(256) k_pair_scatter(SharedArgs a) {
@@ -320,6 +333,8 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
   if (e != hipSuccess) return e;
   const int64_t nblk = list_blocks(a.n_clusters);
+  if (a.nq > 0)
+    hipLaunchKernelGGL(k_touch, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_list_count, dim3((unsigned)nblk), dim3(LIST_THREADS), 0, s, a);
   hipLaunchKernelGGL(k_list_scan, dim3(1), dim3(LIST_THREADS), 0, s, a, nblk);
   hipLaunchKernelGGL(k_list_emit, dim3((unsigned)nblk), dim3(LIST_THREADS), 0, s, a);

@@ -116,7 +116,6 @@ struct CalibArgs {
 // per-query pair counting of the shared schedule (see pair_hist_wave)
 struct PairHistArgs {
   uint32_t *hist;               // [n_clusters + 1] pairs per cluster past the leading clusters
-  uint32_t *touched;            // [ceil(n_clusters / 32)] bit c: cluster c has pairs
   const uint64_t *cl_off;
   int64_t n_clusters;
   uint32_t seed_min;            // rows the leading clusters cover at least
@@ -446,8 +445,7 @@ __device__ __forceinline__ int lower_bound_u64(const uint64_t *a, int n, uint64_
 // One wave, query q with list cl[0..n): the leading clusters covering at
 // least seed_min rows stay with the query (cseed[q]); every later (cluster,
 // query) pair is counted in hist (its rank among the cluster's pairs goes to
-// pair_rank; the first pair of a cluster sets its bit in touched); rfull[q]
-// gets the rows of the leading
+// pair_rank); rfull[q] gets the rows of the leading
 // clusters (of the whole list with eager_rows); for uint8 rows qnorm[q] gets
 // |q|^2 and the part of it over the scan's head.
 __device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const uint32_t *cl, int n) {
@@ -478,11 +476,7 @@ __device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const ui
       }
       run += bcast_u64(incl, upto);
     }
-    if (cs >= 0 && i >= cs && c < h.n_clusters) {
-      const uint32_t r = atomicAdd(&h.hist[c], 1u);
-      h.pair_rank[q * h.cap + i] = r;
-      if (r == 0) atomicOr(&h.touched[c >> 5], 1u << (c & 31));  // the cluster's first pair
-    }
+    if (cs >= 0 && i >= cs && c < h.n_clusters) h.pair_rank[q * h.cap + i] = atomicAdd(&h.hist[c], 1u);
   }
   if (lane == 0) {
     h.cseed[q] = cs < 0 ? n : cs;
