@@ -3,7 +3,9 @@
 //   out[m][n] = act( in_scale * sum_k in[m][k] * W[n][k] + bias[n] )
 // on the fp32 matrix cores (v_mfma_f32_16x16x4f32).  A 256-thread block owns a
 // 64 x 64 output tile, each wave a 32 x 32 quarter (2 x 2 MFMA blocks); K is
-// staged through LDS 16 at a time, uint8 inputs are widened while staging.
+// staged through LDS 32 at a time in two buffers (the next tile is read into
+// registers while the current one is multiplied; one barrier per tile), uint8
+// inputs are widened while staging.
 // Hidden layers fold eval-mode BatchNorm (per-channel scale and shift) and
 // ReLU into the epilogue; the last layer writes the logits.
 #include "nr_internal.h"
@@ -12,56 +14,78 @@ namespace nr {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int EB_M = 64, EB_N = 64, EB_K = 16;
+constexpr int EB_M = 64, EB_N = 64, EB_K = 32;
+constexpr int EB_LD = EB_M + 4;                      // LDS row stride (floats)
+constexpr int EB_PER = EB_M * EB_K / 256;            // tile elements staged per thread
+
+// element e of a K-tile: row e / EB_K, column e % EB_K (consecutive threads
+// read consecutive columns of a row)
+__device__ __forceinline__ float enc_load_in(const EncodeLayerArgs &a, int64_t m, int kg) {
+  if (m >= a.M || kg >= a.K) return 0.f;
+  return a.in_u8 ? (float)((const uint8_t *)a.in)[m * a.K + kg]
+                 : ((const float *)a.in)[m * a.K + kg];
+}
 
 __global__ void __launch_bounds__(256) k_encode_layer(EncodeLayerArgs a) {
-  __shared__ float As[EB_K][EB_M + 4];
-  __shared__ float Ws[EB_K][EB_N + 4];
+  // two K-tiles of A (activations) and W, each [EB_K][EB_LD]: the next tile
+  // is loaded into registers while the current one feeds the matrix cores
+  __shared__ float As[2][EB_K][EB_LD];
+  __shared__ float Ws[2][EB_K][EB_LD];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int64_t m0 = (int64_t)blockIdx.x * EB_M;
   const int n0 = blockIdx.y * EB_N;
   const int wm = (wave & 1) * 32, wn = (wave >> 1) * 32;
   const int K = a.K, N = a.N;
-  const int64_t M = a.M;
   v4f acc[2][2];
   for (int i = 0; i < 2; ++i)
     for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-
+  float ra[EB_PER], rw[EB_PER];
+  auto fetch = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < EB_PER; ++u) {
+      const int e = tid + 256 * u;
+      const int r = e / EB_K, kk = e % EB_K;
+      ra[u] = enc_load_in(a, m0 + r, k0 + kk);
+      const int n = n0 + r, kg = k0 + kk;
+      rw[u] = (n < N && kg < K) ? a.W[(int64_t)n * K + kg] : 0.f;
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < EB_PER; ++u) {
+      const int e = tid + 256 * u;
+      const int r = e / EB_K, kk = e % EB_K;
+      As[buf][kk][r] = ra[u];
+      Ws[buf][kk][r] = rw[u];
+    }
+  };
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  int buf = 0;
   for (int k0 = 0; k0 < K; k0 += EB_K) {
-    for (int e = tid; e < EB_M * EB_K; e += 256) {
-      const int mm = e / EB_K, kk = e % EB_K;
-      const int64_t m = m0 + mm;
-      const int kg = k0 + kk;
-      float v = 0.f;
-      if (m < M && kg < K) {
-        v = a.in_u8 ? (float)((const uint8_t *)a.in)[m * K + kg]
-                    : ((const float *)a.in)[m * K + kg];
-      }
-      As[kk][mm] = v;
-    }
-    for (int e = tid; e < EB_N * EB_K; e += 256) {
-      const int nn = e / EB_K, kk = e % EB_K;
-      const int n = n0 + nn, kg = k0 + kk;
-      Ws[kk][nn] = (n < N && kg < K) ? a.W[(int64_t)n * K + kg] : 0.f;
-    }
-    __syncthreads();
+    const bool more = k0 + EB_K < K;
+    if (more) fetch(k0 + EB_K);
 #pragma unroll
     for (int kk = 0; kk < EB_K; kk += 4) {
       const int kr = kk + (lane >> 4), c = lane & 15;
       float av[2], bv[2];
-      av[0] = As[kr][wm + c];
-      av[1] = As[kr][wm + 16 + c];
-      bv[0] = Ws[kr][wn + c];
-      bv[1] = Ws[kr][wn + 16 + c];
+      av[0] = As[buf][kr][wm + c];
+      av[1] = As[buf][kr][wm + 16 + c];
+      bv[0] = Ws[buf][kr][wn + c];
+      bv[1] = Ws[buf][kr][wn + 16 + c];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
     }
+    if (more) stash(buf ^ 1);
     __syncthreads();
+    buf ^= 1;
   }
+  const int64_t M = a.M;
   // D layout of a 16x16 block: lane l, register r -> row 4*(l/16) + r, column l%16
 #pragma unroll
   for (int i = 0; i < 2; ++i)
