@@ -20,7 +20,10 @@
 //   dL/dl_i = (1 / sum m) sum_j 4 m_ij d_ij (l_i - l_j) / S_lat(i, j),
 // d_ij = S_lat(i, j) - gamma rho S_emb(i, j); the kernel writes the sum
 // without the 1 / sum m factor.  Latent distances are taken directly from the
-// coordinate differences (L <= 32).
+// coordinate differences (L <= 32).  Blocks take 64 rows by a strided share
+// of the columns, so a 4096-row batch spreads over ~1024 blocks; the column
+// blocks of a row add their partial gradients atomically (fp32: the last bits
+// of the gradient depend on their order).
 #include "nr_internal.h"
 
 namespace nr {
@@ -144,7 +147,8 @@ __global__ void __launch_bounds__(256) k_lsim_grad(const float *d2, const float 
   }
   const float lat_thr = gr * tau;
   double num = 0.0, cnt = 0.0;
-  for (int64_t j0 = 0; j0 < B; j0 += LG_ROWS) {
+  // this block's share of the columns: tiles j0 = (blockIdx.y + t * gridDim.y) * LG_ROWS
+  for (int64_t j0 = (int64_t)blockIdx.y * LG_ROWS; j0 < B; j0 += (int64_t)gridDim.y * LG_ROWS) {
     __syncthreads();
     for (int e = tid; e < LG_ROWS * LG_LMAX; e += 256) {
       const int jj = e / LG_LMAX, c = e % LG_LMAX;
@@ -199,7 +203,7 @@ __global__ void __launch_bounds__(256) k_lsim_grad(const float *d2, const float 
     for (int c = 0; c < L; ++c) {
       float v = gsum[0][r][c];
       for (int s2 = 1; s2 < LG_SUB; ++s2) v += gsum[s2][r][c];
-      grad[i * L + c] = v;
+      atomicAdd(&grad[i * L + c], v);   // the column blocks of row i meet here
     }
   if (tid == 0) {
     double tn = 0.0, tc = 0.0;
@@ -235,9 +239,15 @@ hipError_t launch_lsim_grad(const float *d2, const float *lat, int64_t B, int L,
                             float tau, double *num_cnt, float *grad, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   hipError_t e = launch_fill_i32((int32_t *)num_cnt, 4, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t *)grad, B * L, 0, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_lsim_grad, dim3((unsigned)((B + LG_ROWS - 1) / LG_ROWS)), dim3(256), 0, s,
-                     d2, lat, B, L, gr, tau, num_cnt, grad);
+  // row blocks x column blocks: at least ~1024 blocks so every SIMD holds waves
+  const int64_t rb = (B + LG_ROWS - 1) / LG_ROWS;
+  int64_t cb = (1024 + rb - 1) / rb;
+  if (cb > rb) cb = rb;
+  if (cb < 1) cb = 1;
+  hipLaunchKernelGGL(k_lsim_grad, dim3((unsigned)rb, (unsigned)cb), dim3(256), 0, s, d2, lat, B,
+                     L, gr, tau, num_cnt, grad);
   return hipGetLastError();
 }
 

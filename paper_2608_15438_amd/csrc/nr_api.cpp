@@ -478,6 +478,11 @@ hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
 struct RefineOpts {
   const int32_t *qmask = nullptr;      // only these queries (the others keep their outputs)
   const int32_t *own_cseed = nullptr;  // seed pass of the shared schedule: leading clusters only
+  // shared schedule: the scan's prep, started on the second stream once the
+  // seed pass is planned (so that it does not slow the planning kernels)
+  const nr::SharedArgs *prep = nullptr;
+  hipStream_t aux = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
 };
 
 // ev (may be null): events recorded after the plan, the refinement and the merge
@@ -512,6 +517,12 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   // redo of queries whose survivors overflowed adds to them)
   hipError_t e = o.qmask ? hipSuccess : nr::launch_fill_i32((int32_t *)(B.wstats + 6), 2, 0, s);
   if (e == hipSuccess) e = nr::launch_plan(pa, s);
+  if (e == hipSuccess && o.prep) {
+    e = hipEventRecord(o.fork, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(o.aux, o.fork, 0);
+    if (e == hipSuccess) e = nr::launch_shared_prep(*o.prep, o.aux);
+    if (e == hipSuccess) e = hipEventRecord(o.join, o.aux);
+  }
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[0], s);
   nr::RefineArgs ra{};
@@ -643,16 +654,16 @@ hipError_t run_refine_shared(const nr_index *ix, const nr::SharedArgs &a, const 
                              int64_t nq, int k, const uint32_t *clus, const int32_t *nclus,
                              int64_t cap, const Buffers &B, int64_t *out_ids, float *out_dists,
                              int32_t *qstats, hipStream_t s, hipEvent_t *ev) {
-  // the scan's prep needs only the pair counts: it runs on the second stream
-  // while the seed pass runs here
-  hipError_t e = hipEventRecord(B.fork, s);
-  if (e == hipSuccess) e = hipStreamWaitEvent(B.aux, B.fork, 0);
-  if (e == hipSuccess) e = nr::launch_shared_prep(a, B.aux);
-  if (e == hipSuccess) e = hipEventRecord(B.join, B.aux);
-  if (e != hipSuccess) return e;
+  // the scan's prep needs only the route's lists and pair counts: it runs on
+  // the second stream while the seed pass runs here
   RefineOpts own;
   own.own_cseed = B.cseed;
-  e = run_refine(ix, q, nq, k, clus, nclus, cap, B, B.own_ids, B.own_dists, qstats, s, ev, own);
+  own.prep = &a;
+  own.aux = B.aux;
+  own.fork = B.fork;
+  own.join = B.join;
+  hipError_t e = run_refine(ix, q, nq, k, clus, nclus, cap, B, B.own_ids, B.own_dists, qstats,
+                            s, ev, own);
   if (e != hipSuccess) return e;
   e = hipStreamWaitEvent(s, B.join, 0);
   if (e != hipSuccess) return e;

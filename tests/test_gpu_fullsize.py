@@ -198,3 +198,59 @@ def test_sift1b_benchmark_index():
     finally:
         del ix
         _free()
+
+
+# the sweep on the 100M x 96 fp32 index: probe budget x gate margin x early
+# stop x batch size (a batch of 1 or 256 queries runs the per-query schedule,
+# the whole batch the shared one); margins: loose / default / tight knots
+_SWEEP_GATES = {"loose": dict(m_x=[0.0, 1.0], m_y=[1.0, 4.0]),
+                "default": GATE,
+                "tight": dict(m_x=[0.0, 1.0], m_y=[0.1, 0.5])}
+
+
+@pytest.fixture(scope="module")
+def deep100m():
+    dev = _dev()
+    w = CF.WORKLOADS[3]
+    ix = _build(w, dev, "copy")
+    gix = NR.Index.from_built(ix, dev)
+    Q = GpuRows(w, "query", dev).range(0, w.n_queries)
+    lg, mag = O.encode(_oracle_encoder(ix), Q.cpu().numpy(), with_mag=True)
+    yield w, ix, gix, Q, lg, mag
+    gix.close()
+    del ix
+    _free()
+
+
+@pytest.mark.parametrize("P,gate,es,batch", [(4, "tight", True, 10_000), (16, "loose", False, 256),
+                                             (64, "default", True, 1), (256, "tight", False, 10_000),
+                                             (256, "loose", True, 256)])
+def test_deep100m_sweep_points(deep100m, P, gate, es, batch):
+    w, ix, gix, Q, lg, mag = deep100m
+    dev = Q.device
+    params = NR.Params(l_sel=16, r_max=w.r_max, k_c=w.k_c, early_stop_on=es, **_SWEEP_GATES[gate])
+    samp = np.sort(G.seeded_permutation(w.seed("sample") + P, w.n_queries)[:16])
+    if batch >= w.n_queries:
+        _check_sample(w, ix, gix, Q, lg, mag, P, params, samp)
+        return
+    # the sampled queries inside batches of `batch` queries (one call each)
+    lgd = torch.from_numpy(lg).to(dev)
+    ids = torch.empty((w.n_queries, w.k), dtype=torch.int64, device=dev)
+    dists = torch.empty((w.n_queries, w.k), dtype=torch.float32, device=dev)
+    for q in samp:
+        s0 = (int(q) // batch) * batch
+        i, d = gix.nr_search(Q[s0:s0 + batch], w.k, P, params, logits=lgd[s0:s0 + batch])
+        ids[s0:s0 + batch], dists[s0:s0 + batch] = i, d
+    ids, dists = ids.cpu().numpy(), dists.cpu().numpy()
+    bc = ix.bc_off.cpu().numpy().astype(np.uint32)
+    codes, costs, bins, cnt = O.probes(lg[samp], ix.tau, 16, w.r_max, P)
+    lists = O.route(lg[samp], codes, bins, cnt, bc, ix.centroids.cpu().numpy(),
+                    _route_params(params))
+    rows, rid, cl2 = stage_rows(ix, lists)
+    oi, od, _ = O.refine(rows, rid, cl2, Q.cpu().numpy()[samp], lists, w.k)
+    order = np.argsort(rid)
+    rid_sorted = rid[order]
+    Qh = Q.cpu().numpy()
+    check_topk(ids[samp], dists[samp], oi, od, is_u8=False,
+               X_by_id=lambda q_ids: rows[order[np.searchsorted(rid_sorted, q_ids)]],
+               Q=Qh[samp], allowed=lambda j: allowed_ids(cl2, rid, lists[j]))
