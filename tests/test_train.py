@@ -133,7 +133,7 @@ def test_gpu_lsim_against_oracle(B, E, L):
     xt = torch.from_numpy(x).to(dev)
     lt = torch.from_numpy(lat).to(dev).requires_grad_(True)
     loss, _, frac = TR.lsim_loss_gpu(xt, lt, g, tau)
-    assert abs(float(loss) - exp) <= 1e-4 * abs(exp)
+    assert abs(float(loss.detach()) - exp) <= 1e-4 * abs(exp)
     loss.backward()
     lt64 = torch.from_numpy(ld).requires_grad_(True)
     ref, _, _ = TR.lsim_loss(torch.from_numpy(xd), lt64, g, tau)
