@@ -285,7 +285,9 @@ nr_status nr_calibrate(const nr_index *index, const float *logits, int64_t nq,
  *   num_cnt (DEVICE fp64 [2], overwritten) = (sum m d^2, sum m), so that
  *   L_sim = num / cnt; grad_lat (DEVICE fp32 [B x L]) = cnt * dL_sim/dlat
  *   with the mask held fixed, i.e. sum_j 4 m_ij d_ij (l_i - l_j) / S_lat(i,j)
- *   (d2_emb must be symmetric, as nr_pair_sqdist writes it). */
+ *   (d2_emb must be symmetric, as nr_pair_sqdist writes it).  grad_lat and
+ *   the mask count are the same bit for bit on every call with the same
+ *   inputs; the numerator's last bits may vary (a double-precision atomic). */
 size_t nr_pair_sqdist_ws(int64_t B, int32_t D);
 nr_status nr_pair_sqdist(const float *x, int64_t B, int32_t D, float *ws, float *out,
                          hipStream_t stream);

@@ -20,10 +20,12 @@
 //   dL/dl_i = (1 / sum m) sum_j 4 m_ij d_ij (l_i - l_j) / S_lat(i, j),
 // d_ij = S_lat(i, j) - gamma rho S_emb(i, j); the kernel writes the sum
 // without the 1 / sum m factor.  Latent distances are taken directly from the
-// coordinate differences (L <= 32).  Blocks take 64 rows by a strided share
-// of the columns, so a 4096-row batch spreads over ~1024 blocks; the column
-// blocks of a row add their partial gradients atomically (fp32: the last bits
-// of the gradient depend on their order).
+// coordinate differences (L <= 32).  One wave owns a row (a 4096-row batch
+// spreads over 1024 blocks of four rows): its lanes take the columns in turn
+// against 64-column tiles of latents staged in LDS, then the wave adds its
+// lanes' partial gradients in a fixed butterfly order, so the gradient is the
+// same bit for bit on every run.  Only the numerator's block sums meet in a
+// double-precision atomic (its last bits may vary; the mask count is exact).
 #include "nr_internal.h"
 
 namespace nr {
@@ -127,17 +129,16 @@ __global__ void __launch_bounds__(256) k_pair_sqdist(const float *x, int64_t B, 
     }
 }
 
-constexpr int LG_ROWS = 64, LG_SUB = 4, LG_LMAX = 32;
+constexpr int LG_COLS = 64, LG_LMAX = 32, LG_WAVES = 4;
 
 __global__ void __launch_bounds__(256) k_lsim_grad(const float *d2, const float *lat, int64_t B,
                                                     int L, float gr, float tau, double *num_cnt,
                                                     float *grad) {
-  __shared__ float lj_s[LG_ROWS][LG_LMAX + 1];
-  __shared__ float gsum[LG_SUB][LG_ROWS][LG_LMAX + 1];
-  __shared__ double red[2][256 / WAVE];
+  __shared__ float lj_s[LG_COLS][LG_LMAX + 1];
+  __shared__ double red[2][LG_WAVES];
   const int tid = threadIdx.x;
-  const int r = tid % LG_ROWS, sub = tid / LG_ROWS;
-  const int64_t i = (int64_t)blockIdx.x * LG_ROWS + r;
+  const int lane = tid & (WAVE - 1), w = tid / WAVE;
+  const int64_t i = (int64_t)blockIdx.x * LG_WAVES + w;
   const bool row_ok = i < B;
   float li[LG_LMAX], g[LG_LMAX];
 #pragma unroll
@@ -147,69 +148,66 @@ __global__ void __launch_bounds__(256) k_lsim_grad(const float *d2, const float 
   }
   const float lat_thr = gr * tau;
   double num = 0.0, cnt = 0.0;
-  // this block's share of the columns: tiles j0 = (blockIdx.y + t * gridDim.y) * LG_ROWS
-  for (int64_t j0 = (int64_t)blockIdx.y * LG_ROWS; j0 < B; j0 += (int64_t)gridDim.y * LG_ROWS) {
+  for (int64_t j0 = 0; j0 < B; j0 += LG_COLS) {
     __syncthreads();
-    for (int e = tid; e < LG_ROWS * LG_LMAX; e += 256) {
-      const int jj = e / LG_LMAX, c = e % LG_LMAX;
-      const int64_t j = j0 + jj;
-      lj_s[jj][c] = (j < B && c < L) ? lat[j * L + c] : 0.f;
+    // the tile's latents: LG_COLS consecutive rows, read as one contiguous run
+    for (int e = tid; e < LG_COLS * L; e += 256) {
+      const int jj = e / L, c = e - jj * L;
+      lj_s[jj][c] = j0 + jj < B ? lat[j0 * L + e] : 0.f;
     }
     __syncthreads();
-    if (!row_ok) continue;
-    for (int jj = sub; jj < LG_ROWS; jj += LG_SUB) {
-      const int64_t j = j0 + jj;
-      if (j >= B || j == i) continue;
-      float sl2 = 0.f;
+    const int64_t j = j0 + lane;
+    if (!row_ok || j >= B || j == i) continue;
+    float sl2 = 0.f;
 #pragma unroll
-      for (int c = 0; c < LG_LMAX; ++c) {
-        if (c < L) {
-          const float t = li[c] - lj_s[jj][c];
-          sl2 = fmaf(t, t, sl2);
-        }
+    for (int c = 0; c < LG_LMAX; ++c) {
+      if (c < L) {
+        const float t = li[c] - lj_s[lane][c];
+        sl2 = fmaf(t, t, sl2);
       }
-      const float sl = sqrtf(sl2);
-      // the (j, i) entry: consecutive rows i read consecutive words
-      const float se = sqrtf(d2[j * B + i]);
-      const bool m = se <= tau || sl <= lat_thr;
-      if (!m) continue;
-      const float dd = sl - gr * se;
-      num += (double)dd * (double)dd;
-      cnt += 1.0;
-      // the pairs (i, j) and (j, i) contribute alike
-      const float coef = 4.0f * dd;
-      if (coef != 0.f && sl > 0.f) {
-        const float s = coef / sl;
+    }
+    const float sl = sqrtf(sl2);
+    const float se = sqrtf(d2[i * B + j]);
+    const bool m = se <= tau || sl <= lat_thr;
+    if (!m) continue;
+    const float dd = sl - gr * se;
+    num += (double)dd * (double)dd;
+    cnt += 1.0;
+    // the pairs (i, j) and (j, i) contribute alike
+    const float coef = 4.0f * dd;
+    if (coef != 0.f && sl > 0.f) {
+      const float s = coef / sl;
 #pragma unroll
-        for (int c = 0; c < LG_LMAX; ++c)
-          if (c < L) g[c] = fmaf(s, li[c] - lj_s[jj][c], g[c]);
-      }
+      for (int c = 0; c < LG_LMAX; ++c)
+        if (c < L) g[c] = fmaf(s, li[c] - lj_s[lane][c], g[c]);
     }
   }
-  // the row's gradient: the LG_SUB partial sums, added in sub order
+  // the row's gradient: the lanes' partial sums added by a butterfly (the same
+  // operations in the same order on every run; every lane ends with the total)
 #pragma unroll
-  for (int c = 0; c < LG_LMAX; ++c) gsum[sub][r][c] = g[c];
-  // block sums of the numerator and the count
-  for (int m = 32; m >= 1; m >>= 1) {
+  for (int c = 0; c < LG_LMAX; ++c) {
+    if (c < L) {
+      float v = g[c];
+      for (int m = 1; m < WAVE; m <<= 1) v += __shfl_xor(v, m);
+      g[c] = v;
+    }
+  }
+  if (row_ok && lane == 0)
+    for (int c = 0; c < L; ++c) grad[i * L + c] = g[c];
+  for (int m = 1; m < WAVE; m <<= 1) {
     num += __shfl_xor(num, m);
     cnt += __shfl_xor(cnt, m);
   }
-  if ((tid & 63) == 0) {
-    red[0][tid >> 6] = num;
-    red[1][tid >> 6] = cnt;
+  if (lane == 0) {
+    red[0][w] = num;
+    red[1][w] = cnt;
   }
   __syncthreads();
-  if (sub == 0 && row_ok)
-    for (int c = 0; c < L; ++c) {
-      float v = gsum[0][r][c];
-      for (int s2 = 1; s2 < LG_SUB; ++s2) v += gsum[s2][r][c];
-      atomicAdd(&grad[i * L + c], v);   // the column blocks of row i meet here
-    }
   if (tid == 0) {
     double tn = 0.0, tc = 0.0;
-    for (int w = 0; w < 256 / WAVE; ++w) {
-      tn += red[0][w];
-      tc += red[1][w];
+    for (int k = 0; k < LG_WAVES; ++k) {
+      tn += red[0][k];
+      tc += red[1][k];
     }
     atomicAdd(&num_cnt[0], tn);
     atomicAdd(&num_cnt[1], tc);
@@ -239,15 +237,11 @@ hipError_t launch_lsim_grad(const float *d2, const float *lat, int64_t B, int L,
                             float tau, double *num_cnt, float *grad, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   hipError_t e = launch_fill_i32((int32_t *)num_cnt, 4, 0, s);
-  if (e == hipSuccess) e = launch_fill_i32((int32_t *)grad, B * L, 0, s);
   if (e != hipSuccess) return e;
-  // row blocks x column blocks: at least ~1024 blocks so every SIMD holds waves
-  const int64_t rb = (B + LG_ROWS - 1) / LG_ROWS;
-  int64_t cb = (1024 + rb - 1) / rb;
-  if (cb > rb) cb = rb;
-  if (cb < 1) cb = 1;
-  hipLaunchKernelGGL(k_lsim_grad, dim3((unsigned)rb, (unsigned)cb), dim3(256), 0, s, d2, lat, B,
-                     L, gr, tau, num_cnt, grad);
+  // one wave per row: every row's gradient is written once, by its wave
+  const int64_t nb = (B + LG_WAVES - 1) / LG_WAVES;
+  hipLaunchKernelGGL(k_lsim_grad, dim3((unsigned)nb), dim3(256), 0, s, d2, lat, B, L, gr, tau,
+                     num_cnt, grad);
   return hipGetLastError();
 }
 

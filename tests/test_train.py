@@ -141,3 +141,69 @@ def test_gpu_lsim_against_oracle(B, E, L):
     gref = lt64.grad.numpy()
     got = lt.grad.cpu().numpy().astype(np.float64)
     assert np.abs(got - gref).max() <= 1e-4 * np.abs(gref).max()
+
+
+@pytest.mark.gpu
+def test_gpu_lsim_grad_reproducible():
+    """The latent gradient of a 4096-row batch (24-bit codes, the 1B
+    workload's shape) is the same bit for bit on repeated calls, with other
+    work on the device in between, and equals an fp64 sum of the same pairs
+    within 1e-4 of its largest entry; the mask count is exact (tau_emb sits in
+    a gap of width >= 1e-5 relative among the values either threshold sees)."""
+    dev = _gpu()
+    from paper_2608_15438_amd import neuroute as NR
+    B, E, L = 4096, 128, 24
+    x, lat = _batch(B, E, L, 11)
+    xt = torch.from_numpy(x).to(dev)
+    lt = torch.from_numpy(lat).to(dev)
+    d2 = NR.nr_pair_sqdist(xt)
+    g = 0.6 * math.sqrt(L / E)
+    se = np.sqrt(d2.cpu().numpy().astype(np.float64))
+    ld = lat.astype(np.float64)
+    sq = (ld * ld).sum(1)
+    sl = np.sqrt(np.maximum(sq[:, None] + sq[None, :] - 2.0 * ld @ ld.T, 0.0))
+    iu = np.triu_indices(B, 1)
+    vals = np.sort(np.concatenate([se[iu], sl[iu] / g]))
+    lo, hi = np.searchsorted(vals, np.quantile(se[iu], [0.015, 0.025]))
+    k = lo + int(np.argmax(vals[lo + 1:hi + 1] - vals[lo:hi]))
+    tau = float(np.float32(0.5 * (vals[k] + vals[k + 1])))
+    assert vals[k + 1] - vals[k] >= 1e-5 * tau
+    nc1, g1 = NR.nr_lsim_grad(d2, lt, g, tau)
+    for _ in range(3):
+        NR.nr_pair_sqdist(xt)
+        nc2, g2 = NR.nr_lsim_grad(d2, lt, g, tau)
+        assert torch.equal(g1, g2)
+        assert float(nc1[1]) == float(nc2[1])
+    m = (se <= tau) | (sl <= g * tau)
+    np.fill_diagonal(m, False)
+    assert float(nc1[1]) == float(m.sum())
+    ref = np.zeros((B, L))
+    for r0 in range(0, B, 256):
+        r1 = r0 + 256
+        diff = ld[r0:r1, None, :] - ld[None, :, :]
+        slr = np.sqrt((diff ** 2).sum(2))
+        mr = m[r0:r1] & (slr > 0)
+        coef = np.zeros_like(slr)
+        coef[mr] = 4.0 * (slr[mr] - g * se[r0:r1][mr]) / slr[mr]
+        ref[r0:r1] = (coef[:, :, None] * diff).sum(1)
+    got = g1.cpu().numpy().astype(np.float64)
+    assert np.abs(got - ref).max() <= 1e-4 * np.abs(ref).max()
+
+
+@pytest.mark.gpu
+def test_gpu_training_reproducible():
+    """Two L_sim trainings of the seeded 1M x 128 uint8 encoder (20 Adam
+    steps of 4096 rows, the same sampling seed) end with the same weights bit
+    for bit: the index built from them does not change between runs."""
+    dev = _gpu()
+    from synth import configs as CF
+    from synth.gpu import GpuRows
+    from paper_2608_15438_amd import index_build as IB
+    w = CF.WORKLOADS[2]
+    data = GpuRows(w, "data", dev)
+    encs = [TR.train_encoder(IB.seeded_encoder(w), data, w.n, 20, batch=4096, lr=5e-4,
+                             gamma=0.6, seed=5, device=dev) for _ in range(2)]
+    for a, b in zip(encs[0].weights + encs[0].biases, encs[1].weights + encs[1].biases):
+        assert np.array_equal(np.asarray(a), np.asarray(b))
+    w0 = IB.seeded_encoder(w).weights[0]
+    assert not np.array_equal(np.asarray(encs[0].weights[0]), w0)
