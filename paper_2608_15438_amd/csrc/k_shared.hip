@@ -659,9 +659,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
         const uint32_t qsl = (uint32_t)__shfl((int)myq, sl);
         qload[t] = *(const uint4 *)(queries + (uint64_t)qsl * rb + (off < rb ? off : 0));
       }
-      const int64_t own_id = a.own_ids[(int64_t)myq * k + k - 1];
-      const float own_d = a.own_dists[(int64_t)myq * k + k - 1];
-      const uint2 qn = IS_U8 ? a.qnorm[myq] : make_uint2(0, 0);
+      const uint4 rec = a.qrec[myq];
 #pragma unroll
       for (int t = 0; t < QL; ++t) {
         const int c = t * WAVE + lnb;
@@ -670,18 +668,10 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
         qs[c] = sl < nqs && off < rb ? qload[t] : make_uint4(0, 0, 0, 0);
       }
       if (lnb < nqs) {
-        const uint32_t bound =
-            own_id < 0 ? 0xffffffffu : (a.is_u8 ? (uint32_t)own_d : __float_as_uint(own_d));
         qi[lnb] = myq;
-        tk[lnb] = bound;
-        if (IS_U8) {
-          qqs[lnb] = (int32_t)qn.x;
-          th[lnb] = bound == 0xffffffffu ? INT32_MAX : (int32_t)((int64_t)bound - (int64_t)qn.y);
-        } else {
-          qqs[lnb] = 0;
-          th[lnb] = bound == 0xffffffffu ? (int32_t)__float_as_uint(INFINITY)
-                                         : (int32_t)__float_as_uint(__uint_as_float(bound) * 1.0001f);
-        }
+        tk[lnb] = rec.x;
+        th[lnb] = (int32_t)rec.y;
+        qqs[lnb] = (int32_t)rec.z;
       }
       __builtin_amdgcn_wave_barrier();
 
@@ -1026,6 +1016,37 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
   if (lane == 0 && body_bytes) atomicAdd((unsigned long long *)&a.wstats[4], body_bytes);
 }
 
+// The scan's record of each query, one thread per query, once the seed merge
+// has written the query's own top-k: its bound (the k-th key of the seed
+// pass, or all ones while that list is short), the bound the head test
+// compares with, and |q|^2 for uint8 rows.  uint8 keys are integers, so the
+// head bound is the key minus |q head|^2 (a row's head part of the distance
+// is |x_h|^2 - 2 x_h.q_h + |q_h|^2); fp32 rows keep a relative margin of 1e-4
+// over the key for the rounding of the head's partial sum.
+__global__ void __launch_bounds__(256) k_scan_qrec(SharedArgs a) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= a.nq) return;
+  const int k = a.k;
+  const int64_t own_id = a.own_ids[q * k + k - 1];
+  const float own_d = a.own_dists[q * k + k - 1];
+  const uint32_t bound =
+      own_id < 0 ? 0xffffffffu : (a.is_u8 ? (uint32_t)own_d : __float_as_uint(own_d));
+  uint4 r;
+  r.x = bound;
+  r.w = 0;
+  if (a.is_u8) {
+    const uint2 qn = a.qnorm[q];
+    r.y = (uint32_t)(bound == 0xffffffffu ? INT32_MAX
+                                          : (int32_t)((int64_t)bound - (int64_t)qn.y));
+    r.z = qn.x;
+  } else {
+    r.y = bound == 0xffffffffu ? __float_as_uint(INFINITY)
+                               : __float_as_uint(__uint_as_float(bound) * 1.0001f);
+    r.z = 0;
+  }
+  a.qrec[q] = r;
+}
+
 template <int IS_U8, int NSEG>
 static hipError_t launch_scan_h(const SharedArgs &a, int hl, int grid, hipStream_t s) {
   switch (hl) {
@@ -1055,6 +1076,9 @@ hipError_t launch_shared_refine(const SharedArgs &a, int dtype, int n_cu, hipStr
   const int hl = a.scan_head / 16;
   if (nseg > SHARED_MAX_NSEG || a.scan_head % 16 != 0 || a.scan_head > a.row_bytes)
     return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_scan_qrec, dim3((unsigned)((a.nq + 255) / 256)), dim3(256), 0, s, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const int grid = n_cu * NR_SHARED_BLOCKS_PER_CU;
   return dtype == NR_U8 ? launch_scan_t<1>(a, nseg, hl, grid, s)
                         : launch_scan_t<0>(a, nseg, hl, grid, s);

@@ -86,6 +86,7 @@ struct Buffers {
   uint32_t *thr_n, *thr_h, *blk_n, *blk_h;
   uint64_t *thr_w, *blk_w, *lmeta;
   uint2 *qnorm;
+  uint4 *qrec;
   uint64_t *swork_off;
   int64_t *wstats;
   bool shared;
@@ -156,6 +157,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.pair_q = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.pair_rank = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.qnorm = c.take<uint2>((size_t)s.nq);
+    B.qrec = c.take<uint4>((size_t)s.nq);
     B.hist = c.take<uint32_t>(nc1);
     B.touched = c.take<uint32_t>((size_t)nr::list_words(s.n_clusters));
     B.hpos = c.take<uint32_t>(nc1);
@@ -624,6 +626,7 @@ nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q
   a.swork_off = B.swork_off;
   a.pair_q = B.pair_q;
   a.qnorm = B.qnorm;
+  a.qrec = B.qrec;
   a.scnt = B.scnt;
   a.skey = B.skey;
   a.sid = B.sid;

@@ -255,6 +255,8 @@ struct SharedArgs {
   int eager_rows;             // 1: rfull gets the rows of the whole list (else the leading ones)
   uint32_t *pair_q;           // [pairs] query of each scanned pair, grouped by cluster
   uint2 *qnorm;               // [nq] uint8 rows: (|q|^2, |q head|^2 over scan_head bytes)
+  uint4 *qrec;                // [nq] the scan's record of a query, written after the seed
+                              // merge: (bound key, head threshold, |q|^2, 0)
   int32_t *scnt;              // [nq] survivors appended
   uint32_t *skey;             // [nq x SURVIVOR_CAP]
   int64_t *sid;
