@@ -94,6 +94,43 @@ def test_encoder_logits(dev, name):
     assert np.all(err <= 1e-4 * c["mag"] + 1e-30), float((err / c["mag"]).max())
 
 
+@pytest.mark.parametrize("widths,dtype,nq,offset", [
+    ((36, 50, 13), "f32", 301, 0),     # a hidden width not a multiple of 4: one element per load
+    ((32, 64, 9), "f32", 77, 1),       # a query block not 16-byte aligned
+    ((32, 66, 30, 9), "u8", 130, 0),   # uint8 rows, odd hidden widths, three layers
+    ((128, 256, 24), "u8", 1500, 0),   # the 1B encoder's shape: 32 x 64 tiles, then the code layer
+    ((96, 512, 20), "f32", 8200, 0),   # 64 x 64 tiles (the grid fills the chip)
+])
+def test_encoder_layer_shapes(dev, widths, dtype, nq, offset):
+    """Seeded encoders with BatchNorm on the hidden layers, against the
+    oracle within 1e-4 of each logit's magnitude: the tile shapes the layer
+    sizes select, the four-element loads and the one-element path."""
+    from paper_2608_15438_amd import index_build as IB
+    rng = np.random.default_rng(sum(widths) + nq)
+    L = len(widths) - 1
+    Ws = [(rng.standard_normal((widths[l + 1], widths[l])) / np.sqrt(widths[l])).astype(np.float32)
+          for l in range(L)]
+    bs = [(0.1 * rng.standard_normal(widths[l + 1])).astype(np.float32) for l in range(L)]
+    sc = [(1.0 + 0.2 * rng.standard_normal(widths[l + 1])).astype(np.float32) for l in range(L - 1)]
+    sh = [(0.1 * rng.standard_normal(widths[l + 1])).astype(np.float32) for l in range(L - 1)]
+    scale = 1.0 / 255.0 if dtype == "u8" else 1.0
+    enc = IB.Encoder(Ws, bs, scale, sc, sh)
+    if dtype == "u8":
+        Q = rng.integers(0, 256, size=(nq, widths[0]), dtype=np.uint8)
+    else:
+        Q = rng.standard_normal((nq, widths[0])).astype(np.float32)
+    exp, mag = O.encode(O.Encoder(Ws, bs, sc, sh, scale), Q, with_mag=True)
+    gix = NR.Index.encoder_only(enc, NR.NR_U8 if dtype == "u8" else NR.NR_F32)
+    flat = torch.from_numpy(np.ascontiguousarray(Q)).reshape(-1)
+    buf = torch.zeros(flat.numel() + offset, dtype=flat.dtype, device=dev)
+    buf[offset:] = flat.to(dev)
+    Qd = buf[offset:].view(nq, widths[0])
+    got = gix.nr_encode(Qd).cpu().numpy()
+    gix.close()
+    err = np.abs(got.astype(np.float64) - exp)
+    assert np.all(err <= 1e-4 * mag + 1e-30), float((err / mag).max())
+
+
 # ------------------------------------------------------------------ step 2
 @pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("P", [1, 7, 64, 300, 1024, 2048, 4096])
