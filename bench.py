@@ -73,6 +73,9 @@ def parse():
                     help="refinement schedule (the same results either way)")
     ap.add_argument("--seed-rows", type=int, default=0,
                     help="shared schedule: rows of each query's own (seed) pass; 0 = the library's")
+    ap.add_argument("--gt-cache", type=str, default="",
+                    help="directory for the exact top-k of the query and calibration sets "
+                         "(reused by later runs on the same workload)")
     ap.add_argument("--quick", action="store_true",
                     help="no recall ground truth and no oracle (for counter passes)")
     ap.add_argument("--copy-calib", action="store_true",
@@ -179,10 +182,11 @@ def copy_calibration(torch, dev, gib=4, reps=5):
     print(json.dumps({"copy_bytes_per_launch": src.numel(), "launches": reps}), flush=True)
 
 
-def measured_traffic(kernel, workload):
+def measured_traffic(kernel, workload, probe_budget):
     """HBM bytes per launch of `kernel` from the committed counter record
     (FETCH_SIZE + WRITE_SIZE, each scaled by a copy of known size), or None
-    when there is none or the kernel's sources changed since it was taken."""
+    when there is none, the kernel's sources changed since it was taken, or
+    it was taken at another probe budget."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
     try:
         rec = json.load(open(path))
@@ -191,6 +195,10 @@ def measured_traffic(kernel, workload):
     from paper_2608_15438_amd.counters import source_digest
     if rec.get("source_sha256") != source_digest(kernel):
         log(f"traffic record {os.path.basename(path)} is stale (kernel sources changed)")
+        return None
+    if rec.get("probe_budget") != probe_budget:
+        log(f"traffic record {os.path.basename(path)} was taken at P = {rec.get('probe_budget')}, "
+            f"not {probe_budget}")
         return None
     return int(rec["hbm_bytes_per_launch"])
 
@@ -265,9 +273,30 @@ def main():
     ng = 0 if args.quick else min(args.gt_queries, w.n_queries)
     nc = args.calib_queries
     Qc = GpuRows(w, "calib", dev).range(0, nc)
-    gt_all, _ = ground_truth(torch, lambda a, b: IB.payload_range(ix, a, b), w.n, w.dtype == "u8",
-                             ix.row_ids, torch.cat([Q[:ng], Qc]), k)
-    gt_ids, gtc = gt_all[:ng], gt_all[ng:]
+    # exact top-k of the query and calibration sets: they depend on the base
+    # rows and the query sets only, so --gt-cache keeps them across runs
+    cache = {}
+    if args.gt_cache:
+        os.makedirs(args.gt_cache, exist_ok=True)
+        for what, m in (("query", ng), ("calib", nc)):
+            path = os.path.join(args.gt_cache, f"{w.name}-n{w.n}-k{k}-{what}{m}.npy")
+            cache[what] = (path, np.load(path) if m and os.path.exists(path) else None)
+    need_q = ng > 0 and cache.get("query", (None, None))[1] is None
+    need_c = nc > 0 and cache.get("calib", (None, None))[1] is None
+    if need_q or need_c:
+        parts = ([Q[:ng]] if need_q else []) + ([Qc] if need_c else [])
+        gt_new, _ = ground_truth(torch, lambda a, b: IB.payload_range(ix, a, b), w.n,
+                                 w.dtype == "u8", ix.row_ids, torch.cat(parts), k)
+        if need_q:
+            cache["query"] = (cache.get("query", (None, None))[0], gt_new[:ng])
+        if need_c:
+            cache["calib"] = (cache.get("calib", (None, None))[0], gt_new[ng if need_q else 0:])
+        for what in ("query", "calib"):
+            path, arr = cache[what]
+            if path and arr is not None and not os.path.exists(path):
+                np.save(path, arr)
+    gt_ids = cache["query"][1] if ng else np.zeros((0, k), np.int64)
+    gtc = cache["calib"][1] if nc else np.zeros((0, k), np.int64)
     log(f"ground truth for {ng}+{nc} queries in {time.time() - t0:.1f}s")
     targets = torch.from_numpy(gtc).to(dev)
     if args.calib == "bootstrap":
@@ -398,7 +427,7 @@ def main():
     refine_ms = kernels[dom]["avg_launch_ms"]
     alg_bytes = kernels[dom]["alg_bytes_per_launch"]
     achieved = kernels[dom]["achieved_gbs"]
-    traffic = measured_traffic(dom, w.name)
+    traffic = measured_traffic(dom, w.name, P)
     # the whole refinement stage (step 5): every launch from the plan to the merge
     st5 = sum(stage_ms[x] for x in ("plan", "refine", "merge", "shared_prep", "shared_scan",
                                     "shared_open", "shared_merge")) / nt

@@ -11,7 +11,7 @@
 
     python -m paper_2608_15438_amd.counters traffic --kernel NAME --workload W \\
         --fetch F.csv --write W.csv --copy-fetch CF.csv --copy-write CW.csv \\
-        --copy-bytes N [--command TEXT]
+        --copy-bytes N --probe-budget P [--command TEXT]
         HBM traffic record (JSON) of one kernel from two --pmc passes
         (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by what the
         same counter reads for a device copy of N bytes per launch.
@@ -97,6 +97,7 @@ def traffic(a) -> dict:
             "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
             "hbm_fetch_bytes_per_launch": int(fb), "hbm_write_bytes_per_launch": int(wb),
             "hbm_bytes_per_launch": int(fb + wb),
+            "probe_budget": a.probe_budget,
             "command": a.command}
 
 
@@ -180,6 +181,8 @@ def main(argv=None):
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--copy-kernel", default="copy")
     t.add_argument("--command", default="")
+    t.add_argument("--probe-budget", type=int, required=True,
+                   help="probe budget of the profiled search (a record holds for that budget only)")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         print(stats(a.csv))
