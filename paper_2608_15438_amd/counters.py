@@ -102,7 +102,7 @@ def traffic(a) -> dict:
 
 
 def stats(path: str) -> str:
-    keep = ("nr::", "synth", "rocprim")
+    keep = ("nr::", "synth")
     lines = ["| kernel | calls | avg us | min us | max us | total ms |",
              "|---|---:|---:|---:|---:|---:|"]
     for r in _rows(path):
