@@ -203,6 +203,72 @@ __device__ __forceinline__ void topk_insert(TopK &t, int k, uint32_t ck, int64_t
   }
 }
 
+// The refinement's running top-k: like TopK, but an entry's original id is
+// read only when it decides something -- a candidate whose key equals a key in
+// the list (ids order equal keys) -- or when the tile's list is written out,
+// so the row loop does not wait for id loads.  Entries keep their payload row
+// (phys) until then; `known` marks the lanes whose id has been read.
+struct LazyTopK {
+  uint32_t key;
+  int64_t id;
+  uint64_t phys;
+  bool known;
+  int cnt;
+  uint32_t kth_key;
+};
+
+__device__ __forceinline__ void ltopk_init(LazyTopK &t) {
+  t.key = 0xffffffffu;
+  t.id = -1;
+  t.phys = 0;
+  t.known = true;
+  t.cnt = 0;
+  t.kth_key = 0xffffffffu;
+}
+
+// insert the payload row cp with key ck if (ck, its id) ranks among the k best
+// (wave-uniform arguments); ids are ordered as in TopK
+__device__ __forceinline__ void ltopk_insert(LazyTopK &t, int k, uint32_t ck, uint64_t cp,
+                                             const int64_t *row_ids) {
+  const int lane = lane_id();
+  if (t.cnt == k && ck > t.kth_key) return;
+  // ids matter only among equal keys: read the candidate's and those of the
+  // listed entries with its key (one round of loads, rare)
+  const bool eq = lane < t.cnt && t.key == ck;
+  int64_t cid = -1;
+  bool cknown = false;
+  if (ballot(eq)) {
+    cid = row_ids[cp];
+    cknown = true;
+    if (eq && !t.known) {
+      t.id = row_ids[t.phys];
+      t.known = true;
+    }
+    // a tie with the k-th entry: the candidate enters only below its id
+    if (t.cnt == k && ck == t.kth_key &&
+        cid >= (int64_t)bcast_u64((uint64_t)t.id, k - 1)) return;
+  }
+  const bool less = lane < t.cnt && (t.key < ck || (t.key == ck && t.id < cid));
+  const int pos = popc64(ballot(less));
+  const uint32_t up_key = (uint32_t)__shfl_up((int)t.key, 1);
+  const int64_t up_id = (int64_t)shfl_up_u64((uint64_t)t.id, 1);
+  const uint64_t up_phys = shfl_up_u64(t.phys, 1);
+  const bool up_known = __shfl_up((int)t.known, 1) != 0;
+  if (lane == pos) {
+    t.key = ck;
+    t.id = cid;
+    t.phys = cp;
+    t.known = cknown;
+  } else if (lane > pos && lane < k) {
+    t.key = up_key;
+    t.id = up_id;
+    t.phys = up_phys;
+    t.known = up_known;
+  }
+  t.cnt = t.cnt + 1 < k ? t.cnt + 1 : k;
+  if (t.cnt == k) t.kth_key = bcast_u32(t.key, k - 1);
+}
+
 // ------------------------------------------------------------------ refine
 #ifndef NR_REFINE_WAVES1
 #define NR_REFINE_WAVES1 1      // waves per SIMD the registers are sized for (128-byte rows; 1: free)
@@ -276,8 +342,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
       qq += __shfl_xor(qq, 2);
       qq += __shfl_xor(qq, 4);
     }
-    TopK tk;
-    topk_init(tk);
+    LazyTopK tk;
+    ltopk_init(tk);
 
     uint32_t v = v0;
     while (v < v1) {
@@ -291,7 +357,13 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
       if (lane == 0) vs[ns] = pre[c + ns];
       __builtin_amdgcn_wave_barrier();
       const uint32_t vend = v1 < vs[ns] ? v1 : vs[ns];
-      int cur = 0;  // per lane group; rows of a group only increase
+      // per lane group (rows of a group only increase): the staged cluster
+      // holding its rows, its first virtual row and physical row, and the
+      // next cluster's first virtual row, kept in registers so that a row
+      // costs an LDS read only where it crosses into the next cluster
+      int cur = 0;
+      uint32_t vcur = vs[0], vnext = vs[1];
+      uint64_t pcur = ps[0];
       for (uint32_t vb = v; vb < vend; vb += 8 * U) {
         uint64_t phys[U];
         bool ok[U];
@@ -301,8 +373,15 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
           ok[u] = rv < vend;
           phys[u] = 0;
           if (ok[u]) {
-            while (vs[cur + 1] <= rv) ++cur;
-            phys[u] = ps[cur] + (rv - vs[cur]);
+            if (vnext <= rv) {
+              do {
+                ++cur;
+                vnext = vs[cur + 1];
+              } while (vnext <= rv);
+              vcur = vs[cur];
+              pcur = ps[cur];
+            }
+            phys[u] = pcur + (rv - vcur);
           }
         }
         uint32_t key[U];
@@ -452,7 +531,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
           }
         }
         }
-        // candidates that may enter the top-k read their original id
+        // rows that may enter the top-k, in row order
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           uint64_t m = ballot(ok[u] && gl == 0 && key[u] <= tk.kth_key);
@@ -461,9 +540,7 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
             m &= m - 1;
             const uint32_t ck = bcast_u32(key[u], src);
             if (tk.cnt == k && ck > tk.kth_key) continue;
-            const uint64_t cp = bcast_u64(phys[u], src);
-            const int64_t id = a.row_ids[cp];
-            topk_insert(tk, k, ck, id);
+            ltopk_insert(tk, k, ck, bcast_u64(phys[u], src), a.row_ids);
           }
         }
       }
@@ -471,7 +548,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
       c += ns;
       __builtin_amdgcn_wave_barrier();
     }
-    // partial result of this tile
+    // partial result of this tile: the ids not read yet, all at once
+    if (lane < tk.cnt && !tk.known) tk.id = a.row_ids[tk.phys];
     if (lane < k) {
       a.pkey[(int64_t)t * k + lane] = lane < tk.cnt ? tk.key : 0xffffffffu;
       a.pid[(int64_t)t * k + lane] = lane < tk.cnt ? tk.id : -1;
@@ -498,10 +576,11 @@ static hipError_t launch_refine_t(const RefineArgs &a, int nseg, int grid, hipSt
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s) {
+hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, int blocks_per_cu,
+                         hipStream_t s) {
   if (a.nq <= 0) return hipSuccess;
   const int nseg = (a.row_bytes + 127) / 128;
-  const int grid = n_cu * NR_REFINE_BLOCKS_PER_CU;
+  const int grid = n_cu * (blocks_per_cu > 0 ? blocks_per_cu : NR_REFINE_BLOCKS_PER_CU);
   return dtype == NR_U8 ? launch_refine_t<1>(a, nseg, grid, s) : launch_refine_t<0>(a, nseg, grid, s);
 }
 

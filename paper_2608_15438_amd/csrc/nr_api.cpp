@@ -550,7 +550,9 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   ra.pkey = B.pkey;
   ra.pid = B.pid;
   ra.rbytes = (unsigned long long *)(B.wstats + 6);
-  e = nr::launch_refine(ra, ix->d.dtype, ix->n_cu, s);
+  // beside the scan's preparation, four blocks per CU (four waves per SIMD)
+  // leave its kernels room to run under the seed pass instead of after it
+  e = nr::launch_refine(ra, ix->d.dtype, ix->n_cu, o.prep ? 4 : 0, s);
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[1], s);
   nr::MergeArgs ma{};

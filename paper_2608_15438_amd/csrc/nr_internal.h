@@ -288,7 +288,10 @@ constexpr int ROUTE_MID_HEAP = 2048;   // and of its second when K_c is larger s
 size_t route_lds_bytes(int k_c, int pst);
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
-hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, hipStream_t s);
+// blocks_per_cu: 0 for the tuned default; fewer leave room on every CU for
+// work on another stream (the scan's preparation beside the seed pass)
+hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, int blocks_per_cu,
+                         hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
 // fresh: the workspace is new, so clear the pair counts and the bitmap
 hipError_t launch_shared_hist(const SharedArgs &a, bool fresh, hipStream_t s);
