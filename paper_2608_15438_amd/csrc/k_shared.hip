@@ -281,6 +281,8 @@ __global__ void __launch_bounds__(LIST_THREADS) k_list_emit(SharedArgs a) {
       const uint64_t sz = a.cl_off[c + 1] - a.cl_off[c];
       a.hist[c] = 0u;
       a.slist[i] = (uint32_t)c;
+      a.lbase[i] = a.cl_off[c];
+      a.lsz[i] = (uint32_t)sz;
       a.lpair[i] = hp;
       a.lpm[i] = hc;
       a.swork_off[i] = wo;
@@ -488,6 +490,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
   __shared__ uint32_t s_qi[4][QMAX];             // query id
   __shared__ int32_t s_qq[4][QMAX];              // |q|^2 (uint8)
   __shared__ uint32_t s_sv[4][SCAP];             // listed rows: unit << 20 | row << 8 | mask
+  __shared__ uint8_t s_umap[4][WAVE];            // batch formation: unit -> staged entry
+  __shared__ uint32_t s_pslot[4][QMAX];          // batch formation: slot -> pair index
   __shared__ uint32_t s_run[4][LONG && IS_U8 ? SCAP * G : 1];  // long uint8 rows: running x.q per (listed row, query)
   constexpr int OPENL = 128;                     // long fp32 rows: open pairs held before they go out
   __shared__ uint32_t s_ol[4][LONG && !IS_U8 ? OPENL : 1];  // listed row << 8 | query slot
@@ -507,6 +511,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
   uint32_t *qi = s_qi[w];
   int32_t *qqs = s_qq[w];
   uint32_t *sv = s_sv[w];
+  uint8_t *umap = s_umap[w];
+  uint32_t *pslot = s_pslot[w];
   uint32_t *run = s_run[w];
   int32_t *runx = s_runx[w];
   uint32_t *ol = s_ol[w];
@@ -542,108 +548,126 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
       lo = nlo;
       hi = nhi;
     }
+    // the first unit of entry i = lo that starts at or after ws: unit uo of
+    // the entry, units numbered group-major (gi * nch + ch).  The entry
+    // holding ws has work, so sz > 0; the guard keeps the division defined.
     int64_t i = lo;
-    // metadata of entries ib .. ib + 63, one per lane
-    int64_t ib = i;
-    uint64_t l_wo = 0, l_base = 0, l_sz = 0;
-    uint32_t l_hp = 0, l_m = 0;
-    auto stage = [&]() {
-      const int64_t ii = ib + lane;
-      l_wo = 0;
-      l_base = 0;
-      l_sz = 0;
-      l_hp = 0;
-      l_m = 0;
-      if (ii < NS) {
-        const uint32_t c = a.slist[ii];
-        l_wo = a.swork_off[ii];
-        l_base = a.cl_off[c];
-        l_sz = a.cl_off[(uint64_t)c + 1] - l_base;
-        l_hp = a.lpair[ii];
-        l_m = a.lpm[ii];
-      }
-    };
-    stage();
-    uint64_t wo = bcast_u64(l_wo, 0), base = bcast_u64(l_base, 0), sz = bcast_u64(l_sz, 0);
-    uint32_t hp = bcast_u32(l_hp, 0), mq = bcast_u32(l_m, 0);
-    uint64_t nch = (sz + SHARED_ROWS - 1) / SHARED_ROWS;
-    uint32_t ng = (mq + G - 1) / G;
-    // the first unit of entry i that starts at or after ws (the entry holding
-    // ws has work, so sz > 0; the guard keeps the division defined regardless)
-    uint32_t gi = 0;
-    uint64_t ch = 0;
-    if (sz > 0) {
-      const uint64_t rel = ws - wo;
-      gi = (uint32_t)(rel / sz);
-      ch = (rel - (uint64_t)gi * sz + SHARED_ROWS - 1) / SHARED_ROWS;
-    }
-    bool have = true;
-    auto next_entry = [&]() {
-      do {
+    uint32_t uo = 0;
+    {
+      const uint64_t wo0 = a.swork_off[i];
+      const uint64_t sz0 = a.lsz[i];
+      const uint32_t m0 = a.lpm[i];
+      if (sz0 > 0) {
+        const uint64_t rel = ws - wo0;
+        uint64_t gi0 = rel / sz0;
+        uint64_t ch0 = (rel - gi0 * sz0 + SHARED_ROWS - 1) / SHARED_ROWS;
+        const uint64_t nch0 = (sz0 + SHARED_ROWS - 1) / SHARED_ROWS;
+        if (ch0 >= nch0) {
+          ch0 = 0;
+          ++gi0;
+        }
+        if (gi0 >= (m0 + G - 1) / G) {
+          ++i;
+        } else {
+          uo = (uint32_t)(gi0 * nch0 + ch0);
+        }
+      } else {
         ++i;
-        if (i >= NS) {
-          have = false;
-          return;
-        }
-        if (i - ib >= WAVE) {
-          ib = i;
-          stage();
-        }
-        const int src = (int)(i - ib);
-        wo = bcast_u64(l_wo, src);
-        base = bcast_u64(l_base, src);
-        sz = bcast_u64(l_sz, src);
-        hp = bcast_u32(l_hp, src);
-        mq = bcast_u32(l_m, src);
-      } while (sz == 0);
-      nch = (sz + SHARED_ROWS - 1) / SHARED_ROWS;
-      ng = (mq + G - 1) / G;
-      gi = 0;
-      ch = 0;
-    };
-    auto next_unit = [&]() {
-      if (++ch >= nch) {
-        ch = 0;
-        if (++gi >= ng) next_entry();
       }
-    };
-    if (sz == 0) {
-      next_entry();
-    } else if (ch >= nch) {
-      ch = 0;
-      if (++gi >= ng) next_entry();
     }
 
-    while (have && wo + (uint64_t)gi * sz + ch * SHARED_ROWS < we) {
-      // ---- a batch of consecutive units of this tile; lane s fetches the
-      // query of slot s as its unit joins, and nothing waits for those loads
-      // until the batch is complete
+    for (;;) {
+      // ---- a batch: the units of this tile from (i, uo) on, one per lane,
+      // while their query slots fit.  Lane j stages entry i + j; the units of
+      // the staged entries are numbered by a prefix sum and lane u takes unit u
+      if (i >= NS) break;
+      int lnb = lane;
       // the lane id made opaque here, so the addresses derived from it in the
       // batch setup are recomputed per batch rather than kept live (and
       // spilled) across the whole kernel
-      int lnb = lane;
       __asm__ volatile("" : "+v"(lnb));
-      int nu = 0, nqs = 0, gmax = 0;
-      uint32_t vtot = 0;
-      uint32_t myq = 0;
-      while (have && nu < SCAN_UMAX && wo + (uint64_t)gi * sz + ch * SHARED_ROWS < we) {
-        const int gm = mq - gi * G < (uint32_t)G ? (int)(mq - gi * G) : G;
-        if (nqs + gm > QMAX) break;
-        const uint64_t r0 = ch * SHARED_ROWS;
-        const uint32_t nrows = (uint32_t)(r0 + SHARED_ROWS < sz ? SHARED_ROWS : sz - r0);
-        if (lane == 0) {
-          ub[nu] = base + r0;
-          uv[nu] = vtot;
-          uq[nu] = (uint32_t)nqs | ((uint32_t)gm << 16);
-        }
-        if (lnb >= nqs && lnb < nqs + gm) myq = a.pair_q[hp + gi * G + (lnb - nqs)];
-        ++nu;
-        nqs += gm;
-        vtot += nrows;
-        gmax = gm > gmax ? gm : gmax;
-        next_unit();
+      const int64_t e = i + lnb;
+      uint64_t ewo = 0, ebase = 0;
+      uint32_t esz = 0, ehp = 0, em = 0;
+      if (e < NS) {
+        ewo = a.swork_off[e];
+        ebase = a.lbase[e];
+        esz = a.lsz[e];
+        ehp = a.lpair[e];
+        em = a.lpm[e];
       }
-      if (lane == 0) uv[nu] = vtot;
+      const uint32_t enc = (esz + SHARED_ROWS - 1) / SHARED_ROWS;
+      const uint32_t eun = enc * ((em + G - 1) / G) - (lnb == 0 ? uo : 0u);
+      const uint32_t eincl = wave_incl_scan_u32(eun);
+      const uint32_t eexcl = eincl - eun;
+      // unit -> staged entry, for the first 64 units
+      for (uint32_t x = eexcl; x < eincl && x < (uint32_t)WAVE; ++x) umap[x] = (uint8_t)lnb;
+      __builtin_amdgcn_wave_barrier();
+      const uint32_t all_u = bcast_u32(eincl, WAVE - 1);
+      const uint32_t avail = all_u < (uint32_t)WAVE ? all_u : (uint32_t)WAVE;
+      if (avail == 0) {
+        // 64 entries without units (or the end of the list)
+        i += WAVE;
+        uo = 0;
+        continue;
+      }
+      const bool uok = (uint32_t)lnb < avail;
+      const int ej = uok ? (int)umap[lnb] : 0;
+      const uint64_t uwo = shfl_u64(ewo, ej);
+      const uint64_t ubase = shfl_u64(ebase, ej);
+      const uint32_t usz = (uint32_t)__shfl((int)esz, ej);
+      const uint32_t uhp = (uint32_t)__shfl((int)ehp, ej);
+      const uint32_t um = (uint32_t)__shfl((int)em, ej);
+      const uint32_t unc = (uint32_t)__shfl((int)enc, ej);
+      const uint32_t uidx = (uint32_t)lnb - (uint32_t)__shfl((int)eexcl, ej) + (ej == 0 ? uo : 0u);
+      const uint32_t ugi = uok ? uidx / unc : 0u;
+      const uint32_t uch = uidx - ugi * unc;
+      const uint32_t ugm = uok ? (um - ugi * G < (uint32_t)G ? um - ugi * G : (uint32_t)G) : 0u;
+      const uint32_t urows = uok ? (usz - uch * SHARED_ROWS < SHARED_ROWS ? usz - uch * SHARED_ROWS
+                                                                            : SHARED_ROWS)
+                                 : 0u;
+      const uint64_t ustart = uwo + (uint64_t)ugi * usz + (uint64_t)uch * SHARED_ROWS;
+      const uint32_t sincl = wave_incl_scan_u32(ugm);
+      // the units taken: a prefix (unit starts and slot counts only grow)
+      const uint64_t nofit = ballot(!(uok && ustart < we && sincl <= (uint32_t)QMAX));
+      const int nu = nofit ? __ffsll((unsigned long long)nofit) - 1 : WAVE;
+      if (nu == 0) break;  // the next unit starts past this tile
+      const bool take = lnb < nu;
+      const uint32_t vincl = wave_incl_scan_u32(take ? urows : 0u);
+      const uint32_t vtot = bcast_u32(vincl, nu - 1);
+      const int nqs = (int)bcast_u32(sincl, nu - 1);
+      int gmax = 0;
+      {
+        uint32_t g = take ? ugm : 0u;
+        for (int o = 32; o >= 1; o >>= 1) {
+          const uint32_t h = (uint32_t)__shfl_xor((int)g, o);
+          g = h > g ? h : g;
+        }
+        gmax = (int)g;
+      }
+      if (take) {
+        ub[lnb] = ubase + (uint64_t)uch * SHARED_ROWS;
+        uv[lnb] = vincl - urows;
+        uq[lnb] = (sincl - ugm) | (ugm << 16);
+        // slots of this unit: its pairs (the query of slot s is pair_q[pslot[s]])
+        for (uint32_t t = 0; t < ugm; ++t) pslot[sincl - ugm + t] = uhp + ugi * G + t;
+      }
+      if (lnb == 0) uv[nu] = vtot;
+      __builtin_amdgcn_wave_barrier();
+      const uint32_t myq = lnb < nqs ? a.pair_q[pslot[lnb]] : 0u;
+      // where the next batch starts: the entry holding unit nu (units of the
+      // staged entries beyond the first 64 included), else past them
+      {
+        const uint64_t hold = ballot(e < NS && eexcl <= (uint32_t)nu && (uint32_t)nu < eincl);
+        if (hold) {
+          const int j = __ffsll((unsigned long long)hold) - 1;
+          uo = (uint32_t)nu - bcast_u32(eexcl, j) + (j == 0 ? uo : 0u);
+          i += j;
+        } else {
+          i += WAVE;
+          uo = 0;
+        }
+      }
       // ---- the batch's queries: rows into LDS, bounds, |q|^2 (one slot per
       // lane).  myq is a valid query id in every lane (0 in lanes without a
       // slot), so all loads go out unconditionally and together; what lies

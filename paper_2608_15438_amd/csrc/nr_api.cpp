@@ -83,6 +83,8 @@ struct Buffers {
   uint32_t *skey;
   int64_t *sid;
   uint32_t *pair_q, *hist, *pair_rank, *slist, *touched, *hpos, *lpair, *lpm;
+  uint64_t *lbase;
+  uint32_t *lsz;
   uint32_t *thr_n, *thr_h, *blk_n, *blk_h;
   uint64_t *thr_w, *blk_w, *lmeta;
   uint2 *qnorm;
@@ -164,6 +166,8 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.slist = c.take<uint32_t>(nc1);
     B.lpair = c.take<uint32_t>(nc1);
     B.lpm = c.take<uint32_t>(nc1);
+    B.lbase = c.take<uint64_t>(nc1);
+    B.lsz = c.take<uint32_t>(nc1);
     B.swork_off = c.take<uint64_t>(nc1);
     B.lmeta = c.take<uint64_t>(4);
     const size_t nblk = (size_t)nr::list_blocks(s.n_clusters);
@@ -615,6 +619,8 @@ nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q
   a.slist = B.slist;
   a.lpair = B.lpair;
   a.lpm = B.lpm;
+  a.lbase = B.lbase;
+  a.lsz = B.lsz;
   a.lmeta = B.lmeta;
   a.thr_n = B.thr_n;
   a.thr_h = B.thr_h;

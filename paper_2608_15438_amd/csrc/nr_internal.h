@@ -246,6 +246,8 @@ struct SharedArgs {
                               // with pairs only)
   uint32_t *slist;            // [n_clusters] the scan list: clusters with pairs, in order
   uint32_t *lpair, *lpm;      // [list] start in pair_q and number of pairs of entry i
+  uint64_t *lbase;            // [list] first payload row of entry i's cluster
+  uint32_t *lsz;              // [list] rows of entry i's cluster
   uint64_t *swork_off;        // [list + 1] start of entry i in the work space
   uint64_t *lmeta;            // [4] list length, pairs, work
   uint32_t *thr_n, *thr_h;    // [list_blocks x LIST_THREADS] per-thread sums of the prep
@@ -382,6 +384,11 @@ __device__ __forceinline__ uint64_t bcast_u64(uint64_t v, int src) {
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
   uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
   uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src);
+  uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src);
   return ((uint64_t)hi << 32) | lo;
 }
 __device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int m) {
