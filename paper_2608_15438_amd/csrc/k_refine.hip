@@ -364,6 +364,105 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_REFINE_WAVES1 : 1) k_refin
       int cur = 0;
       uint32_t vcur = vs[0], vnext = vs[1];
       uint64_t pcur = ps[0];
+      if constexpr (NSEG == 1) {
+        // rows of one 128-byte segment: a two-stage pipeline, the rows of the
+        // next step loading while those of this one are scored (two register
+        // buffers, the loop unrolled by two).  A row's payload index is kept
+        // only until its load is issued; an entrant's is found again from
+        // the staged clusters.
+        uint4 xa[U], xb[U];
+        auto issue = [&](uint32_t vb, uint4(&x)[U]) __attribute__((always_inline)) {
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const uint32_t rv = vb + 8 * u + g;
+            const bool ok = rv < vend;
+            uint64_t phys = 0;
+            if (ok) {
+              if (vnext <= rv) {
+                do {
+                  ++cur;
+                  vnext = vs[cur + 1];
+                } while (vnext <= rv);
+                vcur = vs[cur];
+                pcur = ps[cur];
+              }
+              phys = pcur + (rv - vcur);
+            }
+            x[u] = (ok && 16 * gl < rb) ? load_payload(a.ra.seg(phys, 16 * gl))
+                                        : make_uint4(0, 0, 0, 0);
+          }
+        };
+        auto score = [&](uint32_t vb, const uint4(&x)[U]) __attribute__((always_inline)) {
+          uint32_t key[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            if (IS_U8) {
+              uint32_t xx = 0, xq = 0;
+              xx = __builtin_amdgcn_udot4(x[u].x, x[u].x, xx, false);
+              xx = __builtin_amdgcn_udot4(x[u].y, x[u].y, xx, false);
+              xx = __builtin_amdgcn_udot4(x[u].z, x[u].z, xx, false);
+              xx = __builtin_amdgcn_udot4(x[u].w, x[u].w, xx, false);
+              xq = __builtin_amdgcn_udot4(x[u].x, qv[0].x, xq, false);
+              xq = __builtin_amdgcn_udot4(x[u].y, qv[0].y, xq, false);
+              xq = __builtin_amdgcn_udot4(x[u].z, qv[0].z, xq, false);
+              xq = __builtin_amdgcn_udot4(x[u].w, qv[0].w, xq, false);
+              int32_t part = (int32_t)xx - 2 * (int32_t)xq;
+              part += __shfl_xor(part, 1);
+              part += __shfl_xor(part, 2);
+              part += __shfl_xor(part, 4);
+              key[u] = (uint32_t)(part + qq);
+            } else {
+              float acc = 0.0f;
+              const float t0 = __uint_as_float(x[u].x) - __uint_as_float(qv[0].x);
+              const float t1 = __uint_as_float(x[u].y) - __uint_as_float(qv[0].y);
+              const float t2 = __uint_as_float(x[u].z) - __uint_as_float(qv[0].z);
+              const float t3 = __uint_as_float(x[u].w) - __uint_as_float(qv[0].w);
+              acc = fmaf(t0, t0, acc);
+              acc = fmaf(t1, t1, acc);
+              acc = fmaf(t2, t2, acc);
+              acc = fmaf(t3, t3, acc);
+              acc += __shfl_xor(acc, 1);
+              acc += __shfl_xor(acc, 2);
+              acc += __shfl_xor(acc, 4);
+              key[u] = __float_as_uint(acc);
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const bool ok = vb + 8 * u + g < vend;
+            if (ok && gl == 0) nbytes += (uint32_t)rb;
+            uint64_t m = ballot(ok && gl == 0 && key[u] <= tk.kth_key);
+            while (m) {
+              const int src = __ffsll((unsigned long long)m) - 1;
+              m &= m - 1;
+              const uint32_t ck = bcast_u32(key[u], src);
+              if (tk.cnt == k && ck > tk.kth_key) continue;
+              // the entrant's payload row: the last staged cluster starting
+              // at or before its virtual row
+              const uint32_t rv = vb + 8 * u + (uint32_t)(src >> 3);
+              int lo = 0, hi = ns - 1;
+              while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (vs[mid] <= rv) lo = mid; else hi = mid - 1;
+              }
+              ltopk_insert(tk, k, ck, ps[lo] + (rv - vs[lo]), a.row_ids);
+            }
+          }
+        };
+        uint32_t vb = v;
+        issue(vb, xa);
+        for (;;) {
+          const uint32_t vn = vb + 8 * U;
+          if (vn < vend) issue(vn, xb);
+          score(vb, xa);
+          if (vn >= vend) break;
+          const uint32_t vn2 = vn + 8 * U;
+          if (vn2 < vend) issue(vn2, xa);
+          score(vn, xb);
+          if (vn2 >= vend) break;
+          vb = vn2;
+        }
+      } else
       for (uint32_t vb = v; vb < vend; vb += 8 * U) {
         uint64_t phys[U];
         bool ok[U];

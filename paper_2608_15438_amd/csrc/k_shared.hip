@@ -13,9 +13,10 @@
 //          the final k-th entry: a later row can only enter the result if it
 //          ranks at or before it;
 //  prep    (on a second stream, beside the seed pass) the clusters with
-//          pairs, marked in a bitmap, form the scan list in cluster order with
-//          their pair and work ranges (rows x groups of <= g queries); the
-//          pairs are then scattered by cluster;
+//          pairs (nonzero pair counts, found by one sequential pass over the
+//          counts) form the scan list in cluster order with their pair and
+//          work ranges (rows x groups of <= g queries); the pairs are then
+//          scattered by cluster;
 //  scan    persistent waves take tiles of SHARED_TILE work from an atomic
 //          counter and gather consecutive units of the tile into batches
 //          whose query rows sit in LDS.  Each row's head (its first
@@ -109,15 +110,13 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
 
 // ------------------------------------------------------------------ hist
 // The pair counts are taken at the end of the route kernel, per query, once
-// its list is final (pair_hist_wave): hist[c] counts cluster c's pairs.  The
-// prep marks every cluster with pairs in the bitmap `touched` (k_touch).
-// Both start a search at zero: the prep clears what it read, so only a fresh
-// workspace needs the full clear below.
+// its list is final (pair_hist_wave): hist[c] counts cluster c's pairs.  They
+// start a search at zero: the prep clears the counts it read, so only a fresh
+// workspace needs the full clear below (hist_words(n_clusters) words, whole
+// 32-count words past the last cluster included).
 hipError_t launch_shared_hist(const SharedArgs &a, bool fresh, hipStream_t s) {
   if (!fresh) return hipSuccess;
-  hipError_t e = launch_fill_i32((int32_t *)a.hist, a.n_clusters + 1, 0, s);
-  if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.touched, list_words(a.n_clusters), 0, s);
-  return e;
+  return launch_fill_i32((int32_t *)a.hist, hist_words(a.n_clusters), 0, s);
 }
 
 PairHistArgs pair_hist_args(const SharedArgs &a) {
@@ -142,19 +141,33 @@ PairHistArgs pair_hist_args(const SharedArgs &a) {
 // ------------------------------------------------------------------ prep
 // The scan list holds the clusters with pairs in cluster order, each with
 // its pair range in pair_q and its range in the scan's work space (rows x
-// groups of <= g queries).  It is built from the `touched` bitmap, so the
-// prep costs one pass over n_clusters / 32 words plus work per listed
-// cluster, not per index cluster:
-//   count  thread t of block b owns LIST_WPT bitmap words; it sums entries,
-//          pairs and work over its set bits (block sums too);
+// groups of <= g queries).  It is built from the pair counts themselves:
+// one coalesced pass over them (4 bytes per index cluster, read 32 counts =
+// one 128-byte word per thread) plus work per listed cluster, with no
+// per-pair atomics to mark the clusters:
+//   count  thread t of block b owns LIST_WPT words of 32 counts; it sums
+//          entries, pairs and work over its nonzero counts (block sums too);
 //   scan   one block turns the block sums into exclusive offsets and the
 //          totals (list length, pairs, work);
-//   emit   each thread scans its block's thread sums, walks its bits again
-//          and writes its entries, each cluster's pair start (for the
-//          scatter), and clears hist and its bitmap words for the next
-//          search;
+//   emit   each thread scans its block's thread sums, walks its nonzero
+//          counts again and writes its entries, each cluster's pair start
+//          (for the scatter), and clears those counts for the next search;
 //   scatter one wave per query puts each pair at its cluster's start plus
 //          the rank its counting atomic returned.
+
+// bit b set: cluster 32 wi + b has pairs.  The counts array holds whole
+// words (hist_words), so each word is read as eight 16-byte loads.
+__device__ __forceinline__ uint32_t hist_word_bits(const SharedArgs &a, int64_t wi) {
+  const uint4 *p = reinterpret_cast<const uint4 *>(a.hist + wi * 32);
+  uint32_t bits = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint4 v = p[k];
+    bits |= ((v.x != 0u ? 1u : 0u) | (v.y != 0u ? 2u : 0u) | (v.z != 0u ? 4u : 0u) |
+             (v.w != 0u ? 8u : 0u)) << (4 * k);
+  }
+  return bits;
+}
 
 struct ListSums {
   uint32_t n, h;
@@ -167,7 +180,7 @@ __device__ __forceinline__ ListSums list_thread_sums(const SharedArgs &a, int64_
   for (int j = 0; j < LIST_WPT; ++j) {
     const int64_t wi = w0 + j;
     if (wi >= nwords) break;
-    uint32_t bits = a.touched[wi];
+    uint32_t bits = hist_word_bits(a, wi);
     while (bits) {
       const uint64_t c = (uint64_t)wi * 32 + (uint64_t)(__ffs(bits) - 1);
       bits &= bits - 1;
@@ -258,53 +271,60 @@ __global__ void __launch_bounds__(LIST_THREADS) k_list_scan(SharedArgs a, int64_
   }
 }
 
+// Each wave first gathers the clusters of its 64 words into a compact list in
+// LDS (at most 64 x 32), then writes their entries with consecutive lanes on
+// consecutive entries, so the list arrays are written in whole lines; the
+// entries' pair and work offsets come from wave prefix sums, round by round.
 __global__ void __launch_bounds__(LIST_THREADS) k_list_emit(SharedArgs a) {
+  static_assert(LIST_WPT == 1, "one word of 32 counts per thread");
+  __shared__ uint32_t s_cl[LIST_THREADS / WAVE][WAVE * 32];
   const int64_t nwords = list_words(a.n_clusters);
   const int64_t t = (int64_t)blockIdx.x * LIST_THREADS + threadIdx.x;
+  const int lane = lane_id(), wv = threadIdx.x / WAVE;
   const ListSums v{a.thr_n[t], a.thr_h[t], a.thr_w[t]};
   ListSums tot;
   const ListSums ex = list_block_scan(v, &tot);
-  uint32_t i = a.blk_n[blockIdx.x] + ex.n;
-  uint32_t hp = a.blk_h[blockIdx.x] + ex.h;
-  uint64_t wo = a.blk_w[blockIdx.x] + ex.w;
-  const int64_t w0 = t * LIST_WPT;
-  for (int j = 0; j < LIST_WPT; ++j) {
-    const int64_t wi = w0 + j;
-    if (wi >= nwords) break;
-    uint32_t bits = a.touched[wi];
-    if (!bits) continue;
-    a.touched[wi] = 0u;
+  // the wave's first entry and its pair and work offsets
+  const uint32_t n0 = bcast_u32(ex.n, 0);
+  const uint32_t nend = bcast_u32(ex.n + v.n, WAVE - 1);
+  uint32_t *cl = s_cl[wv];
+  if (t < nwords) {
+    uint32_t bits = hist_word_bits(a, t);
+    uint32_t o = ex.n - n0;
     while (bits) {
-      const uint64_t c = (uint64_t)wi * 32 + (uint64_t)(__ffs(bits) - 1);
+      cl[o++] = (uint32_t)t * 32u + (uint32_t)(__ffs(bits) - 1);
       bits &= bits - 1;
-      const uint32_t hc = a.hist[c];
-      const uint64_t sz = a.cl_off[c + 1] - a.cl_off[c];
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  const uint32_t ibase = a.blk_n[blockIdx.x] + n0;
+  uint32_t hrun = a.blk_h[blockIdx.x] + bcast_u32(ex.h, 0);
+  uint64_t wrun = a.blk_w[blockIdx.x] + bcast_u64(ex.w, 0);
+  const uint32_t cnt = nend - n0;
+  for (uint32_t e0 = 0; e0 < cnt; e0 += WAVE) {
+    const uint32_t e = e0 + (uint32_t)lane;
+    const bool ok = e < cnt;
+    const uint64_t c = ok ? cl[e] : 0u;
+    const uint32_t hc = ok ? a.hist[c] : 0u;
+    const uint64_t base = ok ? a.cl_off[c] : 0u;
+    const uint64_t sz = ok ? a.cl_off[c + 1] - base : 0u;
+    const uint64_t work = (uint64_t)((hc + a.g - 1) / a.g) * sz;
+    const uint32_t ih = wave_incl_scan_u32(hc);
+    const uint64_t iw = wave_incl_scan_u64(work);
+    if (ok) {
+      const uint32_t i = ibase + e;
+      const uint32_t hp = hrun + ih - hc;
       a.hist[c] = 0u;
       a.slist[i] = (uint32_t)c;
-      a.lbase[i] = a.cl_off[c];
+      a.lbase[i] = base;
       a.lsz[i] = (uint32_t)sz;
       a.lpair[i] = hp;
       a.lpm[i] = hc;
-      a.swork_off[i] = wo;
+      a.swork_off[i] = wrun + iw - work;
       a.hpos[c] = hp;
-      i += 1;
-      hp += hc;
-      wo += (uint64_t)((hc + a.g - 1) / a.g) * sz;
     }
-  }
-}
-
-// one wave per query: the bit of every cluster the query's pairs list (the
-// atomics return nothing, so no lane waits on them)
-__global__ void __launch_bounds__(256) k_touch(SharedArgs a) {
-  const int lane = lane_id();
-  const int64_t q = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (q >= a.nq) return;
-  const int n = clamp_n(a.nclus[q], a.cap);
-  const uint32_t *cl = a.clus + q * a.cap;
-  for (int i = a.cseed[q] + lane; i < n; i += WAVE) {
-    const uint32_t c = cl[i];
-    if (c < a.n_clusters) atomicOr(&a.touched[c >> 5], 1u << (c & 31));
+    hrun += bcast_u32(ih, WAVE - 1);
+    wrun += bcast_u64(iw, WAVE - 1);
   }
 }
 
@@ -335,8 +355,6 @@ hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s) {
   if (e == hipSuccess) e = launch_fill_i32((int32_t *)a.counter, 2, 0, s);
   if (e != hipSuccess) return e;
   const int64_t nblk = list_blocks(a.n_clusters);
-  if (a.nq > 0)
-    hipLaunchKernelGGL(k_touch, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_list_count, dim3((unsigned)nblk), dim3(LIST_THREADS), 0, s, a);
   hipLaunchKernelGGL(k_list_scan, dim3(1), dim3(LIST_THREADS), 0, s, a, nblk);
   hipLaunchKernelGGL(k_list_emit, dim3((unsigned)nblk), dim3(LIST_THREADS), 0, s, a);

@@ -82,7 +82,7 @@ struct Buffers {
   unsigned long long *counter2;
   uint32_t *skey;
   int64_t *sid;
-  uint32_t *pair_q, *hist, *pair_rank, *slist, *touched, *hpos, *lpair, *lpm;
+  uint32_t *pair_q, *hist, *pair_rank, *slist, *hpos, *lpair, *lpm;
   uint64_t *lbase;
   uint32_t *lsz;
   uint32_t *thr_n, *thr_h, *blk_n, *blk_h;
@@ -160,8 +160,7 @@ Buffers carve(char *base, const Shape &s, size_t *bytes) {
     B.pair_rank = c.take<uint32_t>((size_t)s.nq * s.cap);
     B.qnorm = c.take<uint2>((size_t)s.nq);
     B.qrec = c.take<uint4>((size_t)s.nq);
-    B.hist = c.take<uint32_t>(nc1);
-    B.touched = c.take<uint32_t>((size_t)nr::list_words(s.n_clusters));
+    B.hist = c.take<uint32_t>((size_t)nr::hist_words(s.n_clusters));
     B.hpos = c.take<uint32_t>(nc1);
     B.slist = c.take<uint32_t>(nc1);
     B.lpair = c.take<uint32_t>(nc1);
@@ -192,7 +191,7 @@ struct Workspace {
   Buffers last{};
   int64_t last_nq = 0;
   int64_t last_cap = 0;
-  // the shared schedule's pair counts and cluster bitmap are all zero at
+  // the shared schedule's pair counts are all zero at
   // this address of hist (each search's prep clears what it used); any other
   // carving of the workspace may overwrite them, so it resets this
   const uint32_t *clean_hist = nullptr;
@@ -523,12 +522,19 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   // redo of queries whose survivors overflowed adds to them)
   hipError_t e = o.qmask ? hipSuccess : nr::launch_fill_i32((int32_t *)(B.wstats + 6), 2, 0, s);
   if (e == hipSuccess) e = nr::launch_plan(pa, s);
+#ifdef NR_PREP_ON_MAIN
+  if (e == hipSuccess && o.prep) {
+    e = nr::launch_shared_prep(*o.prep, s);
+    if (e == hipSuccess) e = hipEventRecord(o.join, s);
+  }
+#else
   if (e == hipSuccess && o.prep) {
     e = hipEventRecord(o.fork, s);
     if (e == hipSuccess) e = hipStreamWaitEvent(o.aux, o.fork, 0);
     if (e == hipSuccess) e = nr::launch_shared_prep(*o.prep, o.aux);
     if (e == hipSuccess) e = hipEventRecord(o.join, o.aux);
   }
+#endif
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[0], s);
   nr::RefineArgs ra{};
@@ -556,7 +562,10 @@ hipError_t run_refine(const nr_index *ix, const void *q, int64_t nq, int k, cons
   ra.rbytes = (unsigned long long *)(B.wstats + 6);
   // beside the scan's preparation, four blocks per CU (four waves per SIMD)
   // leave its kernels room to run under the seed pass instead of after it
-  e = nr::launch_refine(ra, ix->d.dtype, ix->n_cu, o.prep ? 4 : 0, s);
+#ifndef NR_REFINE_BLOCKS_BESIDE_PREP
+#define NR_REFINE_BLOCKS_BESIDE_PREP 4
+#endif
+  e = nr::launch_refine(ra, ix->d.dtype, ix->n_cu, o.prep ? NR_REFINE_BLOCKS_BESIDE_PREP : 0, s);
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[1], s);
   nr::MergeArgs ma{};
@@ -613,7 +622,6 @@ nr::SharedArgs shared_args(const nr_index *ix, const nr_params *p, const void *q
   a.own_dists = B.own_dists;
   a.own_rows = B.own_rows;
   a.hist = B.hist;
-  a.touched = B.touched;
   a.hpos = B.hpos;
   a.pair_rank = B.pair_rank;
   a.slist = B.slist;
@@ -1039,7 +1047,7 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
       sa = shared_args(ix, p, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
                        out_dists + q0 * k, qs);
       ph = nr::pair_hist_args(sa);
-      // pair counts and bitmap start at zero: cleared in full only for a new
+      // pair counts start at zero: cleared in full only for a new
       // workspace (or after a search that stopped early), else by the last prep
       HIP_OK(nr::launch_shared_hist(sa, w->clean_hist != B.hist, stream));
       w->clean_hist = nullptr;

@@ -46,10 +46,15 @@ constexpr int SHARED_G = 8;               // queries scored per shared work unit
 constexpr int SHARED_MAX_NSEG = 48;       // rows of at most 48 x 128 bytes use the shared scan
 constexpr uint32_t SHARED_ROWS = 2048;    // rows per shared work unit (at most)
 constexpr int MAX_KC = 16384;             // top-K_c heap held in LDS
-// the shared schedule's scan-list build: LIST_WPT bitmap words per thread
+// the shared schedule's scan-list build: LIST_WPT words of 32 pair counts per
+// thread; the counts array is hist_words long (whole words, and at least
+// n_clusters + 1 counts)
 constexpr int LIST_WPT = 1;
 constexpr int LIST_THREADS = 256;
 __host__ __device__ inline int64_t list_words(int64_t n_clusters) { return (n_clusters + 31) / 32; }
+__host__ __device__ inline int64_t hist_words(int64_t n_clusters) {
+  return (list_words(n_clusters) + 1) * 32;
+}
 __host__ __device__ inline int64_t list_blocks(int64_t n_clusters) {
   const int64_t per = (int64_t)LIST_WPT * LIST_THREADS;
   const int64_t b = (list_words(n_clusters) + per - 1) / per;
@@ -240,7 +245,6 @@ struct SharedArgs {
   const float *own_dists;
   uint32_t *own_rows;         // [nq] copy of rtot kept for diagnostics
   uint32_t *hist;             // [n_clusters + 1] pairs per cluster past the leading clusters
-  uint32_t *touched;          // [list_words] bit c: cluster c has pairs
   uint32_t *pair_rank;        // [nq x cap] rank of each counted pair among its cluster's pairs
   uint32_t *hpos;             // [n_clusters] start of cluster c's pairs in pair_q (clusters
                               // with pairs only)
@@ -295,7 +299,7 @@ hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_refine(const RefineArgs &a, int dtype, int n_cu, int blocks_per_cu,
                          hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
-// fresh: the workspace is new, so clear the pair counts and the bitmap
+// fresh: the workspace is new, so clear the pair counts
 hipError_t launch_shared_hist(const SharedArgs &a, bool fresh, hipStream_t s);
 PairHistArgs pair_hist_args(const SharedArgs &a);
 hipError_t launch_shared_prep(const SharedArgs &a, hipStream_t s);
