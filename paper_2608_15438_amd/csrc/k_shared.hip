@@ -735,6 +735,15 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
                                                        : make_uint4(0, 0, 0, 0);
             }
           }
+          // the query slots any of this round's rows lists (of gmax)
+          uint32_t jset = 0;
+          {
+            uint32_t lm = 0;
+#pragma unroll
+            for (int b = 0; b < UB; ++b) lm |= ent[b] & 0xffu;
+            for (int j = 0; j < gmax; ++j)
+              if (ballot(((lm >> j) & 1u) != 0)) jset |= 1u << j;
+          }
 #pragma unroll
           for (int b = 0; b < UB; ++b) {
             const uint32_t mask = ent[b] & 0xffu;
@@ -752,7 +761,8 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
               xx = (int32_t)acc;
             }
             const int slot0 = (int)(uq[ent[b] >> 20] & 0xffffu);
-            for (int j = 0; j < gmax; ++j) {
+            for (uint32_t js = jset; js; js &= js - 1) {
+              const int j = __ffs(js) - 1;
               const bool bit = ((mask >> j) & 1u) != 0;
               if (!ballot(bit)) continue;
               const int slot = slot0 + (bit ? j : 0);
