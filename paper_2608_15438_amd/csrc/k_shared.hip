@@ -982,7 +982,13 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
       // ---- phase A: heads of the batch's virtual rows
       int nsv = 0;
       uint32_t listed = 0;  // rows left open by their heads
-      int cur = 0;  // per lane; its virtual rows only increase
+      // per lane (its virtual rows only increase): the unit holding them, its
+      // first virtual and payload rows and the next unit's first virtual
+      // row, kept in registers so that a load costs an LDS read only where
+      // it crosses into the next unit
+      int cur = 0;
+      uint32_t vcur = uv[0], vnext = uv[1];
+      uint64_t bcur = ub[0];
       for (uint32_t v0 = 0; v0 < vtot; v0 += STEP) {
         if (nsv > SCAP - STEP) {
           phase_b(nsv);
@@ -996,10 +1002,16 @@ __global__ void __launch_bounds__(256, NSEG <= 1 ? NR_SCAN_WAVES1 : (NSEG > 8 ? 
         for (int uu = 0; uu < U; ++uu) {
           const uint32_t v = v0 + uu * RPW + lane / HL;
           const bool ok = v < vtot;
-          if (ok)
-            while (uv[cur + 1] <= v) ++cur;
+          if (ok && vnext <= v) {
+            do {
+              ++cur;
+              vnext = uv[cur + 1];
+            } while (vnext <= v);
+            vcur = uv[cur];
+            bcur = ub[cur];
+          }
           cpack |= (uint64_t)cur << (6 * uu);
-          const uint64_t row = ub[cur] + (v - uv[cur]);
+          const uint64_t row = bcur + (v - vcur);
           hv[uu] = ok ? load_stream(reinterpret_cast<const uint4 *>(a.scan_hb + row * a.scan_hs +
                                                                      16 * hl))
                       : make_uint4(0, 0, 0, 0);
