@@ -154,8 +154,9 @@ def ground_truth(torch, rows_range, n, is_u8, row_ids, Q, k, chunk=1 << 19):
 
 
 def stream_read_ceiling(torch, NR, dev, gib=16, reps=5):
-    """Achievable read rate: the library's streaming-read self-check (the same
-    16-byte loads as the refinement) over a 16 GiB buffer."""
+    """Achievable read rate: the library's streaming-read self-check (8 KB
+    runs per wave, eight 16-byte non-temporal loads in flight per lane) over a
+    16 GiB buffer."""
     x = torch.ones(gib << 28, dtype=torch.float32, device=dev)
     sink = torch.zeros(1, dtype=torch.int32, device=dev)
     NR.nr_stream_read(x, sink)
