@@ -108,11 +108,12 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   const int lane = lane_id();
   const int64_t q = blockIdx.x;
   if (q >= a.nq) return;
-  if (a.pass > 0 && a.redo[q] != a.pass) return;  // a later pass redoes only what the last gave up
+  if (a.tiered && a.redo[q] != a.pass) return;  // another pass routes this query
   S.mk[lane] = 0;
   const int b = a.b, P = a.P, k_c = a.k_c;
   const int hcap = a.hcap;  // heap slots in LDS (k_c, or fewer in a first pass)
-  bool abort_q = false;     // the heap would outgrow hcap: left to the next pass
+  bool abort_q = false;     // the heap would outgrow hcap (guard: the pass of each
+                            // query has room for every cluster it can score)
   const float kx = lane < a.m_knots ? a.m_x[lane] : 0.0f;
   const float ky = lane < a.m_knots ? a.m_y[lane] : 0.0f;
   const float ks = lane < a.m_knots ? a.m_slope[lane] : 0.0f;
@@ -467,8 +468,11 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     }
   }
 
-  if (abort_q) {
-    if (lane == 0) a.redo[q] = a.pass + 1;
+  if (abort_q) {  // unreachable (see k_route_tier): an empty list, never a stale one
+    if (lane == 0) {
+      a.redo[q] = a.pass + 1;
+      a.nclus[q] = 0;
+    }
     return;
   }
   flush(hh, hbn);
@@ -511,19 +515,40 @@ size_t route_lds_bytes(int k_c, int pst) {
   return sizeof(RouteLds) + sizeof(uint64_t) * ((size_t)k_c + buf) + 3 * sizeof(uint32_t) * (size_t)pst;
 }
 
-hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
+// one wave per query: the pass whose heap can hold every cluster the query
+// could score (the clusters of its probed multi-cluster buckets, the most the
+// heap can ever reach), so that no pass gives a query up to the next
+__global__ void __launch_bounds__(256) k_route_tier(RouteArgs a, int nt, int h0, int h1) {
+  const int lane = lane_id();
+  const int64_t q = (int64_t)blockIdx.x * (blockDim.x / WAVE) + threadIdx.x / WAVE;
+  if (q >= a.nq) return;
+  const int cnt = a.counts[q];
+  uint32_t m = 0;
+  for (int i = lane; i < cnt; i += WAVE) {
+    const uint2 r = a.lk[q * a.P + i];
+    const uint32_t c = r.y - r.x;
+    m += c >= 2 ? c : 0u;
+  }
+  m = wave_sum_u32(m);
+  if (lane == 0) a.redo[q] = m <= (uint32_t)h0 ? 0 : (nt > 2 && m <= (uint32_t)h1 ? 1 : nt - 1);
+}
+
+hipError_t launch_route(const RouteArgs &a, hipStream_t s, hipStream_t aux, hipEvent_t fork,
+                        hipEvent_t join) {
   if (a.nq <= 0) return hipSuccess;
   {
     int64_t blocks = (a.nq * a.P + 255) / 256;
     if (blocks > 16384) blocks = 16384;
     hipLaunchKernelGGL(k_route_lookup, dim3((unsigned)blocks), dim3(256), 0, s, a);
   }
-  // A first pass keeps at most ROUTE_LIGHT_HEAP heap keys in LDS, so more
-  // waves fit on a CU; a query whose heap would grow past that gives up and
-  // is redone by the next pass, with ROUTE_MID_HEAP slots and then (for
-  // larger K_c) the full K_c; every pass runs Algorithm 2 from the start.
-  auto launch = [&](int hcap, int pass) -> hipError_t {
-    RouteArgs b = a;
+  // A heap of at most ROUTE_LIGHT_HEAP keys in LDS lets more waves share a
+  // CU.  When K_c is larger, each query goes to the pass with the smallest
+  // heap (ROUTE_LIGHT_HEAP, ROUTE_MID_HEAP, K_c) that holds every cluster it
+  // could score; every pass runs Algorithm 2 whole for its queries, and the
+  // passes with larger heaps (few, long queries) run beside the first on the
+  // second stream when there is one.
+  auto launch = [&](const RouteArgs &b0, int hcap, int pass, hipStream_t st) -> hipError_t {
+    RouteArgs b = b0;
     b.hcap = hcap;
     b.pass = pass;
     // stage every probe's range in LDS while the block stays within 48 KiB
@@ -539,19 +564,31 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
       if (e != hipSuccess) return e;
     }
     if (hcap > ROUTE_LIGHT_HEAP)
-      hipLaunchKernelGGL(k_route<true>, dim3((unsigned)b.nq), dim3(64), lds, s, b);
+      hipLaunchKernelGGL(k_route<true>, dim3((unsigned)b.nq), dim3(64), lds, st, b);
     else
-      hipLaunchKernelGGL(k_route<false>, dim3((unsigned)b.nq), dim3(64), lds, s, b);
+      hipLaunchKernelGGL(k_route<false>, dim3((unsigned)b.nq), dim3(64), lds, st, b);
     return hipGetLastError();
   };
-  if (a.k_c <= ROUTE_LIGHT_HEAP) return launch(a.k_c, 0);
+  if (a.k_c <= ROUTE_LIGHT_HEAP) return launch(a, a.k_c, 0, s);
   int tiers[3], nt = 0;
-  if (!a.skip_light) tiers[nt++] = ROUTE_LIGHT_HEAP;
+  tiers[nt++] = ROUTE_LIGHT_HEAP;
   if (a.k_c > ROUTE_MID_HEAP) tiers[nt++] = ROUTE_MID_HEAP;
   tiers[nt++] = a.k_c;
-  if (nt == 1) return launch(a.k_c, 0);
-  hipError_t e = launch_fill_i32(a.redo, a.nq, 0, s);
-  for (int p = 0; p < nt && e == hipSuccess; ++p) e = launch(tiers[p], p);
+  hipLaunchKernelGGL(k_route_tier, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a, nt,
+                     tiers[0], nt > 2 ? tiers[1] : tiers[0]);
+  hipError_t e = hipGetLastError();
+  RouteArgs b = a;
+  b.tiered = 1;
+  if (aux && fork && join) {
+    if (e == hipSuccess) e = hipEventRecord(fork, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(aux, fork, 0);
+    for (int t = 1; t < nt && e == hipSuccess; ++t) e = launch(b, tiers[t], t, aux);
+    if (e == hipSuccess) e = hipEventRecord(join, aux);
+    if (e == hipSuccess) e = launch(b, tiers[0], 0, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
+    return e;
+  }
+  for (int t = 0; t < nt && e == hipSuccess; ++t) e = launch(b, tiers[t], t, s);
   return e;
 }
 

@@ -448,10 +448,6 @@ hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
   a.redo = B.redo;
   a.centroids = ix->d.centroids;
   a.k_c = (int)kc_eff(ix, p);
-  // about 70 % of the scored centroids pass the gate: with this many clusters
-  // per bucket the light first pass would overflow for nearly every query
-  a.skip_light = (double)ix->d.n_clusters / (double)(1ull << ix->d.b) * P >
-                 2.0 * nr::ROUTE_LIGHT_HEAP;
   a.b_batch = p->b_batch;
   a.b_min = p->b_min;
   a.t_low = p->t_low;
@@ -477,7 +473,7 @@ hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
     a.ph = *ph;
     a.ph_on = 1;
   }
-  return nr::launch_route(a, s);
+  return nr::launch_route(a, s, B.aux, B.fork, B.join);
 }
 
 struct RefineOpts {

@@ -144,8 +144,8 @@ struct RouteArgs {
   uint2 *lk;             // [nq x P] scratch: cluster range of each probe's bucket
   int pst;               // probes per query whose ranges are staged in LDS (set per pass)
   int hcap, pass;        // heap slots in LDS and pass number (set by launch_route)
-  int skip_light;        // start at the middle heap (the light pass would overflow)
-  int32_t *redo;         // [nq] queries the first pass left to the second
+  int tiered;            // redo[q] holds the pass that routes query q
+  int32_t *redo;         // [nq] the pass of each query (tiered), or its next pass
   const float *centroids;
   int k_c, b_batch, b_min, t_low, u_heap, u_front;
   float alpha_front;
@@ -292,7 +292,10 @@ hipError_t launch_probe(const ProbeArgs &a, hipStream_t s);
 constexpr int ROUTE_LIGHT_HEAP = 512;  // heap slots of the route's first pass
 constexpr int ROUTE_MID_HEAP = 2048;   // and of its second when K_c is larger still
 size_t route_lds_bytes(int k_c, int pst);
-hipError_t launch_route(const RouteArgs &a, hipStream_t s);
+// aux, fork, join (may be null): a second stream and two events, on which the
+// passes with larger heaps run beside the first
+hipError_t launch_route(const RouteArgs &a, hipStream_t s, hipStream_t aux = nullptr,
+                        hipEvent_t fork = nullptr, hipEvent_t join = nullptr);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t s);
 // blocks_per_cu: 0 for the tuned default; fewer leave room on every CU for
 // work on another stream (the scan's preparation beside the seed pass)
