@@ -128,6 +128,15 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   // buffer, which is merged into H only when it fills, at a truncation, and at
   // the end, so H itself moves rarely
   int hh = 0, hbn = 0;
+  // Until the kept keys could reach K_c, no key is ever cut and the stop
+  // cannot fire (it needs |H| = K_c), so a batch only appends its gated keys
+  // to H unsorted: H[0, npool).  theta only falls from batch to batch (M is
+  // non-decreasing and d_min only falls), so pruning the pool once by the
+  // latest theta leaves what pruning after every batch would; the pool is
+  // sorted and pruned when a batch could reach K_c, and at the end.
+  bool fastm = true;
+  int npool = 0;
+  uint64_t cut_last = ~0ull;
   float d_min = INFINITY;
   int b_proc = 0, t_low = 0, n_scored = 0, n_batches = 0;
   bool stop = false;
@@ -233,6 +242,31 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
 
   // score the pending batch and fold it into H; with pre >= 0 the batch is
   // window clusters pre, pre + 1, ... whose distances may already be in S.wd
+  // the pool sorted into H[0, hh) and pruned to keys below cutv, 64 keys at
+  // a time: a chunk is read into registers, sorted across the wave and merged
+  // into the sorted prefix, which never reaches past the chunk just read
+  auto normalize = [&](uint64_t cutv) __attribute__((always_inline)) {
+    __builtin_amdgcn_wave_barrier();
+    int sp = 0;
+    for (int c0 = 0; c0 < npool; c0 += WAVE) {
+      const int n = npool - c0 < WAVE ? npool - c0 : WAVE;
+      uint64_t key = lane < n ? H[c0 + lane] : ~0ull;
+      const bool keep = key < cutv;
+      const int nk = popc64(ballot(keep));
+      key = keep ? key : ~0ull;
+      __builtin_amdgcn_wave_barrier();
+      if (nk == 0) continue;
+      key = wave_sort_u64(key, n);
+      merge_keys(H, sp, k_c, key, nk);
+      sp += nk;
+    }
+    hh = sp;
+    hbn = 0;
+    h = sp;
+    npool = 0;
+    fastm = false;
+  };
+
   auto run_batch = [&](int pre) {
     const int nb = npend;
     n_batches += 1;
@@ -253,11 +287,29 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     const float am = a.alpha_front * M;
     const float theta_f = d_min + am;
     const bool valid = lane < nb && d <= theta;
+    const uint64_t cut = ((uint64_t)__float_as_uint(theta) + 1ull) << 32;
+    if (fastm) {
+      const uint64_t vm = ballot(valid);
+      const int nvf = popc64(vm);
+      if (npool + nvf < k_c && npool + nvf <= hcap) {
+        // every gated key is kept: u_heap = their count
+        if (valid) H[npool + popc64(vm & lanemask_lt())] = ((uint64_t)__float_as_uint(d) << 32) | cid;
+        npool += nvf;
+        h = npool;
+        cut_last = cut;
+        const int u_front = popc64(ballot(valid && d <= theta_f));
+        const bool low = a.lowq_or ? (nvf < a.u_heap || u_front < a.u_front)
+                                   : (nvf < a.u_heap && u_front < a.u_front);
+        t_low = low ? t_low + 1 : 0;
+        npend = 0;
+        return;
+      }
+      normalize(cut);
+    }
     uint64_t key = valid ? (((uint64_t)__float_as_uint(d) << 32) | cid) : ~0ull;
     key = nb <= 32 ? rank_sort_u64(key, nb, S.bkey) : wave_sort_u64(key, nb);
     const int nv = popc64(ballot(valid));
     // prune H and the buffer to d <= theta (prefixes, as both are sorted)
-    const uint64_t cut = ((uint64_t)__float_as_uint(theta) + 1ull) << 32;
     const int hvh = wave_lower_bound_u64(H, hh, cut);
     const int hvb = BUF ? wave_lower_bound_u64(HB, hbn, cut) : 0;
     const int hv = hvh + hvb;
@@ -468,6 +520,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     }
   }
 
+  if (fastm) normalize(cut_last);
   if (abort_q) {  // unreachable (see k_route_tier): an empty list, never a stale one
     if (lane == 0) {
       a.redo[q] = a.pass + 1;
