@@ -146,8 +146,11 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     return a.early_stop_on && h == k_c && b_proc >= a.b_min && t_low >= a.t_low;
   };
 
-  // distance of one centroid to the query's logits, dimensions in order
-  auto centroid_dist = [&](uint32_t cid) {
+  // distance of one centroid to the query's logits, dimensions in order.
+  // The logits are read from the lanes holding them (readlane), so every lane
+  // of the wave must be active here: callers run it on all lanes and mask
+  // the result afterwards.
+  auto centroid_dist = [&](uint32_t cid) __attribute__((always_inline)) {
     const float *mu = a.centroids + (int64_t)cid * b;
     // the whole centroid row is loaded at once (b <= 30; unused slots read
     // coordinate 0), then accumulated in dimension order
@@ -175,7 +178,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   auto precompute = [&](int from) __attribute__((always_inline)) {
     const int lim = cnt - wb < WAVE ? cnt - wb : WAVE;
     const int n = (int)wtotal - from < WAVE ? (int)wtotal - from : WAVE;
-    float dw = 0.0f;
+    uint32_t cid = 0;  // lanes past n score cluster 0 and drop it
     if (lane < n) {
       const uint32_t num = (uint32_t)(from + lane);
       // the slot owning number num: the last slot whose prefix is <= num
@@ -184,8 +187,10 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
         const int mid = (lo + hi + 1) >> 1;
         if (S.wpre[mid] <= num) lo = mid; else hi = mid - 1;
       }
-      dw = centroid_dist(S.wc0[lo] + (num - S.wpre[lo]));
+      cid = S.wc0[lo] + (num - S.wpre[lo]);
     }
+    const float dc = centroid_dist(cid);
+    const float dw = lane < n ? dc : 0.0f;
     __builtin_amdgcn_wave_barrier();
     S.wd[lane] = dw;
     __builtin_amdgcn_wave_barrier();
@@ -267,7 +272,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     fastm = false;
   };
 
-  auto run_batch = [&](int pre) {
+  auto run_batch = [&](int pre) __attribute__((always_inline)) {
     const int nb = npend;
     n_batches += 1;
     n_scored += nb;
@@ -276,9 +281,12 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     // a window batch whose distances are not all in S.wd first scores the
     // next 64 of the window's clusters at once
     if (pre >= 0 && (pre < pbase || pre + nb > pbase + npre)) precompute(pre);
-    if (lane < nb) {
-      cid = S.pend[lane];
-      d = pre >= 0 ? S.wd[pre - pbase + lane] : centroid_dist(cid);
+    if (lane < nb) cid = S.pend[lane];
+    if (pre >= 0) {
+      if (lane < nb) d = S.wd[pre - pbase + lane];
+    } else {
+      const float dc = centroid_dist(cid);  // all lanes (cluster 0 past nb)
+      if (lane < nb) d = dc;
     }
     float dm = wave_min_f32(d);
     d_min = dm < d_min ? dm : d_min;
