@@ -100,8 +100,10 @@ __global__ void __launch_bounds__(64) k_calib(CalibArgs a) {
     a.scores[q * K + lane] = INFINITY;
   }
 
-  // the search's latent distance of the query to centroid c
-  auto cdist = [&](int64_t c) {
+  // the search's latent distance of the query to centroid c.  The logits
+  // come from the lanes holding them (readlane), so it runs on every lane:
+  // callers pass a valid cluster in all lanes and mask the result
+  auto cdist = [&](int64_t c) __attribute__((always_inline)) {
     const float *mu = a.centroids + c * b;
     float acc = 0.0f;
     for (int j = 0; j < b; ++j) {
@@ -111,10 +113,15 @@ __global__ void __launch_bounds__(64) k_calib(CalibArgs a) {
     }
     return acc;
   };
-  // y's distance: the targets' own clusters
-  const float dt = has ? cdist(clus) : -INFINITY;
-  // x: every centroid of every distinct target bucket, one bucket at a time
+  // y's distance: the targets' own clusters (with any target there is a
+  // cluster 0, which lanes without one score and drop)
   const uint64_t any = ballot(has);
+  float dt = -INFINITY;
+  if (any) {
+    const float dc = cdist(has ? clus : 0);
+    if (has) dt = dc;
+  }
+  // x: every centroid of every distinct target bucket, one bucket at a time
   uint64_t todo = any;
   float xmin = INFINITY;
   while (todo) {
@@ -123,7 +130,11 @@ __global__ void __launch_bounds__(64) k_calib(CalibArgs a) {
     // drop every target in this bucket from the to-do set
     todo &= ~ballot(has && code == cb);
     const uint32_t c0 = a.bc_off[cb], c1 = a.bc_off[(uint64_t)cb + 1];
-    for (uint32_t c = c0 + lane; c < c1; c += WAVE) xmin = fminf(xmin, cdist(c));
+    for (uint32_t cb0 = c0; cb0 < c1; cb0 += WAVE) {
+      const uint32_t c = cb0 + lane;
+      const float dc = cdist(c < c1 ? c : c0);
+      if (c < c1) xmin = fminf(xmin, dc);
+    }
   }
   const float x = wave_min_f32(xmin);
   float ymax = dt;
