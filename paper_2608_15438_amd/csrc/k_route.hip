@@ -94,10 +94,11 @@ __device__ __forceinline__ int wave_lower_bound_u64(const uint64_t *a, int n, ui
   return lo;
 }
 
-// BUF: the staging buffer in front of H (passes whose heap may grow past the
-// light first pass's size; small heaps merge straight into H)
+// Algorithm 2 for query q, one wave.  BUF: the staging buffer in front of H
+// (passes whose heap may grow past the light first pass's size; small heaps
+// merge straight into H)
 template <bool BUF>
-__global__ void __launch_bounds__(64) k_route(RouteArgs a) {
+__device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   RouteLds &S = *reinterpret_cast<RouteLds *>(smem_raw);
   uint64_t *H = reinterpret_cast<uint64_t *>(smem_raw + sizeof(RouteLds));
@@ -106,9 +107,7 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   uint32_t *st_c1 = st_c0 + a.pst;
   int32_t *st_bin = reinterpret_cast<int32_t *>(st_c1 + a.pst);
   const int lane = lane_id();
-  const int64_t q = blockIdx.x;
-  if (q >= a.nq) return;
-  if (a.tiered && a.redo[q] != a.pass) return;  // another pass routes this query
+  __builtin_amdgcn_wave_barrier();  // the LDS of the block's previous query is done with
   S.mk[lane] = 0;
   const int b = a.b, P = a.P, k_c = a.k_c;
   const int hcap = a.hcap;  // heap slots in LDS (k_c, or fewer in a first pass)
@@ -365,13 +364,15 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   // copy from there (and read the global ranges only past nst)
   const uint2 *lk = a.lk + q * P;
   const int nst = cnt < a.pst ? cnt : a.pst;
-  for (int base = 0; base < nst; base += 8 * WAVE) {
+  // the first round's loads cover slots below pst (all inside the query's P
+  // slots), so they need not wait for cnt; only slots below nst are kept
+  for (int base = 0; base < a.pst && (base == 0 || base < nst); base += 8 * WAVE) {
     uint2 v[8];
     int bv[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int i = base + u * WAVE + lane;
-      const int ii = i < nst ? i : 0;
+      const int ii = i < a.pst ? i : 0;
       v[u] = lk[ii];
       bv[u] = bins[ii];
     }
@@ -556,6 +557,14 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
     __threadfence_block();
     pair_hist_wave(a.ph, q, out, ndir + h);
   }
+}
+
+// One query per block; a pass of a tiered route skips the queries assigned
+// to another pass
+template <bool BUF>
+__global__ void __launch_bounds__(64) k_route(RouteArgs a) {
+  const int64_t q = blockIdx.x;
+  if (q < a.nq && (!a.tiered || a.redo[q] == a.pass)) route_query<BUF>(a, q);
 }
 
 // one thread per probe: the cluster range [c0, c1) of its bucket

@@ -474,28 +474,41 @@ __device__ inline void pair_hist_wave(const PairHistArgs &h, int64_t q, const ui
   const bool all = h.eager_rows != 0;
   uint64_t run = 0;
   int cs = -1;
-  for (int i0 = 0; i0 < n; i0 += WAVE) {
+  // the seed: sizes of the leading clusters until they cover seed_min rows
+  for (int i0 = 0; i0 < n && (cs < 0 || all); i0 += WAVE) {
     const int i = i0 + lane;
-    const bool sizes = cs < 0 || all;
-    uint32_t c = 0xffffffffu;
     uint64_t sz = 0;
     if (i < n) {
-      c = cl[i];
-      if (sizes && c < h.n_clusters) sz = h.cl_off[(uint64_t)c + 1] - h.cl_off[c];
+      const uint32_t c = cl[i];
+      if (c < h.n_clusters) sz = h.cl_off[(uint64_t)c + 1] - h.cl_off[c];
     }
-    if (sizes) {
-      const uint64_t incl = wave_incl_scan_u64(sz);
-      int upto = WAVE - 1;
-      if (cs < 0) {
-        const uint64_t hit = ballot(i < n && run + incl >= h.seed_min);
-        if (hit) {
-          cs = i0 + __ffsll((unsigned long long)hit);  // first position past the seed
-          if (!all) upto = cs - 1 - i0;
-        }
+    const uint64_t incl = wave_incl_scan_u64(sz);
+    int upto = WAVE - 1;
+    if (cs < 0) {
+      const uint64_t hit = ballot(i < n && run + incl >= h.seed_min);
+      if (hit) {
+        cs = i0 + __ffsll((unsigned long long)hit);  // first position past the seed
+        if (!all) upto = cs - 1 - i0;
       }
-      run += bcast_u64(incl, upto);
     }
-    if (cs >= 0 && i >= cs && c < h.n_clusters) h.pair_rank[q * h.cap + i] = atomicAdd(&h.hist[c], 1u);
+    run += bcast_u64(incl, upto);
+  }
+  // the pairs past the seed, four per lane at a time: their cluster ids are
+  // all loaded, then all counted, so each group costs two memory round trips
+  if (cs >= 0) {
+    for (int i0 = cs; i0 < n; i0 += 4 * WAVE) {
+      uint32_t c[4], r[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * WAVE + lane;
+        c[u] = i < n ? cl[i] : 0xffffffffu;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) r[u] = c[u] < h.n_clusters ? atomicAdd(&h.hist[c[u]], 1u) : 0u;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (c[u] < h.n_clusters) h.pair_rank[q * h.cap + i0 + u * WAVE + lane] = r[u];
+    }
   }
   if (lane == 0) {
     h.cseed[q] = cs < 0 ? n : cs;
