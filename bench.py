@@ -292,8 +292,7 @@ def main():
             cache["query"] = (cache.get("query", (None, None))[0], gt_new[:ng])
         if need_c:
             cache["calib"] = (cache.get("calib", (None, None))[0], gt_new[ng if need_q else 0:])
-        for what in ("query", "calib"):
-            path, arr = cache[what]
+        for path, arr in cache.values():
             if path and arr is not None and not os.path.exists(path):
                 np.save(path, arr)
     gt_ids = cache["query"][1] if ng else np.zeros((0, k), np.int64)
