@@ -106,7 +106,7 @@ struct Shape {
 
 Buffers carve(char *base, const Shape &s, size_t *bytes) {
   Carver c{base};
-  Buffers B;
+  Buffers B{};  // what is not carved (the second stream and its events) stays null
   B.logits = c.take<float>((size_t)s.nq * s.b);
   B.act0 = c.take<float>((size_t)s.nq * s.maxw);
   B.act1 = c.take<float>((size_t)s.nq * s.maxw);
