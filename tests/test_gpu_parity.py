@@ -82,6 +82,12 @@ PARAM_SETS = {
     # a heap this large leaves LDS for only the first ~600 probe ranges of a
     # query: the rest of a 1024-probe sequence is read from HBM
     "big_heap": dict(k_c=5000, gate_on=False, early_stop_on=False),
+    # K_c past the first pass's 512 heap keys: long queries go to a pass with
+    # a K_c-key heap, whose unsorted pool is sorted when it could reach K_c,
+    # after which the heap fills and the stop can fire
+    "mid_heap_stop": dict(k_c=600, b_batch=16, b_min=2, t_low=1, gate_on=False),
+    # K_c past 2048: three passes (512, 2048 and K_c keys)
+    "three_tiers": dict(k_c=3000, b_batch=32, gate_on=False, early_stop_on=False),
 }
 
 
