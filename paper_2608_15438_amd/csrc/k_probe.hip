@@ -140,24 +140,66 @@ __global__ void __launch_bounds__(64) k_probe(ProbeArgs a) {
     n = nout;
   }
 
-  // codes, scores and bins of the sequence
-  for (int i = lane; i < n; i += WAVE) {
-    const uint64_t key = L[i];
-    const uint32_t m = (uint32_t)key;
-    uint32_t code = code0;
-    for (int r = 0; r < l_sel; ++r)
-      if ((m >> r) & 1u) code ^= 1u << bcast_u32((uint32_t)sel_dim, r);
-    const float c = __uint_as_float((uint32_t)(key >> 32));
-    int bin = i;
-    if (a.finite) {
-      const int z = (int)floorf(c * a.bin_scale);
-      bin = z < a.n_bins - 1 ? z : a.n_bins - 1;
+  // codes, scores and bins of the sequence, four per lane at a time (every
+  // lane runs each round: the dimension of rank r is read from lane r); for
+  // the search, each probe's bucket range from the directory (the four
+  // lookups of a lane in flight together) and the query's route pass
+  uint32_t msum = 0;  // clusters in the query's multi-cluster buckets
+  for (int i0 = 0; i0 < n; i0 += 4 * WAVE) {
+    uint64_t key[4];
+    uint32_t code[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * WAVE + lane;
+      key[u] = i < n ? L[i] : 0ull;
+      code[u] = code0;
     }
-    a.codes[q * P + i] = code;
-    a.costs[q * P + i] = c;
-    a.bins[q * P + i] = bin;
+    for (int r = 0; r < l_sel; ++r) {
+      const uint32_t bit = 1u << bcast_u32((uint32_t)sel_dim, r);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) code[u] ^= (((uint32_t)key[u] >> r) & 1u) ? bit : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * WAVE + lane;
+      if (i < n) {
+        const float c = __uint_as_float((uint32_t)(key[u] >> 32));
+        int bin = i;
+        if (a.finite) {
+          const int z = (int)floorf(c * a.bin_scale);
+          bin = z < a.n_bins - 1 ? z : a.n_bins - 1;
+        }
+        a.codes[q * P + i] = code[u];
+        a.costs[q * P + i] = c;
+        a.bins[q * P + i] = bin;
+      }
+    }
+    if (a.lk) {
+      uint2 r[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * WAVE + lane;
+        if (i < n) r[u] = make_uint2(a.bc_off[code[u]], a.bc_off[(uint64_t)code[u] + 1]);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * WAVE + lane;
+        if (i < n) {
+          a.lk[q * P + i] = r[u];
+          const uint32_t sz = r[u].y - r[u].x;
+          msum += sz >= 2 ? sz : 0u;
+        }
+      }
+    }
   }
   if (lane == 0) a.counts[q] = n;
+  if (a.tier) {
+    msum = wave_sum_u32(msum);
+    if (lane == 0)
+      a.tier[q] = msum <= (uint32_t)a.tier_h0
+                      ? 0
+                      : (a.tier_n > 2 && msum <= (uint32_t)a.tier_h1 ? 1 : a.tier_n - 1);
+  }
 }
 
 hipError_t launch_probe(const ProbeArgs &a, hipStream_t s) {

@@ -606,7 +606,7 @@ __global__ void __launch_bounds__(256) k_route_tier(RouteArgs a, int nt, int h0,
 hipError_t launch_route(const RouteArgs &a, hipStream_t s, hipStream_t aux, hipEvent_t fork,
                         hipEvent_t join) {
   if (a.nq <= 0) return hipSuccess;
-  {
+  if (!a.looked_up) {  // else the probe kernel has written lk (and the passes)
     int64_t blocks = (a.nq * a.P + 255) / 256;
     if (blocks > 16384) blocks = 16384;
     hipLaunchKernelGGL(k_route_lookup, dim3((unsigned)blocks), dim3(256), 0, s, a);
@@ -639,13 +639,12 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s, hipStream_t aux, hipE
       hipLaunchKernelGGL(k_route<false>, dim3((unsigned)b.nq), dim3(64), lds, st, b);
     return hipGetLastError();
   };
-  if (a.k_c <= ROUTE_LIGHT_HEAP) return launch(a, a.k_c, 0, s);
-  int tiers[3], nt = 0;
-  tiers[nt++] = ROUTE_LIGHT_HEAP;
-  if (a.k_c > ROUTE_MID_HEAP) tiers[nt++] = ROUTE_MID_HEAP;
-  tiers[nt++] = a.k_c;
-  hipLaunchKernelGGL(k_route_tier, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a, nt,
-                     tiers[0], nt > 2 ? tiers[1] : tiers[0]);
+  int tiers[3];
+  const int nt = route_tiers(a.k_c, tiers);
+  if (nt == 1) return launch(a, a.k_c, 0, s);
+  if (!a.looked_up)
+    hipLaunchKernelGGL(k_route_tier, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a, nt,
+                       tiers[0], nt > 2 ? tiers[1] : tiers[0]);
   hipError_t e = hipGetLastError();
   RouteArgs b = a;
   b.tiered = 1;

@@ -409,9 +409,12 @@ hipError_t run_encode(const nr_index *ix, const void *q, int64_t nq, float *logi
   return hipSuccess;
 }
 
+// with route (a search's buffers): the probe kernel also looks up each
+// probe's bucket and assigns each query its route pass, for run_route(...,
+// looked_up = true) on the same buffers
 hipError_t run_probe(const nr_index *ix, const float *logits, int64_t nq, int P,
                      const nr_params *p, uint32_t *codes, float *costs, int32_t *bins,
-                     int32_t *counts, hipStream_t s) {
+                     int32_t *counts, hipStream_t s, const Buffers *route = nullptr) {
   nr::ProbeArgs a{};
   a.logits = logits;
   a.tau = ix->tau;
@@ -428,13 +431,24 @@ hipError_t run_probe(const nr_index *ix, const float *logits, int64_t nq, int P,
   a.costs = costs;
   a.bins = bins;
   a.counts = counts;
+  if (route) {
+    a.bc_off = ix->d.bc_off;
+    a.lk = route->lk;
+    int tiers[3];
+    a.tier_n = nr::route_tiers((int)kc_eff(ix, p), tiers);
+    if (a.tier_n > 1) {
+      a.tier = route->redo;
+      a.tier_h0 = tiers[0];
+      a.tier_h1 = a.tier_n > 2 ? tiers[1] : tiers[0];
+    }
+  }
   return nr::launch_probe(a, s);
 }
 
 hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
                      const nr_params *p, const Buffers &B, uint32_t *clus, int32_t *nclus,
                      int64_t cap, int32_t *qstats, hipStream_t s,
-                     const nr::PairHistArgs *ph = nullptr) {
+                     const nr::PairHistArgs *ph = nullptr, bool looked_up = false) {
   nr::RouteArgs a{};
   a.logits = logits;
   a.nq = nq;
@@ -446,6 +460,7 @@ hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
   a.bc_off = ix->d.bc_off;
   a.lk = B.lk;
   a.redo = B.redo;
+  a.looked_up = looked_up ? 1 : 0;
   a.centroids = ix->d.centroids;
   a.k_c = (int)kc_eff(ix, p);
   a.b_batch = p->b_batch;
@@ -969,9 +984,9 @@ nr_status nr_route(const nr_index *cix, const float *logits, int64_t nq, int32_t
   for (int64_t q0 = 0; q0 < nq; q0 += sh.nq) {
     int64_t n = nq - q0 < sh.nq ? nq - q0 : sh.nq;
     const float *lg = logits + q0 * ix->d.b;
-    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream));
+    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream, &B));
     HIP_OK(run_route(ix, lg, n, P, p, B, clusters + q0 * cap, n_clusters + q0, cap, nullptr,
-                     stream));
+                     stream, nullptr, true));
   }
   return NR_OK;
 }
@@ -1035,7 +1050,7 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
     const float *lg = logits ? logits + q0 * ix->d.b : B.logits;
     if (!logits) HIP_OK(run_encode(ix, qp, n, B.logits, B, stream));
     if (prof) HIP_OK(hipEventRecord(es.ev[1], stream));
-    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream));
+    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream, &B));
     if (prof) HIP_OK(hipEventRecord(es.ev[2], stream));
     nr::SharedArgs sa{};
     nr::PairHistArgs ph{};
@@ -1049,7 +1064,7 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
       w->clean_hist = nullptr;
     }
     HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, qs, stream,
-                     B.shared ? &ph : nullptr));
+                     B.shared ? &ph : nullptr, true));
     if (prof) HIP_OK(hipEventRecord(es.ev[3], stream));
     if (B.shared) {
       HIP_OK(run_refine_shared(ix, sa, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
@@ -1116,8 +1131,8 @@ nr_status nr_search_noalloc(const nr_index *cix, const void *queries, const floa
     const void *qp = (const char *)queries + q0 * qrow;
     const float *lg = logits ? logits + q0 * ix->d.b : B.logits;
     if (!logits) HIP_OK(run_encode(ix, qp, n, B.logits, B, stream));
-    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream));
-    HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, nullptr, stream));
+    HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream, &B));
+    HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, nullptr, stream, nullptr, true));
     HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
                       out_dists + q0 * k, nullptr, stream, nullptr));
   }

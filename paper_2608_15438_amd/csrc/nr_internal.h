@@ -100,6 +100,14 @@ struct ProbeArgs {
   float *costs;
   int32_t *bins;
   int32_t *counts;       // [nq]
+  // optional, for the search: each probe's bucket looked up in the directory
+  // (lk[q x P + i] = [bc_off[code], bc_off[code + 1])) and each query's route
+  // pass (see route_tiers; tier[q] = the first pass whose heap holds the
+  // summed sizes of its multi-cluster buckets)
+  const uint32_t *bc_off;
+  uint2 *lk;             // [nq x P] (NULL: no lookup)
+  int32_t *tier;         // [nq] (NULL: no tiers)
+  int tier_n, tier_h0, tier_h1;
 };
 
 // calibration (k_calib.hip): bucket scores of the targets and margin points
@@ -145,6 +153,7 @@ struct RouteArgs {
   int pst;               // probes per query whose ranges are staged in LDS (set per pass)
   int hcap, pass;        // heap slots in LDS and pass number (set by launch_route)
   int tiered;            // redo[q] holds the pass that routes query q
+  int looked_up;         // lk (and with K_c past the first heap, redo) written by the probe kernel
   int32_t *redo;         // [nq] the pass of each query (tiered), or its next pass
   const float *centroids;
   int k_c, b_batch, b_min, t_low, u_heap, u_front;
@@ -291,6 +300,20 @@ hipError_t launch_encode_layer(const EncodeLayerArgs &a, hipStream_t s);
 hipError_t launch_probe(const ProbeArgs &a, hipStream_t s);
 constexpr int ROUTE_LIGHT_HEAP = 512;  // heap slots of the route's first pass
 constexpr int ROUTE_MID_HEAP = 2048;   // and of its second when K_c is larger still
+// the heap sizes of the route's passes for K_c: one pass of K_c keys up to
+// ROUTE_LIGHT_HEAP, else ROUTE_LIGHT_HEAP, ROUTE_MID_HEAP (when K_c is larger
+// still) and K_c; returns the number of passes
+inline int route_tiers(int k_c, int tiers[3]) {
+  if (k_c <= ROUTE_LIGHT_HEAP) {
+    tiers[0] = k_c;
+    return 1;
+  }
+  int nt = 0;
+  tiers[nt++] = ROUTE_LIGHT_HEAP;
+  if (k_c > ROUTE_MID_HEAP) tiers[nt++] = ROUTE_MID_HEAP;
+  tiers[nt++] = k_c;
+  return nt;
+}
 size_t route_lds_bytes(int k_c, int pst);
 // aux, fork, join (may be null): a second stream and two events, on which the
 // passes with larger heaps run beside the first
