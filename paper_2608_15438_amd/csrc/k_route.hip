@@ -1,5 +1,5 @@
-// Steps 3-4: bucket lookup in the CSR directory and the centroid stage of
-// Algorithm 2 (Sec. 3.4.2), one wavefront per query.
+// Step 4: the centroid stage of Algorithm 2 (Sec. 3.4.2), one wavefront per
+// query, on the bucket ranges the probe kernel looked up in the CSR directory.
 //
 // Bins are visited in increasing order; every visited bin increments b_proc.
 // A probed bucket with one cluster goes straight to C_dir; the clusters of
@@ -13,17 +13,17 @@
 //   stop once |H| = K_c, b_proc >= B_min and t_low >= T_low.
 // C(q) = C_dir (visiting order) followed by H in (d, cluster) order.
 //
-// H is a sorted array of u64 keys (d bits << 32 | cluster) in LDS, fronted by
-// a sorted 64-key staging buffer.  A batch is sorted across the wave
-// (bitonic), then merged by ranks: batch element i lands at slot
-// i + |{h < key_i}|, and the other slots of the moving tail take the old keys
-// in order; the tail is rewritten from the top down, 64 slots at a time, so no
-// key is overwritten before it is read.  A batch that cannot push H past K_c
-// merges into the buffer, which moves into H when it fills, before a batch
-// that needs the K_c-smallest cut, and at the end.  A first pass looks up every probe's bucket in the
-// directory (one thread per probe); the per-query pass stages the ranges of
-// its first pst probes in LDS with one round of loads and walks them 64 at a
-// time.
+// While the kept keys cannot reach K_c, H is an unsorted pool, sorted and
+// pruned once (see route_query).  After that H is a sorted array of u64 keys
+// (d bits << 32 | cluster) in LDS, for larger heaps fronted by a sorted
+// 64-key staging buffer.  A batch is sorted across the wave, then merged by
+// ranks: batch element i lands at slot i + |{h < key_i}|, and the other slots
+// of the moving tail take the old keys in order; the tail is rewritten from
+// the top down, 64 slots at a time, so no key is overwritten before it is
+// read.  A batch that cannot push H past K_c merges into the buffer, which
+// moves into H when it fills, before a batch that needs the K_c-smallest cut,
+// and at the end.  The per-query pass stages the ranges of its first pst
+// probes in LDS with one round of loads and walks them 64 at a time.
 #include "nr_internal.h"
 
 namespace nr {
@@ -530,7 +530,7 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
   }
 
   if (fastm) normalize(cut_last);
-  if (abort_q) {  // unreachable (see k_route_tier): an empty list, never a stale one
+  if (abort_q) {  // unreachable (each query has its pass from k_probe): an empty list, never a stale one
     if (lane == 0) {
       a.redo[q] = a.pass + 1;
       a.nclus[q] = 0;
@@ -567,50 +567,17 @@ __global__ void __launch_bounds__(64) k_route(RouteArgs a) {
   if (q < a.nq && (!a.tiered || a.redo[q] == a.pass)) route_query<BUF>(a, q);
 }
 
-// one thread per probe: the cluster range [c0, c1) of its bucket
-__global__ void k_route_lookup(RouteArgs a) {
-  const int64_t n = a.nq * a.P;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += stride) {
-    const int64_t q = t / a.P;
-    if (t - q * a.P >= a.counts[q]) continue;
-    const uint32_t code = a.codes[t];
-    a.lk[t] = make_uint2(a.bc_off[code], a.bc_off[(uint64_t)code + 1]);
-  }
-}
-
 size_t route_lds_bytes(int k_c, int pst) {
   // the staging buffer only for heaps past the light first pass's size
   const size_t buf = k_c > ROUTE_LIGHT_HEAP ? WAVE : 0;
   return sizeof(RouteLds) + sizeof(uint64_t) * ((size_t)k_c + buf) + 3 * sizeof(uint32_t) * (size_t)pst;
 }
 
-// one wave per query: the pass whose heap can hold every cluster the query
-// could score (the clusters of its probed multi-cluster buckets, the most the
-// heap can ever reach), so that no pass gives a query up to the next
-__global__ void __launch_bounds__(256) k_route_tier(RouteArgs a, int nt, int h0, int h1) {
-  const int lane = lane_id();
-  const int64_t q = (int64_t)blockIdx.x * (blockDim.x / WAVE) + threadIdx.x / WAVE;
-  if (q >= a.nq) return;
-  const int cnt = a.counts[q];
-  uint32_t m = 0;
-  for (int i = lane; i < cnt; i += WAVE) {
-    const uint2 r = a.lk[q * a.P + i];
-    const uint32_t c = r.y - r.x;
-    m += c >= 2 ? c : 0u;
-  }
-  m = wave_sum_u32(m);
-  if (lane == 0) a.redo[q] = m <= (uint32_t)h0 ? 0 : (nt > 2 && m <= (uint32_t)h1 ? 1 : nt - 1);
-}
-
 hipError_t launch_route(const RouteArgs &a, hipStream_t s, hipStream_t aux, hipEvent_t fork,
                         hipEvent_t join) {
   if (a.nq <= 0) return hipSuccess;
-  if (!a.looked_up) {  // else the probe kernel has written lk (and the passes)
-    int64_t blocks = (a.nq * a.P + 255) / 256;
-    if (blocks > 16384) blocks = 16384;
-    hipLaunchKernelGGL(k_route_lookup, dim3((unsigned)blocks), dim3(256), 0, s, a);
-  }
+  // the probe kernel has looked up every probe's bucket range (lk) and, when
+  // K_c is past the first heap, written each query's pass (redo)
   // A heap of at most ROUTE_LIGHT_HEAP keys in LDS lets more waves share a
   // CU.  When K_c is larger, each query goes to the pass with the smallest
   // heap (ROUTE_LIGHT_HEAP, ROUTE_MID_HEAP, K_c) that holds every cluster it
@@ -642,10 +609,7 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s, hipStream_t aux, hipE
   int tiers[3];
   const int nt = route_tiers(a.k_c, tiers);
   if (nt == 1) return launch(a, a.k_c, 0, s);
-  if (!a.looked_up)
-    hipLaunchKernelGGL(k_route_tier, dim3((unsigned)((a.nq + 3) / 4)), dim3(256), 0, s, a, nt,
-                       tiers[0], nt > 2 ? tiers[1] : tiers[0]);
-  hipError_t e = hipGetLastError();
+  hipError_t e = hipSuccess;
   RouteArgs b = a;
   b.tiered = 1;
   if (aux && fork && join) {

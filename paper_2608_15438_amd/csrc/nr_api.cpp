@@ -445,22 +445,20 @@ hipError_t run_probe(const nr_index *ix, const float *logits, int64_t nq, int P,
   return nr::launch_probe(a, s);
 }
 
+// after run_probe(..., &B) on the same buffers (it writes B.lk and B.redo)
 hipError_t run_route(const nr_index *ix, const float *logits, int64_t nq, int P,
                      const nr_params *p, const Buffers &B, uint32_t *clus, int32_t *nclus,
                      int64_t cap, int32_t *qstats, hipStream_t s,
-                     const nr::PairHistArgs *ph = nullptr, bool looked_up = false) {
+                     const nr::PairHistArgs *ph = nullptr) {
   nr::RouteArgs a{};
   a.logits = logits;
   a.nq = nq;
   a.b = ix->d.b;
   a.P = P;
-  a.codes = B.codes;
   a.bins = B.bins;
   a.counts = B.counts;
-  a.bc_off = ix->d.bc_off;
   a.lk = B.lk;
   a.redo = B.redo;
-  a.looked_up = looked_up ? 1 : 0;
   a.centroids = ix->d.centroids;
   a.k_c = (int)kc_eff(ix, p);
   a.b_batch = p->b_batch;
@@ -986,7 +984,7 @@ nr_status nr_route(const nr_index *cix, const float *logits, int64_t nq, int32_t
     const float *lg = logits + q0 * ix->d.b;
     HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream, &B));
     HIP_OK(run_route(ix, lg, n, P, p, B, clusters + q0 * cap, n_clusters + q0, cap, nullptr,
-                     stream, nullptr, true));
+                     stream));
   }
   return NR_OK;
 }
@@ -1064,7 +1062,7 @@ nr_status nr_search_ex(const nr_index *cix, const void *queries, const float *lo
       w->clean_hist = nullptr;
     }
     HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, qs, stream,
-                     B.shared ? &ph : nullptr, true));
+                     B.shared ? &ph : nullptr));
     if (prof) HIP_OK(hipEventRecord(es.ev[3], stream));
     if (B.shared) {
       HIP_OK(run_refine_shared(ix, sa, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
@@ -1132,7 +1130,7 @@ nr_status nr_search_noalloc(const nr_index *cix, const void *queries, const floa
     const float *lg = logits ? logits + q0 * ix->d.b : B.logits;
     if (!logits) HIP_OK(run_encode(ix, qp, n, B.logits, B, stream));
     HIP_OK(run_probe(ix, lg, n, P, p, B.codes, B.costs, B.bins, B.counts, stream, &B));
-    HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, nullptr, stream, nullptr, true));
+    HIP_OK(run_route(ix, lg, n, P, p, B, B.clus, B.nclus, cap, nullptr, stream));
     HIP_OK(run_refine(ix, qp, n, k, B.clus, B.nclus, cap, B, out_ids + q0 * k,
                       out_dists + q0 * k, nullptr, stream, nullptr));
   }

@@ -145,16 +145,13 @@ struct RouteArgs {
   const float *logits;
   int64_t nq;
   int b, P;
-  const uint32_t *codes;
   const int32_t *bins;
   const int32_t *counts;
-  const uint32_t *bc_off;
-  uint2 *lk;             // [nq x P] scratch: cluster range of each probe's bucket
+  uint2 *lk;             // [nq x P] cluster range of each probe's bucket (written by k_probe)
   int pst;               // probes per query whose ranges are staged in LDS (set per pass)
   int hcap, pass;        // heap slots in LDS and pass number (set by launch_route)
   int tiered;            // redo[q] holds the pass that routes query q
-  int looked_up;         // lk (and with K_c past the first heap, redo) written by the probe kernel
-  int32_t *redo;         // [nq] the pass of each query (tiered), or its next pass
+  int32_t *redo;         // [nq] the pass of each query (written by k_probe when tiered)
   const float *centroids;
   int k_c, b_batch, b_min, t_low, u_heap, u_front;
   float alpha_front;
