@@ -149,13 +149,28 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
   // The logits are read from the lanes holding them (readlane), so every lane
   // of the wave must be active here: callers run it on all lanes and mask
   // the result afterwards.
+  // rows of whole 16-byte groups (b a multiple of 4, centroids 16-byte
+  // aligned) load 4 coordinates per instruction
+  const bool cvec = (b & 3) == 0 && (reinterpret_cast<uintptr_t>(a.centroids) & 15) == 0;
   auto centroid_dist = [&](uint32_t cid) __attribute__((always_inline)) {
     const float *mu = a.centroids + (int64_t)cid * b;
-    // the whole centroid row is loaded at once (b <= 30; unused slots read
-    // coordinate 0), then accumulated in dimension order
+    // the whole centroid row is loaded at once (b <= 31; unused slots hold
+    // coordinate 0 or stay unread), then accumulated in dimension order
     float m[32];
+    if (cvec) {
+      const float4 *mu4 = reinterpret_cast<const float4 *>(mu);
 #pragma unroll
-    for (int j = 0; j < 32; ++j) m[j] = mu[j < b ? j : 0];
+      for (int j4 = 0; j4 < 8; ++j4) {
+        const float4 v = 4 * j4 < b ? mu4[j4] : make_float4(0.f, 0.f, 0.f, 0.f);
+        m[4 * j4] = v.x;
+        m[4 * j4 + 1] = v.y;
+        m[4 * j4 + 2] = v.z;
+        m[4 * j4 + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 32; ++j) m[j] = mu[j < b ? j : 0];
+    }
     float acc = 0.0f;
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
