@@ -38,6 +38,7 @@ struct RouteLds {
   uint64_t bkey[WAVE];            // sorted batch keys
   float wd[WAVE];                 // distances of the window's first multi-bucket clusters
   int32_t mk[WAVE];               // merge: batch element (+1) landing in each slot of a chunk
+  float lq[32];                   // the query's logits (read by every lane at once)
 };
 
 // M(x): piecewise linear through the knots, constant outside them.  Knot j
@@ -117,6 +118,7 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
   const float ky = lane < a.m_knots ? a.m_y[lane] : 0.0f;
   const float ks = lane < a.m_knots ? a.m_slope[lane] : 0.0f;
   const float lg = lane < b ? a.logits[q * b + lane] : 0.0f;
+  if (lane < 32) S.lq[lane] = lg;
   const int cnt = a.counts[q];
   const int32_t *bins = a.bins + q * P;
   uint32_t *out = a.clus + q * a.cap;
@@ -146,11 +148,10 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
   };
 
   // distance of one centroid to the query's logits, dimensions in order.
-  // The logits are read from the lanes holding them (readlane), so every lane
-  // of the wave must be active here: callers run it on all lanes and mask
-  // the result afterwards.
-  // rows of whole 16-byte groups (b a multiple of 4, centroids 16-byte
-  // aligned) load 4 coordinates per instruction
+  // The logits come from LDS (S.lq, the same 16 bytes for every lane per
+  // load); callers run it on all lanes and mask the result afterwards.
+  // Centroid rows of whole 16-byte groups (b a multiple of 4, centroids
+  // 16-byte aligned) load 4 coordinates per instruction.
   const bool cvec = (b & 3) == 0 && (reinterpret_cast<uintptr_t>(a.centroids) & 15) == 0;
   auto centroid_dist = [&](uint32_t cid) __attribute__((always_inline)) {
     const float *mu = a.centroids + (int64_t)cid * b;
@@ -171,13 +172,21 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
 #pragma unroll
       for (int j = 0; j < 32; ++j) m[j] = mu[j < b ? j : 0];
     }
+    // the logits from LDS, the same 16 bytes for every lane
+    const float4 *lq4 = reinterpret_cast<const float4 *>(S.lq);
     float acc = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 32; ++j) {
-      if (j < b) {
-        const float lj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lg), j));
-        const float t = lj - m[j];
-        acc = fmaf(t, t, acc);
+    for (int j4 = 0; j4 < 8; ++j4) {
+      if (4 * j4 < b) {
+        const float4 l4 = lq4[j4];
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (4 * j4 + u < b) {
+            const float t = lv[u] - m[4 * j4 + u];
+            acc = fmaf(t, t, acc);
+          }
+        }
       }
     }
     return acc;
