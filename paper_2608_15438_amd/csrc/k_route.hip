@@ -59,6 +59,17 @@ __device__ __forceinline__ float margin_dev(int m, float kx, float ky, float ks,
   return v;
 }
 
+// minimum over the wave with DPP moves inside each row of 16 lanes (pairs,
+// quads, half rows, rows) and the four row minima read from lanes 0, 16, 32
+// and 48; exact, like any order of fminf over finite values and +inf
+__device__ __forceinline__ float route_min_f32(float v) {
+  v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0xB1, 0xF, 0xF, false)));
+  v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x4E, 0xF, 0xF, false)));
+  v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x141, 0xF, 0xF, false)));
+  v = fminf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x140, 0xF, 0xF, false)));
+  return fminf(fminf(bcast_f32(v, 0), bcast_f32(v, 16)), fminf(bcast_f32(v, 32), bcast_f32(v, 48)));
+}
+
 // the keys of lanes 0..n-1 in ascending order (lanes from n on keep theirs):
 // each lane counts the keys ranked before its own (by value, then lane) from
 // scalar broadcasts and places its key at that rank through tmp[0, n) in LDS;
@@ -268,8 +279,6 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
     hbn = 0;
   };
 
-  // score the pending batch and fold it into H; with pre >= 0 the batch is
-  // window clusters pre, pre + 1, ... whose distances may already be in S.wd
   // the pool sorted into H[0, hh) and pruned to keys below cutv, 64 keys at
   // a time: a chunk is read into registers, sorted across the wave and merged
   // into the sorted prefix, which never reaches past the chunk just read
@@ -295,7 +304,10 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
     fastm = false;
   };
 
-  auto run_batch = [&](int pre) __attribute__((always_inline)) {
+  // score the pending batch and fold it into H; with pre >= 0 the batch is
+  // window clusters pre, pre + 1, ... (cluster ids cbase, cbase + 1, ...)
+  // whose distances may already be in S.wd, else the clusters in S.pend
+  auto run_batch = [&](int pre, uint32_t cbase) __attribute__((always_inline)) {
     const int nb = npend;
     n_batches += 1;
     n_scored += nb;
@@ -304,14 +316,14 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
     // a window batch whose distances are not all in S.wd first scores the
     // next 64 of the window's clusters at once
     if (pre >= 0 && (pre < pbase || pre + nb > pbase + npre)) precompute(pre);
-    if (lane < nb) cid = S.pend[lane];
+    if (lane < nb) cid = pre >= 0 ? cbase + (uint32_t)lane : S.pend[lane];
     if (pre >= 0) {
       if (lane < nb) d = S.wd[pre - pbase + lane];
     } else {
       const float dc = centroid_dist(cid);  // all lanes (cluster 0 past nb)
       if (lane < nb) d = dc;
     }
-    float dm = wave_min_f32(d);
+    float dm = route_min_f32(d);
     d_min = dm < d_min ? dm : d_min;
     const float M = margin_dev(a.m_knots, kx, ky, ks, d_min);
     const float theta = a.gate_on ? d_min + M : INFINITY;
@@ -489,10 +501,8 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
         const uint32_t mc0 = S.wc0[first_multi], mc1 = S.wc1[first_multi];
         for (uint32_t v = mc0; v < mc1 && !stop;) {
           uint32_t take = mc1 - v < (uint32_t)a.b_batch ? mc1 - v : (uint32_t)a.b_batch;
-          if ((uint32_t)lane < take) S.pend[lane] = v + lane;
-          __builtin_amdgcn_wave_barrier();
           npend = (int)take;
-          run_batch((int)(S.wpre[first_multi] + (v - mc0)));
+          run_batch((int)(S.wpre[first_multi] + (v - mc0)), v);
           v += take;
         }
         if (!stop && full_and_quiet()) stop = true;
@@ -541,13 +551,13 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
             __builtin_amdgcn_wave_barrier();
             npend += (int)take;
             v += take;
-            if (npend == a.b_batch) run_batch(-1);
+            if (npend == a.b_batch) run_batch(-1, 0u);
           }
         }
         p += run;
         if (off + run < WAVE) break;  // bin z ends inside this window
       }
-      if (!stop && npend > 0) run_batch(-1);
+      if (!stop && npend > 0) run_batch(-1, 0u);
       npend = 0;
       if (!stop && full_and_quiet()) stop = true;
     }
