@@ -47,15 +47,15 @@ __global__ void __launch_bounds__(64) k_probe(ProbeArgs a) {
   // rank of each dimension by (delta, dim): SmallestKIndices
   int rank = 0;
   for (int i = 0; i < b; ++i) {
-    const float di = __shfl(dl, i);
+    const float di = bcast_f32(dl, i);  // i is the same in every lane
     rank += (di < dl) || (di == dl && i < lane);
   }
   // lane r < l_sel: the dimension of rank r and its delta
   int sel_dim = 0;
   float sel_dlt = 0.f;
   for (int i = 0; i < b; ++i) {
-    const int ri = __shfl(rank, i);
-    const float di = __shfl(dl, i);
+    const int ri = (int)bcast_u32((uint32_t)rank, i);
+    const float di = bcast_f32(dl, i);
     if (lane == ri) {
       sel_dim = i;
       sel_dlt = di;
@@ -66,7 +66,7 @@ __global__ void __launch_bounds__(64) k_probe(ProbeArgs a) {
   int n = 1;
   __builtin_amdgcn_wave_barrier();
   for (int r = 0; r < l_sel; ++r) {
-    const float dr = __shfl(sel_dlt, r);
+    const float dr = bcast_f32(sel_dlt, r);
     const uint32_t rbit = 1u << r;
     // E: every kept flip set plus rank r, in L's order (flip sets at R_max
     // or past S_max drop out)
