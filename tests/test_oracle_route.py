@@ -70,6 +70,25 @@ def test_margin_curve(oracle_lib):
     assert O.margin(O.RouteParams(), 5.0) == 0.0  # no knots: M == 0
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_gate_never_rises(oracle_lib, seed):
+    """With knots of increasing x and non-decreasing y (the library rejects
+    others), M is non-decreasing, and so is the fp32 gate x + M(x): as d_min
+    falls the gate never rises, which is what lets the search prune the heap
+    once by the last gate while no key is cut."""
+    rng = np.random.default_rng(seed)
+    m = int(rng.integers(1, 9))
+    mx = np.sort(rng.uniform(0.0, 20.0, m)).astype(np.float32)
+    mx = np.unique(mx)
+    my = np.sort(rng.uniform(0.0, 5.0, len(mx))).astype(np.float32)
+    prm = O.RouteParams(m_x=mx, m_y=my)
+    xs = np.sort(np.concatenate([rng.uniform(-2.0, 25.0, 3000), mx.astype(np.float64)])).astype(np.float32)
+    ms = np.array([O.margin(prm, float(x)) for x in xs], np.float32)
+    assert np.all(np.diff(ms) >= 0)
+    theta = xs + ms  # fp32 additions, as the centroid stage forms the gate
+    assert theta.dtype == np.float32 and np.all(np.diff(theta) >= 0)
+
+
 def _probe_lists(cfg, n, nq, P, **ov):
     w, ix, X, Q = instance(cfg, n, nq, **ov)
     enc = oracle_encoder(ix)
