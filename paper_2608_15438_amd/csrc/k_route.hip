@@ -142,8 +142,8 @@ __device__ __forceinline__ void route_query(const RouteArgs &a, const int64_t q)
   int hh = 0, hbn = 0;
   // Until the kept keys could reach K_c, no key is ever cut and the stop
   // cannot fire (it needs |H| = K_c), so a batch only appends its gated keys
-  // to H unsorted: H[0, npool).  theta only falls from batch to batch (M is
-  // non-decreasing and d_min only falls), so pruning the pool once by the
+  // to H unsorted: H[0, npool).  theta never rises from batch to batch (M is
+  // non-decreasing and d_min never rises), so pruning the pool once by the
   // latest theta leaves what pruning after every batch would; the pool is
   // sorted and pruned when a batch could reach K_c, and at the end.
   bool fastm = true;
